@@ -1,0 +1,307 @@
+"""CPU oracle for Jacobi decoding -- TEST INFRASTRUCTURE ONLY.
+
+Only tests/, the smoke check in __graft_entry__ and the benchmark's CPU-baseline leg may
+import this package. The GPU product path never does. oracle.c holds the arithmetic; this
+module compiles it and marshals numpy arrays through ctypes.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_u64 = ctypes.c_uint64
+_dbl = ctypes.c_double
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32), ("head_dim", _i32),
+                ("ffn_dim", _i32), ("vocab", _i32), ("rms_eps", _dbl), ("rope_base", _dbl),
+                ("round_bf16", _i32)]
+
+
+class _GuessSpec(ctypes.Structure):
+    _fields_ = [("policy", _i32), ("block_policy", _i32), ("stream", _vp), ("stream_len", _i32),
+                ("thr53", _u64), ("seed", _u64)]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int64), ("blocks", ctypes.c_int64), ("tokens", ctypes.c_int64),
+                ("accept_hist", ctypes.c_int64 * 257)]
+
+
+def build(verbose=False):
+    """Compile oracle.c into liboracle.so (always recompiles)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    global _lib
+    _lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        L.orc_num_threads.restype = _i32
+        L.orc_bf16.restype = _dbl
+        L.orc_bf16.argtypes = [_dbl]
+        L.orc_rmsnorm.argtypes = [_vp, _i32, _vp, _dbl, _i32, _vp]
+        L.orc_rope.argtypes = [_vp, _i32, _i32, _dbl]
+        L.orc_attention_row.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _vp]
+        L.orc_linear.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp]
+        L.orc_silu.restype = _dbl
+        L.orc_silu.argtypes = [_dbl]
+        L.orc_argmax.restype = _i32
+        L.orc_argmax.argtypes = [_vp, _i32]
+        L.orc_accept_len.restype = _i32
+        L.orc_accept_len.argtypes = [_vp, _vp, _i32]
+        L.orc_mix.restype = _u64
+        L.orc_mix.argtypes = [_u64]
+        L.orc_guess.restype = _i32
+        L.orc_guess.argtypes = [ctypes.POINTER(_GuessSpec), _i32, _i32, _i32, _i32]
+        L.orc_model_new.restype = _vp
+        L.orc_model_new.argtypes = [ctypes.POINTER(_Config), _vp]
+        L.orc_model_free.argtypes = [_vp]
+        L.orc_state_new.restype = _vp
+        L.orc_state_new.argtypes = [_vp, _i32]
+        L.orc_state_free.argtypes = [_vp]
+        L.orc_state_len.restype = _i32
+        L.orc_state_len.argtypes = [_vp]
+        L.orc_state_pending.restype = _i32
+        L.orc_state_pending.argtypes = [_vp]
+        L.orc_prefill.restype = _i32
+        L.orc_prefill.argtypes = [_vp, _vp, _i32, _vp]
+        L.orc_eval_block.restype = _i32
+        L.orc_eval_block.argtypes = [_vp, _vp, _i32, _vp]
+        L.orc_commit.restype = _i32
+        L.orc_commit.argtypes = [_vp, _i32, _i32]
+        L.orc_jacobi_step.restype = _i32
+        L.orc_jacobi_step.argtypes = [_vp, _vp, _i32, _vp, _vp, _vp]
+        L.orc_forward_full.restype = _i32
+        L.orc_forward_full.argtypes = [_vp, _vp, _i32, _vp]
+        L.orc_ar_decode.restype = _i32
+        L.orc_ar_decode.argtypes = [_vp, _vp, _i32, _i32, _vp]
+        L.orc_jacobi_decode.restype = _i32
+        L.orc_jacobi_decode.argtypes = [_vp, _vp, _i32, _i32, _i32, ctypes.POINTER(_GuessSpec), _i32, _vp,
+                                        ctypes.POINTER(_Stats), _vp, _vp, _i32]
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data
+
+
+def num_threads():
+    return int(lib().orc_num_threads())
+
+
+# ---- scalar and row operations (exposed for pinning) -------------------------------------
+
+def bf16(x):
+    return float(lib().orc_bf16(float(x)))
+
+
+def rmsnorm(x, g, eps, round_bf16=False):
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    out = np.empty_like(x)
+    lib().orc_rmsnorm(_p(x), x.size, _p(g), eps, int(round_bf16), _p(out))
+    return out
+
+
+def rope(x, t, base=10000.0):
+    x = np.array(x, dtype=np.float64)
+    lib().orc_rope(_p(x), x.size, int(t), base)
+    return x
+
+
+def attention_row(q, K, V):
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    K = np.ascontiguousarray(K, dtype=np.float64)
+    V = np.ascontiguousarray(V, dtype=np.float64)
+    out = np.empty(q.size, dtype=np.float64)
+    lib().orc_attention_row(_p(q), _p(K), _p(V), K.shape[0], K.shape[1], q.size, _p(out))
+    return out
+
+
+def linear(a, W):
+    """y = a . W^T with a: rows x in (float64), W: out x in (float32)."""
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    y = np.empty((a.shape[0], W.shape[0]), dtype=np.float64)
+    lib().orc_linear(_p(a), a.shape[0], _p(W), W.shape[1], W.shape[0], _p(y))
+    return y
+
+
+def silu(x):
+    return float(lib().orc_silu(float(x)))
+
+
+def argmax(logits):
+    a = np.ascontiguousarray(logits, dtype=np.float64)
+    return int(lib().orc_argmax(_p(a), a.size))
+
+
+def accept_len(z, pred):
+    z = np.ascontiguousarray(z, dtype=np.int32)
+    pred = np.ascontiguousarray(pred, dtype=np.int32)
+    return int(lib().orc_accept_len(_p(z), _p(pred), z.size))
+
+
+def mix(x):
+    return int(lib().orc_mix(x))
+
+
+def thr53(p):
+    """Corruption threshold for rate p: corrupt when the top 53 bits of a draw are below it."""
+    return int(round(min(max(p, 0.0), 1.0) * float(1 << 53)))
+
+
+class GuessSpec:
+    def __init__(self, policy=0, block_policy=0, stream=None, p=0.0, seed=0):
+        self.stream = None if stream is None else np.ascontiguousarray(stream, dtype=np.int32)
+        self.c = _GuessSpec(policy, block_policy, None if self.stream is None else _p(self.stream),
+                            0 if self.stream is None else self.stream.size, thr53(p), seed)
+
+
+def guess(spec: GuessSpec, seq, t, d, vocab):
+    return int(lib().orc_guess(ctypes.byref(spec.c), seq, t, d, vocab))
+
+
+# ---- model --------------------------------------------------------------------------------
+
+class Model:
+    """The LLaMA-style decoder on fp32 weight arrays (bf16 values for bf16 models)."""
+
+    def __init__(self, cfg, tensors_f32, round_bf16=None):
+        self.cfg = cfg
+        self.tensors = [np.ascontiguousarray(t, dtype=np.float32) for t in tensors_f32]
+        if round_bf16 is None:
+            round_bf16 = cfg.dtype == "bf16"
+        self.round_bf16 = bool(round_bf16)
+        self._cc = _Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab,
+                           cfg.rms_eps, cfg.rope_base, int(self.round_bf16))
+        ptrs = (ctypes.c_void_p * len(self.tensors))(*[_p(t) for t in self.tensors])
+        self._ptrs = ptrs
+        self.h = lib().orc_model_new(ctypes.byref(self._cc), ctypes.cast(ptrs, ctypes.c_void_p))
+        if not self.h:
+            raise MemoryError("orc_model_new failed")
+
+    def __del__(self):
+        try:
+            if self.h:
+                lib().orc_model_free(self.h)
+                self.h = None
+        except Exception:
+            pass
+
+    def forward_full(self, tokens):
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        out = np.empty((t.size, self.cfg.vocab), dtype=np.float64)
+        rc = lib().orc_forward_full(self.h, _p(t), t.size, _p(out))
+        if rc:
+            raise RuntimeError(f"orc_forward_full failed: {rc}")
+        return out
+
+    def ar_decode(self, prompt, max_new):
+        p = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.empty(max_new, dtype=np.int32)
+        rc = lib().orc_ar_decode(self.h, _p(p), p.size, max_new, _p(out))
+        if rc:
+            raise RuntimeError(f"orc_ar_decode failed: {rc}")
+        return out
+
+    def jacobi_decode(self, prompt, n, max_new, spec: GuessSpec, seq=0, max_steps=None):
+        p = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.empty(max_new, dtype=np.int32)
+        st = _Stats()
+        cap = max_steps or max_new
+        sm = np.zeros(cap, dtype=np.int32)
+        sa = np.zeros(cap, dtype=np.int32)
+        rc = lib().orc_jacobi_decode(self.h, _p(p), p.size, n, max_new, ctypes.byref(spec.c), seq, _p(out),
+                                     ctypes.byref(st), _p(sm), _p(sa), cap)
+        if rc:
+            raise RuntimeError(f"orc_jacobi_decode failed: {rc}")
+        steps = int(st.steps)
+        stats = {"steps": steps, "blocks": int(st.blocks), "tokens": int(st.tokens),
+                 "accept_hist": [int(x) for x in st.accept_hist],
+                 "step_m": sm[:min(steps, cap)].copy(), "step_a": sa[:min(steps, cap)].copy()}
+        return out, stats
+
+
+class State:
+    """KV cache and committed length of one sequence, for step-by-step (teacher-forced) use."""
+
+    def __init__(self, model: Model, max_ctx):
+        self.model = model
+        self.h = lib().orc_state_new(model.h, max_ctx)
+        if not self.h:
+            raise MemoryError("orc_state_new failed")
+
+    def __del__(self):
+        try:
+            if self.h:
+                lib().orc_state_free(self.h)
+                self.h = None
+        except Exception:
+            pass
+
+    @property
+    def L(self):
+        return int(lib().orc_state_len(self.h))
+
+    @property
+    def pending(self):
+        return int(lib().orc_state_pending(self.h))
+
+    def prefill(self, prompt, want_logits=False):
+        p = np.ascontiguousarray(prompt, dtype=np.int32)
+        lg = np.empty(self.model.cfg.vocab, dtype=np.float64) if want_logits else None
+        y0 = lib().orc_prefill(self.h, _p(p), p.size, None if lg is None else _p(lg))
+        if y0 < 0:
+            raise RuntimeError(f"orc_prefill failed: {y0}")
+        return (y0, lg) if want_logits else y0
+
+    def eval_block(self, block):
+        b = np.ascontiguousarray(block, dtype=np.int32)
+        lg = np.empty((b.size, self.model.cfg.vocab), dtype=np.float64)
+        rc = lib().orc_eval_block(self.h, _p(b), b.size, _p(lg))
+        if rc:
+            raise RuntimeError(f"orc_eval_block failed: {rc}")
+        return lg
+
+    def commit(self, a, pending):
+        rc = lib().orc_commit(self.h, int(a), int(pending))
+        if rc:
+            raise RuntimeError(f"orc_commit failed: {rc}")
+
+    def jacobi_step(self, block, want_logits=False):
+        b = np.ascontiguousarray(block, dtype=np.int32)
+        out = np.empty(b.size, dtype=np.int32)
+        a = ctypes.c_int32(0)
+        lg = np.empty((b.size, self.model.cfg.vocab), dtype=np.float64) if want_logits else None
+        rc = lib().orc_jacobi_step(self.h, _p(b), b.size, _p(out), ctypes.byref(a),
+                                   None if lg is None else _p(lg))
+        if rc:
+            raise RuntimeError(f"orc_jacobi_step failed: {rc}")
+        return (out, int(a.value), lg) if want_logits else (out, int(a.value))
+
+
+def load_model(cfg, seed=0, round_bf16=None):
+    """Oracle model on the seeded synthetic weights of cfg."""
+    from paper_2403_00835_amd import workload
+    tensors = [workload.as_f32(cfg, t) for t in workload.make_weights(cfg, seed)]
+    return Model(cfg, tensors, round_bf16=round_bf16)

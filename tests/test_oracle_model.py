@@ -1,0 +1,211 @@
+"""Pins of the oracle's whole decoder on constructed weights whose greedy output or logits
+have a closed form, plus the KV-cache property of Section 3.1 (the keys and values of fixed
+tokens need not be recomputed): a cached block forward equals a full recompute.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+import oracle
+from paper_2403_00835_amd.configs import ModelConfig
+from paper_2403_00835_amd import workload
+
+D, V, H, HD, F = 64, 48, 4, 16, 80
+
+
+def _cfg(n_layers=1):
+    return ModelConfig(n_layers=n_layers, d_model=D, n_heads=H, head_dim=HD, ffn_dim=F, vocab=V, dtype="f32")
+
+
+def _perm_matrix(perm, n):
+    """P with P[perm[i], i] = 1, so P @ e_i = e_{perm[i]}."""
+    P = np.zeros((n, n), dtype=np.float32)
+    P[perm, np.arange(n)] = 1.0
+    return P
+
+
+def _base_tensors(cfg, s=1.0):
+    """One-hot embedding s * e_v, LM head equal to the embedding, every matrix zero."""
+    E = np.zeros((V, D), dtype=np.float32)
+    E[np.arange(V), np.arange(V)] = s
+    ts = [E]
+    for _ in range(cfg.n_layers):
+        ts += [np.ones(D, np.float32), np.zeros((D, D), np.float32), np.zeros((D, D), np.float32),
+               np.zeros((D, D), np.float32), np.zeros((D, D), np.float32), np.ones(D, np.float32),
+               np.zeros((F, D), np.float32), np.zeros((F, D), np.float32), np.zeros((D, F), np.float32)]
+    ts += [np.ones(D, np.float32), E.copy()]
+    return ts
+
+
+def _cycle_on_vocab(shift):
+    perm = np.arange(D)
+    perm[:V] = (np.arange(V) + shift) % V
+    return perm
+
+
+def test_zero_layers_repeat_last_token():
+    # All sub-layers zero: the residual stream stays E[x_t]; with the LM head equal to the
+    # one-hot embedding the greedy next token is the current token.
+    cfg = _cfg(1)
+    m = oracle.Model(cfg, _base_tensors(cfg))
+    prompt = np.array([3, 9, 17, 5], dtype=np.int32)
+    np.testing.assert_array_equal(m.ar_decode(prompt, 6), [5] * 6)
+
+
+def test_lm_head_permutation_gives_orbit():
+    cfg = _cfg(1)
+    ts = _base_tensors(cfg)
+    perm = _cycle_on_vocab(7)[:V]
+    lm = np.zeros((V, D), dtype=np.float32)
+    lm[perm, np.arange(V)] = 1.0  # logit of perm[v] reads component v
+    ts[-1] = lm
+    m = oracle.Model(cfg, ts)
+    prompt = np.array([1, 2, 40], dtype=np.int32)
+    out = m.ar_decode(prompt, 8)
+    expect, y = [], 40
+    for _ in range(8):
+        y = int(perm[y])
+        expect.append(y)
+    np.testing.assert_array_equal(out, expect)
+
+
+def _mode_rule(tokens, pv, po):
+    """Greedy next token of the uniform-attention model, by counting: the most frequent
+    po(pv(x_u)) over the causal prefix u <= t; the current token wins ties it is part of,
+    other ties go to the lowest id."""
+    cnt = np.zeros(V, dtype=np.int64)
+    for x in tokens:
+        cnt[po[pv[x]]] += 1
+    score = cnt * 2 + (np.arange(V) == tokens[-1])
+    return int(np.argmax(score))
+
+
+def test_uniform_attention_counts_causal_prefix():
+    # q = k = 0 makes every score equal, so attention averages v over u <= t exactly.
+    # Wv and Wo are non-symmetric permutations (scaled), so a transposed operand or a
+    # non-causal mask changes the greedy tokens.
+    cfg = _cfg(1)
+    ts = _base_tensors(cfg)
+    pv, po = _cycle_on_vocab(5), _cycle_on_vocab(11)
+    ts[1 + 3] = _perm_matrix(pv, D) * 1.0   # wv
+    ts[1 + 4] = _perm_matrix(po, D) * 16.0  # wo
+    m = oracle.Model(cfg, ts)
+    rng = np.random.default_rng(0)
+    prompt = rng.integers(0, 12, size=9).astype(np.int32)
+    out = m.ar_decode(prompt, 20)
+    seq = list(prompt)
+    for y in out:
+        assert y == _mode_rule(seq, pv, po)
+        seq.append(int(y))
+    # full (uncached) forward: the argmax at every position follows the same rule
+    lg = m.forward_full(np.array(seq, dtype=np.int32))
+    for t in range(len(seq)):
+        assert oracle.argmax(lg[t]) == _mode_rule(seq[:t + 1], pv, po)
+
+
+def test_swiglu_ffn_closed_form_logits():
+    # Attention off; the FFN maps e_x to a known vector:
+    #   gate = gam * b[x] at feature sig1(x), up = dlt * b[x] at sig1(x) and sig2(x),
+    #   down sends feature f to component tau(f) with weight zeta.
+    # h = s e_x + zeta * silu(gam c) * dlt c * e_{tau(sig1(x))}, c = rmsnorm scale of s e_x.
+    cfg = _cfg(1)
+    ts = _base_tensors(cfg)
+    # weights are fp32 arrays: take the constants at fp32 precision
+    gam, dlt, zeta, s = (float(np.float32(v)) for v in (1.3, 0.7, 0.05, 1.0))
+    sig1 = (np.arange(V) * 3 + 1) % F
+    sig2 = (np.arange(V) * 3 + 2) % F
+    tau = (np.arange(F) * 7 + 3) % V
+    Wg = np.zeros((F, D), np.float32)
+    Wu = np.zeros((F, D), np.float32)
+    Wd = np.zeros((D, F), np.float32)
+    Wg[sig1, np.arange(V)] = gam
+    Wu[sig1, np.arange(V)] = dlt
+    Wu[sig2, np.arange(V)] = dlt
+    Wd[tau, np.arange(F)] = zeta
+    ts[1 + 6], ts[1 + 7], ts[1 + 8] = np.float32(Wg), np.float32(Wu), np.float32(Wd)
+    m = oracle.Model(cfg, ts)
+    tokens = np.array([4, 30, 11], dtype=np.int32)
+    lg = m.forward_full(tokens)
+    c = s / math.sqrt(s * s / D + cfg.rms_eps)
+    for t, x in enumerate(tokens):
+        h = np.zeros(D)
+        h[x] += s
+        gv = gam * c
+        h[tau[sig1[x]]] += zeta * (gv * expit(gv)) * (dlt * c)
+        nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps)
+        np.testing.assert_allclose(lg[t], s * nh[:V], rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cached_blocks_equal_full_recompute(dtype):
+    cfg = ModelConfig(n_layers=2, d_model=64, n_heads=4, head_dim=16, ffn_dim=172, vocab=256, dtype=dtype)
+    m = oracle.load_model(cfg)
+    toks = workload.make_prompt(cfg, 40, seed=9)
+    full = m.forward_full(toks)
+    st = oracle.State(m, 64)
+    y0, lg0 = st.prefill(toks[:11], want_logits=True)
+    np.testing.assert_allclose(lg0, full[10], rtol=0, atol=1e-12)
+    pos = 11
+    for blk in [1, 7, 3, 12, 6]:
+        b = toks[pos:pos + blk]
+        lg = st.eval_block(b)
+        np.testing.assert_allclose(lg, full[pos:pos + blk], rtol=0, atol=1e-12)
+        st.commit(blk, int(toks[pos + blk]) if pos + blk < len(toks) else 0)
+        pos += blk
+    assert st.L == 40
+
+
+def test_provisional_rows_are_overwritten():
+    # A rejected block's cache rows do not leak into later iterations.
+    cfg = ModelConfig(n_layers=2, d_model=64, n_heads=4, head_dim=16, ffn_dim=172, vocab=256, dtype="f32")
+    m = oracle.load_model(cfg)
+    toks = workload.make_prompt(cfg, 30, seed=10)
+    full = m.forward_full(toks)
+    st = oracle.State(m, 64)
+    st.prefill(toks[:20])
+    junk = (toks[20:28] + 17) % 256
+    junk[0] = toks[20]
+    st.eval_block(junk)  # provisional rows 20..27 hold junk
+    st.commit(1, int(toks[21]))
+    lg = st.eval_block(toks[21:30])
+    np.testing.assert_allclose(lg, full[21:30], rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("key_coord", [0, HD // 2])
+def test_two_token_rope_attention_closed_form(key_coord):
+    # Head 0 only: the second token's query is c*e_0, the first token's key is kap*c*e_j
+    # (j = 0 or the rotate-half partner hd/2), the second token's key is zero. After RoPE at
+    # positions 1 and 0 the score of key 0 is c^2 kap cos(1) / sqrt(hd) for j = 0 and
+    # c^2 kap sin(1) / sqrt(hd) for j = hd/2; the score of key 1 is 0. So the attention weight
+    # of token 0 is the logistic function of that score. Values route to distinct outputs.
+    cfg = _cfg(1)
+    ts = _base_tensors(cfg)
+    x0, x1, kap, beta, s = 10, 20, 1.75, 0.875, 1.0
+    Wq = np.zeros((D, D), np.float32)
+    Wk = np.zeros((D, D), np.float32)
+    Wv = np.zeros((D, D), np.float32)
+    Wo = np.zeros((D, D), np.float32)
+    Wq[0, x1] = 1.0
+    Wk[key_coord, x0] = kap
+    Wv[2, x0] = 1.0
+    Wv[5, x1] = 1.0
+    Wo[33, 2] = beta
+    Wo[44, 5] = beta
+    ts[1 + 1], ts[1 + 2], ts[1 + 3], ts[1 + 4] = Wq, Wk, Wv, Wo
+    m = oracle.Model(cfg, ts)
+    lg = m.forward_full(np.array([x0, x1], dtype=np.int32))
+    c = s / math.sqrt(s * s / D + cfg.rms_eps)
+    trig = math.cos(1.0) if key_coord == 0 else math.sin(1.0)
+    w = expit(c * c * kap * trig / math.sqrt(HD))
+    expect_h = [np.zeros(D), np.zeros(D)]
+    expect_h[0][x0] += s
+    expect_h[0][33] += beta * c
+    expect_h[1][x1] += s
+    expect_h[1][33] += beta * c * w
+    expect_h[1][44] += beta * c * (1 - w)
+    for t in range(2):
+        h = expect_h[t]
+        nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps)
+        np.testing.assert_allclose(lg[t], s * nh[:V], rtol=0, atol=1e-12)

@@ -1,0 +1,192 @@
+"""Benchmark of the Jacobi-decoding hot path on one MI355X.
+
+A step is one request through the whole path: prefill of a 512-token prompt, then Jacobi
+decoding of 256 tokens in blocks of n = 16 on the LLaMA-2-7B shape (bf16, seeded random
+weights). Guesses are the GPU's own greedy AR continuation with a fraction p = 0.3 of
+positions corrupted and re-drawn after every iteration (emulating a consistency-trained model);
+the block shrinks as in the paper's algorithm. value = generated tokens / second over the
+timed steps (inputs resident on the device when timing starts).
+
+Prints one JSON line. --gpus above 1 is refused: this build runs on one GPU.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_gemm_gate_up_llama7b_n16.md")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "device.h", "launch.h"):
+        with open(os.path.join(ROOT, "paper_2403_00835_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source; otherwise None."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    text = open(TRAFFIC_SUMMARY).read()
+    m_hash = re.search(r"kernel_source_hash:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(cfg, ws, mean_accept, n):
+    """The oracle as it stands, timed on this host: one Jacobi iteration of n rows at the 7B
+    shape after a 16-token prefill (attention over 16 instead of ~640 keys is about 2% of the
+    iteration's work), scaled to tokens/s with the mean accepted length of the GPU run."""
+    import oracle
+    from paper_2403_00835_amd import workload
+    log("[bench] cpu baseline: oracle on the host")
+    tensors = [workload.as_f32(cfg, t) for t in ws]
+    om = oracle.Model(cfg, tensors)
+    st = oracle.State(om, 64)
+    prompt = workload.make_prompt(cfg, 16, seed=11)
+    y0 = st.prefill(prompt)
+    block = np.array([y0] + list(workload.make_prompt(cfg, n - 1, seed=12)), dtype=np.int32)
+    t0 = time.perf_counter()
+    st.eval_block(block)
+    dt = time.perf_counter() - t0
+    del om, tensors
+    return {"value": mean_accept / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"one Jacobi iteration of {n} rows at the 7B shape after a 16-token prefill "
+                      f"({dt:.2f} s), scaled by the GPU run's mean accepted length {mean_accept:.2f}",
+            "iteration_s": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long"])
+    ap.add_argument("--p", type=float, default=0.3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (--gpus must be 1)",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+    from paper_2403_00835_amd import binding, workload
+    from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT, WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    cfg = wl.model
+    P, n, max_new = wl.prompt_len, wl.n, wl.max_new
+    torch.cuda.init()
+    stream = torch.cuda.current_stream()
+    log(f"[bench] generating {cfg.streamed_params() / 1e9:.2f} B streamed parameters")
+    t0 = time.time()
+    ws = workload.make_weights(cfg)
+    log(f"[bench] weights drawn in {time.time() - t0:.1f} s; uploading")
+    model = binding.Model(cfg, max_ctx=P + max_new + n + 64, max_block=max(n, 16), max_new=max_new,
+                          stream=stream.cuda_stream, weights=ws)
+    prompt = workload.make_prompt(cfg, P)
+    log("[bench] GPU AR decode (guess stream and AR baseline)")
+    ar, ar_stats = model.ar_decode(prompt, max_new)
+    ar_tps = max_new / ((ar_stats["prefill_ms"] + ar_stats["decode_ms"]) / 1e3)
+
+    def one_step():
+        return model.jacobi_decode(prompt, n, max_new, policy=GUESS_STREAM_REINJECT, block_policy=BLOCK_SHRINK,
+                                   stream=ar, p=args.p, seed=3)
+
+    for _ in range(args.warmup):
+        out, _ = one_step()
+        if not np.array_equal(out, ar):
+            raise RuntimeError("Jacobi output differs from greedy AR output")
+    torch.cuda.synchronize()
+    model.timing_enable("gate_up")
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out, st = one_step()
+        stats.append(st)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launches, gu_ms = model.timing_read()
+    model.timing_enable(-1)
+    if not np.array_equal(out, ar):
+        raise RuntimeError("Jacobi output differs from greedy AR output")
+
+    tokens = args.steps * max_new
+    value = tokens / elapsed
+    iters = sum(s["steps"] for s in stats)
+    decode_ms = sum(s["decode_ms"] for s in stats)
+    prefill_ms = sum(s["prefill_ms"] for s in stats) / len(stats)
+    iter_ms = decode_ms / iters
+    mean_accept = tokens / iters
+    wbytes = model.streamed_weight_bytes()
+    d, F = cfg.d_model, cfg.ffn_dim
+    # gate/up launch: packed weights (2 * F_pad * d bf16) + fp32 X rows read + bf16 H rows written
+    f_pad = (F + 31) // 32 * 32
+    gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * F * 2
+    gu_avg_s = gu_ms / 1e3 / max(launches, 1)
+    achieved = gu_bytes / gu_avg_s / 1e9
+    traffic = measured_traffic()
+    mean_ctx = P + max_new / 2
+    kv_bytes = cfg.n_layers * 2 * mean_ctx * d * 2
+    step_gbps = (wbytes + kv_bytes) / (iter_ms / 1e3) / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, ws, mean_accept, n)
+
+    line = {
+        "metric": "Jacobi-step ms & accepted tokens/s, 7B-shape bf16 n=16; HBM GB/s vs peak",
+        "value": round(value, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: prompt {P}, n={n}, {max_new} new tokens, guesses = GPU greedy "
+                               f"continuation corrupted at p={args.p} and re-drawn each iteration, shrink blocks",
+                   "prompt_len": P, "n": n, "max_new": max_new, "p": args.p, "batch": 1,
+                   "layers": cfg.n_layers, "d_model": cfg.d_model},
+        "jacobi_step_ms": round(iter_ms, 4),
+        "iterations_per_step": iters / args.steps,
+        "mean_accepted": round(mean_accept, 3),
+        "prefill_ms": round(prefill_ms, 3),
+        "ar_tokens_per_s": round(ar_tps, 3),
+        "speedup_vs_ar": round(value / ar_tps, 3),
+        "step_hbm_gbps": round(step_gbps, 1),
+        "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (per layer)", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
+                     "launches": launches},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

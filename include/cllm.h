@@ -1,0 +1,191 @@
+/*
+ * cllm.h -- C ABI of libcllm.so: the Jacobi-decoding iteration of CLLMs
+ * ("CLLMs: Consistency Large Language Models", arXiv 2403.00835) on one AMD MI355X (gfx950).
+ *
+ * The library runs a LLaMA-style causal decoder (pre-norm RMSNorm, rotate-half RoPE,
+ * multi-head attention, SwiGLU FFN, untied LM head, no biases) with hand-written HIP
+ * kernels and decodes greedily, either autoregressively (eq. ar_decoding) or by Jacobi
+ * iteration with a KV cache (Section 3.1, eq. jacobi_decoding, and the appendix algorithm
+ * "Jacobi Decoding with KV Cache").
+ *
+ * Conventions for every call:
+ *   - Token arrays are HOST int32 arrays owned by the caller; they are read or written only
+ *     during the call. Ids must lie in [0, vocab).
+ *   - The library owns all device memory (weights, KV cache, workspace); everything is
+ *     released by cllm_model_free.
+ *   - Work is queued on the stream given at creation (a hipStream_t; NULL = the default
+ *     stream). cllm_prefill, cllm_jacobi_step, cllm_jacobi_decode and cllm_ar_decode return
+ *     after the device work has completed.
+ *   - Every call returns a cllm_status and never aborts. A failed argument check leaves the
+ *     state unchanged. A device error is sticky: every later call on the context returns
+ *     CLLM_ERR_DEVICE. cllm_last_error gives a message.
+ *   - A context is not thread-safe; use one host thread per context.
+ */
+#ifndef CLLM_H
+#define CLLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cllm_status {
+    CLLM_OK = 0,
+    CLLM_ERR_ARG = 1,      /* bad argument: NULL pointer, id out of range, bad size */
+    CLLM_ERR_STATE = 2,    /* call not valid in the current state (e.g. step before prefill) */
+    CLLM_ERR_CAPACITY = 3, /* would exceed max_ctx, max_block or max_new */
+    CLLM_ERR_OOM = 4,      /* device or host allocation failed */
+    CLLM_ERR_IO = 5,       /* weight file could not be read */
+    CLLM_ERR_FORMAT = 6,   /* weight file header or size is wrong */
+    CLLM_ERR_DEVICE = 7,   /* a HIP call failed; the context is unusable */
+    CLLM_ERR_NUMERIC = 8   /* a logit was NaN */
+} cllm_status;
+
+#define CLLM_DTYPE_F32 0
+#define CLLM_DTYPE_BF16 1
+
+/* Decoder shape. head_dim must be even; n_heads * head_dim == d_model.
+ * dtype CLLM_DTYPE_BF16: bf16 weights, bf16 KV cache and bf16 matrix-product inputs with fp32
+ * accumulation, fp32 residual stream and softmax. CLLM_DTYPE_F32: fp32 everywhere. */
+typedef struct cllm_config {
+    int32_t n_layers, d_model, n_heads, head_dim, ffn_dim, vocab;
+    float rms_eps, rope_base;
+    int32_t dtype;
+} cllm_config;
+
+/* Capacity of a context. max_ctx bounds prompt + generated tokens + one block;
+ * max_block (1..64) bounds the Jacobi block length n; max_new bounds tokens per decode. */
+typedef struct cllm_runtime_opts {
+    int32_t max_ctx, max_block, max_new;
+    int32_t device;  /* HIP device ordinal */
+    void *stream;    /* hipStream_t or NULL */
+} cllm_runtime_opts;
+
+/* Guess provider of the decode (reading of the paper's random initial n-token sequence).
+ * policy CLLM_GUESS_UNIFORM: uniform ids. CLLM_GUESS_STREAM: stream[t], corrupted with rate p,
+ * initialises each block, then the model's own predictions iterate (the printed algorithm).
+ * CLLM_GUESS_STREAM_REINJECT: after every iteration each unfixed position is re-drawn from
+ * the corrupted stream (emulates a consistency-trained model).
+ * block_policy CLLM_BLOCK_SHRINK: the state shrinks by the accepted length until the block of
+ * n is fixed (the printed algorithm); CLLM_BLOCK_SLIDE: the state is always the next
+ * min(n, remaining) positions.
+ * A draw for output position t at draw index d is h = mix(mix(mix(mix(seed)^seq)^t)^d) with the
+ * SplitMix64 output function mix; uniform ids are ((h >> 32) * vocab) >> 32; a stream id is
+ * corrupted when (h >> 11) < thr53 and then replaced by
+ * (stream[t] + 1 + (((mix(h) >> 32) * (vocab - 1)) >> 32)) mod vocab. d is 0 for the initial
+ * guesses and, under REINJECT, the number of iterations done so far. */
+#define CLLM_GUESS_UNIFORM 0
+#define CLLM_GUESS_STREAM 1
+#define CLLM_GUESS_STREAM_REINJECT 2
+#define CLLM_BLOCK_SHRINK 0
+#define CLLM_BLOCK_SLIDE 1
+typedef struct cllm_guess_spec {
+    int32_t policy, block_policy;
+    const int32_t *stream; /* host, stream_len >= max_new ids; NULL for UNIFORM */
+    int32_t stream_len;
+    uint64_t thr53;        /* round(p * 2^53), p in [0, 1] */
+    uint64_t seed;
+} cllm_guess_spec;
+
+typedef struct cllm_decode_stats {
+    int64_t steps;            /* Jacobi iterations (forward passes after the prefill) */
+    int64_t blocks;
+    int64_t tokens;           /* tokens emitted (== max_new) */
+    int64_t accept_hist[65];  /* accept_hist[a]: iterations that accepted a tokens */
+    double prefill_ms;        /* device time of the prefill */
+    double decode_ms;         /* device time of the iterations */
+} cllm_decode_stats;
+
+typedef struct cllm_ctx cllm_ctx;
+
+/* Create a context with zero weights (set them with cllm_model_set_weights).
+ * Errors: ERR_ARG (bad shape or options), ERR_OOM, ERR_DEVICE. */
+cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *opts, cllm_ctx **out);
+
+/* Upload all weights from host arrays, in this order (n_tensors = 3 + 9 * n_layers):
+ *   embed [vocab][d]; per layer: attn_norm [d], wq [d][d], wk [d][d], wv [d][d], wo [d][d],
+ *   ffn_norm [d], w_gate [ffn][d], w_up [ffn][d], w_down [d][ffn]; final_norm [d];
+ *   lm_head [vocab][d].
+ * Matrices are row-major [out][in] (y = x W^T). Elements are bf16 bit patterns (uint16) for a
+ * bf16 model and float for an f32 model; norm gains are always float. The library repacks the
+ * matrices into its streaming layout on the device; the host arrays are not retained.
+ * Resets every sequence. Errors: ERR_ARG, ERR_DEVICE. */
+cllm_status cllm_model_set_weights(cllm_ctx *ctx, const void *const *tensors, int32_t n_tensors);
+
+/* Create a context from a weight file: a 64-byte header (magic "CLLMWTS1", int32 version 1,
+ * then the cllm_config fields in order, zero padding) followed by the tensors of
+ * cllm_model_set_weights in order, little-endian, no gaps.
+ * Errors: ERR_IO, ERR_FORMAT, and those of cllm_model_create. */
+cllm_status cllm_model_load(const char *path, const cllm_runtime_opts *opts, cllm_ctx **out);
+
+void cllm_model_free(cllm_ctx *ctx);
+
+/* Prefill (the algorithm's first forward): run the prompt through the decoder, fill the KV
+ * cache of positions [0, len) and return the greedy first token y0 (the pending token).
+ * Replaces any previous state of the sequence. seq must be 0 (one sequence per context).
+ * Errors: ERR_ARG (len < 1, ids), ERR_CAPACITY (len + 1 > max_ctx), ERR_NUMERIC, ERR_DEVICE. */
+cllm_status cllm_prefill(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t *first_token);
+
+/* One Jacobi iteration (eq. jacobi_decoding with the cache). block_in[0..m) holds the pending
+ * token followed by m-1 guesses for the next positions. On return block_out[i] is the greedy
+ * prediction of the token after block_in[i] (argmax of row i, ties to the lowest id) and
+ * accepted_len = a = 1 + the number of leading k >= 1 with block_in[k] == block_out[k-1]. The
+ * KV of block_in[0..a) is committed (committed length L += a) and the pending token becomes
+ * block_out[a-1]. Preconditions: prefilled; 1 <= m <= max_block; L + m <= max_ctx;
+ * block_in[0] == pending. Errors: ERR_ARG, ERR_STATE, ERR_CAPACITY, ERR_NUMERIC, ERR_DEVICE. */
+cllm_status cllm_jacobi_step(cllm_ctx *ctx, int32_t seq, const int32_t *block_in, int32_t m, int32_t *block_out,
+                             int32_t *accepted_len);
+
+/* Jacobi decoding of max_new tokens after a prefill of the prompt, in blocks of n
+ * (1 <= n <= max_block), with the iteration loop resident on the device (no host round trip
+ * per iteration). out_tokens receives max_new ids (y0 first). guess may be NULL (uniform
+ * guesses, shrink). stats may be NULL. The output equals greedy AR decoding.
+ * Errors: those of cllm_prefill, ERR_ARG (n, max_new, guess stream too short),
+ * ERR_CAPACITY (len + max_new + n > max_ctx or max_new above the context's max_new). */
+cllm_status cllm_jacobi_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t n,
+                               int32_t max_new, const cllm_guess_spec *guess, int32_t *out_tokens,
+                               cllm_decode_stats *stats);
+
+/* Greedy AR decoding of max_new tokens (eq. ar_decoding): one forward per token, on the same
+ * kernels as the Jacobi iteration with a block of one token. stats may be NULL. */
+cllm_status cllm_ar_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t max_new,
+                           int32_t *out_tokens, cllm_decode_stats *stats);
+
+/* Debug: when enabled, every later cllm_jacobi_step (and the last chunk of cllm_prefill)
+ * also copies the fp32 logits of its m rows into host_buf (row-major m x vocab; capacity
+ * host_floats floats, at least max_block * vocab). Errors: ERR_ARG. */
+cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, size_t host_floats);
+
+/* Committed length L and pending token of a sequence. Errors: ERR_ARG, ERR_STATE. */
+cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
+
+/* Kernel timing for measurement: kernel_class selects one class of kernels
+ * (CLLM_KT_* below); while enabled, each launch of that class is bracketed by HIP events on
+ * the context's stream. cllm_timing_read returns the number of timed launches and their total
+ * device time since the last enable, and clears them. kernel_class < 0 disables. */
+#define CLLM_KT_GEMM_QKV 0
+#define CLLM_KT_ATTN 1
+#define CLLM_KT_GEMM_O 2
+#define CLLM_KT_GEMM_GATE_UP 3
+#define CLLM_KT_GEMM_DOWN 4
+#define CLLM_KT_LM_HEAD 5
+#define CLLM_KT_SCAN 6
+#define CLLM_KT_ATTN_COMBINE 7
+#define CLLM_KT_EMBED 8
+cllm_status cllm_timing_enable(cllm_ctx *ctx, int32_t kernel_class);
+cllm_status cllm_timing_read(cllm_ctx *ctx, int64_t *launches, double *total_ms);
+
+/* Bytes of weights streamed by one forward pass (all matrices except the embedding), after
+ * padding to the kernels' tiles. */
+int64_t cllm_streamed_weight_bytes(const cllm_ctx *ctx);
+
+const char *cllm_status_string(cllm_status s);
+const char *cllm_last_error(const cllm_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLLM_H */

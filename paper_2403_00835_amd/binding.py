@@ -1,0 +1,223 @@
+"""ctypes binding of libcllm.so (C ABI in include/cllm.h). Argument marshalling only: every
+step of the decode runs in the library's HIP kernels. Importing this module fails loudly when
+the library has not been built; there is no fallback path.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from .configs import ModelConfig
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcllm.so")
+
+CLLM_OK = 0
+STATUS_NAMES = {0: "OK", 1: "ERR_ARG", 2: "ERR_STATE", 3: "ERR_CAPACITY", 4: "ERR_OOM", 5: "ERR_IO",
+                6: "ERR_FORMAT", 7: "ERR_DEVICE", 8: "ERR_NUMERIC"}
+KT = {"qkv": 0, "attn": 1, "o": 2, "gate_up": 3, "down": 4, "lm_head": 5, "scan": 6, "attn_combine": 7,
+      "embed": 8}
+
+_i32, _i64, _u64, _f32, _dbl, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float,
+                                     ctypes.c_double, ctypes.c_void_p)
+
+
+class cllm_config(ctypes.Structure):
+    _fields_ = [("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32), ("head_dim", _i32),
+                ("ffn_dim", _i32), ("vocab", _i32), ("rms_eps", _f32), ("rope_base", _f32), ("dtype", _i32)]
+
+
+class cllm_runtime_opts(ctypes.Structure):
+    _fields_ = [("max_ctx", _i32), ("max_block", _i32), ("max_new", _i32), ("device", _i32), ("stream", _vp)]
+
+
+class cllm_guess_spec(ctypes.Structure):
+    _fields_ = [("policy", _i32), ("block_policy", _i32), ("stream", _vp), ("stream_len", _i32),
+                ("thr53", _u64), ("seed", _u64)]
+
+
+class cllm_decode_stats(ctypes.Structure):
+    _fields_ = [("steps", _i64), ("blocks", _i64), ("tokens", _i64), ("accept_hist", _i64 * 65),
+                ("prefill_ms", _dbl), ("decode_ms", _dbl)]
+
+
+EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
+           "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_debug_logits", "cllm_seq_state",
+           "cllm_timing_enable", "cllm_timing_read", "cllm_streamed_weight_bytes", "cllm_status_string",
+           "cllm_last_error"]
+
+_lib = None
+
+
+def lib():
+    """Load libcllm.so (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2403_00835_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.cllm_model_create.argtypes = [P(cllm_config), P(cllm_runtime_opts), P(_vp)]
+        L.cllm_model_set_weights.argtypes = [_vp, _vp, _i32]
+        L.cllm_model_load.argtypes = [ctypes.c_char_p, P(cllm_runtime_opts), P(_vp)]
+        L.cllm_model_free.argtypes = [_vp]
+        L.cllm_model_free.restype = None
+        L.cllm_prefill.argtypes = [_vp, _i32, _vp, _i32, P(_i32)]
+        L.cllm_jacobi_step.argtypes = [_vp, _i32, _vp, _i32, _vp, P(_i32)]
+        L.cllm_jacobi_decode.argtypes = [_vp, _i32, _vp, _i32, _i32, _i32, P(cllm_guess_spec), _vp,
+                                         P(cllm_decode_stats)]
+        L.cllm_ar_decode.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp, P(cllm_decode_stats)]
+        L.cllm_debug_logits.argtypes = [_vp, _i32, _vp, ctypes.c_size_t]
+        L.cllm_seq_state.argtypes = [_vp, _i32, P(_i32), P(_i32)]
+        L.cllm_timing_enable.argtypes = [_vp, _i32]
+        L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
+        L.cllm_streamed_weight_bytes.argtypes = [_vp]
+        L.cllm_streamed_weight_bytes.restype = _i64
+        L.cllm_status_string.argtypes = [_i32]
+        L.cllm_status_string.restype = ctypes.c_char_p
+        L.cllm_last_error.argtypes = [_vp]
+        L.cllm_last_error.restype = ctypes.c_char_p
+        for name in EXPORTS:
+            if name not in ("cllm_model_free", "cllm_streamed_weight_bytes", "cllm_status_string",
+                            "cllm_last_error"):
+                getattr(L, name).restype = _i32
+        _lib = L
+    return _lib
+
+
+class CllmError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _p(a):
+    return a.ctypes.data
+
+
+def make_config(cfg: ModelConfig):
+    return cllm_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab,
+                       cfg.rms_eps, cfg.rope_base, cfg.dtype_code)
+
+
+def thr53(p):
+    return int(round(min(max(float(p), 0.0), 1.0) * float(1 << 53)))
+
+
+class Model:
+    """One context of libcllm.so: model weights, KV cache and workspace on one GPU."""
+
+    def __init__(self, cfg: ModelConfig, max_ctx, max_block=16, max_new=256, device=0, stream=None,
+                 weights=None, path=None):
+        self.cfg = cfg
+        self.L = lib()
+        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream)
+        h = _vp()
+        if path is not None:
+            st = self.L.cllm_model_load(os.fsencode(path), ctypes.byref(opts), ctypes.byref(h))
+        else:
+            st = self.L.cllm_model_create(ctypes.byref(make_config(cfg)), ctypes.byref(opts), ctypes.byref(h))
+        if st != CLLM_OK:
+            raise CllmError(st, "model creation failed")
+        self.h = h
+        self._dbg = None
+        if weights is not None:
+            self.set_weights(weights)
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.L.cllm_model_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, st):
+        if st != CLLM_OK:
+            msg = self.L.cllm_last_error(self.h)
+            raise CllmError(st, msg.decode() if msg else "")
+
+    def set_weights(self, tensors):
+        ts = [np.ascontiguousarray(t) for t in tensors]
+        arr = (_vp * len(ts))(*[_p(t) for t in ts])
+        self._check(self.L.cllm_model_set_weights(self.h, ctypes.cast(arr, _vp), len(ts)))
+
+    def streamed_weight_bytes(self):
+        return int(self.L.cllm_streamed_weight_bytes(self.h))
+
+    def prefill(self, prompt, seq=0):
+        p = np.ascontiguousarray(prompt, dtype=np.int32)
+        y0 = _i32(0)
+        self._check(self.L.cllm_prefill(self.h, seq, _p(p), p.size, ctypes.byref(y0)))
+        return int(y0.value)
+
+    def jacobi_step(self, block_in, seq=0):
+        b = np.ascontiguousarray(block_in, dtype=np.int32)
+        out = np.empty(b.size, dtype=np.int32)
+        a = _i32(0)
+        self._check(self.L.cllm_jacobi_step(self.h, seq, _p(b), b.size, _p(out), ctypes.byref(a)))
+        return out, int(a.value)
+
+    def jacobi_decode(self, prompt, n, max_new, policy=0, block_policy=0, stream=None, p=0.0, seed=0, seq=0):
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.empty(max_new, dtype=np.int32)
+        st = cllm_decode_stats()
+        s_arr = None if stream is None else np.ascontiguousarray(stream, dtype=np.int32)
+        g = cllm_guess_spec(policy, block_policy, None if s_arr is None else _p(s_arr),
+                            0 if s_arr is None else s_arr.size, thr53(p), seed)
+        self._check(self.L.cllm_jacobi_decode(self.h, seq, _p(pr), pr.size, n, max_new, ctypes.byref(g), _p(out),
+                                              ctypes.byref(st)))
+        return out, _stats(st)
+
+    def ar_decode(self, prompt, max_new, seq=0):
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.empty(max_new, dtype=np.int32)
+        st = cllm_decode_stats()
+        self._check(self.L.cllm_ar_decode(self.h, seq, _p(pr), pr.size, max_new, _p(out), ctypes.byref(st)))
+        return out, _stats(st)
+
+    def debug_logits(self, enable, rows=64):
+        if enable:
+            self._dbg = np.zeros((rows, self.cfg.vocab), dtype=np.float32)
+            self._check(self.L.cllm_debug_logits(self.h, 1, _p(self._dbg), self._dbg.size))
+        else:
+            self._check(self.L.cllm_debug_logits(self.h, 0, None, 0))
+            self._dbg = None
+
+    def last_logits(self, m):
+        return self._dbg[:m].copy()
+
+    def seq_state(self, seq=0):
+        L, pend = _i32(0), _i32(0)
+        self._check(self.L.cllm_seq_state(self.h, seq, ctypes.byref(L), ctypes.byref(pend)))
+        return int(L.value), int(pend.value)
+
+    def timing_enable(self, kernel_class):
+        cls = KT[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
+        self._check(self.L.cllm_timing_enable(self.h, cls))
+
+    def timing_read(self):
+        n, ms = _i64(0), _dbl(0.0)
+        self._check(self.L.cllm_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms)))
+        return int(n.value), float(ms.value)
+
+
+def _stats(st):
+    return {"steps": int(st.steps), "blocks": int(st.blocks), "tokens": int(st.tokens),
+            "accept_hist": [int(x) for x in st.accept_hist], "prefill_ms": float(st.prefill_ms),
+            "decode_ms": float(st.decode_ms)}
+
+
+def write_weight_file(path, cfg: ModelConfig, tensors):
+    """Write the weight-file format of cllm_model_load: 64-byte header, then the tensors."""
+    import struct
+    hdr = b"CLLMWTS1" + struct.pack("<i6i2fi", 1, cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim,
+                                    cfg.ffn_dim, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype_code)
+    hdr = hdr + b"\0" * (64 - len(hdr))
+    with open(path, "wb") as f:
+        f.write(hdr)
+        for t in tensors:
+            f.write(np.ascontiguousarray(t).tobytes())

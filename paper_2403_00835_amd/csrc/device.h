@@ -1,0 +1,105 @@
+// Device-side types shared by the kernels and the runtime of libcllm.so (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cllm {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+constexpr int kWave = 64;
+constexpr int kMaxBlock = 64;      // largest Jacobi block (rows per iteration)
+constexpr int kMaxRows = 64;       // rows of the activation buffers (block or prefill chunk)
+constexpr int kGemmWaves = 8;      // waves per GEMM workgroup; they split K
+constexpr int kAttnChunk = 64;     // keys per attention workgroup, at absolute positions
+constexpr int kTileBytes = 1024;   // one packed weight tile: 16 rows x 16 bytes x 4 lane groups
+
+// Precision traits. A "k-step" is the K extent one wave covers with one 16-byte load per lane:
+// 4 lane groups x VEC elements. bf16: one 16x16x32 MFMA per k-step; fp32: four 16x16x4 MFMAs.
+enum class Prec { BF16 = 1, F32 = 0 };
+template <Prec P> struct PrecT;
+template <> struct PrecT<Prec::BF16> {
+    using T = uint16_t;  // bf16 bit pattern
+    static constexpr int VEC = 8;
+    static constexpr int KSTEP = 32;
+};
+template <> struct PrecT<Prec::F32> {
+    using T = float;
+    static constexpr int VEC = 4;
+    static constexpr int KSTEP = 16;
+};
+
+__device__ __forceinline__ uint16_t f2bf(float x) {
+    __bf16 h = (__bf16)x;  // gfx950 converts with round-to-nearest-even
+    return __builtin_bit_cast(uint16_t, h);
+}
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+template <Prec P> __device__ __forceinline__ typename PrecT<P>::T to_elem(float x);
+template <> __device__ __forceinline__ uint16_t to_elem<Prec::BF16>(float x) { return f2bf(x); }
+template <> __device__ __forceinline__ float to_elem<Prec::F32>(float x) { return x; }
+template <Prec P> __device__ __forceinline__ float from_elem(typename PrecT<P>::T x);
+template <> __device__ __forceinline__ float from_elem<Prec::BF16>(uint16_t x) { return bf2f(x); }
+template <> __device__ __forceinline__ float from_elem<Prec::F32>(float x) { return x; }
+
+// One k-step of C += A * B on 16x16 tiles. a holds this lane's 16 bytes of the activation row
+// (row = lane % 16), b this lane's 16 bytes of the weight row (column = lane % 16); both hold
+// the same K indices, so the K-slot assignment inside the instruction does not matter.
+template <Prec P> __device__ __forceinline__ f32x4 mfma_kstep(u32x4 a, u32x4 b, f32x4 c);
+template <> __device__ __forceinline__ f32x4 mfma_kstep<Prec::BF16>(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+}
+template <> __device__ __forceinline__ f32x4 mfma_kstep<Prec::F32>(u32x4 a, u32x4 b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+}
+
+// Step modes of the shared iteration kernels.
+enum StepMode : int32_t {
+    MODE_STEP = 0,     // one host-driven iteration: commit a, keep the predictions for the host
+    MODE_DECODE = 1,   // device-resident decode: commit, emit, build the next block
+    MODE_PREFILL = 2,  // prompt chunk: every row is committed; the last row's argmax is pending
+};
+
+// Per-sequence control block, resident on the device. Every kernel of an iteration reads the
+// live block length m and the committed length L from here, so one launch sequence (and one
+// captured graph) serves every iteration.
+struct Ctl {
+    int32_t L;         // committed length (cache rows [0, L) are final)
+    int32_t m;         // rows of the current iteration (0 = nothing to do)
+    int32_t pending;   // known-correct next token (block row 0)
+    int32_t mode;      // StepMode
+    int32_t e;         // tokens emitted so far in this decode
+    int32_t b0, nb;    // first output position and size of the current block (shrink policy)
+    int32_t steps, blocks;
+    int32_t done;
+    int32_t a_last;    // accepted length of the last iteration
+    int32_t err;       // bit 0: NaN logit
+    int32_t n, max_new;
+    int32_t policy, block_policy;
+    int32_t seq, stream_len;
+    int32_t vocab, pad0;
+    uint64_t seed, thr53;
+    int32_t z[kMaxBlock];     // tokens of the current iteration
+    int32_t pred[kMaxBlock];  // greedy predictions of the last iteration
+    int32_t hist[kMaxBlock + 1];
+    int32_t pad1[3];
+};
+
+// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014) and the guess draw of the
+// C ABI's guess provider.
+__device__ __forceinline__ uint64_t mix64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+}  // namespace cllm

@@ -83,22 +83,20 @@ def tensor_specs(cfg: ModelConfig):
 
 
 def make_tensor(cfg: ModelConfig, spec, seed=SEED_WEIGHTS):
-    """One weight tensor: uint16 bf16 bit patterns for bf16 models, float32 for f32 models."""
+    """One weight tensor: matrices are uint16 bf16 bit patterns for bf16 models and float32 for
+    f32 models; norm gains are always float32."""
     name, shape, stream, kind = spec
     n = int(np.prod(shape))
     L = lib()
-    if cfg.dtype == "bf16":
+    if kind == "ones":
+        out = np.empty(shape, dtype=np.float32)
+        L.wl_fill_const_f32(1.0, out.ctypes.data, n)
+    elif cfg.dtype == "bf16":
         out = np.empty(shape, dtype=np.uint16)
-        if kind == "normal":
-            L.wl_fill_normal_bf16(seed, stream, WEIGHT_STD, out.ctypes.data, n)
-        else:
-            L.wl_fill_const_bf16(1.0, out.ctypes.data, n)
+        L.wl_fill_normal_bf16(seed, stream, WEIGHT_STD, out.ctypes.data, n)
     else:
         out = np.empty(shape, dtype=np.float32)
-        if kind == "normal":
-            L.wl_fill_normal_f32(seed, stream, WEIGHT_STD, out.ctypes.data, n)
-        else:
-            L.wl_fill_const_f32(1.0, out.ctypes.data, n)
+        L.wl_fill_normal_f32(seed, stream, WEIGHT_STD, out.ctypes.data, n)
     return out
 
 
@@ -113,7 +111,8 @@ def bf16_bits_to_f32(a: np.ndarray) -> np.ndarray:
 
 
 def as_f32(cfg: ModelConfig, t: np.ndarray) -> np.ndarray:
-    return bf16_bits_to_f32(t) if cfg.dtype == "bf16" else t
+    """float32 view of a weight tensor (bf16 bit patterns are widened exactly)."""
+    return bf16_bits_to_f32(t) if t.dtype == np.uint16 else t
 
 
 def make_prompt(cfg: ModelConfig, length, seed=SEED_PROMPT, seq=0):

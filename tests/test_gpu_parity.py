@@ -1,0 +1,254 @@
+"""GPU parity of the HIP path (through the C ABI) against the oracle, on the tiny fp32 and the
+small bf16 configurations: prefill logits, teacher-forced Jacobi iterations (logits within the
+tolerance, tokens bit-exact outside the tie margin, accepted length by the acceptance rule),
+whole decodes checked as valid greedy continuations, and bit-exact equality of GPU AR and GPU
+Jacobi decoding."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2403_00835_amd import workload
+from paper_2403_00835_amd.configs import (BLOCK_SHRINK, BLOCK_SLIDE, GUESS_STREAM, GUESS_STREAM_REINJECT,
+                                          GUESS_UNIFORM, SMALL, TINY)
+from tests.parity import TOL, check_rows, log, verify_greedy_sequence
+
+pytestmark = pytest.mark.gpu
+
+
+class Pair:
+    def __init__(self, cfg, max_ctx, max_block, max_new):
+        from paper_2403_00835_amd import binding
+        self.cfg = cfg
+        ws = workload.make_weights(cfg)
+        self.gpu = binding.Model(cfg, max_ctx=max_ctx, max_block=max_block, max_new=max_new, weights=ws)
+        self.orc = oracle.Model(cfg, [workload.as_f32(cfg, t) for t in ws])
+        self.tol = TOL[cfg.dtype]
+        self.max_ctx = max_ctx
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    log("[gpu] building tiny fp32 pair")
+    return Pair(TINY, max_ctx=256, max_block=64, max_new=128)
+
+
+@pytest.fixture(scope="module")
+def small():
+    log("[gpu] building small bf16 pair")
+    return Pair(SMALL, max_ctx=512, max_block=64, max_new=256)
+
+
+def _teacher_forced(pair, prompt, n, steps, stream=None, p=0.3, seed=5, policy=GUESS_STREAM_REINJECT):
+    gpu, orc, tol, V = pair.gpu, pair.orc, pair.tol, pair.cfg.vocab
+    spec = oracle.GuessSpec(GUESS_UNIFORM if stream is None else policy, 0, stream, p=p, seed=seed)
+    gpu.debug_logits(True)
+    try:
+        y0 = gpu.prefill(prompt)
+        st = oracle.State(orc, pair.max_ctx)
+        _, lg0 = st.prefill(prompt, want_logits=True)
+        P = len(prompt)
+        last = (P - 1) % 64
+        g0 = gpu.last_logits(last + 1)[last]
+        err0 = np.abs(g0 - lg0).max()
+        log(f"  prefill: y0={y0} max|dlogit|={err0:.3g}")
+        assert err0 <= tol
+        check_rows([y0], lg0[None], tol, "prefill")
+        e, pending, worst, inside = 0, y0, err0, 0
+        z = np.array([pending] + [oracle.guess(spec, 0, j, 0, V) for j in range(1, n)], dtype=np.int32)
+        for it in range(steps):
+            m = z.size
+            out, a = gpu.jacobi_step(z)
+            lg_g = gpu.last_logits(m)
+            lg_o = st.eval_block(z)
+            err = np.abs(lg_g - lg_o).max()
+            worst = max(worst, err)
+            assert err <= tol, f"iteration {it}: max|dlogit| {err} > {tol}"
+            inside += check_rows(out, lg_o, tol, f"iteration {it}")
+            assert a == oracle.accept_len(z, out)
+            assert 1 <= a <= m
+            st.commit(a, int(out[a - 1]))
+            L, pend = gpu.seq_state()
+            assert L == st.L and pend == int(out[a - 1])
+            e += a
+            pending = int(out[a - 1])
+            # next state: shrink within a block of n; re-drawn guesses when a stream is given
+            left = m - a
+            if left == 0:
+                left = n
+            nz = [pending]
+            for j in range(1, left):
+                if stream is not None:
+                    nz.append(oracle.guess(spec, 0, e + j, it + 1, V))
+                else:
+                    nz.append(int(out[a - 1 + j]) if a - 1 + j < m else oracle.guess(spec, 0, e + j, 0, V))
+            z = np.array(nz, dtype=np.int32)
+        log(f"  {steps} iterations, {e} tokens, worst max|dlogit|={worst:.3g}, rows inside margin={inside}")
+    finally:
+        gpu.debug_logits(False)
+
+
+def test_tiny_teacher_forced_iterations(tiny):
+    log("[gpu] tiny teacher-forced iterations n=8")
+    prompt = workload.make_prompt(TINY, 16)
+    _teacher_forced(tiny, prompt, n=8, steps=20)
+
+
+def test_tiny_long_prompt_spans_chunks(tiny):
+    # 150-token prompt: three prefill chunks, several attention chunks, ragged tails.
+    log("[gpu] tiny teacher-forced, prompt 150, n=13")
+    prompt = workload.make_prompt(TINY, 150, seed=7)
+    _teacher_forced(tiny, prompt, n=13, steps=8)
+
+
+def test_tiny_full_block_of_64(tiny):
+    log("[gpu] tiny teacher-forced, n=64 (four row groups)")
+    prompt = workload.make_prompt(TINY, 40, seed=8)
+    _teacher_forced(tiny, prompt, n=64, steps=3)
+
+
+def test_tiny_decode_equals_oracle(tiny):
+    log("[gpu] tiny decode vs oracle AR")
+    prompt = workload.make_prompt(TINY, 16)
+    ar_o = tiny.orc.ar_decode(prompt, 32)
+    out, st = tiny.gpu.jacobi_decode(prompt, 8, 32, policy=GUESS_UNIFORM, seed=2)
+    log(f"  steps={st['steps']} blocks={st['blocks']}")
+    inside = verify_greedy_sequence(tiny.orc, prompt, out, tiny.tol)
+    if inside == 0:
+        np.testing.assert_array_equal(out, ar_o)
+    assert st["tokens"] == 32 and st["steps"] <= 32
+    assert sum(a * c for a, c in enumerate(st["accept_hist"])) == 32
+
+
+@pytest.mark.parametrize("policy,block_policy", [(GUESS_UNIFORM, BLOCK_SHRINK), (GUESS_STREAM, BLOCK_SHRINK),
+                                                 (GUESS_STREAM_REINJECT, BLOCK_SHRINK),
+                                                 (GUESS_STREAM_REINJECT, BLOCK_SLIDE), (GUESS_STREAM, BLOCK_SLIDE)])
+def test_tiny_gpu_ar_equals_gpu_jacobi(tiny, policy, block_policy):
+    log(f"[gpu] tiny AR == Jacobi policy={policy} block={block_policy}")
+    prompt = workload.make_prompt(TINY, 16, seed=3)
+    ar, _ = tiny.gpu.ar_decode(prompt, 100)
+    for n in (1, 5, 8, 16, 64):
+        out, st = tiny.gpu.jacobi_decode(prompt, n, 100, policy=policy, block_policy=block_policy, stream=ar, p=0.3,
+                                         seed=4)
+        np.testing.assert_array_equal(out, ar)
+        # the oracle's Jacobi loop under the same guess policy takes the same iterations
+        spec = oracle.GuessSpec(policy, block_policy, ar, p=0.3, seed=4)
+        _, so = tiny.orc.jacobi_decode(prompt, n, 100, spec)
+        assert so["steps"] == st["steps"] and so["blocks"] == st["blocks"], (n, so["steps"], st["steps"])
+
+
+def test_tiny_exact_and_fully_corrupted_guesses(tiny):
+    log("[gpu] tiny special cases of the guess stream")
+    prompt = workload.make_prompt(TINY, 16, seed=5)
+    ar, _ = tiny.gpu.ar_decode(prompt, 40)
+    out, st = tiny.gpu.jacobi_decode(prompt, 8, 40, policy=GUESS_STREAM, stream=ar, p=0.0)
+    np.testing.assert_array_equal(out, ar)
+    assert st["steps"] == 5 and st["accept_hist"][8] == 5
+    out, st = tiny.gpu.jacobi_decode(prompt, 8, 40, policy=GUESS_STREAM_REINJECT, block_policy=BLOCK_SLIDE,
+                                     stream=ar, p=1.0)
+    np.testing.assert_array_equal(out, ar)
+    assert st["steps"] == 40 and st["accept_hist"][1] == 40
+
+
+def test_small_teacher_forced_iterations(small):
+    log("[gpu] small bf16 teacher-forced iterations n=16")
+    prompt = workload.make_prompt(SMALL, 128)
+    ar = small.orc.ar_decode(prompt, 96)
+    _teacher_forced(small, prompt, n=16, steps=10, stream=ar, p=0.3)
+
+
+def test_small_decode_is_valid_greedy(small):
+    log("[gpu] small bf16 decode, stream re-drawn p=0.3, n=16, 96 new")
+    prompt = workload.make_prompt(SMALL, 128)
+    ar_o = small.orc.ar_decode(prompt, 96)
+    out, st = small.gpu.jacobi_decode(prompt, 16, 96, policy=GUESS_STREAM_REINJECT, stream=ar_o, p=0.3, seed=3)
+    log(f"  steps={st['steps']} mean a={96 / st['steps']:.2f}")
+    inside = verify_greedy_sequence(small.orc, prompt, out, small.tol)
+    log(f"  positions inside the tie margin: {inside}")
+    ar_g, _ = small.gpu.ar_decode(prompt, 96)
+    np.testing.assert_array_equal(out, ar_g)
+
+
+def test_small_gpu_ar_equals_gpu_jacobi(small):
+    log("[gpu] small bf16 AR == Jacobi over n")
+    prompt = workload.make_prompt(SMALL, 128, seed=2)
+    ar, _ = small.gpu.ar_decode(prompt, 128)
+    for n, pol, bp in [(16, GUESS_STREAM_REINJECT, BLOCK_SHRINK), (16, GUESS_STREAM, BLOCK_SHRINK),
+                       (32, GUESS_STREAM_REINJECT, BLOCK_SLIDE), (64, GUESS_UNIFORM, BLOCK_SHRINK),
+                       (7, GUESS_STREAM_REINJECT, BLOCK_SLIDE)]:
+        out, st = small.gpu.jacobi_decode(prompt, n, 128, policy=pol, block_policy=bp, stream=ar, p=0.3, seed=9)
+        np.testing.assert_array_equal(out, ar)
+
+
+def test_small_acceptance_closed_form(small):
+    # Re-drawn guesses are right independently with probability 1-p, so a full window accepts
+    # E[a] = 1 + (1-p)(1-(1-p)^(n-1))/p tokens per iteration.
+    log("[gpu] small acceptance under re-drawn guesses vs closed form")
+    prompt = workload.make_prompt(SMALL, 128, seed=4)
+    ar, _ = small.gpu.ar_decode(prompt, 256)
+    n, p = 16, 0.3
+    out, st = small.gpu.jacobi_decode(prompt, n, 256, policy=GUESS_STREAM_REINJECT, block_policy=BLOCK_SLIDE,
+                                      stream=ar, p=p, seed=12)
+    np.testing.assert_array_equal(out, ar)
+    hist = np.array(st["accept_hist"], dtype=np.float64)
+    a = np.arange(hist.size)
+    steps = hist.sum()
+    mean_a = (a * hist).sum() / steps
+    sd = np.sqrt(((a - mean_a) ** 2 * hist).sum() / (steps - 1))
+    expect = 1 + (1 - p) * (1 - (1 - p) ** (n - 1)) / p
+    log(f"  steps={int(steps)} mean a={mean_a:.3f} closed form={expect:.3f} se={sd / np.sqrt(steps):.3f}")
+    # the last few windows are shorter than n, which only lowers the mean slightly
+    assert expect - 4 * sd / np.sqrt(steps) - 0.3 < mean_a < expect + 4 * sd / np.sqrt(steps)
+
+
+def test_determinism_run_twice(small):
+    log("[gpu] small decode twice, identical")
+    prompt = workload.make_prompt(SMALL, 100, seed=6)
+    a1, s1 = small.gpu.jacobi_decode(prompt, 16, 64, policy=GUESS_UNIFORM, seed=1)
+    a2, s2 = small.gpu.jacobi_decode(prompt, 16, 64, policy=GUESS_UNIFORM, seed=1)
+    np.testing.assert_array_equal(a1, a2)
+    assert s1["steps"] == s2["steps"]
+
+
+def test_abi_errors_on_device(tiny):
+    from paper_2403_00835_amd import binding
+    log("[gpu] ABI error paths")
+    g = binding.Model(TINY, max_ctx=64, max_block=8, max_new=16, weights=workload.make_weights(TINY))
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_step(np.array([1, 2], dtype=np.int32))
+    assert e.value.status == 2  # before prefill
+    prompt = workload.make_prompt(TINY, 10)
+    y0 = g.prefill(prompt)
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_step(np.array([(y0 + 1) % 256, 2], dtype=np.int32))
+    assert e.value.status == 2  # block_in[0] is not the pending token
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_step(np.array([y0] + [0] * 8, dtype=np.int32))
+    assert e.value.status == 1  # m > max_block
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_step(np.array([y0, 999], dtype=np.int32))
+    assert e.value.status == 1  # id out of range
+    with pytest.raises(binding.CllmError) as e:
+        g.prefill(np.zeros(70, dtype=np.int32))
+    assert e.value.status == 3  # prompt beyond max_ctx
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_decode(prompt, 8, 17)
+    assert e.value.status == 3  # max_new beyond the context's max_new
+    with pytest.raises(binding.CllmError) as e:
+        g.jacobi_decode(prompt, 8, 16, policy=GUESS_STREAM, stream=np.zeros(4, dtype=np.int32))
+    assert e.value.status == 1  # stream too short
+    # state unchanged by the failures: a valid iteration still works
+    out, a = g.jacobi_step(np.array([y0, 3, 4], dtype=np.int32))
+    assert 1 <= a <= 3
+
+
+def test_weight_file_roundtrip(tiny, tmp_path):
+    from paper_2403_00835_amd import binding
+    log("[gpu] weight file load")
+    ws = workload.make_weights(TINY)
+    path = tmp_path / "tiny.bin"
+    binding.write_weight_file(str(path), TINY, ws)
+    g = binding.Model(TINY, max_ctx=256, max_block=64, max_new=128, path=str(path))
+    prompt = workload.make_prompt(TINY, 16)
+    a, _ = g.ar_decode(prompt, 24)
+    b, _ = tiny.gpu.ar_decode(prompt, 24)
+    np.testing.assert_array_equal(a, b)

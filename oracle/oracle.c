@@ -19,9 +19,12 @@
  *
  * Precision: every intermediate is a double. With round_bf16 set, values are rounded to
  * bfloat16 (round to nearest, ties to even) at the points of the precision contract: the
- * inputs of every matrix product (norm outputs, attention output, SwiGLU output) and q, k, v
- * after RoPE (which are also the cached keys and values). Argmax decisions are taken on the
- * logits rounded to fp32, the precision the GPU path decides in; ties go to the lowest id.
+ * inputs of every matrix product and q, k, v after RoPE (which are also the cached keys and
+ * values). The input of a product that follows an RMSNorm is x (.) g, rounded; the RMSNorm row
+ * factor 1/sqrt(mean(x^2) + eps) scales the product's output (mathematically the same as
+ * normalising first). The other product inputs are the attention output and the SwiGLU output.
+ * Argmax decisions are taken on the logits rounded to fp32, the precision the GPU path decides
+ * in; ties go to the lowest id.
  *
  * Reading of the acceptance rule (the algorithm's fast-forward count): the block z holds the
  * known-correct pending token at index 0, the model's output at row k is the prediction for
@@ -105,15 +108,37 @@ double orc_bf16(double x) {
 
 static inline double rnd(const orc_model *m, double x) { return m->c.round_bf16 ? orc_bf16(x) : x; }
 
-/* RMSNorm: out_k = x_k / sqrt(mean(x^2) + eps) * g_k (rounded to bf16 if asked). */
-void orc_rmsnorm(const double *x, int32_t n, const float *g, double eps, int32_t round_bf16, double *out) {
+/* RMSNorm row factor: 1 / sqrt(mean(x^2) + eps). */
+double orc_rms_inv(const double *x, int32_t n, double eps) {
     double ss = 0.0;
     for (int32_t k = 0; k < n; ++k) ss += x[k] * x[k];
-    double inv = 1.0 / sqrt(ss / n + eps);
+    return 1.0 / sqrt(ss / n + eps);
+}
+
+/* RMSNorm: out_k = x_k / sqrt(mean(x^2) + eps) * g_k (rounded to bf16 if asked). */
+void orc_rmsnorm(const double *x, int32_t n, const float *g, double eps, int32_t round_bf16, double *out) {
+    double inv = orc_rms_inv(x, n, eps);
     for (int32_t k = 0; k < n; ++k) {
         double y = x[k] * inv * (double)g[k];
         out[k] = round_bf16 ? orc_bf16(y) : y;
     }
+}
+
+/* Input of a matrix product that follows an RMSNorm, under the precision contract: the
+ * operand is x (.) g (rounded to bf16 in the bf16 contract) and the row factor inv is applied
+ * to the product, y = inv * (operand . W^T). Without rounding this equals rmsnorm(x) . W^T. */
+static void norm_operand(const double *x, int32_t n, const float *g, double eps, int32_t round_bf16, double *a,
+                         double *inv) {
+    *inv = orc_rms_inv(x, n, eps);
+    for (int32_t k = 0; k < n; ++k) {
+        double y = x[k] * (double)g[k];
+        a[k] = round_bf16 ? orc_bf16(y) : y;
+    }
+}
+
+static void scale_rows(double *y, int32_t rows, int32_t cols, const double *inv) {
+    for (int32_t r = 0; r < rows; ++r)
+        for (int32_t c = 0; c < cols; ++c) y[(size_t)r * cols + c] *= inv[r];
 }
 
 /* Rotate-half RoPE at absolute position t: the pair (x_j, x_{j+hd/2}) is rotated by the angle
@@ -265,8 +290,9 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
     double *y = (double *)calloc((size_t)m * d, sizeof(double));
     double *g = (double *)calloc((size_t)m * F, sizeof(double));
     double *u = (double *)calloc((size_t)m * F, sizeof(double));
-    if (!h || !a || !q || !kk || !vv || !o || !y || !g || !u) {
-        free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u);
+    double *inv = (double *)calloc((size_t)m, sizeof(double));
+    if (!h || !a || !q || !kk || !vv || !o || !y || !g || !u || !inv) {
+        free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u); free(inv);
         return -2;
     }
 
@@ -278,10 +304,13 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         double *Vc = st->v + (size_t)l * st->max_ctx * d;
         /* attention sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            orc_rmsnorm(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d);
+            norm_operand(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
         linear(a, m, M->wq[l], d, d, q);
         linear(a, m, M->wk[l], d, d, kk);
         linear(a, m, M->wv[l], d, d, vv);
+        scale_rows(q, m, d, inv);
+        scale_rows(kk, m, d, inv);
+        scale_rows(vv, m, d, inv);
         for (int32_t i = 0; i < m; ++i) {
             for (int32_t hh = 0; hh < H; ++hh) {
                 orc_rope(q + (size_t)i * d + hh * hd, hd, pos0 + i, c->rope_base);
@@ -304,19 +333,22 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
         /* SwiGLU feed-forward sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            orc_rmsnorm(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d);
+            norm_operand(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
         linear(a, m, M->wg[l], d, F, g);
         linear(a, m, M->wu[l], d, F, u);
+        scale_rows(g, m, F, inv);
+        scale_rows(u, m, F, inv);
         for (size_t ix = 0; ix < (size_t)m * F; ++ix) g[ix] = rnd(M, orc_silu(g[ix]) * u[ix]);
         linear(g, m, M->wd[l], F, d, y);
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
     }
     if (logits) {
         for (int32_t i = 0; i < m; ++i)
-            orc_rmsnorm(h + (size_t)i * d, d, M->final_norm, c->rms_eps, c->round_bf16, a + (size_t)i * d);
+            norm_operand(h + (size_t)i * d, d, M->final_norm, c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
         linear(a, m, M->lm_head, d, V, logits);
+        scale_rows(logits, m, V, inv);
     }
-    free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u);
+    free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u); free(inv);
     return 0;
 }
 

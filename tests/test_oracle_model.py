@@ -105,15 +105,21 @@ def test_uniform_attention_counts_causal_prefix():
         assert oracle.argmax(lg[t]) == _mode_rule(seq[:t + 1], pv, po)
 
 
-def test_swiglu_ffn_closed_form_logits():
+@pytest.mark.parametrize("unit_gains", [True, False])
+def test_swiglu_ffn_closed_form_logits(unit_gains):
     # Attention off; the FFN maps e_x to a known vector:
     #   gate = gam * b[x] at feature sig1(x), up = dlt * b[x] at sig1(x) and sig2(x),
-    #   down sends feature f to component tau(f) with weight zeta.
-    # h = s e_x + zeta * silu(gam c) * dlt c * e_{tau(sig1(x))}, c = rmsnorm scale of s e_x.
+    #   down sends feature f to component tau(f) with weight zeta,
+    # where b = rmsnorm(s e_x) (.) g_ffn, so b[x] = c g_ffn[x] with c the RMSNorm scale of s e_x.
+    # h = s e_x + zeta * silu(gam c g_ffn[x]) * dlt c g_ffn[x] * e_{tau(sig1(x))};
+    # logits = s * rmsnorm(h) (.) g_final.
     cfg = _cfg(1)
     ts = _base_tensors(cfg)
     # weights are fp32 arrays: take the constants at fp32 precision
     gam, dlt, zeta, s = (float(np.float32(v)) for v in (1.3, 0.7, 0.05, 1.0))
+    rng = np.random.default_rng(3)
+    g_ffn = np.ones(D, np.float32) if unit_gains else rng.uniform(0.5, 1.5, D).astype(np.float32)
+    g_fin = np.ones(D, np.float32) if unit_gains else rng.uniform(0.5, 1.5, D).astype(np.float32)
     sig1 = (np.arange(V) * 3 + 1) % F
     sig2 = (np.arange(V) * 3 + 2) % F
     tau = (np.arange(F) * 7 + 3) % V
@@ -124,7 +130,8 @@ def test_swiglu_ffn_closed_form_logits():
     Wu[sig1, np.arange(V)] = dlt
     Wu[sig2, np.arange(V)] = dlt
     Wd[tau, np.arange(F)] = zeta
-    ts[1 + 6], ts[1 + 7], ts[1 + 8] = np.float32(Wg), np.float32(Wu), np.float32(Wd)
+    ts[1 + 5], ts[1 + 6], ts[1 + 7], ts[1 + 8] = g_ffn, Wg, Wu, Wd
+    ts[-2] = g_fin
     m = oracle.Model(cfg, ts)
     tokens = np.array([4, 30, 11], dtype=np.int32)
     lg = m.forward_full(tokens)
@@ -132,9 +139,9 @@ def test_swiglu_ffn_closed_form_logits():
     for t, x in enumerate(tokens):
         h = np.zeros(D)
         h[x] += s
-        gv = gam * c
-        h[tau[sig1[x]]] += zeta * (gv * expit(gv)) * (dlt * c)
-        nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps)
+        b = c * float(g_ffn[x])
+        h[tau[sig1[x]]] += zeta * (gam * b * expit(gam * b)) * (dlt * b)
+        nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps) * g_fin.astype(np.float64)
         np.testing.assert_allclose(lg[t], s * nh[:V], rtol=0, atol=1e-12)
 
 

@@ -118,7 +118,7 @@ def main():
         if not np.array_equal(out, ar):
             raise RuntimeError("Jacobi output differs from greedy AR output")
     torch.cuda.synchronize()
-    model.timing_enable("gate_up")
+    model.timing_enable("gate_up", max_rows=n)  # iteration launches only, not prefill chunks
     stats = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -140,9 +140,9 @@ def main():
     mean_accept = tokens / iters
     wbytes = model.streamed_weight_bytes()
     d, F = cfg.d_model, cfg.ffn_dim
-    # gate/up launch: packed weights (2 * F_pad * d bf16) + fp32 X rows read + bf16 H rows written
+    # gate/up launch: packed weights (2 * F_pad * d bf16) + operand rows read + H rows written
     f_pad = (F + 31) // 32 * 32
-    gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * F * 2
+    gu_bytes = 2 * f_pad * d * 2 + n * d * 2 + n * F * 2
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
     traffic = measured_traffic()

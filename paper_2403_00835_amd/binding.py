@@ -69,7 +69,7 @@ def lib():
         L.cllm_ar_decode.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp, P(cllm_decode_stats)]
         L.cllm_debug_logits.argtypes = [_vp, _i32, _vp, ctypes.c_size_t]
         L.cllm_seq_state.argtypes = [_vp, _i32, P(_i32), P(_i32)]
-        L.cllm_timing_enable.argtypes = [_vp, _i32]
+        L.cllm_timing_enable.argtypes = [_vp, _i32, _i32]
         L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
         L.cllm_streamed_weight_bytes.argtypes = [_vp]
         L.cllm_streamed_weight_bytes.restype = _i64
@@ -195,9 +195,9 @@ class Model:
         self._check(self.L.cllm_seq_state(self.h, seq, ctypes.byref(L), ctypes.byref(pend)))
         return int(L.value), int(pend.value)
 
-    def timing_enable(self, kernel_class):
+    def timing_enable(self, kernel_class, max_rows=0):
         cls = KT[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
-        self._check(self.L.cllm_timing_enable(self.h, cls))
+        self._check(self.L.cllm_timing_enable(self.h, cls, max_rows))
 
     def timing_read(self):
         n, ms = _i64(0), _dbl(0.0)

@@ -26,7 +26,6 @@ struct cllm_ctx {
     int Fp = 0;         // ffn width padded to 32
     int ctx_alloc = 0;  // KV capacity, multiple of the attention chunk
     int nch = 0;        // attention chunks of ctx_alloc
-    int nt_qkv = 2;
     int ks_d = 0, ks_f = 0;
     int n_wg_qkv = 0, n_wg_o = 0, n_wg_gu = 0, n_wg_d = 0, n_wg_lm = 0;
     int64_t streamed_bytes = 0;
@@ -45,6 +44,7 @@ struct cllm_ctx {
           *dbg = nullptr;
     int *pidx = nullptr;
     void *Q = nullptr, *O = nullptr, *Hb = nullptr;
+    void *An = nullptr;  // RMSNorm operand x (.) g of the next normed product
     Ctl *ctl = nullptr;
     int32_t *out_dev = nullptr, *stream_dev = nullptr;
     int stream_cap = 0;
@@ -60,6 +60,7 @@ struct cllm_ctx {
     size_t dbg_cap = 0;
     // kernel timing
     int kt_class = -1;
+    int kt_rg = 0;  // time only launches for this many 16-row groups (0 = all)
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
     int64_t kt_launches = 0;
@@ -114,10 +115,10 @@ cllm_status dalloc_t(cllm_ctx *c, T **p, size_t count) {
     return s;
 }
 
-// Timing events for the selected kernel class (null when that class is not being timed).
-void timing_events(cllm_ctx *c, int cls, hipEvent_t *e0, hipEvent_t *e1) {
+// Timing events for the selected kernel class and row-group count (null when not timed).
+void timing_events(cllm_ctx *c, int cls, int rg, hipEvent_t *e0, hipEvent_t *e1) {
     *e0 = *e1 = nullptr;
-    if (c->kt_class != cls) return;
+    if (c->kt_class != cls || (c->kt_rg > 0 && c->kt_rg != rg)) return;
     while (c->ev_pool.size() < c->ev_used + 2) {
         hipEvent_t e;
         if (hipEventCreate(&e) != hipSuccess) return;
@@ -195,14 +196,12 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
     hipStream_t s = c->stream;
     hipEvent_t e0, e1;
 
-    EmbedParams ep{c->embed, c->X, c->ssq, c->d, c->ctl};
-    timing_events(c, CLLM_KT_EMBED, &e0, &e1);
+    EmbedParams ep{c->embed, c->X, c->ssq, c->An, c->g_attn[0], c->d, c->ctl};
+    timing_events(c, CLLM_KT_EMBED, rg, &e0, &e1);
     HIPCHK(c, launch_embed(c->bf16, 16 * rg, ep, s, e0, e1));
 
     GemmParams base{};
     base.ctl = c->ctl;
-    base.X = c->X;
-    base.ldx = c->d;
     base.ssq = c->ssq;
     base.T = c->d / 16;
     base.K = c->d;
@@ -214,6 +213,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
     base.rsin = c->rsin;
     base.Xout = c->X;
     base.ssq_out = c->ssq;
+    base.ldx = c->d;
+    base.An = c->An;
     base.Fp = c->Fp;
     base.V = c->V;
 
@@ -236,50 +237,54 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         void *kc = static_cast<uint8_t *>(c->kc) + l * kv_layer;
         void *vt = static_cast<uint8_t *>(c->vt) + l * kv_layer;
 
-        GemmParams q = base;
+        GemmParams q = base;  // operand: attention RMSNorm of X, written by the previous producer
         q.W = c->w_qkv[l];
         q.Ks = c->ks_d;
         q.n_wg = c->n_wg_qkv;
-        q.gain = c->g_attn[l];
+        q.A = c->An;
+        q.lda = c->d;
         q.Q = c->Q;
         q.Kc = kc;
         q.Vt = vt;
-        timing_events(c, CLLM_KT_GEMM_QKV, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_QKV, c->bf16, rg, c->nt_qkv, q, s, e0, e1));
+        timing_events(c, CLLM_KT_GEMM_QKV, rg, &e0, &e1);
+        HIPCHK(c, launch_gemm(GEMM_QKV, c->bf16, rg, q, s, e0, e1));
 
         ap.Kc = kc;
         ap.Vt = vt;
-        timing_events(c, CLLM_KT_ATTN, &e0, &e1);
+        timing_events(c, CLLM_KT_ATTN, rg, &e0, &e1);
         HIPCHK(c, launch_attn(c->bf16, rg, nch_launch, ap, s, e0, e1));
-        timing_events(c, CLLM_KT_ATTN_COMBINE, &e0, &e1);
+        timing_events(c, CLLM_KT_ATTN_COMBINE, rg, &e0, &e1);
         HIPCHK(c, launch_attn_combine(c->bf16, 16 * rg, ap, s, e0, e1));
 
-        GemmParams o = base;
+        GemmParams o = base;  // X += O W_o^T; writes the FFN RMSNorm operand
         o.W = c->w_o[l];
         o.Ks = c->ks_d;
         o.n_wg = c->n_wg_o;
         o.A = c->O;
         o.lda = c->d;
-        timing_events(c, CLLM_KT_GEMM_O, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_O, c->bf16, rg, 1, o, s, e0, e1));
+        o.gain = c->g_ffn[l];
+        timing_events(c, CLLM_KT_GEMM_O, rg, &e0, &e1);
+        HIPCHK(c, launch_gemm(GEMM_O, c->bf16, rg, o, s, e0, e1));
 
         GemmParams gu = base;
         gu.W = c->w_gu[l];
         gu.Ks = c->ks_d;
         gu.n_wg = c->n_wg_gu;
-        gu.gain = c->g_ffn[l];
+        gu.A = c->An;
+        gu.lda = c->d;
         gu.H = c->Hb;
-        timing_events(c, CLLM_KT_GEMM_GATE_UP, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_GATE_UP, c->bf16, rg, 1, gu, s, e0, e1));
+        timing_events(c, CLLM_KT_GEMM_GATE_UP, rg, &e0, &e1);
+        HIPCHK(c, launch_gemm(GEMM_GATE_UP, c->bf16, rg, gu, s, e0, e1));
 
-        GemmParams dn = base;
+        GemmParams dn = base;  // X += H W_d^T; writes the next layer's (or the final) RMSNorm operand
         dn.W = c->w_d[l];
         dn.Ks = c->ks_f;
         dn.n_wg = c->n_wg_d;
         dn.A = c->Hb;
         dn.lda = c->Fp;
-        timing_events(c, CLLM_KT_GEMM_DOWN, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, 1, dn, s, e0, e1));
+        dn.gain = l + 1 < c->NL ? c->g_attn[l + 1] : c->g_final;
+        timing_events(c, CLLM_KT_GEMM_DOWN, rg, &e0, &e1);
+        HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, dn, s, e0, e1));
     }
 
     ScanParams sp{};
@@ -294,17 +299,18 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         lm.W = c->w_lm;
         lm.Ks = c->ks_d;
         lm.n_wg = c->n_wg_lm;
-        lm.gain = c->g_final;
+        lm.A = c->An;
+        lm.lda = c->d;
         lm.pmax = c->pmax;
         lm.pidx = c->pidx;
         lm.dbg = c->dbg_on ? c->dbg : nullptr;
-        timing_events(c, CLLM_KT_LM_HEAD, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, 1, lm, s, e0, e1));
+        timing_events(c, CLLM_KT_LM_HEAD, rg, &e0, &e1);
+        HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, lm, s, e0, e1));
         sp.advance_only = 0;
     } else {
         sp.advance_only = 1;
     }
-    timing_events(c, CLLM_KT_SCAN, &e0, &e1);
+    timing_events(c, CLLM_KT_SCAN, rg, &e0, &e1);
     HIPCHK(c, launch_scan(sp, s, e0, e1));
     return CLLM_OK;
 }
@@ -390,11 +396,14 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     const bool bf16 = cfg->dtype == CLLM_DTYPE_BF16;
     const int kstep = bf16 ? 32 : 16;
     if ((cfg->dtype != CLLM_DTYPE_BF16 && cfg->dtype != CLLM_DTYPE_F32) || cfg->n_layers < 1 || cfg->d_model < 1 ||
-        cfg->n_heads < 1 || cfg->head_dim < 2 || cfg->n_heads * cfg->head_dim != cfg->d_model ||
-        cfg->head_dim % kstep != 0 || cfg->head_dim % 16 != 0 || cfg->head_dim > 1024 || cfg->d_model % 32 != 0 ||
+        cfg->n_heads < 1 || cfg->n_heads * cfg->head_dim != cfg->d_model ||
+        !(cfg->head_dim == 32 || cfg->head_dim == 64 || cfg->head_dim == 128 ||
+          (bf16 ? cfg->head_dim == 256 : cfg->head_dim == 16)) ||
+        cfg->d_model % 64 != 0 || cfg->d_model > 8192 ||
         cfg->ffn_dim < 1 || cfg->vocab < 2 || !(cfg->rms_eps >= 0.0f) || !(cfg->rope_base > 0.0f))
         return CLLM_ERR_ARG;
-    if (opts->max_block < 1 || opts->max_block > kMaxBlock || opts->max_ctx < 2 || opts->max_new < 1)
+    if (opts->max_block < 1 || opts->max_block > kMaxBlock || opts->max_ctx < 2 ||
+        opts->max_ctx > kMaxChunks * kAttnChunk - 2 * kMaxRows || opts->max_new < 1)
         return CLLM_ERR_ARG;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || opts->device < 0 || opts->device >= ndev) {
@@ -416,13 +425,12 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->Fp = round_up(c->F, 32);
     c->ctx_alloc = round_up(opts->max_ctx + kMaxRows, kAttnChunk);
     c->nch = c->ctx_alloc / kAttnChunk;
-    c->nt_qkv = c->hd >= 32 ? 2 : 1;
     c->ks_d = c->d / kstep;
     c->ks_f = c->Fp / kstep;
-    c->n_wg_qkv = 3 * c->d / 16 / c->nt_qkv;
-    c->n_wg_o = c->d / 16;
-    c->n_wg_gu = c->Fp / 16;
-    c->n_wg_d = c->d / 16;
+    c->n_wg_qkv = 3 * c->d / 16 / kNtQkv;
+    c->n_wg_o = c->d / 16 / kNtResid;
+    c->n_wg_gu = 2 * c->Fp / 16 / kNtGateUp;
+    c->n_wg_d = c->d / 16 / kNtResid;
     c->n_wg_lm = round_up(c->V, 16 * kLmTiles) / (16 * kLmTiles);
     c->stream = static_cast<hipStream_t>(opts->stream);
 
@@ -456,6 +464,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->ssq, (size_t)(c->d / 16) * rows))) return bail(s);
     if ((s = dalloc(c, &c->Q, rows * c->d * E))) return bail(s);
     if ((s = dalloc(c, &c->O, rows * c->d * E))) return bail(s);
+    if ((s = dalloc(c, &c->An, rows * c->d * E))) return bail(s);
     if ((s = dalloc(c, &c->Hb, rows * c->Fp * E))) return bail(s);
     if ((s = dalloc_t(c, &c->pmax, (size_t)c->n_wg_lm * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->pidx, (size_t)c->n_wg_lm * rows))) return bail(s);
@@ -817,10 +826,12 @@ cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_le
     return CLLM_OK;
 }
 
-cllm_status cllm_timing_enable(cllm_ctx *c, int32_t kernel_class) {
+cllm_status cllm_timing_enable(cllm_ctx *c, int32_t kernel_class, int32_t max_rows) {
     if (!c) return CLLM_ERR_ARG;
-    if (kernel_class > CLLM_KT_EMBED) return fail(c, CLLM_ERR_ARG, "unknown kernel class");
+    if (kernel_class > CLLM_KT_EMBED || max_rows < 0 || max_rows > kMaxRows)
+        return fail(c, CLLM_ERR_ARG, "unknown kernel class or bad max_rows");
     c->kt_class = kernel_class < 0 ? -1 : kernel_class;
+    c->kt_rg = max_rows == 0 ? 0 : rows_to_rg(max_rows);
     c->ev_used = 0;
     c->kt_launches = 0;
     c->kt_ms = 0.0;

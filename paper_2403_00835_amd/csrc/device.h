@@ -15,7 +15,13 @@ constexpr int kMaxBlock = 64;      // largest Jacobi block (rows per iteration)
 constexpr int kMaxRows = 64;       // rows of the activation buffers (block or prefill chunk)
 constexpr int kGemmWaves = 8;      // waves per GEMM workgroup; they split K
 constexpr int kAttnChunk = 64;     // keys per attention workgroup, at absolute positions
+constexpr int kMaxChunks = 1024;   // attention chunks per sequence: context <= 65536
 constexpr int kTileBytes = 1024;   // one packed weight tile: 16 rows x 16 bytes x 4 lane groups
+#ifndef CLLM_WEIGHTS_NT
+#define CLLM_WEIGHTS_NT 1
+#endif
+constexpr bool kWeightsNonTemporal = CLLM_WEIGHTS_NT;  // weights are streamed once per iteration
+constexpr int kGainVecs = 4;       // RMSNorm gain staging: d_model <= 4 * 4 * 512
 
 // Precision traits. A "k-step" is the K extent one wave covers with one 16-byte load per lane:
 // 4 lane groups x VEC elements. bf16: one 16x16x32 MFMA per k-step; fp32: four 16x16x4 MFMAs.

@@ -31,115 +31,61 @@ namespace cllm {
 // takes k-steps w, w+8, w+16, ... and accumulates them in order with MFMA; the 8 partial tiles
 // are then summed in a fixed tree ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)). Weights are read once,
 // straight into registers (no LDS); the activation rows (a few KiB, L2-resident) are re-read.
+//
+// Products that follow an RMSNorm take the operand x (.) g written by the producer of x and
+// scale each output row by 1/sqrt(mean(x^2) + eps), reduced from the producer's per-16-column
+// sums of squares.
 // ------------------------------------------------------------------------------------------
 
-enum ALoad { A_ACT = 0, A_NORM = 1 };
 enum Epi { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_ARGMAX = 3 };
 
-template <Prec P, int RG>
-struct ARaw;
-template <int RG>
-struct ARaw<Prec::BF16, RG> {  // norm loader keeps 8 fp32 values per row group
-    u32x4 lo[RG], hi[RG];
-};
-template <int RG>
-struct ARaw<Prec::F32, RG> {
-    u32x4 lo[RG];
+template <Prec P, int NT, int RG>
+struct Stage {  // operands of one k-step
+    u32x4 b[NT];  // weight tiles
+    u32x4 a[RG];  // activation rows
 };
 
-template <Prec P, int NT, int RG, int AL>
-struct Stage {
-    u32x4 b[2][NT];            // two k-steps per stage
-    u32x4 a[2][RG];            // activation operand (A_ACT)
-    ARaw<P, RG> x[2];          // raw fp32 rows (A_NORM)
-};
-
-template <Prec P, int NT, int RG, int AL>
-__device__ __forceinline__ void gemm_load(Stage<P, NT, RG, AL> &st, const GemmParams &p, int t0, int base,
-                                          int lane) {
+// Loads of one k-step (s_raw = this wave's step index; clamped to the last k-step, so every
+// load is issued and the compiler can count outstanding loads exactly).
+template <Prec P, int NT, int RG>
+__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int s_raw, int lane) {
     using PT = PrecT<P>;
+    using T = typename PT::T;
     const int g = lane >> 4, r16 = lane & 15;
+    const int s = min(s_raw, p.Ks - 1);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int s = base + u * kGemmWaves;
-        if (s < p.Ks) {
-#pragma unroll
-            for (int j = 0; j < NT; ++j) {
-                const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)(t0 + j) * p.Ks + s) * kTileBytes) + lane;
-                st.b[u][j] = __builtin_nontemporal_load(src);
-            }
-            const int k = s * PT::KSTEP + g * PT::VEC;
-            if constexpr (AL == A_ACT) {
-                using T = typename PT::T;
-                const T *A = reinterpret_cast<const T *>(p.A);
-#pragma unroll
-                for (int r = 0; r < RG; ++r)
-                    st.a[u][r] = *reinterpret_cast<const u32x4 *>(A + (size_t)(16 * r + r16) * p.lda + k);
-            } else {
-#pragma unroll
-                for (int r = 0; r < RG; ++r) {
-                    const float *xr = p.X + (size_t)(16 * r + r16) * p.ldx + k;
-                    st.x[u].lo[r] = *reinterpret_cast<const u32x4 *>(xr);
-                    if constexpr (P == Prec::BF16) st.x[u].hi[r] = *reinterpret_cast<const u32x4 *>(xr + 4);
-                }
-            }
-        }
+    for (int j = 0; j < NT; ++j) {
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)(t0 + j) * p.Ks + s) * kTileBytes) + lane;
+        if constexpr (kWeightsNonTemporal) st.b[j] = __builtin_nontemporal_load(src);
+        else st.b[j] = *src;
     }
+    const int k = s * PT::KSTEP + g * PT::VEC;
+    const T *A = reinterpret_cast<const T *>(p.A);
+#pragma unroll
+    for (int r = 0; r < RG; ++r) st.a[r] = *reinterpret_cast<const u32x4 *>(A + (size_t)(16 * r + r16) * p.lda + k);
 }
 
-template <Prec P, int NT, int RG, int AL>
-__device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG, AL> &st, const GemmParams &p, int base,
-                                             int lane, f32x4 (&acc)[RG][NT], const float *s_inv,
-                                             const float *s_gain) {
-    using PT = PrecT<P>;
-    const int g = lane >> 4, r16 = lane & 15;
+// MFMAs of one k-step. Branch-free: a k-step past the end (its loads were clamped to a valid
+// tile) gets a zero activation operand, so it adds exact zeros.
+template <Prec P, int NT, int RG>
+__device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG> &st, const GemmParams &p, int s_raw,
+                                             f32x4 (&acc)[RG][NT]) {
+    const bool valid = s_raw < p.Ks;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int s = base + u * kGemmWaves;
-        if (s < p.Ks) {
+    for (int r = 0; r < RG; ++r) {
+        const u32x4 a = valid ? st.a[r] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int r = 0; r < RG; ++r) {
-                u32x4 a;
-                if constexpr (AL == A_ACT) {
-                    a = st.a[u][r];
-                } else {
-                    const int k = s * PT::KSTEP + g * PT::VEC;
-                    const float inv = s_inv[16 * r + r16];
-                    const float *gk = s_gain + k;
-                    if constexpr (P == Prec::BF16) {
-                        const u32x4 lo = st.x[u].lo[r], hi = st.x[u].hi[r];
-                        float v[8] = {__uint_as_float(lo.x), __uint_as_float(lo.y), __uint_as_float(lo.z),
-                                      __uint_as_float(lo.w), __uint_as_float(hi.x), __uint_as_float(hi.y),
-                                      __uint_as_float(hi.z), __uint_as_float(hi.w)};
-                        uint32_t w[4];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            uint32_t e0 = f2bf(v[2 * q] * inv * gk[2 * q]);
-                            uint32_t e1 = f2bf(v[2 * q + 1] * inv * gk[2 * q + 1]);
-                            w[q] = e0 | (e1 << 16);
-                        }
-                        a = u32x4{w[0], w[1], w[2], w[3]};
-                    } else {
-                        const u32x4 lo = st.x[u].lo[r];
-                        a = u32x4{__float_as_uint(__uint_as_float(lo.x) * inv * gk[0]),
-                                  __float_as_uint(__uint_as_float(lo.y) * inv * gk[1]),
-                                  __float_as_uint(__uint_as_float(lo.z) * inv * gk[2]),
-                                  __float_as_uint(__uint_as_float(lo.w) * inv * gk[3])};
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < NT; ++j) acc[r][j] = mfma_kstep<P>(a, st.b[u][j], acc[r][j]);
-            }
-        }
+        for (int j = 0; j < NT; ++j) acc[r][j] = mfma_kstep<P>(a, st.b[j], acc[r][j]);
     }
 }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
-template <Prec P, int NT, int RG, int AL, int EP>
+template <Prec P, int NT, int RG, int EP, int D>
 __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
+    constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
     const Ctl *ctl = p.ctl;
     const int m = ctl->m;
     if (m <= 0) return;
@@ -150,25 +96,43 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
 
     extern __shared__ float smem[];
-    float *s_red = smem;                          // 4 x NT x 64 x 4 (also ROWS x 16 for E_RESID)
-    float *s_tile = s_red + 4 * NT * 256;         // ROWS x (COLS + 1)
-    float *s_inv = s_tile + ROWS * (COLS + 1);    // ROWS
-    float *s_gain = s_inv + kMaxRows;             // K (A_NORM only)
+    float *s_red = smem;                            // 8 waves x NT x 256 (also ROWS x COLS for E_RESID)
+    float *s_tile = s_red + kGemmWaves * NT * 256;  // ROWS x (COLS + 1)
+    float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
 
-    if constexpr (AL == A_NORM) {
-        for (int k = tid; k < p.K; k += kGemmWaves * kWave) s_gain[k] = p.gain[k];
-        // Row factor 1/sqrt(mean(x^2) + eps) from the producer's per-16-column partial sums:
-        // 8 threads per row sum strided partials in order, then a fixed xor tree.
+    // This wave's k-steps are w, w+8, w+16, ... (nmy of them); the first D-1 are requested first.
+    const int nmy = w < p.Ks ? (p.Ks - w + kGemmWaves - 1) / kGemmWaves : 0;
+    Stage<P, NT, RG> ring[D];
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, w + j * kGemmWaves, lane);
+
+    if constexpr (ROWSCALE) {
+        // Row factor 1/sqrt(mean(x^2) + eps) from the producer's per-16-column sums of squares
+        // (layout [row][T]): 8 threads per row each add a contiguous run of q partials in order,
+        // then a fixed xor tree. The scheme does not depend on the number of rows. Only the first
+        // ROWS*8 threads take part; the barrier of the reduction below publishes s_inv.
         if (tid < ROWS * 8) {
             const int row = tid >> 3, part = tid & 7;
+            const int q = (p.T + 7) >> 3;
+            const int t_begin = part * q;
+            const float *src = p.ssq + (size_t)row * p.T;
             float sum = 0.0f;
-            for (int t = part; t < p.T; t += 8) sum += p.ssq[(size_t)t * kMaxRows + row];
+            for (int i0 = 0; i0 < q; i0 += 16) {  // 16 loads in flight, then 16 ordered adds
+                float v[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int t = t_begin + i0 + i;
+                    v[i] = (i0 + i < q && t < p.T) ? src[t] : 0.0f;
+                }
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (i0 + i < q && t_begin + i0 + i < p.T) sum += v[i];
+            }
             sum += __shfl_xor(sum, 4, 8);
             sum += __shfl_xor(sum, 2, 8);
             sum += __shfl_xor(sum, 1, 8);
             if (part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
         }
-        __syncthreads();
     }
 
     f32x4 acc[RG][NT];
@@ -177,54 +141,54 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // Two-stage software pipeline over this wave's k-steps (each stage = 2 k-steps).
-    {
-        Stage<P, NT, RG, AL> s0, s1;
-        int base = w;
-        gemm_load(s0, p, t0, base, lane);
-        while (true) {
-            int nb = base + 2 * kGemmWaves;
-            if (nb < p.Ks) gemm_load(s1, p, t0, nb, lane);
-            gemm_compute(s0, p, base, lane, acc, s_inv, s_gain);
-            if (nb >= p.Ks) break;
-            base = nb;
-            nb = base + 2 * kGemmWaves;
-            if (nb < p.Ks) gemm_load(s0, p, t0, nb, lane);
-            gemm_compute(s1, p, base, lane, acc, s_inv, s_gain);
-            if (nb >= p.Ks) break;
-            base = nb;
+    // Software pipeline: a ring of D k-steps whose loads are in flight while the oldest one's
+    // MFMAs run. The steady state is branch-free (exact wait counts); the drain issues no loads
+    // past the end.
+    if (nmy > 0) {
+        // blocks of D steps whose prefetches (up to step b*D + 2D - 2) are all in range
+        const int nfull = nmy >= 2 * D - 1 ? (nmy - (D - 1)) / D : 0;
+        for (int bi = 0; bi < nfull; ++bi) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                // sched_barrier keeps the scheduler from sinking loads to their uses.
+                gemm_load(ring[(j + D - 1) % D], p, t0, w + (bi * D + j + D - 1) * kGemmWaves, lane);
+                __builtin_amdgcn_sched_barrier(0);
+                gemm_compute(ring[j], p, w + (bi * D + j) * kGemmWaves, acc);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const int v0 = nfull * D;
+#pragma unroll
+        for (int j = 0; j < 2 * D - 1; ++j) {
+            const int v = v0 + j;
+            if (v < nmy) {
+                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, w + (v + D - 1) * kGemmWaves, lane);
+                gemm_compute(ring[j % D], p, w + v * kGemmWaves, acc);
+            }
         }
     }
 
-    // Fixed-tree reduction of the 8 waves' partial tiles through LDS, one row group at a time:
-    // ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)) for every element.
+    // Sum of the 8 waves' partial tiles through LDS, one row group at a time, in the fixed tree
+    // ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)) for every element; then the RMSNorm row factor.
 #pragma unroll
     for (int r = 0; r < RG; ++r) {
 #pragma unroll
-        for (int half = 4; half >= 1; half >>= 1) {
-            if (w >= half && w < 2 * half) {
-                float *dst = s_red + (size_t)(w - half) * NT * 256;
+        for (int j = 0; j < NT; ++j)
+            *reinterpret_cast<f32x4 *>(s_red + ((size_t)(w * NT + j) * 64 + lane) * 4) = acc[r][j];
+        __syncthreads();
+        for (int e = tid; e < NT * 256; e += kGemmWaves * kWave) {
+            float x[kGemmWaves];
 #pragma unroll
-                for (int j = 0; j < NT; ++j) *reinterpret_cast<f32x4 *>(dst + (j * 64 + lane) * 4) = acc[r][j];
-            }
-            __syncthreads();
-            if (w < half) {
-                const float *src = s_red + (size_t)w * NT * 256;
-#pragma unroll
-                for (int j = 0; j < NT; ++j) acc[r][j] += *reinterpret_cast<const f32x4 *>(src + (j * 64 + lane) * 4);
-            }
-            __syncthreads();
+            for (int q = 0; q < kGemmWaves; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
+            float sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
+            // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
+            const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
+            const int row = 16 * r + 4 * (l >> 4) + v;
+            if constexpr (ROWSCALE) sum *= s_inv[row];
+            s_tile[row * (COLS + 1) + 16 * j + (l & 15)] = sum;
         }
-        if (w == 0) {
-            // C layout of a 16x16 MFMA tile: lane l holds rows 4*(l/16)+v, column l%16.
-#pragma unroll
-            for (int j = 0; j < NT; ++j)
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    s_tile[(16 * r + 4 * (lane >> 4) + v) * (COLS + 1) + 16 * j + (lane & 15)] = acc[r][j][v];
-        }
+        __syncthreads();
     }
-    __syncthreads();
 
     // ---------------------------------------------------------------- epilogues
     if constexpr (EP == E_QKV) {
@@ -269,34 +233,41 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
                 reinterpret_cast<T *>(p.Vt)[(size_t)col * p.ctx_alloc + pos] = e;
         }
     } else if constexpr (EP == E_RESID) {
-        static_assert(NT == 1, "residual epilogue owns one 16-column tile");
+        // X += Y over this workgroup's columns, then the per-16-column sums of squares of the
+        // new rows (summed in column order) for the next RMSNorm.
         const int c0 = t0 * 16;
-        float *s_sq = s_red;  // reuse: ROWS x 16
-        for (int idx = tid; idx < ROWS * 16; idx += kGemmWaves * kWave) {
-            const int row = idx >> 4, c = idx & 15;
+        float *s_sq = s_red;  // ROWS x COLS
+        for (int idx = tid; idx < ROWS * COLS; idx += kGemmWaves * kWave) {
+            const int row = idx / COLS, c = idx % COLS;
             float v = 0.0f;
             if (row < m) {
                 float *xp = p.Xout + (size_t)row * p.ldx + c0 + c;
                 v = *xp + s_tile[row * (COLS + 1) + c];
                 *xp = v;
+                // operand of the next RMSNorm-ed product: x (.) g
+                reinterpret_cast<T *>(p.An)[(size_t)row * p.ldx + c0 + c] = to_elem<P>(v * p.gain[c0 + c]);
             }
             s_sq[idx] = v * v;
         }
         __syncthreads();
-        if (tid < ROWS && tid < m) {
-            float sum = 0.0f;
+        if (tid < ROWS * NT) {
+            const int row = tid / NT, j = tid % NT;
+            if (row < m) {
+                float sum = 0.0f;
 #pragma unroll
-            for (int c = 0; c < 16; ++c) sum += s_sq[tid * 16 + c];
-            p.ssq_out[(size_t)t0 * kMaxRows + tid] = sum;
+                for (int c = 0; c < 16; ++c) sum += s_sq[row * COLS + 16 * j + c];
+                p.ssq_out[(size_t)row * p.T + t0 + j] = sum;
+            }
         }
     } else if constexpr (EP == E_SWIGLU) {
-        static_assert(NT == 2, "gate/up epilogue pairs a gate tile with an up tile");
-        for (int idx = tid; idx < ROWS * 16; idx += kGemmWaves * kWave) {
-            const int row = idx >> 4, c = idx & 15;
+        // Tiles come in (gate, up) pairs of the same 16 features.
+        static_assert(NT % 2 == 0, "gate/up epilogue pairs a gate tile with an up tile");
+        for (int idx = tid; idx < ROWS * COLS / 2; idx += kGemmWaves * kWave) {
+            const int row = idx / (COLS / 2), f = idx % (COLS / 2), q = f >> 4, c = f & 15;
             if (row >= m) continue;
-            const float gt = s_tile[row * (COLS + 1) + c];
-            const float up = s_tile[row * (COLS + 1) + 16 + c];
-            reinterpret_cast<T *>(p.H)[(size_t)row * p.Fp + wg * 16 + c] = to_elem<P>(silu(gt) * up);
+            const float gt = s_tile[row * (COLS + 1) + 32 * q + c];
+            const float up = s_tile[row * (COLS + 1) + 32 * q + 16 + c];
+            reinterpret_cast<T *>(p.H)[(size_t)row * p.Fp + wg * (COLS / 2) + f] = to_elem<P>(silu(gt) * up);
         }
     } else {  // E_ARGMAX
         // One wave per row: (max, lowest column) over this workgroup's columns < V.
@@ -330,8 +301,8 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
 }
 
 // ------------------------------------------------------------------------------------------
-// Embedding gather: X[i] = E[z_i] (fp32) and the per-16-column sums of squares for the first
-// RMSNorm.
+// Embedding gather: X[i] = E[z_i] (fp32), the operand X[i] (.) g of the first layer's QKV product
+// and the per-16-column sums of squares for its RMSNorm.
 // ------------------------------------------------------------------------------------------
 template <Prec P>
 __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
@@ -343,15 +314,17 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     const int tok = ctl->z[row];
     const T *e = reinterpret_cast<const T *>(p.E) + (size_t)tok * p.d;
     float *x = p.X + (size_t)row * p.d;
+    T *an = reinterpret_cast<T *>(p.An) + (size_t)row * p.d;
     for (int t = threadIdx.x; t < p.d / 16; t += blockDim.x) {
         float sum = 0.0f;
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
             const float v = from_elem<P>(e[16 * t + c]);
             x[16 * t + c] = v;
+            an[16 * t + c] = to_elem<P>(v * p.gain[16 * t + c]);
             sum += v * v;
         }
-        p.ssq[(size_t)t * kMaxRows + row] = sum;
+        p.ssq[(size_t)row * (p.d / 16) + t] = sum;
     }
 }
 
@@ -365,10 +338,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
 //                          the same K-slot assignment)
 // Each (h, c, row) writes a partial (max, sum, unnormalised output).
 // ------------------------------------------------------------------------------------------
-template <Prec P, int RG>
+template <Prec P, int HD, int RG>
 __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
+    constexpr int NKK = HD / PT::KSTEP;  // k-steps of the score product
+    constexpr int NDT = HD / 16;         // 16-dim tiles of the output
     const Ctl *ctl = p.ctl;
     const int m = ctl->m;
     if (m <= 0) return;
@@ -378,24 +353,45 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     if (key0 >= L + m) return;  // no key of this chunk is visible to any row
     const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
     const int g = lane >> 4, r16 = lane & 15;
-    const int hd = p.hd, d = p.d;
+    const int d = p.d;
     const int qrow = 16 * rg + r16;
     const int qpos = L + qrow;
     const T *Kc = reinterpret_cast<const T *>(p.Kc);
     const T *Vt = reinterpret_cast<const T *>(p.Vt);
     const T *Q = reinterpret_cast<const T *>(p.Q);
 
+    // Every load of the workgroup is issued up front: Q rows, the chunk's 64 keys and values.
+    u32x4 qv[NKK], kv[4][NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+        const int dcol = h * HD + kk * PT::KSTEP + g * PT::VEC;
+        qv[kk] = *reinterpret_cast<const u32x4 *>(Q + (size_t)qrow * d + dcol);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            kv[kt][kk] = *reinterpret_cast<const u32x4 *>(Kc + (size_t)(key0 + 16 * kt + r16) * d + dcol);
+    }
+    // V^T operand: row = dim 16*dt + lane%16; K slots = keys 32kp+4g+(0..3), 32kp+16+4g+(0..3) (bf16),
+    // or keys 16kt+4g+(0..3) (fp32).
+    u32x4 vv[NDT][2];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+        const T *vrow = Vt + (size_t)(h * HD + 16 * dt + r16) * p.ctx_alloc + key0;
+        if constexpr (P == Prec::BF16) {
+#pragma unroll
+            for (int kp = 0; kp < 2; ++kp) {
+                const u32x2 va = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 4 * g);
+                const u32x2 vb = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 16 + 4 * g);
+                vv[dt][kp] = u32x4{va.x, va.y, vb.x, vb.y};
+            }
+        }
+    }
+
     f32x4 st[4];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int kk = 0; kk < hd / PT::KSTEP; ++kk) {
-        const int dcol = h * hd + kk * PT::KSTEP + g * PT::VEC;
-        const u32x4 qv = *reinterpret_cast<const u32x4 *>(Q + (size_t)qrow * d + dcol);
+    for (int kt = 0; kt < 4; ++kt) {
+        st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-            const u32x4 kv = *reinterpret_cast<const u32x4 *>(Kc + (size_t)(key0 + 16 * kt + r16) * d + dcol);
-            st[kt] = mfma_kstep<P>(kv, qv, st[kt]);
-        }
+        for (int kk = 0; kk < NKK; ++kk) st[kt] = mfma_kstep<P>(kv[kt][kk], qv[kk], st[kt]);
     }
     // st[kt][v] = S^T[key0 + 16kt + 4g + v][qrow]
     float mx = -INFINITY;
@@ -404,9 +400,9 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int key = key0 + 16 * kt + 4 * g + v;
-            const float s = key <= qpos ? st[kt][v] * p.scale_log2 : -INFINITY;
-            st[kt][v] = s;
-            mx = fmaxf(mx, s);
+            const float sc = key <= qpos ? st[kt][v] * p.scale_log2 : -INFINITY;
+            st[kt][v] = sc;
+            mx = fmaxf(mx, sc);
         }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -424,23 +420,21 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     l += __shfl_xor(l, 32);
 
     const size_t pbase = ((size_t)h * p.nch + c) * kMaxRows + qrow;
-    for (int dt = 0; dt < hd / 16; ++dt) {
-        const T *vrow = Vt + (size_t)(h * hd + 16 * dt + r16) * p.ctx_alloc + key0;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
         f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
         if constexpr (P == Prec::BF16) {
 #pragma unroll
             for (int kp = 0; kp < 2; ++kp) {
-                // K slots: keys 32kp + 4g + (0..3) and 32kp + 16 + 4g + (0..3).
-                const u32x2 va = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 4 * g);
-                const u32x2 vb = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 16 + 4 * g);
                 const f32x4 pa = st[2 * kp], pb = st[2 * kp + 1];
                 const u32x4 bop = u32x4{(uint32_t)f2bf(pa[0]) | ((uint32_t)f2bf(pa[1]) << 16),
                                         (uint32_t)f2bf(pa[2]) | ((uint32_t)f2bf(pa[3]) << 16),
                                         (uint32_t)f2bf(pb[0]) | ((uint32_t)f2bf(pb[1]) << 16),
                                         (uint32_t)f2bf(pb[2]) | ((uint32_t)f2bf(pb[3]) << 16)};
-                o = mfma_kstep<P>(u32x4{va.x, va.y, vb.x, vb.y}, bop, o);
+                o = mfma_kstep<P>(vv[dt][kp], bop, o);
             }
         } else {
+            const T *vrow = Vt + (size_t)(h * HD + 16 * dt + r16) * p.ctx_alloc + key0;
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
                 const u32x4 va = *reinterpret_cast<const u32x4 *>(vrow + 16 * kt + 4 * g);
@@ -451,7 +445,7 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
             }
         }
         // o[v] = O^T[16dt + 4g + v][qrow]
-        *reinterpret_cast<f32x4 *>(p.Opart + pbase * hd + 16 * dt + 4 * g) = o;
+        *reinterpret_cast<f32x4 *>(p.Opart + pbase * HD + 16 * dt + 4 * g) = o;
     }
     if (g == 0) {
         p.Mpart[pbase] = mx;
@@ -459,9 +453,11 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     }
 }
 
-// Combine the chunk partials of one (head, row) in chunk order and write bf16/fp32 O.
+// Combine the chunk partials of one (head, row) in chunk order and write O (compute dtype).
+// Wave 0 derives the chunk weights w_c = 2^(m_c - M) into LDS; every thread (one output dim)
+// then sums w_c * O_c in chunk order.
 template <Prec P>
-__global__ void attn_combine_kernel(AttnParams p) {
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
     using T = typename PrecT<P>::T;
     const Ctl *ctl = p.ctl;
     const int m = ctl->m;
@@ -469,19 +465,40 @@ __global__ void attn_combine_kernel(AttnParams p) {
     if (row >= m) return;
     const int L = ctl->L;
     const int nlive = (L + m + kAttnChunk - 1) / kAttnChunk;
-    const int dim = threadIdx.x;
+    const int tid = threadIdx.x;
     const size_t b0 = (size_t)h * p.nch * kMaxRows + row;
-    float M = -INFINITY;
-    for (int c = 0; c < nlive; ++c) M = fmaxf(M, p.Mpart[b0 + (size_t)c * kMaxRows]);
-    float den = 0.0f, num = 0.0f;
-    for (int c = 0; c < nlive; ++c) {
-        const size_t b = b0 + (size_t)c * kMaxRows;
-        const float mc = p.Mpart[b];
-        const float wc = mc == -INFINITY ? 0.0f : exp2f(mc - M);
-        den += wc * p.Lpart[b];
-        num += wc * p.Opart[b * p.hd + dim];
+    __shared__ float s_w[kMaxChunks];
+    __shared__ float s_den;
+    if (tid < kWave) {
+        float M = -INFINITY;
+        for (int c = tid; c < nlive; c += kWave) M = fmaxf(M, p.Mpart[b0 + (size_t)c * kMaxRows]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+        for (int c = tid; c < nlive; c += kWave) {
+            const float mc = p.Mpart[b0 + (size_t)c * kMaxRows];
+            s_w[c] = mc == -INFINITY ? 0.0f : exp2f(mc - M);
+        }
     }
-    reinterpret_cast<T *>(p.O)[(size_t)row * p.d + h * p.hd + dim] = to_elem<P>(num / den);
+    __syncthreads();
+    if (tid == 0) {
+        float den = 0.0f;
+        for (int c = 0; c < nlive; ++c) den += s_w[c] * p.Lpart[b0 + (size_t)c * kMaxRows];
+        s_den = den;
+    }
+    __syncthreads();
+    for (int dim = tid; dim < p.hd; dim += blockDim.x) {
+        float num = 0.0f;
+        int c = 0;
+        for (; c + 4 <= nlive; c += 4) {
+            float o[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * kMaxRows) * p.hd + dim];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
+        }
+        for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * kMaxRows) * p.hd + dim];
+        reinterpret_cast<T *>(p.O)[(size_t)row * p.d + h * p.hd + dim] = to_elem<P>(num / s_den);
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -521,28 +538,61 @@ __global__ void decode_init_kernel(ScanParams p) {
     c->m = c->nb;
 }
 
-__global__ __launch_bounds__(kWave) void scan_commit_kernel(ScanParams p) {
+__global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     Ctl *c = p.ctl;
     const int m = c->m;
     if (m <= 0) return;
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid;
     if (p.advance_only) {
-        if (lane == 0) {
+        if (tid == 0) {
             c->L += m;
             c->m = 0;
         }
         return;
     }
-    if (lane < m) {
+    // Final argmax of each row over the LM-head workgroups: 16 threads per row take strided
+    // workgroups, then a 16-lane xor tree. (max, lowest id) is exact, so the order is free.
+    {
+        const int row = tid & 63, j = tid >> 6;
         float bv = -INFINITY;
-        int bi = -2;
-        for (int g = 0; g < p.n_wg; ++g) {
-            const int idx = p.pidx[(size_t)g * kMaxRows + lane];
-            const float v = p.pmax[(size_t)g * kMaxRows + lane];
-            if (idx < 0) { bi = -1; break; }
-            if (bi == -2 || v > bv) { bv = v; bi = idx; }
+        int bi = 0x7fffffff;
+        int nan = 0;
+        if (row < m) {
+            for (int g0 = j; g0 < p.n_wg; g0 += 16 * 8) {
+                float v[8];
+                int ix[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int g = g0 + 16 * u;
+                    ix[u] = g < p.n_wg ? p.pidx[(size_t)g * kMaxRows + row] : 0x7fffffff;
+                    v[u] = g < p.n_wg ? p.pmax[(size_t)g * kMaxRows + row] : -INFINITY;
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    if (ix[u] < 0) nan = 1;
+                    else if (v[u] > bv || (v[u] == bv && ix[u] < bi)) { bv = v[u]; bi = ix[u]; }
+                }
+            }
         }
-        c->pred[lane] = bi;
+        __shared__ float s_v[1024];
+        __shared__ int s_i[1024];
+        __shared__ int s_nan[1024];
+        s_v[tid] = bv;
+        s_i[tid] = bi;
+        s_nan[tid] = nan;
+        __syncthreads();
+        if (tid < 64 && tid < m) {
+            float b = s_v[tid];
+            int i = s_i[tid], nn = s_nan[tid];
+            for (int jj = 1; jj < 16; ++jj) {
+                const float ov = s_v[jj * 64 + tid];
+                const int oi = s_i[jj * 64 + tid];
+                nn |= s_nan[jj * 64 + tid];
+                if (ov > b || (ov == b && oi < i)) { b = ov; i = oi; }
+            }
+            c->pred[tid] = (nn || i == 0x7fffffff) ? -1 : i;
+        }
     }
     __syncthreads();
     if (lane != 0) return;
@@ -630,18 +680,12 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
-template <Prec P, int NT, int RG, int AL, int EP>
+template <Prec P, int NT, int RG, int EP, int D = kGemmDepth>
 static hipError_t launch_gemm_t(const GemmParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    static_assert(4 * NT * 256 >= ROWS * 16, "E_RESID reuses the reduction buffer");
-    size_t lds = (size_t)(4 * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
-    if (AL == A_NORM) lds += (size_t)p.K * sizeof(float);
-    auto kern = gemm_kernel<P, NT, RG, AL, EP>;
-    if (lds > 64 * 1024) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (err != hipSuccess) return err;
-    }
+    static_assert(kGemmWaves * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
+    const size_t lds = (size_t)(kGemmWaves * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
+    auto kern = gemm_kernel<P, NT, RG, EP, D>;
     if (e0) {
         hipExtLaunchKernelGGL(kern, dim3(p.n_wg), dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, p);
     } else {
@@ -651,33 +695,31 @@ static hipError_t launch_gemm_t(const GemmParams &p, hipStream_t s, hipEvent_t e
 }
 
 template <Prec P, int RG>
-static hipError_t launch_gemm_rg(GemmKind kind, int nt_qkv, const GemmParams &p, hipStream_t s, hipEvent_t e0,
-                                 hipEvent_t e1) {
+static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     switch (kind) {
     case GEMM_QKV:
-        return nt_qkv == 2 ? launch_gemm_t<P, 2, RG, A_NORM, E_QKV>(p, s, e0, e1)
-                           : launch_gemm_t<P, 1, RG, A_NORM, E_QKV>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, s, e0, e1);
     case GEMM_O:
     case GEMM_DOWN:
-        return launch_gemm_t<P, 1, RG, A_ACT, E_RESID>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtResid, RG, E_RESID>(p, s, e0, e1);
     case GEMM_GATE_UP:
-        return launch_gemm_t<P, 2, RG, A_NORM, E_SWIGLU>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, s, e0, e1);
     case GEMM_LM:
-        return launch_gemm_t<P, kLmTiles, RG, A_NORM, E_ARGMAX>(p, s, e0, e1);
+        return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX>(p, s, e0, e1);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int nt_qkv, const GemmParams &p, hipStream_t s,
-                       hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, const GemmParams &p, hipStream_t s, hipEvent_t e0,
+                       hipEvent_t e1) {
     if (bf16) {
-        if (rg == 1) return launch_gemm_rg<Prec::BF16, 1>(kind, nt_qkv, p, s, e0, e1);
-        if (rg == 2) return launch_gemm_rg<Prec::BF16, 2>(kind, nt_qkv, p, s, e0, e1);
-        return launch_gemm_rg<Prec::BF16, 4>(kind, nt_qkv, p, s, e0, e1);
+        if (rg == 1) return launch_gemm_rg<Prec::BF16, 1>(kind, p, s, e0, e1);
+        if (rg == 2) return launch_gemm_rg<Prec::BF16, 2>(kind, p, s, e0, e1);
+        return launch_gemm_rg<Prec::BF16, 4>(kind, p, s, e0, e1);
     }
-    if (rg == 1) return launch_gemm_rg<Prec::F32, 1>(kind, nt_qkv, p, s, e0, e1);
-    if (rg == 2) return launch_gemm_rg<Prec::F32, 2>(kind, nt_qkv, p, s, e0, e1);
-    return launch_gemm_rg<Prec::F32, 4>(kind, nt_qkv, p, s, e0, e1);
+    if (rg == 1) return launch_gemm_rg<Prec::F32, 1>(kind, p, s, e0, e1);
+    if (rg == 2) return launch_gemm_rg<Prec::F32, 2>(kind, p, s, e0, e1);
+    return launch_gemm_rg<Prec::F32, 4>(kind, p, s, e0, e1);
 }
 
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
@@ -689,11 +731,12 @@ hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s
     return hipGetLastError();
 }
 
-template <Prec P>
-static hipError_t launch_attn_p(int rg, const AttnParams &p, int nch_launch, hipStream_t s, hipEvent_t e0,
-                                hipEvent_t e1) {
+template <Prec P, int HD>
+static hipError_t launch_attn_hd(int rg, const AttnParams &p, int nch_launch, hipStream_t s, hipEvent_t e0,
+                                 hipEvent_t e1) {
     dim3 grid(nch_launch, p.n_heads);
-    auto kern = rg == 1 ? attn_partial_kernel<P, 1> : (rg == 2 ? attn_partial_kernel<P, 2> : attn_partial_kernel<P, 4>);
+    auto kern = rg == 1 ? attn_partial_kernel<P, HD, 1>
+                        : (rg == 2 ? attn_partial_kernel<P, HD, 2> : attn_partial_kernel<P, HD, 4>);
     if (e0)
         hipExtLaunchKernelGGL(kern, grid, dim3(kWave * rg), 0, s, e0, e1, 0, p);
     else
@@ -703,26 +746,41 @@ static hipError_t launch_attn_p(int rg, const AttnParams &p, int nch_launch, hip
 
 hipError_t launch_attn(bool bf16, int rg, int nch_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                        hipEvent_t e1) {
-    return bf16 ? launch_attn_p<Prec::BF16>(rg, p, nch_launch, s, e0, e1)
-                : launch_attn_p<Prec::F32>(rg, p, nch_launch, s, e0, e1);
+    if (bf16) {
+        switch (p.hd) {
+        case 32: return launch_attn_hd<Prec::BF16, 32>(rg, p, nch_launch, s, e0, e1);
+        case 64: return launch_attn_hd<Prec::BF16, 64>(rg, p, nch_launch, s, e0, e1);
+        case 128: return launch_attn_hd<Prec::BF16, 128>(rg, p, nch_launch, s, e0, e1);
+        case 256: return launch_attn_hd<Prec::BF16, 256>(rg, p, nch_launch, s, e0, e1);
+        }
+    } else {
+        switch (p.hd) {
+        case 16: return launch_attn_hd<Prec::F32, 16>(rg, p, nch_launch, s, e0, e1);
+        case 32: return launch_attn_hd<Prec::F32, 32>(rg, p, nch_launch, s, e0, e1);
+        case 64: return launch_attn_hd<Prec::F32, 64>(rg, p, nch_launch, s, e0, e1);
+        case 128: return launch_attn_hd<Prec::F32, 128>(rg, p, nch_launch, s, e0, e1);
+        }
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_combine(bool bf16, int rows, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                                hipEvent_t e1) {
     dim3 grid(p.n_heads, rows);
+    const unsigned threads = p.hd < 256 ? (unsigned)p.hd : 256u;
     auto kern = bf16 ? attn_combine_kernel<Prec::BF16> : attn_combine_kernel<Prec::F32>;
     if (e0)
-        hipExtLaunchKernelGGL(kern, grid, dim3(p.hd), 0, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(kern, grid, dim3(threads), 0, s, e0, e1, 0, p);
     else
-        hipLaunchKernelGGL(kern, grid, dim3(p.hd), 0, s, p);
+        hipLaunchKernelGGL(kern, grid, dim3(threads), 0, s, p);
     return hipGetLastError();
 }
 
 hipError_t launch_scan(const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     if (e0)
-        hipExtLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(kWave), 0, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(1024), 0, s, e0, e1, 0, p);
     else
-        hipLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(kWave), 0, s, p);
+        hipLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(1024), 0, s, p);
     return hipGetLastError();
 }
 

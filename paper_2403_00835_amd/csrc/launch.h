@@ -7,7 +7,11 @@ namespace cllm {
 
 struct Ctl;
 
-constexpr int kLmTiles = 4;  // 16-column tiles per LM-head workgroup
+constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
+constexpr int kNtQkv = 4;     // QKV (pairs of rotate-half partner tiles)
+constexpr int kNtGateUp = 2;  // gate/up ((gate, up) tile pairs)
+constexpr int kNtResid = 1;   // O and down projections
+constexpr int kGemmDepth = 2; // k-steps in flight per wave
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
@@ -15,13 +19,10 @@ struct GemmParams {
     const uint8_t *W;  // packed tiles
     int Ks;            // k-steps per 16-row tile
     int n_wg;          // workgroups (tiles / NT)
-    // activation operand
-    const void *A;     // compute dtype, rows of lda elements (A_ACT)
+    const void *A;     // activation operand (compute dtype), rows of lda elements
     int lda;
-    const float *X;    // fp32 residual stream, rows of ldx floats (A_NORM reads it; E_RESID updates it)
-    int ldx;
-    const float *gain; // RMSNorm gain [K]
-    const float *ssq;  // per-16-column sums of squares [T][kMaxRows]
+    // RMSNorm row factor (QKV, gate/up, LM head): per-16-column sums of squares [row][T]
+    const float *ssq;
     int T, K;
     float eps;
     const Ctl *ctl;
@@ -30,8 +31,11 @@ struct GemmParams {
     int ctx_alloc;
     const float *rcos, *rsin;
     int d, hd;
-    // E_RESID
+    // E_RESID: X += Y (rows of ldx floats); next RMSNorm operand An = X (.) gain; new partials
     float *Xout, *ssq_out;
+    int ldx;
+    const float *gain;
+    void *An;
     // E_SWIGLU
     void *H;
     int Fp;
@@ -45,6 +49,8 @@ struct GemmParams {
 struct EmbedParams {
     const void *E;
     float *X, *ssq;
+    void *An;           // first RMSNorm operand X (.) gain
+    const float *gain;
     int d;
     const Ctl *ctl;
 };
@@ -76,8 +82,8 @@ struct SetupParams {
 };
 hipError_t launch_setup(const SetupParams &p, hipStream_t s);
 
-hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int nt_qkv, const GemmParams &p, hipStream_t s,
-                       hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, const GemmParams &p, hipStream_t s, hipEvent_t e0,
+                       hipEvent_t e1);
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_attn(bool bf16, int rg, int nch_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                        hipEvent_t e1);

@@ -82,6 +82,9 @@ def main():
     ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long"])
     ap.add_argument("--p", type=float, default=0.3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the timed steps, copy 1 GiB device-to-device (a kernel of known traffic "
+                         "for scaling hardware byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -149,6 +152,15 @@ def main():
     mean_ctx = P + max_new / 2
     kv_bytes = cfg.n_layers * 2 * mean_ctx * d * 2
     step_gbps = (wbytes + kv_bytes) / (iter_ms / 1e3) / 1e9
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] calibration copy: 1073741824 bytes read, 1073741824 bytes written")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

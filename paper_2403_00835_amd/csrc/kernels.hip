@@ -306,7 +306,9 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
 // ------------------------------------------------------------------------------------------
 template <Prec P>
 __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
-    using T = typename PrecT<P>::T;
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    constexpr int V16 = 16 / sizeof(T);  // elements per 16-byte vector
     const Ctl *ctl = p.ctl;
     const int m = ctl->m;
     const int row = blockIdx.x;
@@ -315,15 +317,29 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     const T *e = reinterpret_cast<const T *>(p.E) + (size_t)tok * p.d;
     float *x = p.X + (size_t)row * p.d;
     T *an = reinterpret_cast<T *>(p.An) + (size_t)row * p.d;
-    for (int t = threadIdx.x; t < p.d / 16; t += blockDim.x) {
+    for (int t = threadIdx.x; t < p.d / 16; t += blockDim.x) {  // one 16-column tile per thread
+        alignas(16) T ev[16];
+        alignas(16) T av[16];
+        alignas(16) float xv[16];
+        alignas(16) float gv[16];
+#pragma unroll
+        for (int q = 0; q < 16 / V16; ++q)
+            *reinterpret_cast<u32x4 *>(ev + q * V16) = *reinterpret_cast<const u32x4 *>(e + 16 * t + q * V16);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f32x4 *>(gv + 4 * q) = *reinterpret_cast<const f32x4 *>(p.gain + 16 * t + 4 * q);
         float sum = 0.0f;
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
-            const float v = from_elem<P>(e[16 * t + c]);
-            x[16 * t + c] = v;
-            an[16 * t + c] = to_elem<P>(v * p.gain[16 * t + c]);
-            sum += v * v;
+            xv[c] = from_elem<P>(ev[c]);
+            av[c] = to_elem<P>(xv[c] * gv[c]);
+            sum += xv[c] * xv[c];
         }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<f32x4 *>(x + 16 * t + 4 * q) = *reinterpret_cast<f32x4 *>(xv + 4 * q);
+#pragma unroll
+        for (int q = 0; q < 16 / V16; ++q)
+            *reinterpret_cast<u32x4 *>(an + 16 * t + q * V16) = *reinterpret_cast<u32x4 *>(av + q * V16);
         p.ssq[(size_t)row * (p.d / 16) + t] = sum;
     }
 }

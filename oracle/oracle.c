@@ -17,14 +17,13 @@
  * Deepseek-coder-7B). The decoder below is the LLaMA-style one: pre-norm RMSNorm,
  * rotate-half RoPE, causal softmax attention, SwiGLU FFN, untied LM head, no biases.
  *
- * Precision: every intermediate is a double. With round_bf16 set, values are rounded to
- * bfloat16 (round to nearest, ties to even) at the points of the precision contract: the
- * inputs of every matrix product and q, k, v after RoPE (which are also the cached keys and
- * values). The input of a product that follows an RMSNorm is x (.) g, rounded; the RMSNorm row
- * factor 1/sqrt(mean(x^2) + eps) scales the product's output (mathematically the same as
- * normalising first). The other product inputs are the attention output and the SwiGLU output.
- * Argmax decisions are taken on the logits rounded to fp32, the precision the GPU path decides
- * in; ties go to the lowest id.
+ * Precision: every intermediate is a double. With round_bf16 set (the bf16 precision contract),
+ * the weights hold bf16 values and the keys and values written to the cache (after RoPE) are
+ * rounded to bfloat16 (round to nearest, ties to even); no other value is rounded. The input of
+ * a product that follows an RMSNorm is x (.) g and the RMSNorm row factor
+ * 1/sqrt(mean(x^2) + eps) scales the product's output (mathematically the same as normalising
+ * first). Argmax decisions are taken on the logits rounded to fp32, the precision the GPU path
+ * decides in; ties go to the lowest id.
  *
  * Reading of the acceptance rule (the algorithm's fast-forward count): the block z holds the
  * known-correct pending token at index 0, the model's output at row k is the prediction for
@@ -106,7 +105,8 @@ double orc_bf16(double x) {
     return r;
 }
 
-static inline double rnd(const orc_model *m, double x) { return m->c.round_bf16 ? orc_bf16(x) : x; }
+/* Rounding of a key or value stored in the cache (bf16 contract). */
+static inline double rnd_cache(const orc_model *m, double x) { return m->c.round_bf16 ? orc_bf16(x) : x; }
 
 /* RMSNorm row factor: 1 / sqrt(mean(x^2) + eps). */
 double orc_rms_inv(const double *x, int32_t n, double eps) {
@@ -124,16 +124,11 @@ void orc_rmsnorm(const double *x, int32_t n, const float *g, double eps, int32_t
     }
 }
 
-/* Input of a matrix product that follows an RMSNorm, under the precision contract: the
- * operand is x (.) g (rounded to bf16 in the bf16 contract) and the row factor inv is applied
- * to the product, y = inv * (operand . W^T). Without rounding this equals rmsnorm(x) . W^T. */
-static void norm_operand(const double *x, int32_t n, const float *g, double eps, int32_t round_bf16, double *a,
-                         double *inv) {
+/* Input of a matrix product that follows an RMSNorm: the operand is x (.) g and the row factor
+ * inv is applied to the product, y = inv * (operand . W^T), which equals rmsnorm(x) . W^T. */
+static void norm_operand(const double *x, int32_t n, const float *g, double eps, double *a, double *inv) {
     *inv = orc_rms_inv(x, n, eps);
-    for (int32_t k = 0; k < n; ++k) {
-        double y = x[k] * (double)g[k];
-        a[k] = round_bf16 ? orc_bf16(y) : y;
-    }
+    for (int32_t k = 0; k < n; ++k) a[k] = x[k] * (double)g[k];
 }
 
 static void scale_rows(double *y, int32_t rows, int32_t cols, const double *inv) {
@@ -304,7 +299,7 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         double *Vc = st->v + (size_t)l * st->max_ctx * d;
         /* attention sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
+            norm_operand(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, a + (size_t)i * d, inv + i);
         linear(a, m, M->wq[l], d, d, q);
         linear(a, m, M->wk[l], d, d, kk);
         linear(a, m, M->wv[l], d, d, vv);
@@ -318,9 +313,8 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
             }
             for (int32_t k = 0; k < d; ++k) {
                 size_t ix = (size_t)i * d + k;
-                q[ix] = rnd(M, q[ix]);
-                Kc[(size_t)(pos0 + i) * d + k] = rnd(M, kk[ix]);
-                Vc[(size_t)(pos0 + i) * d + k] = rnd(M, vv[ix]);
+                Kc[(size_t)(pos0 + i) * d + k] = rnd_cache(M, kk[ix]);
+                Vc[(size_t)(pos0 + i) * d + k] = rnd_cache(M, vv[ix]);
             }
         }
 #pragma omp parallel for collapse(2) schedule(static)
@@ -328,23 +322,22 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
             for (int32_t hh = 0; hh < H; ++hh)
                 orc_attention_row(q + (size_t)i * d + hh * hd, Kc + hh * hd, Vc + hh * hd, pos0 + i + 1, d, hd,
                                   o + (size_t)i * d + hh * hd);
-        for (size_t ix = 0; ix < (size_t)m * d; ++ix) o[ix] = rnd(M, o[ix]);
         linear(o, m, M->wo[l], d, d, y);
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
         /* SwiGLU feed-forward sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
+            norm_operand(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, a + (size_t)i * d, inv + i);
         linear(a, m, M->wg[l], d, F, g);
         linear(a, m, M->wu[l], d, F, u);
         scale_rows(g, m, F, inv);
         scale_rows(u, m, F, inv);
-        for (size_t ix = 0; ix < (size_t)m * F; ++ix) g[ix] = rnd(M, orc_silu(g[ix]) * u[ix]);
+        for (size_t ix = 0; ix < (size_t)m * F; ++ix) g[ix] = orc_silu(g[ix]) * u[ix];
         linear(g, m, M->wd[l], F, d, y);
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
     }
     if (logits) {
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->final_norm, c->rms_eps, c->round_bf16, a + (size_t)i * d, inv + i);
+            norm_operand(h + (size_t)i * d, d, M->final_norm, c->rms_eps, a + (size_t)i * d, inv + i);
         linear(a, m, M->lm_head, d, V, logits);
         scale_rows(logits, m, V, inv);
     }

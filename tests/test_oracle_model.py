@@ -180,13 +180,15 @@ def test_provisional_rows_are_overwritten():
     np.testing.assert_allclose(lg, full[21:30], rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("bf16_cache", [False, True])
 @pytest.mark.parametrize("key_coord", [0, HD // 2])
-def test_two_token_rope_attention_closed_form(key_coord):
+def test_two_token_rope_attention_closed_form(key_coord, bf16_cache):
     # Head 0 only: the second token's query is c*e_0, the first token's key is kap*c*e_j
     # (j = 0 or the rotate-half partner hd/2), the second token's key is zero. After RoPE at
     # positions 1 and 0 the score of key 0 is c^2 kap cos(1) / sqrt(hd) for j = 0 and
     # c^2 kap sin(1) / sqrt(hd) for j = hd/2; the score of key 1 is 0. So the attention weight
     # of token 0 is the logistic function of that score. Values route to distinct outputs.
+    # Under the bf16 contract the cached key kap*c and values c enter as their bf16 roundings.
     cfg = _cfg(1)
     ts = _base_tensors(cfg)
     x0, x1, kap, beta, s = 10, 20, 1.75, 0.875, 1.0
@@ -201,17 +203,19 @@ def test_two_token_rope_attention_closed_form(key_coord):
     Wo[33, 2] = beta
     Wo[44, 5] = beta
     ts[1 + 1], ts[1 + 2], ts[1 + 3], ts[1 + 4] = Wq, Wk, Wv, Wo
-    m = oracle.Model(cfg, ts)
+    m = oracle.Model(cfg, ts, round_bf16=bf16_cache)
     lg = m.forward_full(np.array([x0, x1], dtype=np.int32))
     c = s / math.sqrt(s * s / D + cfg.rms_eps)
+    cached = oracle.bf16 if bf16_cache else (lambda v: v)
     trig = math.cos(1.0) if key_coord == 0 else math.sin(1.0)
-    w = expit(c * c * kap * trig / math.sqrt(HD))
+    w = expit(c * trig * cached(kap * c) / math.sqrt(HD))
+    vc = cached(c)
     expect_h = [np.zeros(D), np.zeros(D)]
     expect_h[0][x0] += s
-    expect_h[0][33] += beta * c
+    expect_h[0][33] += beta * vc
     expect_h[1][x1] += s
-    expect_h[1][33] += beta * c * w
-    expect_h[1][44] += beta * c * (1 - w)
+    expect_h[1][33] += beta * vc * w
+    expect_h[1][44] += beta * vc * (1 - w)
     for t in range(2):
         h = expect_h[t]
         nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps)

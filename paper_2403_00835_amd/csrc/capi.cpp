@@ -462,10 +462,11 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->rsin, (size_t)c->ctx_alloc * h2))) return bail(s);
     if ((s = dalloc_t(c, &c->X, rows * c->d))) return bail(s);
     if ((s = dalloc_t(c, &c->ssq, (size_t)(c->d / 16) * rows))) return bail(s);
-    if ((s = dalloc(c, &c->Q, rows * c->d * E))) return bail(s);
-    if ((s = dalloc(c, &c->O, rows * c->d * E))) return bail(s);
-    if ((s = dalloc(c, &c->An, rows * c->d * E))) return bail(s);
-    if ((s = dalloc(c, &c->Hb, rows * c->Fp * E))) return bail(s);
+    // activation operands: one fp32 plane, or hi and lo bf16 planes (4 bytes per element either way)
+    if ((s = dalloc(c, &c->Q, act_plane(c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->O, act_plane(c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->An, act_plane(c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->Hb, act_plane(c->Fp) * 4))) return bail(s);
     if ((s = dalloc_t(c, &c->pmax, (size_t)c->n_wg_lm * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->pidx, (size_t)c->n_wg_lm * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->opart, (size_t)c->H * c->nch * rows * c->hd))) return bail(s);

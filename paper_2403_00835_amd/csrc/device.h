@@ -27,15 +27,19 @@ constexpr int kGainVecs = 4;       // RMSNorm gain staging: d_model <= 4 * 4 * 5
 // 4 lane groups x VEC elements. bf16: one 16x16x32 MFMA per k-step; fp32: four 16x16x4 MFMAs.
 enum class Prec { BF16 = 1, F32 = 0 };
 template <Prec P> struct PrecT;
+// PLANES: activation operands of the bf16 products carry their fp32 values as two bf16 planes
+// (hi = bf16(x), lo = bf16(x - hi): 16 significant bits); fp32 operands have one plane.
 template <> struct PrecT<Prec::BF16> {
     using T = uint16_t;  // bf16 bit pattern
     static constexpr int VEC = 8;
     static constexpr int KSTEP = 32;
+    static constexpr int PLANES = 2;
 };
 template <> struct PrecT<Prec::F32> {
     using T = float;
     static constexpr int VEC = 4;
     static constexpr int KSTEP = 16;
+    static constexpr int PLANES = 1;
 };
 
 __device__ __forceinline__ uint16_t f2bf(float x) {
@@ -50,6 +54,32 @@ template <> __device__ __forceinline__ float to_elem<Prec::F32>(float x) { retur
 template <Prec P> __device__ __forceinline__ float from_elem(typename PrecT<P>::T x);
 template <> __device__ __forceinline__ float from_elem<Prec::BF16>(uint16_t x) { return bf2f(x); }
 template <> __device__ __forceinline__ float from_elem<Prec::F32>(float x) { return x; }
+
+// Activation operands (the A side of every product, and the attention queries) are stored in the
+// MFMA operand order: for 16-row group rg and k-step s, the 64 lanes' 16-byte vectors are
+// contiguous (1 KiB), lane = 16 * (k-group within the k-step) + row % 16. A k-step load is one
+// contiguous KiB per row group. Each plane holds kMaxRows rows of K elements; the lo plane of a
+// bf16 operand follows the hi plane.
+__host__ __device__ constexpr size_t act_plane(int K) { return (size_t)kMaxRows * (size_t)K; }
+
+template <Prec P>
+__device__ __forceinline__ size_t act_idx(int row, int k, int K) {
+    constexpr int VEC = PrecT<P>::VEC, KSTEP = PrecT<P>::KSTEP;
+    const int s = k / KSTEP, w = k % KSTEP;
+    return ((size_t)((row >> 4) * (K / KSTEP) + s) * kWave + (w / VEC) * 16 + (row & 15)) * VEC + (w % VEC);
+}
+
+// Store x at element i of an activation operand (both planes for bf16).
+template <Prec P>
+__device__ __forceinline__ void put_act(typename PrecT<P>::T *base, size_t plane, size_t i, float x) {
+    if constexpr (P == Prec::BF16) {
+        const uint16_t hi = f2bf(x);
+        base[i] = hi;
+        base[plane + i] = f2bf(x - bf2f(hi));  // x - hi is exact in fp32
+    } else {
+        base[i] = x;
+    }
+}
 
 // One k-step of C += A * B on 16x16 tiles. a holds this lane's 16 bytes of the activation row
 // (row = lane % 16), b this lane's 16 bytes of the weight row (column = lane % 16); both hold

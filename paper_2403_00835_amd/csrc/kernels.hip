@@ -31,6 +31,9 @@ namespace cllm {
 // takes k-steps w, w+8, w+16, ... and accumulates them in order with MFMA; the 8 partial tiles
 // are then summed in a fixed tree ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)). Weights are read once,
 // straight into registers (no LDS); the activation rows (a few KiB, L2-resident) are re-read.
+// In bf16 the activations are fp32 values split into hi and lo bf16 planes, and each k-step runs
+// one MFMA per plane against the same weight tile: products are exact in fp32, so the operand
+// keeps 16 significant bits instead of bf16's 8.
 //
 // Products that follow an RMSNorm take the operand x (.) g written by the producer of x and
 // scale each output row by 1/sqrt(mean(x^2) + eps), reduced from the producer's per-16-column
@@ -41,48 +44,49 @@ enum Epi { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_ARGMAX = 3 };
 
 template <Prec P, int NT, int RG>
 struct Stage {  // operands of one k-step
-    u32x4 b[NT];  // weight tiles
-    u32x4 a[RG];  // activation rows
+    u32x4 b[NT];                      // weight tiles
+    u32x4 a[PrecT<P>::PLANES][RG];    // activation rows (hi, lo planes for bf16)
 };
 
-// Loads of one k-step (s_raw = this wave's step index; clamped to the last k-step, so every
-// load is issued and the compiler can count outstanding loads exactly).
+// Loads of one k-step s (callers clamp s into [0, Ks), so every load is issued and the compiler
+// can count outstanding loads exactly).
 template <Prec P, int NT, int RG>
-__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int s_raw, int lane) {
+__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int s, int lane) {
     using PT = PrecT<P>;
     using T = typename PT::T;
-    const int g = lane >> 4, r16 = lane & 15;
-    const int s = min(s_raw, p.Ks - 1);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)(t0 + j) * p.Ks + s) * kTileBytes) + lane;
         if constexpr (kWeightsNonTemporal) st.b[j] = __builtin_nontemporal_load(src);
         else st.b[j] = *src;
     }
-    const int k = s * PT::KSTEP + g * PT::VEC;
     const T *A = reinterpret_cast<const T *>(p.A);
+    const int ks_a = p.lda / PT::KSTEP;
 #pragma unroll
-    for (int r = 0; r < RG; ++r) st.a[r] = *reinterpret_cast<const u32x4 *>(A + (size_t)(16 * r + r16) * p.lda + k);
+    for (int pl = 0; pl < PT::PLANES; ++pl)
+#pragma unroll
+        for (int r = 0; r < RG; ++r)
+            st.a[pl][r] = *reinterpret_cast<const u32x4 *>(A + pl * act_plane(p.lda) +
+                                                          ((size_t)(r * ks_a + s) * kWave + lane) * PT::VEC);
 }
 
-// MFMAs of one k-step. Branch-free: a k-step past the end (its loads were clamped to a valid
-// tile) gets a zero activation operand, so it adds exact zeros.
+// MFMAs of one k-step: every hi-plane product, then every lo-plane product (bf16).
 template <Prec P, int NT, int RG>
-__device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG> &st, const GemmParams &p, int s_raw,
-                                             f32x4 (&acc)[RG][NT]) {
-    const bool valid = s_raw < p.Ks;
+__device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG> &st, f32x4 (&acc)[RG][NT]) {
 #pragma unroll
-    for (int r = 0; r < RG; ++r) {
-        const u32x4 a = valid ? st.a[r] : u32x4{0u, 0u, 0u, 0u};
+    for (int pl = 0; pl < PrecT<P>::PLANES; ++pl)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) acc[r][j] = mfma_kstep<P>(a, st.b[j], acc[r][j]);
-    }
+        for (int r = 0; r < RG; ++r)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) acc[r][j] = mfma_kstep<P>(st.a[pl][r], st.b[j], acc[r][j]);
 }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
-template <Prec P, int NT, int RG, int EP, int D>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) {
+// W waves per workgroup split K; KC selects each wave's k-steps: interleaved (w, w+W, ...) or a
+// contiguous range.
+template <Prec P, int NT, int RG, int EP, int D, int W, bool KC>
+__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
@@ -96,44 +100,33 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
 
     extern __shared__ float smem[];
-    float *s_red = smem;                            // 8 waves x NT x 256 (also ROWS x COLS for E_RESID)
-    float *s_tile = s_red + kGemmWaves * NT * 256;  // ROWS x (COLS + 1)
+    float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
+    float *s_tile = s_red + W * NT * 256;  // ROWS x (COLS + 1)
     float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
 
-    // This wave's k-steps are w, w+8, w+16, ... (nmy of them); the first D-1 are requested first.
-    const int nmy = w < p.Ks ? (p.Ks - w + kGemmWaves - 1) / kGemmWaves : 0;
+    // Row factor inputs (products that follow an RMSNorm): the producer's per-16-column sums of
+    // squares, layout [row][T] with T a multiple of 4. 32 threads per row each own a contiguous
+    // run of q = 4 * ceil(T/128) partials, read as 16-byte vectors; the first two vectors of the
+    // first row pass are requested before the weights, so their latency overlaps the first
+    // k-step's, and everything is reduced after the main loop.
+    constexpr int RPP = W * kWave / 32;  // rows per pass
+    static_assert(ROWS % RPP == 0, "row passes cover the row groups");
+    const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) {
+        const float *src = p.ssq + (size_t)(tid >> 5) * p.T;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)  // clamped, unconditional
+            sq_pre[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + 4 * i, p.T - 4));
+    }
+
+    // This wave's k-steps (nmy of them); the first D-1 are requested first.
+    const int nper = (p.Ks + W - 1) / W;
+    const int nmy = KC ? max(0, min(nper, p.Ks - w * nper)) : (w < p.Ks ? (p.Ks - w + W - 1) / W : 0);
+    auto step_of = [&](int q) { return min(KC ? w * nper + q : w + q * W, p.Ks - 1); };
     Stage<P, NT, RG> ring[D];
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, w + j * kGemmWaves, lane);
-
-    if constexpr (ROWSCALE) {
-        // Row factor 1/sqrt(mean(x^2) + eps) from the producer's per-16-column sums of squares
-        // (layout [row][T]): 8 threads per row each add a contiguous run of q partials in order,
-        // then a fixed xor tree. The scheme does not depend on the number of rows. Only the first
-        // ROWS*8 threads take part; the barrier of the reduction below publishes s_inv.
-        if (tid < ROWS * 8) {
-            const int row = tid >> 3, part = tid & 7;
-            const int q = (p.T + 7) >> 3;
-            const int t_begin = part * q;
-            const float *src = p.ssq + (size_t)row * p.T;
-            float sum = 0.0f;
-            for (int i0 = 0; i0 < q; i0 += 16) {  // 16 loads in flight, then 16 ordered adds
-                float v[16];
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int t = t_begin + i0 + i;
-                    v[i] = (i0 + i < q && t < p.T) ? src[t] : 0.0f;
-                }
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (i0 + i < q && t_begin + i0 + i < p.T) sum += v[i];
-            }
-            sum += __shfl_xor(sum, 4, 8);
-            sum += __shfl_xor(sum, 2, 8);
-            sum += __shfl_xor(sum, 1, 8);
-            if (part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
-        }
-    }
+    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, step_of(j), lane);
 
     f32x4 acc[RG][NT];
 #pragma unroll
@@ -151,9 +144,9 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
 #pragma unroll
             for (int j = 0; j < D; ++j) {
                 // sched_barrier keeps the scheduler from sinking loads to their uses.
-                gemm_load(ring[(j + D - 1) % D], p, t0, w + (bi * D + j + D - 1) * kGemmWaves, lane);
+                gemm_load(ring[(j + D - 1) % D], p, t0, step_of(bi * D + j + D - 1), lane);
                 __builtin_amdgcn_sched_barrier(0);
-                gemm_compute(ring[j], p, w + (bi * D + j) * kGemmWaves, acc);
+                gemm_compute(ring[j], acc);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -162,25 +155,56 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
         for (int j = 0; j < 2 * D - 1; ++j) {
             const int v = v0 + j;
             if (v < nmy) {
-                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, w + (v + D - 1) * kGemmWaves, lane);
-                gemm_compute(ring[j % D], p, w + v * kGemmWaves, acc);
+                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, step_of(v + D - 1), lane);
+                gemm_compute(ring[j % D], acc);
             }
         }
     }
 
-    // Sum of the 8 waves' partial tiles through LDS, one row group at a time, in the fixed tree
-    // ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)) for every element; then the RMSNorm row factor.
+    if constexpr (ROWSCALE) {
+        // Row factor 1/sqrt(mean(x^2) + eps): each thread adds its run in order, then a fixed xor
+        // tree over the row's 32 threads. The scheme depends only on T, never on the number of
+        // rows. The barrier of the reduction below publishes s_inv.
+        for (int pass = 0; pass < ROWS / RPP; ++pass) {
+            const int row = pass * RPP + (tid >> 5);
+            const float *src = p.ssq + (size_t)row * p.T;
+            float sum = 0.0f;
+            for (int i0 = 0; i0 < sq_q; i0 += 8) {
+                f32x4 v[2];
+                if (pass == 0 && i0 == 0) {
+                    v[0] = sq_pre[0];
+                    v[1] = sq_pre[1];
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+                        v[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + i0 + 4 * i, p.T - 4));
+                }
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    if (i0 + i < sq_q && sq_part * sq_q + i0 + i < p.T) sum += v[i >> 2][i & 3];
+            }
+#pragma unroll
+            for (int off = 16; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 32);
+            if (sq_part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
+        }
+    }
+
+    // Sum of the W waves' partial tiles through LDS, one row group at a time, in a fixed tree
+    // (W = 8: ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); W = 4: (w0+w2)+(w1+w3)); then the RMSNorm row
+    // factor.
 #pragma unroll
     for (int r = 0; r < RG; ++r) {
 #pragma unroll
         for (int j = 0; j < NT; ++j)
             *reinterpret_cast<f32x4 *>(s_red + ((size_t)(w * NT + j) * 64 + lane) * 4) = acc[r][j];
         __syncthreads();
-        for (int e = tid; e < NT * 256; e += kGemmWaves * kWave) {
-            float x[kGemmWaves];
+        for (int e = tid; e < NT * 256; e += W * kWave) {
+            float x[W];
 #pragma unroll
-            for (int q = 0; q < kGemmWaves; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
-            float sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
+            for (int q = 0; q < W; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
+            float sum;
+            if constexpr (W == 8) sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
+            else sum = (x[0] + x[2]) + (x[1] + x[3]);
             // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
             const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
             const int row = 16 * r + 4 * (l >> 4) + v;
@@ -196,7 +220,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
         // dims [16b, 16b+16) and [hd/2+16b, hd/2+16b+16) of one head (rotate-half partners);
         // with head_dim 16 one tile is a whole head.
         const int hd = p.hd, d = p.d, h2 = hd >> 1;
-        for (int idx = tid; idx < ROWS * COLS; idx += kGemmWaves * kWave) {
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
             const int row = idx / COLS, pc = idx % COLS;
             if (row >= m) continue;
             const int R = t0 * 16 + pc;  // packed row index
@@ -223,10 +247,10 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
                 const float c = p.rcos[(size_t)pos * h2 + j], s = p.rsin[(size_t)pos * h2 + j];
                 x = dim < h2 ? (x * c - y * s) : (x * c + y * s);
             }
-            const T e = to_elem<P>(x);
+            const T e = to_elem<P>(x);  // cached keys and values are rounded to the cache dtype
             const int col = head * hd + dim;
             if (sec == 0)
-                reinterpret_cast<T *>(p.Q)[(size_t)row * d + col] = e;
+                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(d), act_idx<P>(row, col, d), x);
             else if (sec == 1)
                 reinterpret_cast<T *>(p.Kc)[(size_t)pos * d + col] = e;
             else
@@ -237,7 +261,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
         // new rows (summed in column order) for the next RMSNorm.
         const int c0 = t0 * 16;
         float *s_sq = s_red;  // ROWS x COLS
-        for (int idx = tid; idx < ROWS * COLS; idx += kGemmWaves * kWave) {
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
             const int row = idx / COLS, c = idx % COLS;
             float v = 0.0f;
             if (row < m) {
@@ -245,7 +269,8 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
                 v = *xp + s_tile[row * (COLS + 1) + c];
                 *xp = v;
                 // operand of the next RMSNorm-ed product: x (.) g
-                reinterpret_cast<T *>(p.An)[(size_t)row * p.ldx + c0 + c] = to_elem<P>(v * p.gain[c0 + c]);
+                put_act<P>(reinterpret_cast<T *>(p.An), act_plane(p.ldx), act_idx<P>(row, c0 + c, p.ldx),
+                           v * p.gain[c0 + c]);
             }
             s_sq[idx] = v * v;
         }
@@ -262,16 +287,17 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_kernel(GemmParams p) 
     } else if constexpr (EP == E_SWIGLU) {
         // Tiles come in (gate, up) pairs of the same 16 features.
         static_assert(NT % 2 == 0, "gate/up epilogue pairs a gate tile with an up tile");
-        for (int idx = tid; idx < ROWS * COLS / 2; idx += kGemmWaves * kWave) {
+        for (int idx = tid; idx < ROWS * COLS / 2; idx += W * kWave) {
             const int row = idx / (COLS / 2), f = idx % (COLS / 2), q = f >> 4, c = f & 15;
             if (row >= m) continue;
             const float gt = s_tile[row * (COLS + 1) + 32 * q + c];
             const float up = s_tile[row * (COLS + 1) + 32 * q + 16 + c];
-            reinterpret_cast<T *>(p.H)[(size_t)row * p.Fp + wg * (COLS / 2) + f] = to_elem<P>(silu(gt) * up);
+            put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.Fp), act_idx<P>(row, wg * (COLS / 2) + f, p.Fp),
+                       silu(gt) * up);
         }
     } else {  // E_ARGMAX
         // One wave per row: (max, lowest column) over this workgroup's columns < V.
-        for (int row = w; row < ROWS; row += kGemmWaves) {
+        for (int row = w; row < ROWS; row += W) {
             if (row >= m) break;
             float bv = -INFINITY;
             int bi = 0x7fffffff;
@@ -309,6 +335,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
     constexpr int V16 = 16 / sizeof(T);  // elements per 16-byte vector
+    static_assert(V16 == PT::VEC, "an operand vector is one 16-byte load");
     const Ctl *ctl = p.ctl;
     const int m = ctl->m;
     const int row = blockIdx.x;
@@ -316,10 +343,10 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     const int tok = ctl->z[row];
     const T *e = reinterpret_cast<const T *>(p.E) + (size_t)tok * p.d;
     float *x = p.X + (size_t)row * p.d;
-    T *an = reinterpret_cast<T *>(p.An) + (size_t)row * p.d;
+    T *an = reinterpret_cast<T *>(p.An);
     for (int t = threadIdx.x; t < p.d / 16; t += blockDim.x) {  // one 16-column tile per thread
         alignas(16) T ev[16];
-        alignas(16) T av[16];
+        alignas(16) T av[PT::PLANES][16];
         alignas(16) float xv[16];
         alignas(16) float gv[16];
 #pragma unroll
@@ -332,14 +359,19 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
             xv[c] = from_elem<P>(ev[c]);
-            av[c] = to_elem<P>(xv[c] * gv[c]);
+            const float a = xv[c] * gv[c];
+            av[0][c] = to_elem<P>(a);
+            if constexpr (PT::PLANES == 2) av[PT::PLANES - 1][c] = to_elem<P>(a - from_elem<P>(av[0][c]));
             sum += xv[c] * xv[c];
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) *reinterpret_cast<f32x4 *>(x + 16 * t + 4 * q) = *reinterpret_cast<f32x4 *>(xv + 4 * q);
 #pragma unroll
-        for (int q = 0; q < 16 / V16; ++q)
-            *reinterpret_cast<u32x4 *>(an + 16 * t + q * V16) = *reinterpret_cast<u32x4 *>(av + q * V16);
+        for (int pl = 0; pl < PT::PLANES; ++pl)
+#pragma unroll
+            for (int q = 0; q < 16 / V16; ++q)  // V16 == VEC: one vector is contiguous in the packed layout
+                *reinterpret_cast<u32x4 *>(an + pl * act_plane(p.d) + act_idx<P>(row, 16 * t + q * V16, p.d)) =
+                    *reinterpret_cast<u32x4 *>(&av[pl][q * V16]);
         p.ssq[(size_t)row * (p.d / 16) + t] = sum;
     }
 }
@@ -348,7 +380,8 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
 // Block-causal attention, split over fixed 64-key chunks at absolute positions.
 // Workgroup (chunk c, head h), one wave per 16 query rows. With the cache K [pos][d] and the
 // transposed value cache Vt [d][pos]:
-//   S^T = K_chunk * Q^T   (MFMA A operand = key rows, B operand = query rows)
+//   S^T = K_chunk * Q^T   (MFMA A operand = key rows, B operand = query rows; bf16 queries as
+//                          hi and lo planes, one MFMA each)
 //   softmax over keys j <= L + i (fp32, base-2 exponent with the 1/sqrt(hd) scale folded in)
 //   O^T = Vt_chunk * P^T  (the lane's own S^T registers are the B operand; the V^T loads use
 //                          the same K-slot assignment)
@@ -377,11 +410,13 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     const T *Q = reinterpret_cast<const T *>(p.Q);
 
     // Every load of the workgroup is issued up front: Q rows, the chunk's 64 keys and values.
-    u32x4 qv[NKK], kv[4][NKK];
+    u32x4 qv[PT::PLANES][NKK], kv[4][NKK];
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
         const int dcol = h * HD + kk * PT::KSTEP + g * PT::VEC;
-        qv[kk] = *reinterpret_cast<const u32x4 *>(Q + (size_t)qrow * d + dcol);
+#pragma unroll
+        for (int pl = 0; pl < PT::PLANES; ++pl)
+            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(d) + act_idx<P>(qrow, dcol, d));
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
             kv[kt][kk] = *reinterpret_cast<const u32x4 *>(Kc + (size_t)(key0 + 16 * kt + r16) * d + dcol);
@@ -407,7 +442,9 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     for (int kt = 0; kt < 4; ++kt) {
         st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) st[kt] = mfma_kstep<P>(kv[kt][kk], qv[kk], st[kt]);
+        for (int pl = 0; pl < PT::PLANES; ++pl)
+#pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) st[kt] = mfma_kstep<P>(kv[kt][kk], qv[pl][kk], st[kt]);
     }
     // st[kt][v] = S^T[key0 + 16kt + 4g + v][qrow]
     float mx = -INFINITY;
@@ -427,8 +464,7 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            float pr = (mx == -INFINITY || st[kt][v] == -INFINITY) ? 0.0f : exp2f(st[kt][v] - mx);
-            if constexpr (P == Prec::BF16) pr = bf2f(f2bf(pr));  // the PV product consumes bf16
+            const float pr = (mx == -INFINITY || st[kt][v] == -INFINITY) ? 0.0f : exp2f(st[kt][v] - mx);
             st[kt][v] = pr;
             l += pr;
         }
@@ -442,12 +478,22 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
         if constexpr (P == Prec::BF16) {
 #pragma unroll
             for (int kp = 0; kp < 2; ++kp) {
+                // P = hi + lo with hi = bf16(P), lo = bf16(P - hi): two bf16 products carry P to
+                // ~2^-17 relative, so the probabilities are not rounded to bf16.
                 const f32x4 pa = st[2 * kp], pb = st[2 * kp + 1];
-                const u32x4 bop = u32x4{(uint32_t)f2bf(pa[0]) | ((uint32_t)f2bf(pa[1]) << 16),
-                                        (uint32_t)f2bf(pa[2]) | ((uint32_t)f2bf(pa[3]) << 16),
-                                        (uint32_t)f2bf(pb[0]) | ((uint32_t)f2bf(pb[1]) << 16),
-                                        (uint32_t)f2bf(pb[2]) | ((uint32_t)f2bf(pb[3]) << 16)};
-                o = mfma_kstep<P>(vv[dt][kp], bop, o);
+                const float pv[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+                uint32_t hi[8], lo[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    hi[q] = f2bf(pv[q]);
+                    lo[q] = f2bf(pv[q] - bf2f((uint16_t)hi[q]));
+                }
+                const u32x4 bhi = u32x4{hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16),
+                                        hi[6] | (hi[7] << 16)};
+                const u32x4 blo = u32x4{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16),
+                                        lo[6] | (lo[7] << 16)};
+                o = mfma_kstep<P>(vv[dt][kp], bhi, o);
+                o = mfma_kstep<P>(vv[dt][kp], blo, o);
             }
         } else {
             const T *vrow = Vt + (size_t)(h * HD + 16 * dt + r16) * p.ctx_alloc + key0;
@@ -513,7 +559,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
             for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
         }
         for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * kMaxRows) * p.hd + dim];
-        reinterpret_cast<T *>(p.O)[(size_t)row * p.d + h * p.hd + dim] = to_elem<P>(num / s_den);
+        put_act<P>(reinterpret_cast<T *>(p.O), act_plane(p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
     }
 }
 
@@ -696,16 +742,16 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
-template <Prec P, int NT, int RG, int EP, int D = kGemmDepth>
+template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves, bool KC = kGemmKContig>
 static hipError_t launch_gemm_t(const GemmParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    static_assert(kGemmWaves * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
-    const size_t lds = (size_t)(kGemmWaves * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
-    auto kern = gemm_kernel<P, NT, RG, EP, D>;
+    static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
+    const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
+    auto kern = gemm_kernel<P, NT, RG, EP, D, W, KC>;
     if (e0) {
-        hipExtLaunchKernelGGL(kern, dim3(p.n_wg), dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(kern, dim3(p.n_wg), dim3(W * kWave), lds, s, e0, e1, 0, p);
     } else {
-        hipLaunchKernelGGL(kern, dim3(p.n_wg), dim3(kGemmWaves * kWave), lds, s, p);
+        hipLaunchKernelGGL(kern, dim3(p.n_wg), dim3(W * kWave), lds, s, p);
     }
     return hipGetLastError();
 }

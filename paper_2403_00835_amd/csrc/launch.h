@@ -12,6 +12,7 @@ constexpr int kNtQkv = 4;     // QKV (pairs of rotate-half partner tiles)
 constexpr int kNtGateUp = 2;  // gate/up ((gate, up) tile pairs)
 constexpr int kNtResid = 1;   // O and down projections
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
+constexpr bool kGemmKContig = false;  // k-steps per wave: interleaved (false) or contiguous
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 

@@ -143,9 +143,10 @@ def main():
     mean_accept = tokens / iters
     wbytes = model.streamed_weight_bytes()
     d, F = cfg.d_model, cfg.ffn_dim
-    # gate/up launch: packed weights (2 * F_pad * d bf16) + operand rows read + H rows written
+    # gate/up launch: packed weights (2 * F_pad * d bf16) + operand rows read (hi and lo bf16
+    # planes, 4 bytes per value) + SwiGLU rows written (4 bytes per value) + row-factor partials
     f_pad = (F + 31) // 32 * 32
-    gu_bytes = 2 * f_pad * d * 2 + n * d * 2 + n * F * 2
+    gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * f_pad * 4 + n * (d // 16) * 4
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
     traffic = measured_traffic()

@@ -7,6 +7,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcllm.so")
+KERNEL_BENCH = os.path.join(HERE, "kernel_bench")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -40,6 +41,11 @@ def build(verbose=False):
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
+    # standalone GEMM driver (per-kernel timing, hardware byte counters): links the kernels object
+    kb_obj = os.path.join(objdir, "kernel_bench.hip.o")
+    _run([HIPCC, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "kernel_bench.hip"), "-o", kb_obj], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH, kb_obj, objs[0], "-o", KERNEL_BENCH + ".tmp"], verbose)
+    os.replace(KERNEL_BENCH + ".tmp", KERNEL_BENCH)
     from . import workload
     workload.build(verbose)
     return LIB

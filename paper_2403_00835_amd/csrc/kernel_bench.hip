@@ -1,0 +1,170 @@
+// kernel_bench: standalone driver of libcllm's weight-streaming GEMM kernels at the LLaMA-2-7B
+// shape (d 4096, FFN 11008, vocab 32000, head_dim 128, bf16) for one iteration of `rows` rows.
+//
+// Each product of an iteration (QKV, O, gate/up, down, LM head) is launched `iters` times through
+// the library's own launchers, in the library's launch configuration, over rotating copies of its
+// packed weights inside a 2 GiB buffer, so no launch finds its weights in the last-level cache.
+// A plain device copy of a known byte count runs first: it scales the hardware byte counters
+// (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE) to bytes. Weights and activations hold arbitrary
+// finite values: the timing and the traffic of these kernels do not depend on them.
+//
+// Usage: kernel_bench [rows (1..64, default 16)] [iters (default 20)]
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+
+#include "device.h"
+#include "launch.h"
+
+using namespace cllm;
+
+#define CK(x)                                                                                    \
+    do {                                                                                         \
+        hipError_t e_ = (x);                                                                     \
+        if (e_ != hipSuccess) {                                                                  \
+            std::fprintf(stderr, "kernel_bench: %s failed: %s\n", #x, hipGetErrorString(e_));   \
+            std::exit(1);                                                                        \
+        }                                                                                        \
+    } while (0)
+
+__global__ __launch_bounds__(256) void copy_known(const u32x4 *__restrict__ src, u32x4 *__restrict__ dst,
+                                                  size_t n16) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+namespace {
+
+constexpr int kD = 4096, kF = 11008, kV = 32000, kHd = 128, kCtx = 1024, kL = 512;
+constexpr int kFp = (kF + 31) / 32 * 32;
+constexpr size_t kWBytes = (size_t)2 << 30;
+
+template <typename T>
+T *dev(size_t count, int byte) {
+    T *p = nullptr;
+    CK(hipMalloc(&p, count * sizeof(T)));
+    CK(hipMemset(p, byte, count * sizeof(T)));
+    return p;
+}
+
+struct Shape {
+    const char *name;
+    GemmKind kind;
+    int nt;    // 16-column tiles per workgroup
+    int cols;  // packed output columns
+    int K;
+};
+
+}  // namespace
+
+int main(int argc, char **argv) {
+    const int rows = argc > 1 ? std::atoi(argv[1]) : 16;
+    const int iters = argc > 2 ? std::atoi(argv[2]) : 20;
+    if (rows < 1 || rows > kMaxRows || iters < 1) {
+        std::fprintf(stderr, "usage: kernel_bench [rows 1..%d] [iters >= 1]\n", kMaxRows);
+        return 2;
+    }
+    const int rg = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
+
+    uint8_t *W = dev<uint8_t>(kWBytes, 0x11);  // bf16 0x1111 in every weight
+    Ctl h{};
+    h.L = kL;
+    h.m = rows;
+    Ctl *ctl = dev<Ctl>(1, 0);
+    CK(hipMemcpy(ctl, &h, sizeof(Ctl), hipMemcpyHostToDevice));
+    // activation operands: two bf16 planes of kMaxRows rows (act_plane elements each)
+    void *A_d = dev<uint16_t>(2 * act_plane(kD), 0);
+    void *A_f = dev<uint16_t>(2 * act_plane(kFp), 0);
+    void *An = dev<uint16_t>(2 * act_plane(kD), 0);
+    void *Q = dev<uint16_t>(2 * act_plane(kD), 0);
+    void *H = dev<uint16_t>(2 * act_plane(kFp), 0);
+    void *Kc = dev<uint16_t>((size_t)kCtx * kD, 0);
+    void *Vt = dev<uint16_t>((size_t)kD * kCtx, 0);
+    float *ssq = dev<float>((size_t)(kD / 16) * kMaxRows, 0);
+    float *ssq_out = dev<float>((size_t)(kD / 16) * kMaxRows, 0);
+    float *X = dev<float>((size_t)kMaxRows * kD, 0);
+    float *gain = dev<float>(kD, 0);
+    float *rcos = dev<float>((size_t)kCtx * (kHd / 2), 0);
+    float *rsin = dev<float>((size_t)kCtx * (kHd / 2), 0);
+    const int n_wg_lm = (kV + 16 * kLmTiles - 1) / (16 * kLmTiles);
+    float *pmax = dev<float>((size_t)n_wg_lm * kMaxRows, 0);
+    int *pidx = dev<int>((size_t)n_wg_lm * kMaxRows, 0);
+
+    {  // 256 MiB copy: read 268435456 bytes, write 268435456 bytes, inside the weight buffer
+        const size_t bytes = (size_t)256 << 20;
+        hipLaunchKernelGGL(copy_known, dim3(4096), dim3(256), 0, 0, reinterpret_cast<const u32x4 *>(W),
+                           reinterpret_cast<u32x4 *>(W + ((size_t)1 << 30)), bytes / 16);
+        CK(hipGetLastError());
+        CK(hipDeviceSynchronize());
+        std::printf("copy_known: %zu bytes read, %zu bytes written\n", bytes, bytes);
+    }
+
+    const Shape shapes[] = {
+        {"qkv", GEMM_QKV, kNtQkv, 3 * kD, kD},
+        {"o", GEMM_O, kNtResid, kD, kD},
+        {"gate_up", GEMM_GATE_UP, kNtGateUp, 2 * kFp, kD},
+        {"down", GEMM_DOWN, kNtResid, kD, kFp},
+        {"lm_head", GEMM_LM, kLmTiles, n_wg_lm * 16 * kLmTiles, kD},
+    };
+    hipEvent_t e0, e1;
+    CK(hipEventCreate(&e0));
+    CK(hipEventCreate(&e1));
+    for (const Shape &s : shapes) {
+        GemmParams p{};
+        p.Ks = s.K / 32;
+        p.n_wg = s.cols / 16 / s.nt;
+        p.A = s.kind == GEMM_DOWN ? A_f : A_d;
+        p.lda = s.K;
+        p.ssq = ssq;
+        p.T = kD / 16;
+        p.K = kD;
+        p.eps = 1e-6f;
+        p.ctl = ctl;
+        p.Q = Q;
+        p.Kc = Kc;
+        p.Vt = Vt;
+        p.ctx_alloc = kCtx;
+        p.rcos = rcos;
+        p.rsin = rsin;
+        p.d = kD;
+        p.hd = kHd;
+        p.Xout = X;
+        p.ssq_out = ssq_out;
+        p.ldx = kD;
+        p.gain = gain;
+        p.An = An;
+        p.H = H;
+        p.Fp = kFp;
+        p.pmax = pmax;
+        p.pidx = pidx;
+        p.dbg = nullptr;
+        p.V = kV;
+        const size_t per = (size_t)p.n_wg * s.nt * p.Ks * kTileBytes;  // packed weight bytes per launch
+        const int copies = (int)(kWBytes / per);
+        if (copies < 2 || p.n_wg * s.nt * 16 != s.cols) {
+            std::fprintf(stderr, "kernel_bench: shape %s does not fit the buffers\n", s.name);
+            return 1;
+        }
+        for (int i = 0; i < 2; ++i) {  // warm-up
+            p.W = W + (size_t)(i % copies) * per;
+            CK(launch_gemm(s.kind, true, rg, p, 0, nullptr, nullptr));
+        }
+        CK(hipDeviceSynchronize());
+        CK(hipEventRecord(e0, 0));
+        for (int i = 0; i < iters; ++i) {
+            p.W = W + (size_t)((i + 2) % copies) * per;
+            CK(launch_gemm(s.kind, true, rg, p, 0, nullptr, nullptr));
+        }
+        CK(hipEventRecord(e1, 0));
+        CK(hipEventSynchronize(e1));
+        float ms = 0.0f;
+        CK(hipEventElapsedTime(&ms, e0, e1));
+        const double us = ms * 1e3 / iters;
+        std::printf("%-8s rows=%d NT=%d workgroups=%4d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s\n", s.name, rows,
+                    s.nt, p.n_wg, per, us, per / us / 1e3);
+    }
+    CK(hipDeviceSynchronize());
+    std::printf("done\n");
+    return 0;
+}

@@ -94,7 +94,10 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     const int m = ctl->m;
     if (m <= 0) return;
     const int L = ctl->L;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
+    // every load shares one per-lane offset
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wg = blockIdx.x;
     const int t0 = wg * NT;
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;

@@ -47,20 +47,26 @@ typedef enum cllm_status {
 #define CLLM_DTYPE_BF16 1
 
 /* Decoder shape. head_dim must be even; n_heads * head_dim == d_model.
- * dtype CLLM_DTYPE_BF16: bf16 weights, bf16 KV cache and bf16 matrix-product inputs with fp32
- * accumulation, fp32 residual stream and softmax. CLLM_DTYPE_F32: fp32 everywhere. */
+ * dtype CLLM_DTYPE_BF16: bf16 weights and a bf16 KV cache; every other value (residual stream,
+ * norm outputs, queries, attention probabilities, FFN hidden) keeps ~fp32 precision (matrix
+ * products take it as two bf16 planes, hi + lo) with fp32 accumulation and softmax.
+ * CLLM_DTYPE_F32: fp32 everywhere. */
 typedef struct cllm_config {
     int32_t n_layers, d_model, n_heads, head_dim, ffn_dim, vocab;
     float rms_eps, rope_base;
     int32_t dtype;
 } cllm_config;
 
-/* Capacity of a context. max_ctx bounds prompt + generated tokens + one block;
- * max_block (1..64) bounds the Jacobi block length n; max_new bounds tokens per decode. */
+/* Capacity of a context. max_ctx bounds prompt + generated tokens + one block, per sequence;
+ * max_block (1..64) bounds the Jacobi block length n; max_new bounds tokens per decode;
+ * max_batch (1..64; 0 means 1) is the number of sequence slots. Each slot is an independent
+ * sequence with its own KV cache and state; every call taking `seq` addresses slot seq in
+ * [0, max_batch). A batched iteration runs up to max_batch blocks of up to max_block rows. */
 typedef struct cllm_runtime_opts {
     int32_t max_ctx, max_block, max_new;
     int32_t device;  /* HIP device ordinal */
     void *stream;    /* hipStream_t or NULL */
+    int32_t max_batch;
 } cllm_runtime_opts;
 
 /* Guess provider of the decode (reading of the paper's random initial n-token sequence).
@@ -124,8 +130,8 @@ void cllm_model_free(cllm_ctx *ctx);
 
 /* Prefill (the algorithm's first forward): run the prompt through the decoder, fill the KV
  * cache of positions [0, len) and return the greedy first token y0 (the pending token).
- * Replaces any previous state of the sequence. seq must be 0 (one sequence per context).
- * Errors: ERR_ARG (len < 1, ids), ERR_CAPACITY (len + 1 > max_ctx), ERR_NUMERIC, ERR_DEVICE. */
+ * Replaces any previous state of sequence slot seq.
+ * Errors: ERR_ARG (seq, len < 1, ids), ERR_CAPACITY (len + 1 > max_ctx), ERR_NUMERIC, ERR_DEVICE. */
 cllm_status cllm_prefill(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t *first_token);
 
 /* One Jacobi iteration (eq. jacobi_decoding with the cache). block_in[0..m) holds the pending
@@ -153,12 +159,40 @@ cllm_status cllm_jacobi_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt
 cllm_status cllm_ar_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t max_new,
                            int32_t *out_tokens, cllm_decode_stats *stats);
 
-/* Debug: when enabled, every later cllm_jacobi_step (and the last chunk of cllm_prefill)
- * also copies the fp32 logits of its m rows into host_buf (row-major m x vocab; capacity
- * host_floats floats, at least max_block * vocab). Errors: ERR_ARG. */
+/* Batched Jacobi iteration (the batched ragged variant of the iteration): one forward pass over
+ * the blocks of B sequence slots at once, each against its own cache. Entry b is slot
+ * seq_ids[b] (distinct, prefilled) with block blocks_in[b * max_block + i], i < m[b]
+ * (1 <= m[b] <= max_block, blocks_in[b * max_block] == the slot's pending token). Outputs as
+ * cllm_jacobi_step, per entry: blocks_out[b * max_block + i] and accepted[b]. Every row is
+ * computed exactly as cllm_jacobi_step computes it: the results of a sequence do not depend
+ * on the other sequences of the batch. 1 <= B <= max_batch.
+ * Errors: those of cllm_jacobi_step (the state is unchanged on an argument error). */
+cllm_status cllm_jacobi_step_batch(cllm_ctx *ctx, int32_t B, const int32_t *seq_ids, const int32_t *blocks_in,
+                                   const int32_t *m, int32_t *blocks_out, int32_t *accepted);
+
+/* Batched Jacobi decoding: prefill B prompts (prompt b is prompts[off_b .. off_b + lens[b]),
+ * off_b = lens[0] + ... + lens[b-1]) into slots seq_ids[b], then decode max_new tokens for
+ * each in blocks of n, all sequences in one device-resident loop whose iterations run the
+ * blocks of every unfinished sequence together (sequences finish at different iterations).
+ * guesses: B specs (NULL = uniform guesses, shrink); a spec's draws use its slot id as `seq`.
+ * out_tokens: B x max_new (row b = sequence b). stats: B entries (may be NULL): steps and the
+ * accept histogram per sequence; prefill_ms and decode_ms are the batch's.
+ * Output b equals greedy AR decoding of prompt b.
+ * Errors: those of cllm_jacobi_decode, ERR_ARG (B, seq_ids). */
+cllm_status cllm_jacobi_decode_batch(cllm_ctx *ctx, int32_t B, const int32_t *seq_ids, const int32_t *prompts,
+                                     const int32_t *lens, int32_t n, int32_t max_new, const cllm_guess_spec *guesses,
+                                     int32_t *out_tokens, cllm_decode_stats *stats);
+
+/* Forget the state of a slot (it must be prefilled again). Errors: ERR_ARG. */
+cllm_status cllm_reset(cllm_ctx *ctx, int32_t seq);
+
+/* Debug: when enabled, every later cllm_jacobi_step / cllm_jacobi_step_batch (and the last
+ * chunk of cllm_prefill) also copies the fp32 logits of its rows into host_buf (row-major
+ * rows x vocab, batch entries' rows in order; capacity host_floats floats, at least
+ * max(64, max_batch * max_block) * vocab). Errors: ERR_ARG. */
 cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, size_t host_floats);
 
-/* Committed length L and pending token of a sequence. Errors: ERR_ARG, ERR_STATE. */
+/* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 
 /* Kernel timing for measurement: kernel_class selects one class of kernels (CLLM_KT_*

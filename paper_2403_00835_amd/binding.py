@@ -28,7 +28,8 @@ class cllm_config(ctypes.Structure):
 
 
 class cllm_runtime_opts(ctypes.Structure):
-    _fields_ = [("max_ctx", _i32), ("max_block", _i32), ("max_new", _i32), ("device", _i32), ("stream", _vp)]
+    _fields_ = [("max_ctx", _i32), ("max_block", _i32), ("max_new", _i32), ("device", _i32), ("stream", _vp),
+                ("max_batch", _i32)]
 
 
 class cllm_guess_spec(ctypes.Structure):
@@ -42,9 +43,9 @@ class cllm_decode_stats(ctypes.Structure):
 
 
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
-           "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_debug_logits", "cllm_seq_state",
-           "cllm_timing_enable", "cllm_timing_read", "cllm_streamed_weight_bytes", "cllm_status_string",
-           "cllm_last_error"]
+           "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
+           "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_seq_state", "cllm_timing_enable",
+           "cllm_timing_read", "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
 
@@ -67,6 +68,9 @@ def lib():
         L.cllm_jacobi_decode.argtypes = [_vp, _i32, _vp, _i32, _i32, _i32, P(cllm_guess_spec), _vp,
                                          P(cllm_decode_stats)]
         L.cllm_ar_decode.argtypes = [_vp, _i32, _vp, _i32, _i32, _vp, P(cllm_decode_stats)]
+        L.cllm_jacobi_step_batch.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _vp]
+        L.cllm_jacobi_decode_batch.argtypes = [_vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp]
+        L.cllm_reset.argtypes = [_vp, _i32]
         L.cllm_debug_logits.argtypes = [_vp, _i32, _vp, ctypes.c_size_t]
         L.cllm_seq_state.argtypes = [_vp, _i32, P(_i32), P(_i32)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32]
@@ -108,10 +112,12 @@ class Model:
     """One context of libcllm.so: model weights, KV cache and workspace on one GPU."""
 
     def __init__(self, cfg: ModelConfig, max_ctx, max_block=16, max_new=256, device=0, stream=None,
-                 weights=None, path=None):
+                 weights=None, path=None, max_batch=1):
         self.cfg = cfg
         self.L = lib()
-        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream)
+        self.max_block = max_block
+        self.max_batch = max_batch
+        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream, max_batch)
         h = _vp()
         if path is not None:
             st = self.L.cllm_model_load(os.fsencode(path), ctypes.byref(opts), ctypes.byref(h))
@@ -179,8 +185,53 @@ class Model:
         self._check(self.L.cllm_ar_decode(self.h, seq, _p(pr), pr.size, max_new, _p(out), ctypes.byref(st)))
         return out, _stats(st)
 
-    def debug_logits(self, enable, rows=64):
+    def jacobi_step_batch(self, seq_ids, blocks):
+        """One batched iteration: blocks[b] is the block of slot seq_ids[b]. Returns the list of
+        (block_out, accepted) per entry."""
+        B = len(seq_ids)
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int32)
+        zin = np.zeros((B, self.max_block), dtype=np.int32)
+        m = np.zeros(B, dtype=np.int32)
+        for b, blk in enumerate(blocks):
+            blk = np.asarray(blk, dtype=np.int32)
+            zin[b, :blk.size] = blk
+            m[b] = blk.size
+        out = np.zeros((B, self.max_block), dtype=np.int32)
+        acc = np.zeros(B, dtype=np.int32)
+        self._check(self.L.cllm_jacobi_step_batch(self.h, B, _p(ids), _p(zin), _p(m), _p(out), _p(acc)))
+        return [(out[b, :m[b]].copy(), int(acc[b])) for b in range(B)]
+
+    def jacobi_decode_batch(self, seq_ids, prompts, n, max_new, specs=None):
+        """Batched decode. specs: per entry dict(policy, block_policy, stream, p, seed) or None.
+        Returns (out [B, max_new], list of stats dicts)."""
+        B = len(seq_ids)
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int32)
+        lens = np.array([len(p) for p in prompts], dtype=np.int32)
+        cat = np.ascontiguousarray(np.concatenate([np.asarray(p, dtype=np.int32) for p in prompts]))
+        out = np.zeros((B, max_new), dtype=np.int32)
+        stats = (cllm_decode_stats * B)()
+        gs_arr, keep = None, []
+        if specs is not None:
+            gs_arr = (cllm_guess_spec * B)()
+            for b, sp in enumerate(specs):
+                st = sp.get("stream")
+                s_arr = None if st is None else np.ascontiguousarray(st, dtype=np.int32)
+                keep.append(s_arr)
+                gs_arr[b] = cllm_guess_spec(sp.get("policy", 0), sp.get("block_policy", 0),
+                                            None if s_arr is None else _p(s_arr),
+                                            0 if s_arr is None else s_arr.size, thr53(sp.get("p", 0.0)),
+                                            sp.get("seed", 0))
+        self._check(self.L.cllm_jacobi_decode_batch(self.h, B, _p(ids), _p(cat), _p(lens), n, max_new,
+                                                    None if gs_arr is None else ctypes.cast(gs_arr, _vp), _p(out),
+                                                    ctypes.cast(stats, _vp)))
+        return out, [_stats(stats[b]) for b in range(B)]
+
+    def reset(self, seq=0):
+        self._check(self.L.cllm_reset(self.h, seq))
+
+    def debug_logits(self, enable, rows=None):
         if enable:
+            rows = rows or max(64, -(-self.max_batch * self.max_block // 64) * 64)
             self._dbg = np.zeros((rows, self.cfg.vocab), dtype=np.float32)
             self._check(self.L.cllm_debug_logits(self.h, 1, _p(self._dbg), self._dbg.size))
         else:

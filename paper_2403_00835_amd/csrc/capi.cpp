@@ -2,6 +2,7 @@
 // device-resident decode loop and the C ABI of include/cllm.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -28,6 +29,9 @@ struct cllm_ctx {
     int nch = 0;        // attention chunks of ctx_alloc
     int ks_d = 0, ks_f = 0;
     int n_wg_qkv = 0, n_wg_o = 0, n_wg_gu = 0, n_wg_d = 0, n_wg_lm = 0;
+    int max_batch = 1;
+    int cap = 0;        // row capacity of one iteration (multiple of 64): activation buffer rows
+    size_t kv_seq = 0;  // KV cache elements per sequence slot
     int64_t streamed_bytes = 0;
 
     // weights
@@ -36,7 +40,7 @@ struct cllm_ctx {
     float *g_final = nullptr;
     std::vector<uint8_t *> w_qkv, w_o, w_gu, w_d;
     uint8_t *w_lm = nullptr;
-    // KV cache: K [layer][ctx_alloc][d], V transposed [layer][d][ctx_alloc]
+    // KV cache per slot: K [slot][layer][ctx_alloc][d], V transposed [slot][layer][d][ctx_alloc]
     void *kc = nullptr, *vt = nullptr;
     float *rcos = nullptr, *rsin = nullptr;
     // workspace
@@ -45,14 +49,21 @@ struct cllm_ctx {
     int *pidx = nullptr;
     void *Q = nullptr, *O = nullptr, *Hb = nullptr;
     void *An = nullptr;  // RMSNorm operand x (.) g of the next normed product
-    Ctl *ctl = nullptr;
-    int32_t *out_dev = nullptr, *stream_dev = nullptr;
+    Ctl *ctl = nullptr;  // one control block per slot
+    RowTab *tab = nullptr;
+    RowInfo *rows = nullptr;
+    int32_t *zin = nullptr;  // staging of host tokens (blocks, prefill chunks)
+    int zin_cap = 0;
+    int32_t *out_dev = nullptr, *stream_dev = nullptr;  // per slot: max_new outputs, stream_cap guesses
     int stream_cap = 0;
     std::vector<void *> allocs;
 
-    // host state
-    bool prefilled = false;
-    int L = 0, pending = 0;
+    // host state per slot
+    struct Slot {
+        bool prefilled = false;
+        int L = 0, pending = 0;
+    };
+    std::vector<Slot> slot;
     bool dead = false;
     std::string err;
     bool dbg_on = false;
@@ -92,6 +103,7 @@ cllm_status fail(cllm_ctx *c, cllm_status s, const char *fmt, ...) {
 
 inline int round_up(int x, int a) { return (x + a - 1) / a * a; }
 inline int rows_to_rg(int rows) { return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4); }
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 cllm_status dalloc(cllm_ctx *c, void **p, size_t bytes) {
     if (bytes == 0) bytes = 16;
@@ -189,19 +201,28 @@ cllm_status upload_packed(cllm_ctx *c, const void *host, int N, int K, int Ks, c
     return CLLM_OK;
 }
 
-// One iteration's launch sequence for up to `rows` rows (the device control block holds m).
-cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_lm, int32_t *out_dev,
-                              const int32_t *stream_dev) {
-    const int rg = rows_to_rg(rows);
+// Launch shape of one iteration: at most R rows in total, nseq batch entries, at most maxm rows
+// per entry, attention over nch chunks. The row table on the device holds the actual rows.
+struct IterShape {
+    int R, nseq, maxm, nch;
+    bool with_lm;
+    int lm_rt0;  // >= 0: the LM head runs only on this 64-row tile (a prefill chunk's last row)
+};
+
+cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev, const int32_t *stream_dev) {
+    const bool tiled = sh.R > kMaxRows;
+    const int rg = tiled ? 4 : rows_to_rg(sh.R);
+    const int row_tiles = tiled ? ceil_div(sh.R, kMaxRows) : 1;
     hipStream_t s = c->stream;
     hipEvent_t e0, e1;
+    const RowsRef rr{c->tab, c->rows, c->cap};
 
-    EmbedParams ep{c->embed, c->X, c->ssq, c->An, c->g_attn[0], c->d, c->ctl};
+    EmbedParams ep{c->embed, c->X, c->ssq, c->An, c->g_attn[0], c->d, rr};
     timing_events(c, CLLM_KT_EMBED, rg, &e0, &e1);
-    HIPCHK(c, launch_embed(c->bf16, 16 * rg, ep, s, e0, e1));
+    HIPCHK(c, launch_embed(c->bf16, sh.R, ep, s, e0, e1));
 
     GemmParams base{};
-    base.ctl = c->ctl;
+    base.rr = rr;
     base.ssq = c->ssq;
     base.T = c->d / 16;
     base.K = c->d;
@@ -209,6 +230,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
     base.d = c->d;
     base.hd = c->hd;
     base.ctx_alloc = c->ctx_alloc;
+    base.kv_seq = c->kv_seq;
     base.rcos = c->rcos;
     base.rsin = c->rsin;
     base.Xout = c->X;
@@ -218,9 +240,11 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
     base.Fp = c->Fp;
     base.V = c->V;
 
+    const int arg = std::min(4, ceil_div(std::max(sh.maxm, 1), 16));
     AttnParams ap{};
     ap.Q = c->Q;
     ap.O = c->O;
+    ap.kv_seq = c->kv_seq;
     ap.Opart = c->opart;
     ap.Mpart = c->mpart;
     ap.Lpart = c->lpart;
@@ -229,8 +253,10 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
     ap.n_heads = c->H;
     ap.nch = c->nch;
     ap.ctx_alloc = c->ctx_alloc;
+    ap.nrb = ceil_div(std::max(sh.maxm, 1), 16 * (arg == 3 ? 4 : arg));
     ap.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->hd));
-    ap.ctl = c->ctl;
+    ap.rr = rr;
+    const int attn_rg = arg == 3 ? 4 : arg;
 
     const size_t kv_layer = (size_t)c->ctx_alloc * c->d * c->elem;
     for (int l = 0; l < c->NL; ++l) {
@@ -247,14 +273,14 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         q.Kc = kc;
         q.Vt = vt;
         timing_events(c, CLLM_KT_GEMM_QKV, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_QKV, c->bf16, rg, q, s, e0, e1));
+        HIPCHK(c, launch_gemm(GEMM_QKV, c->bf16, rg, row_tiles, q, s, e0, e1));
 
         ap.Kc = kc;
         ap.Vt = vt;
         timing_events(c, CLLM_KT_ATTN, rg, &e0, &e1);
-        HIPCHK(c, launch_attn(c->bf16, rg, nch_launch, ap, s, e0, e1));
+        HIPCHK(c, launch_attn(c->bf16, attn_rg, sh.nch, sh.nseq, ap, s, e0, e1));
         timing_events(c, CLLM_KT_ATTN_COMBINE, rg, &e0, &e1);
-        HIPCHK(c, launch_attn_combine(c->bf16, 16 * rg, ap, s, e0, e1));
+        HIPCHK(c, launch_attn_combine(c->bf16, sh.R, ap, s, e0, e1));
 
         GemmParams o = base;  // X += O W_o^T; writes the FFN RMSNorm operand
         o.W = c->w_o[l];
@@ -264,7 +290,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         o.lda = c->d;
         o.gain = c->g_ffn[l];
         timing_events(c, CLLM_KT_GEMM_O, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_O, c->bf16, rg, o, s, e0, e1));
+        HIPCHK(c, launch_gemm(GEMM_O, c->bf16, rg, row_tiles, o, s, e0, e1));
 
         GemmParams gu = base;
         gu.W = c->w_gu[l];
@@ -274,7 +300,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         gu.lda = c->d;
         gu.H = c->Hb;
         timing_events(c, CLLM_KT_GEMM_GATE_UP, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_GATE_UP, c->bf16, rg, gu, s, e0, e1));
+        HIPCHK(c, launch_gemm(GEMM_GATE_UP, c->bf16, rg, row_tiles, gu, s, e0, e1));
 
         GemmParams dn = base;  // X += H W_d^T; writes the next layer's (or the final) RMSNorm operand
         dn.W = c->w_d[l];
@@ -284,17 +310,23 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         dn.lda = c->Fp;
         dn.gain = l + 1 < c->NL ? c->g_attn[l + 1] : c->g_final;
         timing_events(c, CLLM_KT_GEMM_DOWN, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, dn, s, e0, e1));
+        HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, row_tiles, dn, s, e0, e1));
     }
 
     ScanParams sp{};
     sp.ctl = c->ctl;
+    sp.tab = c->tab;
+    sp.rows = c->rows;
+    sp.cap = c->cap;
     sp.pmax = c->pmax;
     sp.pidx = c->pidx;
     sp.n_wg = c->n_wg_lm;
     sp.out = out_dev;
     sp.stream = stream_dev;
-    if (with_lm) {
+    sp.out_stride = c->opts.max_new;
+    sp.stream_stride = c->stream_cap;
+    sp.plan_inline = sh.nseq == 1;
+    if (sh.with_lm) {
         GemmParams lm = base;
         lm.W = c->w_lm;
         lm.Ks = c->ks_d;
@@ -304,31 +336,52 @@ cllm_status enqueue_iteration(cllm_ctx *c, int rows, int nch_launch, bool with_l
         lm.pmax = c->pmax;
         lm.pidx = c->pidx;
         lm.dbg = c->dbg_on ? c->dbg : nullptr;
+        int lm_tiles = row_tiles;
+        if (sh.lm_rt0 >= 0 && tiled) {
+            lm.rt0 = sh.lm_rt0;
+            lm_tiles = 1;
+        }
         timing_events(c, CLLM_KT_LM_HEAD, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, lm, s, e0, e1));
+        HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, lm_tiles, lm, s, e0, e1));
         sp.advance_only = 0;
     } else {
         sp.advance_only = 1;
     }
     timing_events(c, CLLM_KT_SCAN, rg, &e0, &e1);
-    HIPCHK(c, launch_scan(sp, s, e0, e1));
+    HIPCHK(c, launch_scan(sh.nseq, sp, s, e0, e1));
+    if (!sp.plan_inline) HIPCHK(c, launch_plan(PlanParams{c->ctl, c->tab, c->rows, c->cap}, s));
     return CLLM_OK;
 }
 
-cllm_status setup(cllm_ctx *c, int mode, int m, const int32_t *z, bool set_L, int L) {
+// Host edits for nseq batch entries: slot seq[b] gets mode and block size m[b]; its tokens are
+// copied from host zs + b * zstride. set_L (one entry: a prefill's first chunk) resets L to 0.
+cllm_status setup(cllm_ctx *c, int mode, int nseq, const int32_t *seq, const int32_t *m, const int32_t *zs, int zstride,
+                  bool set_L) {
     SetupParams sp{};
     sp.ctl = c->ctl;
+    sp.tab = c->tab;
+    sp.rows = c->rows;
+    sp.zin = c->zin;
+    sp.zstride = zstride;
+    sp.nseq = nseq;
     sp.mode = mode;
-    sp.m = m;
     sp.set_L = set_L ? 1 : 0;
-    sp.L = L;
-    for (int i = 0; i < m; ++i) sp.z[i] = z[i];
+    sp.L = 0;
+    size_t ntok = 0;
+    for (int b = 0; b < nseq; ++b) {
+        sp.seq[b] = seq[b];
+        sp.m[b] = m[b];
+        ntok = std::max(ntok, (size_t)b * zstride + m[b]);
+    }
+    if (ntok > (size_t)c->zin_cap) return fail(c, CLLM_ERR_CAPACITY, "token staging too small");
+    if (ntok) HIPCHK(c, hipMemcpyAsync(c->zin, zs, ntok * 4, hipMemcpyHostToDevice, c->stream));
     HIPCHK(c, launch_setup(sp, c->stream));
     return CLLM_OK;
 }
 
+// Read the control blocks of every slot (h: max_batch entries).
 cllm_status read_ctl(cllm_ctx *c, Ctl *h) {
-    HIPCHK(c, hipMemcpyAsync(h, c->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipMemcpyAsync(h, c->ctl, sizeof(Ctl) * c->max_batch, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
     if (c->kt_class >= 0) timing_collect(c);
     return CLLM_OK;
@@ -340,19 +393,214 @@ cllm_status check_ids(cllm_ctx *c, const int32_t *ids, int n) {
     return CLLM_OK;
 }
 
-cllm_status prefill_impl(cllm_ctx *c, const int32_t *prompt, int len, int nch_launch_extra) {
-    c->prefilled = false;
-    const int nchunks = (len + kMaxRows - 1) / kMaxRows;
+// Prefill of one slot in chunks of the row capacity; the LM head runs on the last chunk's last
+// row tile only.
+cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
+    c->slot[seq].prefilled = false;
+    const int chunk = c->cap;
+    const int nchunks = ceil_div(len, chunk);
     for (int k = 0; k < nchunks; ++k) {
-        const int start = k * kMaxRows;
-        const int rows = std::min(kMaxRows, len - start);
-        cllm_status st = setup(c, MODE_PREFILL, rows, prompt + start, k == 0, 0);
+        const int start = k * chunk;
+        const int rows = std::min(chunk, len - start);
+        cllm_status st = setup(c, MODE_PREFILL, 1, &seq, &rows, prompt + start, chunk, k == 0);
         if (st) return st;
-        const int nch = std::min(c->nch, (start + rows + kAttnChunk - 1) / kAttnChunk);
-        st = enqueue_iteration(c, rows, nch, k == nchunks - 1, nullptr, nullptr);
+        const bool last = k == nchunks - 1;
+        const IterShape sh{rows, 1, rows, std::min(c->nch, ceil_div(start + rows, kAttnChunk)), last,
+                           last ? (rows - 1) / kMaxRows : -1};
+        st = enqueue_iteration(c, sh, nullptr, nullptr);
         if (st) return st;
     }
-    (void)nch_launch_extra;
+    return CLLM_OK;
+}
+
+cllm_status check_ctx(cllm_ctx *c) {
+    if (c->dead) return fail(c, CLLM_ERR_DEVICE, "context unusable after a device error: %s", c->err.c_str());
+    return CLLM_OK;
+}
+
+cllm_status check_seq(cllm_ctx *c, int32_t seq) {
+    if (seq < 0 || seq >= c->max_batch) return fail(c, CLLM_ERR_ARG, "seq %d outside [0, %d)", seq, c->max_batch);
+    return CLLM_OK;
+}
+
+// One batched iteration over B entries (host-driven step): validate, run, read back.
+cllm_status step_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, const int32_t *blocks_in, int32_t zstride,
+                            const int32_t *m, int32_t *blocks_out, int32_t ostride, int32_t *accepted) {
+    if (B < 1 || B > c->max_batch) return fail(c, CLLM_ERR_ARG, "B=%d outside [1, max_batch]", B);
+    if (!seq_ids || !blocks_in || !m || !blocks_out || !accepted) return fail(c, CLLM_ERR_ARG, "NULL pointer");
+    std::vector<char> seen(c->max_batch, 0);
+    int R = 0, maxm = 0, nch = 1;
+    cllm_status s;
+    for (int b = 0; b < B; ++b) {
+        const int q = seq_ids[b];
+        if ((s = check_seq(c, q))) return s;
+        if (seen[q]) return fail(c, CLLM_ERR_ARG, "slot %d appears twice", q);
+        seen[q] = 1;
+        if (m[b] < 1 || m[b] > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "m=%d outside [1, max_block]", m[b]);
+        if (!c->slot[q].prefilled) return fail(c, CLLM_ERR_STATE, "jacobi step before prefill (slot %d)", q);
+        const int32_t *z = blocks_in + (size_t)b * zstride;
+        if ((s = check_ids(c, z, m[b]))) return s;
+        if (z[0] != c->slot[q].pending)
+            return fail(c, CLLM_ERR_STATE, "block_in[0]=%d is not the pending token %d (slot %d)", z[0],
+                        c->slot[q].pending, q);
+        if (c->slot[q].L + m[b] > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "L + m exceeds max_ctx");
+        R += m[b];
+        maxm = std::max(maxm, m[b]);
+        nch = std::max(nch, ceil_div(c->slot[q].L + m[b], kAttnChunk));
+    }
+    if ((s = setup(c, MODE_STEP, B, seq_ids, m, blocks_in, zstride, false))) return s;
+    const IterShape sh{R, B, maxm, nch, true, -1};
+    if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
+    std::vector<Ctl> h(c->max_batch);
+    if ((s = read_ctl(c, h.data()))) return s;
+    for (int b = 0; b < B; ++b)
+        if (h[seq_ids[b]].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
+    if (c->dbg_on && c->dbg_host)
+        HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)std::min(R, c->cap) * c->V * 4, hipMemcpyDeviceToHost));
+    for (int b = 0; b < B; ++b) {
+        const Ctl &ct = h[seq_ids[b]];
+        for (int i = 0; i < m[b]; ++i) blocks_out[(size_t)b * ostride + i] = ct.pred[i];
+        accepted[b] = ct.a_last;
+        c->slot[seq_ids[b]].L = ct.L;
+        c->slot[seq_ids[b]].pending = ct.pending;
+    }
+    return CLLM_OK;
+}
+
+// Prefill B prompts, then decode max_new tokens each in one device-resident loop.
+cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, const int32_t *prompts,
+                              const int32_t *lens, int32_t n, int32_t max_new, const cllm_guess_spec *guesses,
+                              int32_t *out_tokens, cllm_decode_stats *stats) {
+    if (B < 1 || B > c->max_batch) return fail(c, CLLM_ERR_ARG, "B=%d outside [1, max_batch]", B);
+    if (!seq_ids || !prompts || !lens || !out_tokens) return fail(c, CLLM_ERR_ARG, "NULL pointer");
+    if (n < 1 || n > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "n=%d outside [1, max_block]", n);
+    if (max_new < 1) return fail(c, CLLM_ERR_ARG, "max_new must be >= 1");
+    if (max_new > c->opts.max_new) return fail(c, CLLM_ERR_CAPACITY, "max_new exceeds the context's max_new");
+    cllm_status s;
+    std::vector<char> seen(c->max_batch, 0);
+    std::vector<cllm_guess_spec> gs(B);
+    std::vector<size_t> off(B + 1, 0);
+    int maxlen = 0;
+    for (int b = 0; b < B; ++b) {
+        const int q = seq_ids[b];
+        if ((s = check_seq(c, q))) return s;
+        if (seen[q]) return fail(c, CLLM_ERR_ARG, "slot %d appears twice", q);
+        seen[q] = 1;
+        if (lens[b] < 1) return fail(c, CLLM_ERR_ARG, "bad prompt length");
+        if (lens[b] + max_new + n > c->opts.max_ctx)
+            return fail(c, CLLM_ERR_CAPACITY, "len + max_new + n exceeds max_ctx");
+        off[b + 1] = off[b] + lens[b];
+        maxlen = std::max(maxlen, lens[b]);
+        if (guesses) gs[b] = guesses[b];
+        const cllm_guess_spec &g = gs[b];
+        if (g.policy < 0 || g.policy > 2 || g.block_policy < 0 || g.block_policy > 1)
+            return fail(c, CLLM_ERR_ARG, "bad guess policy");
+        if (g.policy != CLLM_GUESS_UNIFORM) {
+            if (!g.stream || g.stream_len < max_new) return fail(c, CLLM_ERR_ARG, "guess stream shorter than max_new");
+            if (g.thr53 > (1ull << 53)) return fail(c, CLLM_ERR_ARG, "thr53 above 2^53");
+        }
+    }
+    for (int b = 0; b < B; ++b) {
+        if ((s = check_ids(c, prompts + off[b], lens[b]))) return s;
+        if (gs[b].policy != CLLM_GUESS_UNIFORM && (s = check_ids(c, gs[b].stream, max_new))) return s;
+    }
+
+    hipEvent_t ev[3];
+    for (auto &e : ev) HIPCHK(c, hipEventCreate(&e));
+    struct EvGuard {
+        hipEvent_t *e;
+        ~EvGuard() {
+            for (int i = 0; i < 3; ++i) (void)hipEventDestroy(e[i]);
+        }
+    } guard{ev};
+
+    bool any_stream = false;
+    for (int b = 0; b < B; ++b)
+        if (gs[b].policy != CLLM_GUESS_UNIFORM) {
+            any_stream = true;
+            HIPCHK(c, hipMemcpyAsync(c->stream_dev + (size_t)seq_ids[b] * c->stream_cap, gs[b].stream,
+                                     (size_t)max_new * 4, hipMemcpyHostToDevice, c->stream));
+        }
+    HIPCHK(c, hipEventRecord(ev[0], c->stream));
+    for (int b = 0; b < B; ++b)
+        if ((s = prefill_impl(c, seq_ids[b], prompts + off[b], lens[b]))) return s;
+    HIPCHK(c, hipEventRecord(ev[1], c->stream));
+    // Decode parameters into the control blocks (the prefill left L and pending there).
+    std::vector<Ctl> h(c->max_batch);
+    if ((s = read_ctl(c, h.data()))) return s;
+    for (int b = 0; b < B; ++b) {
+        Ctl &ct = h[seq_ids[b]];
+        if (ct.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill (slot %d)", seq_ids[b]);
+        ct.n = n;
+        ct.max_new = max_new;
+        ct.policy = gs[b].policy;
+        ct.block_policy = gs[b].block_policy;
+        ct.seq = seq_ids[b];
+        ct.stream_len = gs[b].policy != CLLM_GUESS_UNIFORM ? max_new : 0;
+        ct.vocab = c->V;
+        ct.seed = gs[b].seed;
+        ct.thr53 = gs[b].thr53;
+    }
+    HIPCHK(c, hipMemcpyAsync(c->ctl, h.data(), sizeof(Ctl) * c->max_batch, hipMemcpyHostToDevice, c->stream));
+    // the batch entries into the row table, then the first blocks and their rows
+    std::vector<int32_t> zero_m(B, 0);
+    if ((s = setup(c, MODE_DECODE, B, seq_ids, zero_m.data(), nullptr, 0, false))) return s;
+    ScanParams sp{};
+    sp.ctl = c->ctl;
+    sp.tab = c->tab;
+    sp.stream = any_stream ? c->stream_dev : nullptr;
+    sp.stream_stride = c->stream_cap;
+    HIPCHK(c, launch_decode_init(B, sp, c->stream));
+    HIPCHK(c, launch_plan(PlanParams{c->ctl, c->tab, c->rows, c->cap}, c->stream));
+    const IterShape sh{B * n, B, n, std::min(c->nch, ceil_div(maxlen + max_new + n, kAttnChunk)), true, -1};
+    // Device-resident loop: every launch reads its rows from the row table. The host only
+    // queues iterations: as many as are certainly needed by the sequence with the most tokens
+    // left (each iteration fixes at most n tokens of a sequence), then reads the control blocks.
+    int64_t queued = 0;
+    while (true) {
+        int need = 0;
+        for (int b = 0; b < B; ++b) {
+            const Ctl &ct = h[seq_ids[b]];
+            const int left = ct.done ? 0 : max_new - (queued ? ct.e : 0);
+            need = std::max(need, ceil_div(left, n));
+        }
+        if (need == 0) break;
+        for (int i = 0; i < need; ++i)
+            if ((s = enqueue_iteration(c, sh, c->out_dev, any_stream ? c->stream_dev : nullptr))) return s;
+        queued += need;
+        HIPCHK(c, hipEventRecord(ev[2], c->stream));
+        if ((s = read_ctl(c, h.data()))) return s;
+        bool all_done = true;
+        for (int b = 0; b < B; ++b) {
+            const Ctl &ct = h[seq_ids[b]];
+            if (ct.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
+            all_done = all_done && ct.done;
+        }
+        if (all_done) break;
+        if (queued > (int64_t)max_new + 1) return fail(c, CLLM_ERR_STATE, "decode did not finish");
+    }
+    float pre_ms = 0.f, dec_ms = 0.f;
+    (void)hipEventElapsedTime(&pre_ms, ev[0], ev[1]);
+    (void)hipEventElapsedTime(&dec_ms, ev[1], ev[2]);
+    for (int b = 0; b < B; ++b) {
+        const int q = seq_ids[b];
+        HIPCHK(c, hipMemcpy(out_tokens + (size_t)b * max_new, c->out_dev + (size_t)q * c->opts.max_new,
+                            (size_t)max_new * 4, hipMemcpyDeviceToHost));
+        const Ctl &ct = h[q];
+        if (stats) {
+            cllm_decode_stats &st = stats[b];
+            memset(&st, 0, sizeof(st));
+            st.steps = ct.steps;
+            st.blocks = ct.blocks;
+            st.tokens = ct.e;
+            for (int i = 0; i <= kMaxBlock; ++i) st.accept_hist[i] = ct.hist[i];
+            st.prefill_ms = pre_ms;
+            st.decode_ms = dec_ms;
+        }
+        c->slot[q].prefilled = true;
+        c->slot[q].L = ct.L;
+        c->slot[q].pending = ct.pending;
+    }
     return CLLM_OK;
 }
 
@@ -403,7 +651,8 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
         cfg->ffn_dim < 1 || cfg->vocab < 2 || !(cfg->rms_eps >= 0.0f) || !(cfg->rope_base > 0.0f))
         return CLLM_ERR_ARG;
     if (opts->max_block < 1 || opts->max_block > kMaxBlock || opts->max_ctx < 2 ||
-        opts->max_ctx > kMaxChunks * kAttnChunk - 2 * kMaxRows || opts->max_new < 1)
+        opts->max_ctx > kMaxChunks * kAttnChunk - 2 * kMaxRows || opts->max_new < 1 || opts->max_batch < 0 ||
+        opts->max_batch > kMaxSeqs)
         return CLLM_ERR_ARG;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || opts->device < 0 || opts->device >= ndev) {
@@ -433,6 +682,11 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->n_wg_d = c->d / 16 / kNtResid;
     c->n_wg_lm = round_up(c->V, 16 * kLmTiles) / (16 * kLmTiles);
     c->stream = static_cast<hipStream_t>(opts->stream);
+    c->max_batch = opts->max_batch > 0 ? opts->max_batch : 1;
+    c->opts.max_batch = c->max_batch;
+    c->cap = round_up(std::max(kMaxRows, c->max_batch * opts->max_block), kMaxRows);
+    c->kv_seq = (size_t)c->NL * c->ctx_alloc * c->d;
+    c->slot.assign(c->max_batch, cllm_ctx::Slot{});
 
     auto bail = [&](cllm_status s) {
         cllm_model_free(c);
@@ -441,7 +695,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if (hipSetDevice(opts->device) != hipSuccess) return bail(CLLM_ERR_DEVICE);
     cllm_status s;
     const size_t E = c->elem;
-    const size_t rows = kMaxRows;
+    const size_t rows = c->cap;
     if ((s = dalloc(c, &c->embed, (size_t)c->V * c->d * E))) return bail(s);
     c->g_attn.assign(c->NL, nullptr);
     c->g_ffn.assign(c->NL, nullptr);
@@ -454,7 +708,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
         if ((s = dalloc_t(c, &c->g_ffn[l], c->d))) return bail(s);
     }
     if ((s = dalloc_t(c, &c->g_final, c->d))) return bail(s);
-    const size_t kv = (size_t)c->NL * c->ctx_alloc * c->d * E;
+    const size_t kv = c->kv_seq * c->max_batch * E;
     if ((s = dalloc(c, &c->kc, kv))) return bail(s);
     if ((s = dalloc(c, &c->vt, kv))) return bail(s);
     const int h2 = c->hd / 2;
@@ -463,20 +717,24 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->X, rows * c->d))) return bail(s);
     if ((s = dalloc_t(c, &c->ssq, (size_t)(c->d / 16) * rows))) return bail(s);
     // activation operands: one fp32 plane, or hi and lo bf16 planes (4 bytes per element either way)
-    if ((s = dalloc(c, &c->Q, act_plane(c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->O, act_plane(c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->An, act_plane(c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->Hb, act_plane(c->Fp) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->Q, act_plane(c->cap, c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->O, act_plane(c->cap, c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->An, act_plane(c->cap, c->d) * 4))) return bail(s);
+    if ((s = dalloc(c, &c->Hb, act_plane(c->cap, c->Fp) * 4))) return bail(s);
     if ((s = dalloc_t(c, &c->pmax, (size_t)c->n_wg_lm * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->pidx, (size_t)c->n_wg_lm * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->opart, (size_t)c->H * c->nch * rows * c->hd))) return bail(s);
     if ((s = dalloc_t(c, &c->mpart, (size_t)c->H * c->nch * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->lpart, (size_t)c->H * c->nch * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->dbg, rows * c->V))) return bail(s);
-    if ((s = dalloc_t(c, &c->ctl, 1))) return bail(s);
-    if ((s = dalloc_t(c, &c->out_dev, (size_t)opts->max_new))) return bail(s);
+    if ((s = dalloc_t(c, &c->ctl, (size_t)c->max_batch))) return bail(s);
+    if ((s = dalloc_t(c, &c->tab, 1))) return bail(s);
+    if ((s = dalloc_t(c, &c->rows, rows))) return bail(s);
+    c->zin_cap = std::max(c->cap, c->max_batch * opts->max_block);
+    if ((s = dalloc_t(c, &c->zin, (size_t)c->zin_cap))) return bail(s);
+    if ((s = dalloc_t(c, &c->out_dev, (size_t)opts->max_new * c->max_batch))) return bail(s);
     c->stream_cap = opts->max_new + kMaxBlock;
-    if ((s = dalloc_t(c, &c->stream_dev, (size_t)c->stream_cap))) return bail(s);
+    if ((s = dalloc_t(c, &c->stream_dev, (size_t)c->stream_cap * c->max_batch))) return bail(s);
 
     // RoPE table: angle t * base^(-2j/hd) in double, rounded once to fp32.
     std::vector<float> hc((size_t)c->ctx_alloc * h2), hs((size_t)c->ctx_alloc * h2);
@@ -568,7 +826,7 @@ cllm_status cllm_model_set_weights(cllm_ctx *c, const void *const *tensors, int3
     (void)hipFree(perm_dev);
     if (s) return s;
     if (e != hipSuccess) return fail(c, CLLM_ERR_DEVICE, "weight upload failed: %s", hipGetErrorString(e));
-    c->prefilled = false;
+    for (auto &q : c->slot) q = cllm_ctx::Slot{};
     return CLLM_OK;
 }
 
@@ -649,165 +907,86 @@ cllm_status cllm_model_load(const char *path, const cllm_runtime_opts *opts, cll
 
 cllm_status cllm_prefill(cllm_ctx *c, int32_t seq, const int32_t *prompt, int32_t len, int32_t *first_token) {
     if (!c) return CLLM_ERR_ARG;
-    if (c->dead) return fail(c, CLLM_ERR_DEVICE, "context unusable after a device error: %s", c->err.c_str());
-    if (seq != 0) return fail(c, CLLM_ERR_ARG, "seq must be 0");
+    cllm_status s;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
     if (!prompt || !first_token || len < 1) return fail(c, CLLM_ERR_ARG, "bad prompt");
     if (len + 1 > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "prompt of %d exceeds max_ctx", len);
-    cllm_status s;
     if ((s = check_ids(c, prompt, len))) return s;
-    if ((s = prefill_impl(c, prompt, len, 0))) return s;
-    Ctl h;
-    if ((s = read_ctl(c, &h))) return s;
-    if (h.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill");
-    if (c->dbg_on && c->dbg_host) {
-        const int rows = len - (len - 1) / kMaxRows * kMaxRows;
-        HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)rows * c->V * 4, hipMemcpyDeviceToHost));
+    if ((s = prefill_impl(c, seq, prompt, len))) return s;
+    std::vector<Ctl> h(c->max_batch);
+    if ((s = read_ctl(c, h.data()))) return s;
+    if (h[seq].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill");
+    if (c->dbg_on && c->dbg_host) {  // rows of the last chunk's last 64-row tile, at their chunk rows
+        const int last = (len - 1) % c->cap;
+        const int r0 = last / kMaxRows * kMaxRows;
+        HIPCHK(c, hipMemcpy(c->dbg_host + (size_t)r0 * c->V, c->dbg + (size_t)r0 * c->V,
+                            (size_t)(last + 1 - r0) * c->V * 4, hipMemcpyDeviceToHost));
     }
-    c->prefilled = true;
-    c->L = h.L;
-    c->pending = h.pending;
-    *first_token = h.pending;
+    c->slot[seq].prefilled = true;
+    c->slot[seq].L = h[seq].L;
+    c->slot[seq].pending = h[seq].pending;
+    *first_token = h[seq].pending;
     return CLLM_OK;
 }
 
 cllm_status cllm_jacobi_step(cllm_ctx *c, int32_t seq, const int32_t *block_in, int32_t m, int32_t *block_out,
                              int32_t *accepted_len) {
     if (!c) return CLLM_ERR_ARG;
-    if (c->dead) return fail(c, CLLM_ERR_DEVICE, "context unusable after a device error: %s", c->err.c_str());
-    if (seq != 0) return fail(c, CLLM_ERR_ARG, "seq must be 0");
-    if (!block_in || !block_out || !accepted_len) return fail(c, CLLM_ERR_ARG, "NULL pointer");
-    if (m < 1 || m > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "m=%d outside [1, max_block]", m);
-    if (!c->prefilled) return fail(c, CLLM_ERR_STATE, "jacobi_step before prefill");
     cllm_status s;
-    if ((s = check_ids(c, block_in, m))) return s;
-    if (block_in[0] != c->pending)
-        return fail(c, CLLM_ERR_STATE, "block_in[0]=%d is not the pending token %d", block_in[0], c->pending);
-    if (c->L + m > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "L + m exceeds max_ctx");
-    if ((s = setup(c, MODE_STEP, m, block_in, false, 0))) return s;
-    const int nch = (c->L + m + kAttnChunk - 1) / kAttnChunk;
-    if ((s = enqueue_iteration(c, m, nch, true, nullptr, nullptr))) return s;
-    Ctl h;
-    if ((s = read_ctl(c, &h))) return s;
-    if (h.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit");
-    if (c->dbg_on && c->dbg_host) HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)m * c->V * 4, hipMemcpyDeviceToHost));
-    for (int i = 0; i < m; ++i) block_out[i] = h.pred[i];
-    *accepted_len = h.a_last;
-    c->L = h.L;
-    c->pending = h.pending;
-    return CLLM_OK;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
+    return step_batch_impl(c, 1, &seq, block_in, m, &m, block_out, m, accepted_len);
 }
 
-static cllm_status decode_impl(cllm_ctx *c, const int32_t *prompt, int32_t len, int32_t n, int32_t max_new,
-                               const cllm_guess_spec *g, int32_t *out_tokens, cllm_decode_stats *stats) {
-    if (!prompt || !out_tokens || len < 1) return fail(c, CLLM_ERR_ARG, "bad prompt or output");
-    if (n < 1 || n > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "n=%d outside [1, max_block]", n);
-    if (max_new < 1) return fail(c, CLLM_ERR_ARG, "max_new must be >= 1");
-    if (max_new > c->opts.max_new) return fail(c, CLLM_ERR_CAPACITY, "max_new exceeds the context's max_new");
-    if (len + max_new + n > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "len + max_new + n exceeds max_ctx");
-    cllm_guess_spec gs{};
-    if (g) gs = *g;
-    if (gs.policy < 0 || gs.policy > 2 || gs.block_policy < 0 || gs.block_policy > 1)
-        return fail(c, CLLM_ERR_ARG, "bad guess policy");
-    if (gs.policy != CLLM_GUESS_UNIFORM) {
-        if (!gs.stream || gs.stream_len < max_new) return fail(c, CLLM_ERR_ARG, "guess stream shorter than max_new");
-        if (gs.thr53 > (1ull << 53)) return fail(c, CLLM_ERR_ARG, "thr53 above 2^53");
-    }
+cllm_status cllm_jacobi_step_batch(cllm_ctx *c, int32_t B, const int32_t *seq_ids, const int32_t *blocks_in,
+                                   const int32_t *m, int32_t *blocks_out, int32_t *accepted) {
+    if (!c) return CLLM_ERR_ARG;
     cllm_status s;
-    if ((s = check_ids(c, prompt, len))) return s;
-    if (gs.policy != CLLM_GUESS_UNIFORM && (s = check_ids(c, gs.stream, max_new))) return s;
-
-    hipEvent_t ev[3];
-    for (auto &e : ev) HIPCHK(c, hipEventCreate(&e));
-    struct EvGuard {
-        hipEvent_t *e;
-        ~EvGuard() {
-            for (int i = 0; i < 3; ++i) (void)hipEventDestroy(e[i]);
-        }
-    } guard{ev};
-
-    if (gs.policy != CLLM_GUESS_UNIFORM)
-        HIPCHK(c, hipMemcpyAsync(c->stream_dev, gs.stream, (size_t)max_new * 4, hipMemcpyHostToDevice, c->stream));
-    HIPCHK(c, hipEventRecord(ev[0], c->stream));
-    if ((s = prefill_impl(c, prompt, len, 0))) return s;
-    HIPCHK(c, hipEventRecord(ev[1], c->stream));
-    // Decode parameters into the control block (the prefill left L and pending there).
-    Ctl h;
-    if ((s = read_ctl(c, &h))) return s;
-    if (h.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill");
-    h.n = n;
-    h.max_new = max_new;
-    h.policy = gs.policy;
-    h.block_policy = gs.block_policy;
-    h.seq = 0;
-    h.stream_len = gs.policy != CLLM_GUESS_UNIFORM ? max_new : 0;
-    h.vocab = c->V;
-    h.seed = gs.seed;
-    h.thr53 = gs.thr53;
-    HIPCHK(c, hipMemcpyAsync(c->ctl, &h, sizeof(Ctl), hipMemcpyHostToDevice, c->stream));
-    ScanParams sp{};
-    sp.ctl = c->ctl;
-    sp.stream = gs.policy != CLLM_GUESS_UNIFORM ? c->stream_dev : nullptr;
-    HIPCHK(c, launch_decode_init(sp, c->stream));
-    const int nch = std::min(c->nch, (len + max_new + n + kAttnChunk - 1) / kAttnChunk);
-    // Device-resident loop: every launch reads its block from the control block. The host only
-    // queues iterations; it queues as many as are certainly needed (each iteration fixes at most
-    // n tokens) and then reads the emitted count once.
-    int emitted = 0;
-    int64_t guard_iters = 0;
-    while (true) {
-        const int need = (max_new - emitted + n - 1) / n;
-        for (int i = 0; i < need; ++i)
-            if ((s = enqueue_iteration(c, n, nch, true, c->out_dev,
-                                       gs.policy != CLLM_GUESS_UNIFORM ? c->stream_dev : nullptr)))
-                return s;
-        guard_iters += need;
-        HIPCHK(c, hipEventRecord(ev[2], c->stream));
-        if ((s = read_ctl(c, &h))) return s;
-        if (h.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit");
-        emitted = h.e;
-        if (h.done) break;
-        if (guard_iters > (int64_t)max_new + 1) return fail(c, CLLM_ERR_STATE, "decode did not finish");
-    }
-    HIPCHK(c, hipMemcpy(out_tokens, c->out_dev, (size_t)max_new * 4, hipMemcpyDeviceToHost));
-    if (stats) {
-        memset(stats, 0, sizeof(*stats));
-        stats->steps = h.steps;
-        stats->blocks = h.blocks;
-        stats->tokens = h.e;
-        for (int i = 0; i <= kMaxBlock; ++i) stats->accept_hist[i] = h.hist[i];
-        float ms = 0.f;
-        if (hipEventElapsedTime(&ms, ev[0], ev[1]) == hipSuccess) stats->prefill_ms = ms;
-        if (hipEventElapsedTime(&ms, ev[1], ev[2]) == hipSuccess) stats->decode_ms = ms;
-    }
-    c->prefilled = true;
-    c->L = h.L;
-    c->pending = h.pending;
-    return CLLM_OK;
+    if ((s = check_ctx(c))) return s;
+    return step_batch_impl(c, B, seq_ids, blocks_in, c->opts.max_block, m, blocks_out, c->opts.max_block, accepted);
 }
 
 cllm_status cllm_jacobi_decode(cllm_ctx *c, int32_t seq, const int32_t *prompt, int32_t len, int32_t n,
                                int32_t max_new, const cllm_guess_spec *guess, int32_t *out_tokens,
                                cllm_decode_stats *stats) {
     if (!c) return CLLM_ERR_ARG;
-    if (c->dead) return fail(c, CLLM_ERR_DEVICE, "context unusable after a device error: %s", c->err.c_str());
-    if (seq != 0) return fail(c, CLLM_ERR_ARG, "seq must be 0");
-    return decode_impl(c, prompt, len, n, max_new, guess, out_tokens, stats);
+    cllm_status s;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
+    if (!prompt || !out_tokens || len < 1) return fail(c, CLLM_ERR_ARG, "bad prompt or output");
+    return decode_batch_impl(c, 1, &seq, prompt, &len, n, max_new, guess, out_tokens, stats);
 }
 
 cllm_status cllm_ar_decode(cllm_ctx *c, int32_t seq, const int32_t *prompt, int32_t len, int32_t max_new,
                            int32_t *out_tokens, cllm_decode_stats *stats) {
     if (!c) return CLLM_ERR_ARG;
-    if (c->dead) return fail(c, CLLM_ERR_DEVICE, "context unusable after a device error: %s", c->err.c_str());
-    if (seq != 0) return fail(c, CLLM_ERR_ARG, "seq must be 0");
+    cllm_status s;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
+    if (!prompt || !out_tokens || len < 1) return fail(c, CLLM_ERR_ARG, "bad prompt or output");
     cllm_guess_spec g{};
-    return decode_impl(c, prompt, len, 1, max_new, &g, out_tokens, stats);
+    return decode_batch_impl(c, 1, &seq, prompt, &len, 1, max_new, &g, out_tokens, stats);
+}
+
+cllm_status cllm_jacobi_decode_batch(cllm_ctx *c, int32_t B, const int32_t *seq_ids, const int32_t *prompts,
+                                     const int32_t *lens, int32_t n, int32_t max_new, const cllm_guess_spec *guesses,
+                                     int32_t *out_tokens, cllm_decode_stats *stats) {
+    if (!c) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c))) return s;
+    return decode_batch_impl(c, B, seq_ids, prompts, lens, n, max_new, guesses, out_tokens, stats);
+}
+
+cllm_status cllm_reset(cllm_ctx *c, int32_t seq) {
+    if (!c) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_seq(c, seq))) return s;
+    c->slot[seq] = cllm_ctx::Slot{};
+    return CLLM_OK;
 }
 
 cllm_status cllm_debug_logits(cllm_ctx *c, int32_t enable, float *host_buf, size_t host_floats) {
     if (!c) return CLLM_ERR_ARG;
     if (enable) {
-        if (!host_buf || host_floats < (size_t)std::max(c->opts.max_block, kMaxRows) * c->V)
-            return fail(c, CLLM_ERR_ARG, "debug buffer needs %zu floats", (size_t)std::max(c->opts.max_block, kMaxRows) * c->V);
+        if (!host_buf || host_floats < (size_t)c->cap * c->V)
+            return fail(c, CLLM_ERR_ARG, "debug buffer needs %zu floats", (size_t)c->cap * c->V);
         c->dbg_on = true;
         c->dbg_host = host_buf;
         c->dbg_cap = host_floats;
@@ -820,10 +999,10 @@ cllm_status cllm_debug_logits(cllm_ctx *c, int32_t enable, float *host_buf, size
 }
 
 cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_len, int32_t *pending) {
-    if (!c || seq != 0 || !committed_len || !pending) return CLLM_ERR_ARG;
-    if (!c->prefilled) return CLLM_ERR_STATE;
-    *committed_len = c->L;
-    *pending = c->pending;
+    if (!c || seq < 0 || seq >= c->max_batch || !committed_len || !pending) return CLLM_ERR_ARG;
+    if (!c->slot[seq].prefilled) return CLLM_ERR_STATE;
+    *committed_len = c->slot[seq].L;
+    *pending = c->slot[seq].pending;
     return CLLM_OK;
 }
 

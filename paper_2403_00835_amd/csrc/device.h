@@ -12,7 +12,8 @@ typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
 constexpr int kWave = 64;
 constexpr int kMaxBlock = 64;      // largest Jacobi block (rows per iteration)
-constexpr int kMaxRows = 64;       // rows of the activation buffers (block or prefill chunk)
+constexpr int kMaxRows = 64;       // rows of one GEMM row tile; activation buffers hold a multiple
+constexpr int kMaxSeqs = 64;       // sequences of one batched iteration
 constexpr int kGemmWaves = 8;      // waves per GEMM workgroup; they split K
 constexpr int kAttnChunk = 64;     // keys per attention workgroup, at absolute positions
 constexpr int kMaxChunks = 1024;   // attention chunks per sequence: context <= 65536
@@ -58,9 +59,9 @@ template <> __device__ __forceinline__ float from_elem<Prec::F32>(float x) { ret
 // Activation operands (the A side of every product, and the attention queries) are stored in the
 // MFMA operand order: for 16-row group rg and k-step s, the 64 lanes' 16-byte vectors are
 // contiguous (1 KiB), lane = 16 * (k-group within the k-step) + row % 16. A k-step load is one
-// contiguous KiB per row group. Each plane holds kMaxRows rows of K elements; the lo plane of a
-// bf16 operand follows the hi plane.
-__host__ __device__ constexpr size_t act_plane(int K) { return (size_t)kMaxRows * (size_t)K; }
+// contiguous KiB per row group. Each plane holds `rows` rows (the context's row capacity) of K
+// elements; the lo plane of a bf16 operand follows the hi plane.
+__host__ __device__ constexpr size_t act_plane(int rows, int K) { return (size_t)rows * (size_t)K; }
 
 template <Prec P>
 __device__ __forceinline__ size_t act_idx(int row, int k, int K) {
@@ -102,6 +103,27 @@ enum StepMode : int32_t {
     MODE_STEP = 0,     // one host-driven iteration: commit a, keep the predictions for the host
     MODE_DECODE = 1,   // device-resident decode: commit, emit, build the next block
     MODE_PREFILL = 2,  // prompt chunk: every row is committed; the last row's argmax is pending
+};
+
+// Row table of one iteration. The block rows of every participating sequence are packed in
+// batch order: batch entry b (sequence slot seq[b]) owns rows [r0[b], r0[b] + m[b]), at absolute
+// positions L[b] .. L[b] + m[b] - 1. Written on the device before each iteration (setup, scan
+// and plan kernels); every kernel of the iteration reads it, so one launch sequence serves any
+// block sizes.
+struct RowTab {
+    int32_t R;     // rows of the iteration
+    int32_t nseq;  // batch entries
+    int32_t pad[2];
+    int32_t seq[kMaxSeqs];
+    int32_t r0[kMaxSeqs];
+    int32_t m[kMaxSeqs];
+    int32_t L[kMaxSeqs];
+};
+struct RowInfo {
+    int32_t b;    // batch entry
+    int32_t pos;  // absolute position
+    int32_t tok;  // token
+    int32_t i;    // index within the entry's block
 };
 
 // Per-sequence control block, resident on the device. Every kernel of an iteration reads the

@@ -68,17 +68,24 @@ int main(int argc, char **argv) {
     const int rg = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
 
     uint8_t *W = dev<uint8_t>(kWBytes, 0x11);  // bf16 0x1111 in every weight
-    Ctl h{};
-    h.L = kL;
-    h.m = rows;
-    Ctl *ctl = dev<Ctl>(1, 0);
-    CK(hipMemcpy(ctl, &h, sizeof(Ctl), hipMemcpyHostToDevice));
+    // one sequence (slot 0) with a block of `rows` rows at positions kL ..
+    RowTab th{};
+    th.R = rows;
+    th.nseq = 1;
+    th.m[0] = rows;
+    th.L[0] = kL;
+    RowTab *tab = dev<RowTab>(1, 0);
+    CK(hipMemcpy(tab, &th, sizeof(RowTab), hipMemcpyHostToDevice));
+    RowInfo rh[kMaxRows];
+    for (int i = 0; i < kMaxRows; ++i) rh[i] = RowInfo{0, kL + i, 0, i};
+    RowInfo *rinfo = dev<RowInfo>(kMaxRows, 0);
+    CK(hipMemcpy(rinfo, rh, sizeof(rh), hipMemcpyHostToDevice));
     // activation operands: two bf16 planes of kMaxRows rows (act_plane elements each)
-    void *A_d = dev<uint16_t>(2 * act_plane(kD), 0);
-    void *A_f = dev<uint16_t>(2 * act_plane(kFp), 0);
-    void *An = dev<uint16_t>(2 * act_plane(kD), 0);
-    void *Q = dev<uint16_t>(2 * act_plane(kD), 0);
-    void *H = dev<uint16_t>(2 * act_plane(kFp), 0);
+    void *A_d = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
+    void *A_f = dev<uint16_t>(2 * act_plane(kMaxRows, kFp), 0);
+    void *An = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
+    void *Q = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
+    void *H = dev<uint16_t>(2 * act_plane(kMaxRows, kFp), 0);
     void *Kc = dev<uint16_t>((size_t)kCtx * kD, 0);
     void *Vt = dev<uint16_t>((size_t)kD * kCtx, 0);
     float *ssq = dev<float>((size_t)(kD / 16) * kMaxRows, 0);
@@ -120,7 +127,7 @@ int main(int argc, char **argv) {
         p.T = kD / 16;
         p.K = kD;
         p.eps = 1e-6f;
-        p.ctl = ctl;
+        p.rr = RowsRef{tab, rinfo, kMaxRows};
         p.Q = Q;
         p.Kc = Kc;
         p.Vt = Vt;
@@ -148,13 +155,13 @@ int main(int argc, char **argv) {
         }
         for (int i = 0; i < 2; ++i) {  // warm-up
             p.W = W + (size_t)(i % copies) * per;
-            CK(launch_gemm(s.kind, true, rg, p, 0, nullptr, nullptr));
+            CK(launch_gemm(s.kind, true, rg, 1, p, 0, nullptr, nullptr));
         }
         CK(hipDeviceSynchronize());
         CK(hipEventRecord(e0, 0));
         for (int i = 0; i < iters; ++i) {
             p.W = W + (size_t)((i + 2) % copies) * per;
-            CK(launch_gemm(s.kind, true, rg, p, 0, nullptr, nullptr));
+            CK(launch_gemm(s.kind, true, rg, 1, p, 0, nullptr, nullptr));
         }
         CK(hipEventRecord(e1, 0));
         CK(hipEventSynchronize(e1));

@@ -7,12 +7,14 @@
 //                       -> O GEMM (+residual) -> gate/up GEMM (+RMSNorm prologue, +SwiGLU)
 //                       -> down GEMM (+residual)]
 //   -> LM-head GEMM (+RMSNorm prologue, +argmax partials) -> scan/commit.
-// Every kernel reads m and L from the device control block, so the same sequence serves every
-// iteration without host round trips.
+// A batched iteration runs the blocks of several sequences at once (their rows packed one after
+// another). Every kernel reads the rows, their sequences and positions from the device row
+// table, so the same launch sequence serves every iteration without host round trips.
 //
 // Determinism: every reduction has a fixed order that depends only on the model shape, never on
-// m, so a row's results do not depend on how many rows are in the block. Hence greedy decoding
-// with blocks of one token (AR) and Jacobi decoding produce bit-identical tokens.
+// the number of rows or their packing, so a row's results do not depend on how many rows (or
+// which other sequences) share the iteration. Hence greedy decoding with blocks of one token
+// (AR), Jacobi decoding and batched Jacobi decoding produce bit-identical tokens.
 #include <hip/hip_ext.h>
 
 #include "device.h"
@@ -51,7 +53,7 @@ struct Stage {  // operands of one k-step
 // Loads of one k-step s (callers clamp s into [0, Ks), so every load is issued and the compiler
 // can count outstanding loads exactly).
 template <Prec P, int NT, int RG>
-__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int s, int lane) {
+__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int rg0, int s, int lane) {
     using PT = PrecT<P>;
     using T = typename PT::T;
 #pragma unroll
@@ -66,8 +68,8 @@ __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams
     for (int pl = 0; pl < PT::PLANES; ++pl)
 #pragma unroll
         for (int r = 0; r < RG; ++r)
-            st.a[pl][r] = *reinterpret_cast<const u32x4 *>(A + pl * act_plane(p.lda) +
-                                                          ((size_t)(r * ks_a + s) * kWave + lane) * PT::VEC);
+            st.a[pl][r] = *reinterpret_cast<const u32x4 *>(A + pl * act_plane(p.rr.cap, p.lda) +
+                                                          ((size_t)((rg0 + r) * ks_a + s) * kWave + lane) * PT::VEC);
 }
 
 // MFMAs of one k-step: every hi-plane product, then every lo-plane product (bf16).
@@ -90,17 +92,18 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
-    const Ctl *ctl = p.ctl;
-    const int m = ctl->m;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration; m of them are live.
+    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    const int m = p.rr.tab->R - row0;
     if (m <= 0) return;
-    const int L = ctl->L;
+    const int rg0 = row0 >> 4;
     const int tid = threadIdx.x, lane = tid & 63;
     // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
     // every load shares one per-lane offset
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wg = blockIdx.x;
     const int t0 = wg * NT;
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
 
     extern __shared__ float smem[];
     float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
@@ -117,7 +120,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
     f32x4 sq_pre[2];
     if constexpr (ROWSCALE) {
-        const float *src = p.ssq + (size_t)(tid >> 5) * p.T;
+        const float *src = p.ssq + (size_t)(row0 + (tid >> 5)) * p.T;
 #pragma unroll
         for (int i = 0; i < 2; ++i)  // clamped, unconditional
             sq_pre[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + 4 * i, p.T - 4));
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     auto step_of = [&](int q) { return min(KC ? w * nper + q : w + q * W, p.Ks - 1); };
     Stage<P, NT, RG> ring[D];
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, step_of(j), lane);
+    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, rg0, step_of(j), lane);
 
     f32x4 acc[RG][NT];
 #pragma unroll
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
 #pragma unroll
             for (int j = 0; j < D; ++j) {
                 // sched_barrier keeps the scheduler from sinking loads to their uses.
-                gemm_load(ring[(j + D - 1) % D], p, t0, step_of(bi * D + j + D - 1), lane);
+                gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
                 __builtin_amdgcn_sched_barrier(0);
                 gemm_compute(ring[j], acc);
                 __builtin_amdgcn_sched_barrier(0);
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
         for (int j = 0; j < 2 * D - 1; ++j) {
             const int v = v0 + j;
             if (v < nmy) {
-                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, step_of(v + D - 1), lane);
+                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
                 gemm_compute(ring[j % D], acc);
             }
         }
@@ -170,7 +173,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
         // rows. The barrier of the reduction below publishes s_inv.
         for (int pass = 0; pass < ROWS / RPP; ++pass) {
             const int row = pass * RPP + (tid >> 5);
-            const float *src = p.ssq + (size_t)row * p.T;
+            const float *src = p.ssq + (size_t)(row0 + row) * p.T;
             float sum = 0.0f;
             for (int i0 = 0; i0 < sq_q; i0 += 8) {
                 f32x4 v[2];
@@ -242,7 +245,9 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
                 dim = R % hd;
                 partner = pc ^ h2;
             }
-            const int pos = L + row;
+            const RowInfo ri = p.rr.rows[row0 + row];
+            const int pos = ri.pos;
+            const size_t kvo = (size_t)p.rr.tab->seq[ri.b] * p.kv_seq;  // this row's sequence slot
             float x = s_tile[row * (COLS + 1) + pc];
             if (sec < 2) {
                 const float y = s_tile[row * (COLS + 1) + partner];
@@ -253,11 +258,11 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
             const T e = to_elem<P>(x);  // cached keys and values are rounded to the cache dtype
             const int col = head * hd + dim;
             if (sec == 0)
-                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(d), act_idx<P>(row, col, d), x);
+                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(p.rr.cap, d), act_idx<P>(row0 + row, col, d), x);
             else if (sec == 1)
-                reinterpret_cast<T *>(p.Kc)[(size_t)pos * d + col] = e;
+                reinterpret_cast<T *>(p.Kc)[kvo + (size_t)pos * d + col] = e;
             else
-                reinterpret_cast<T *>(p.Vt)[(size_t)col * p.ctx_alloc + pos] = e;
+                reinterpret_cast<T *>(p.Vt)[kvo + (size_t)col * p.ctx_alloc + pos] = e;
         }
     } else if constexpr (EP == E_RESID) {
         // X += Y over this workgroup's columns, then the per-16-column sums of squares of the
@@ -268,12 +273,12 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
             const int row = idx / COLS, c = idx % COLS;
             float v = 0.0f;
             if (row < m) {
-                float *xp = p.Xout + (size_t)row * p.ldx + c0 + c;
+                float *xp = p.Xout + (size_t)(row0 + row) * p.ldx + c0 + c;
                 v = *xp + s_tile[row * (COLS + 1) + c];
                 *xp = v;
                 // operand of the next RMSNorm-ed product: x (.) g
-                put_act<P>(reinterpret_cast<T *>(p.An), act_plane(p.ldx), act_idx<P>(row, c0 + c, p.ldx),
-                           v * p.gain[c0 + c]);
+                put_act<P>(reinterpret_cast<T *>(p.An), act_plane(p.rr.cap, p.ldx),
+                           act_idx<P>(row0 + row, c0 + c, p.ldx), v * p.gain[c0 + c]);
             }
             s_sq[idx] = v * v;
         }
@@ -284,7 +289,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
                 float sum = 0.0f;
 #pragma unroll
                 for (int c = 0; c < 16; ++c) sum += s_sq[row * COLS + 16 * j + c];
-                p.ssq_out[(size_t)row * p.T + t0 + j] = sum;
+                p.ssq_out[(size_t)(row0 + row) * p.T + t0 + j] = sum;
             }
         }
     } else if constexpr (EP == E_SWIGLU) {
@@ -295,8 +300,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
             if (row >= m) continue;
             const float gt = s_tile[row * (COLS + 1) + 32 * q + c];
             const float up = s_tile[row * (COLS + 1) + 32 * q + 16 + c];
-            put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.Fp), act_idx<P>(row, wg * (COLS / 2) + f, p.Fp),
-                       silu(gt) * up);
+            put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.rr.cap, p.Fp),
+                       act_idx<P>(row0 + row, wg * (COLS / 2) + f, p.Fp), silu(gt) * up);
         }
     } else {  // E_ARGMAX
         // One wave per row: (max, lowest column) over this workgroup's columns < V.
@@ -309,7 +314,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
                 const int col = t0 * 16 + c;
                 if (col < p.V) {
                     const float v = s_tile[row * (COLS + 1) + c];
-                    if (p.dbg) p.dbg[(size_t)row * p.V + col] = v;
+                    if (p.dbg) p.dbg[(size_t)(row0 + row) * p.V + col] = v;
                     if (v != v) nan = 1;
                     else if (v > bv || (v == bv && col < bi)) { bv = v; bi = col; }
                 }
@@ -322,8 +327,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
                 if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
             }
             if (lane == 0) {
-                p.pmax[(size_t)wg * kMaxRows + row] = bv;
-                p.pidx[(size_t)wg * kMaxRows + row] = nan ? -1 : bi;
+                p.pmax[(size_t)wg * p.rr.cap + row0 + row] = bv;
+                p.pidx[(size_t)wg * p.rr.cap + row0 + row] = nan ? -1 : bi;
             }
         }
     }
@@ -339,11 +344,9 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     using T = typename PT::T;
     constexpr int V16 = 16 / sizeof(T);  // elements per 16-byte vector
     static_assert(V16 == PT::VEC, "an operand vector is one 16-byte load");
-    const Ctl *ctl = p.ctl;
-    const int m = ctl->m;
     const int row = blockIdx.x;
-    if (row >= m) return;
-    const int tok = ctl->z[row];
+    if (row >= p.rr.tab->R) return;
+    const int tok = p.rr.rows[row].tok;
     const T *e = reinterpret_cast<const T *>(p.E) + (size_t)tok * p.d;
     float *x = p.X + (size_t)row * p.d;
     T *an = reinterpret_cast<T *>(p.An);
@@ -373,7 +376,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
         for (int pl = 0; pl < PT::PLANES; ++pl)
 #pragma unroll
             for (int q = 0; q < 16 / V16; ++q)  // V16 == VEC: one vector is contiguous in the packed layout
-                *reinterpret_cast<u32x4 *>(an + pl * act_plane(p.d) + act_idx<P>(row, 16 * t + q * V16, p.d)) =
+                *reinterpret_cast<u32x4 *>(an + pl * act_plane(p.rr.cap, p.d) + act_idx<P>(row, 16 * t + q * V16, p.d)) =
                     *reinterpret_cast<u32x4 *>(&av[pl][q * V16]);
         p.ssq[(size_t)row * (p.d / 16) + t] = sum;
     }
@@ -396,20 +399,27 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     using T = typename PT::T;
     constexpr int NKK = HD / PT::KSTEP;  // k-steps of the score product
     constexpr int NDT = HD / 16;         // 16-dim tiles of the output
-    const Ctl *ctl = p.ctl;
-    const int m = ctl->m;
-    if (m <= 0) return;
-    const int L = ctl->L;
+    const RowTab *tab = p.rr.tab;
+    const int b = blockIdx.z / p.nrb;            // batch entry
+    const int rbase = (blockIdx.z % p.nrb) * 16 * RG;  // first block row of this workgroup
+    if (b >= tab->nseq) return;
+    const int m = tab->m[b];
+    const int L = tab->L[b];
+    if (rbase >= m) return;
     const int c = blockIdx.x, h = blockIdx.y;
     const int key0 = c * kAttnChunk;
-    if (key0 >= L + m) return;  // no key of this chunk is visible to any row
+    if (key0 > L + min(m - 1, rbase + 16 * RG - 1)) return;  // no key of this chunk is visible to any row
     const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    if (rbase + 16 * rg >= m) return;  // this wave's rows are all past the block
     const int g = lane >> 4, r16 = lane & 15;
     const int d = p.d;
-    const int qrow = 16 * rg + r16;
-    const int qpos = L + qrow;
-    const T *Kc = reinterpret_cast<const T *>(p.Kc);
-    const T *Vt = reinterpret_cast<const T *>(p.Vt);
+    const int qi = rbase + 16 * rg + r16;   // row within the block
+    const int qrow = tab->r0[b] + qi;       // row of the iteration
+    const int qld = min(qrow, p.rr.cap - 1);  // rows past the block load in-bounds filler
+    const int qpos = L + qi;
+    const size_t kvo = (size_t)tab->seq[b] * p.kv_seq;
+    const T *Kc = reinterpret_cast<const T *>(p.Kc) + kvo;
+    const T *Vt = reinterpret_cast<const T *>(p.Vt) + kvo;
     const T *Q = reinterpret_cast<const T *>(p.Q);
 
     // Every load of the workgroup is issued up front: Q rows, the chunk's 64 keys and values.
@@ -419,7 +429,7 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
         const int dcol = h * HD + kk * PT::KSTEP + g * PT::VEC;
 #pragma unroll
         for (int pl = 0; pl < PT::PLANES; ++pl)
-            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(d) + act_idx<P>(qrow, dcol, d));
+            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, dcol, d));
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
             kv[kt][kk] = *reinterpret_cast<const u32x4 *>(Kc + (size_t)(key0 + 16 * kt + r16) * d + dcol);
@@ -474,7 +484,8 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
 
-    const size_t pbase = ((size_t)h * p.nch + c) * kMaxRows + qrow;
+    const bool live = qi < m;  // rows past the block belong to the next entry: not written
+    const size_t pbase = ((size_t)h * p.nch + c) * p.rr.cap + qrow;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
         f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -510,44 +521,44 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
             }
         }
         // o[v] = O^T[16dt + 4g + v][qrow]
-        *reinterpret_cast<f32x4 *>(p.Opart + pbase * HD + 16 * dt + 4 * g) = o;
+        if (live) *reinterpret_cast<f32x4 *>(p.Opart + pbase * HD + 16 * dt + 4 * g) = o;
     }
-    if (g == 0) {
+    if (g == 0 && live) {
         p.Mpart[pbase] = mx;
         p.Lpart[pbase] = l;
     }
 }
 
-// Combine the chunk partials of one (head, row) in chunk order and write O (compute dtype).
+// Combine the chunk partials of one (head, row) in chunk order and write the O operand.
 // Wave 0 derives the chunk weights w_c = 2^(m_c - M) into LDS; every thread (one output dim)
 // then sums w_c * O_c in chunk order.
 template <Prec P>
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
     using T = typename PrecT<P>::T;
-    const Ctl *ctl = p.ctl;
-    const int m = ctl->m;
+    const RowTab *tab = p.rr.tab;
     const int h = blockIdx.x, row = blockIdx.y;
-    if (row >= m) return;
-    const int L = ctl->L;
-    const int nlive = (L + m + kAttnChunk - 1) / kAttnChunk;
+    if (row >= tab->R) return;
+    // chunks holding a key at or before this row's position (later chunks hold none)
+    const int nlive = p.rr.rows[row].pos / kAttnChunk + 1;
     const int tid = threadIdx.x;
-    const size_t b0 = (size_t)h * p.nch * kMaxRows + row;
+    const int cap = p.rr.cap;
+    const size_t b0 = (size_t)h * p.nch * cap + row;
     __shared__ float s_w[kMaxChunks];
     __shared__ float s_den;
     if (tid < kWave) {
         float M = -INFINITY;
-        for (int c = tid; c < nlive; c += kWave) M = fmaxf(M, p.Mpart[b0 + (size_t)c * kMaxRows]);
+        for (int c = tid; c < nlive; c += kWave) M = fmaxf(M, p.Mpart[b0 + (size_t)c * cap]);
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
         for (int c = tid; c < nlive; c += kWave) {
-            const float mc = p.Mpart[b0 + (size_t)c * kMaxRows];
+            const float mc = p.Mpart[b0 + (size_t)c * cap];
             s_w[c] = mc == -INFINITY ? 0.0f : exp2f(mc - M);
         }
     }
     __syncthreads();
     if (tid == 0) {
         float den = 0.0f;
-        for (int c = 0; c < nlive; ++c) den += s_w[c] * p.Lpart[b0 + (size_t)c * kMaxRows];
+        for (int c = 0; c < nlive; ++c) den += s_w[c] * p.Lpart[b0 + (size_t)c * cap];
         s_den = den;
     }
     __syncthreads();
@@ -557,12 +568,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
         for (; c + 4 <= nlive; c += 4) {
             float o[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * kMaxRows) * p.hd + dim];
+            for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * cap) * p.hd + dim];
 #pragma unroll
             for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
         }
-        for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * kMaxRows) * p.hd + dim];
-        put_act<P>(reinterpret_cast<T *>(p.O), act_plane(p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
+        for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * cap) * p.hd + dim];
+        put_act<P>(reinterpret_cast<T *>(p.O), act_plane(cap, p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
     }
 }
 
@@ -585,10 +596,46 @@ __device__ int32_t draw_guess(const Ctl *c, const int32_t *stream, int32_t t, in
     return s;
 }
 
-// Lay out the first block of a decode after the prefill.
+// Row table of the batch entries already listed in tab (seq[], nseq), from their control blocks:
+// r0 prefix sums of the live block sizes (bounded by the row capacity cap), then one RowInfo per
+// row. Called by a whole workgroup.
+__device__ void plan_rows(Ctl *ctl, RowTab *tab, RowInfo *rows, int cap) {
+    __shared__ int s_r0[kMaxSeqs], s_m[kMaxSeqs], s_L[kMaxSeqs], s_R;
+    const int nseq = tab->nseq;
+    if (threadIdx.x == 0) {
+        int R = 0;
+        for (int b = 0; b < nseq; ++b) {
+            const Ctl *c = ctl + tab->seq[b];
+            int m = c->m > 0 ? (c->m < kMaxBlock ? c->m : kMaxBlock) : 0;
+            m = m < cap - R ? m : cap - R;
+            tab->r0[b] = R;
+            tab->m[b] = m;
+            tab->L[b] = c->L;
+            s_r0[b] = R;
+            s_m[b] = m;
+            s_L[b] = c->L;
+            R += m;
+        }
+        tab->R = R;
+        s_R = R;
+    }
+    __syncthreads();
+    for (int row = threadIdx.x; row < s_R; row += blockDim.x) {
+        int b = 0;
+        while (b + 1 < nseq && row >= s_r0[b + 1]) ++b;  // the last entry starting at or before row
+        const int i = row - s_r0[b];
+        rows[row] = RowInfo{b, s_L[b] + i, ctl[tab->seq[b]].z[i], i};
+    }
+}
+
+__global__ __launch_bounds__(256) void plan_kernel(PlanParams p) { plan_rows(p.ctl, p.tab, p.rows, p.cap); }
+
+// Lay out the first block of a decode after the prefill, for batch entry blockIdx.x.
 __global__ void decode_init_kernel(ScanParams p) {
-    Ctl *c = p.ctl;
-    if (threadIdx.x != 0) return;
+    if (threadIdx.x != 0 || (int)blockIdx.x >= p.tab->nseq) return;
+    const int seq = p.tab->seq[blockIdx.x];
+    Ctl *c = p.ctl + seq;
+    const int32_t *stream = p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr;
     c->mode = MODE_DECODE;
     c->e = 0;
     c->b0 = 0;
@@ -599,78 +646,23 @@ __global__ void decode_init_kernel(ScanParams p) {
     c->err = 0;
     for (int i = 0; i <= kMaxBlock; ++i) c->hist[i] = 0;
     c->z[0] = c->pending;
-    for (int j = 1; j < c->nb; ++j) c->z[j] = draw_guess(c, p.stream, j, 0);
+    for (int j = 1; j < c->nb; ++j) c->z[j] = draw_guess(c, stream, j, 0);
     c->m = c->nb;
 }
 
-__global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
-    Ctl *c = p.ctl;
-    const int m = c->m;
-    if (m <= 0) return;
-    const int tid = threadIdx.x;
-    const int lane = tid;
-    if (p.advance_only) {
-        if (tid == 0) {
-            c->L += m;
-            c->m = 0;
-        }
-        return;
-    }
-    // Final argmax of each row over the LM-head workgroups: 16 threads per row take strided
-    // workgroups, then a 16-lane xor tree. (max, lowest id) is exact, so the order is free.
-    {
-        const int row = tid & 63, j = tid >> 6;
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
-        int nan = 0;
-        if (row < m) {
-            for (int g0 = j; g0 < p.n_wg; g0 += 16 * 8) {
-                float v[8];
-                int ix[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int g = g0 + 16 * u;
-                    ix[u] = g < p.n_wg ? p.pidx[(size_t)g * kMaxRows + row] : 0x7fffffff;
-                    v[u] = g < p.n_wg ? p.pmax[(size_t)g * kMaxRows + row] : -INFINITY;
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    if (ix[u] < 0) nan = 1;
-                    else if (v[u] > bv || (v[u] == bv && ix[u] < bi)) { bv = v[u]; bi = ix[u]; }
-                }
-            }
-        }
-        __shared__ float s_v[1024];
-        __shared__ int s_i[1024];
-        __shared__ int s_nan[1024];
-        s_v[tid] = bv;
-        s_i[tid] = bi;
-        s_nan[tid] = nan;
-        __syncthreads();
-        if (tid < 64 && tid < m) {
-            float b = s_v[tid];
-            int i = s_i[tid], nn = s_nan[tid];
-            for (int jj = 1; jj < 16; ++jj) {
-                const float ov = s_v[jj * 64 + tid];
-                const int oi = s_i[jj * 64 + tid];
-                nn |= s_nan[jj * 64 + tid];
-                if (ov > b || (ov == b && oi < i)) { b = ov; i = oi; }
-            }
-            c->pred[tid] = (nn || i == 0x7fffffff) ? -1 : i;
-        }
-    }
-    __syncthreads();
-    if (lane != 0) return;
-    for (int i = 0; i < m; ++i)
+// Acceptance, commit, emit and the next block of one sequence, from its predictions c->pred
+// (one thread).
+__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream) {
+    for (int i = 0; i < (c->mode == MODE_PREFILL ? 1 : m); ++i)
         if (c->pred[i] < 0) {
             c->err |= 1;
             c->done = 1;
             c->m = 0;
             return;
         }
-    if (c->mode == MODE_PREFILL) {
+    if (c->mode == MODE_PREFILL) {  // every row is committed; pred[0] is the last row's argmax
         c->L += m;
-        c->pending = c->pred[m - 1];
+        c->pending = c->pred[0];
         c->m = 0;
         return;
     }
@@ -685,7 +677,7 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
         c->m = 0;
         return;
     }
-    for (int k = 0; k < a; ++k) p.out[c->e + k] = c->z[k];
+    for (int k = 0; k < a; ++k) out[c->e + k] = c->z[k];
     c->e += a;
     if (c->e >= c->max_new) {
         c->done = 1;
@@ -701,21 +693,94 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
             c->nb = (c->max_new - e) < n ? (c->max_new - e) : n;
             c->blocks += 1;
             newm = c->nb;
-            for (int j = 1; j < newm; ++j) c->z[j] = draw_guess(c, p.stream, e + j, draw);
+            for (int j = 1; j < newm; ++j) c->z[j] = draw_guess(c, stream, e + j, draw);
         } else {
             newm = c->b0 + c->nb - e;
             for (int j = 1; j < newm; ++j)
-                c->z[j] = c->policy == 2 ? draw_guess(c, p.stream, e + j, draw) : c->pred[a - 1 + j];
+                c->z[j] = c->policy == 2 ? draw_guess(c, stream, e + j, draw) : c->pred[a - 1 + j];
         }
     } else {
         newm = (c->max_new - e) < n ? (c->max_new - e) : n;
         for (int j = 1; j < newm; ++j) {
             const int src = a - 1 + j;
-            c->z[j] = (c->policy != 2 && src < m) ? c->pred[src] : draw_guess(c, p.stream, e + j, draw);
+            c->z[j] = (c->policy != 2 && src < m) ? c->pred[src] : draw_guess(c, stream, e + j, draw);
         }
     }
     c->z[0] = c->pending;
     c->m = newm;
+}
+
+// One workgroup per batch entry: the final argmax of each of its rows over the LM-head
+// workgroups (16 threads per row take strided workgroups, then a 16-way tree; (max, lowest id)
+// is exact, so the order is free), then commit_and_next. A prefill chunk needs only its last
+// row. With one batch entry the workgroup also lays out the next row table.
+__global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
+    const int bi = blockIdx.x;
+    const RowTab *tab = p.tab;
+    if (bi >= tab->nseq) return;
+    const int seq = tab->seq[bi];
+    const int m = tab->m[bi], r0 = tab->r0[bi];
+    Ctl *c = p.ctl + seq;
+    const int tid = threadIdx.x;
+    if (m > 0) {
+        if (p.advance_only) {
+            if (tid == 0) {
+                c->L += m;
+                c->m = 0;
+            }
+        } else {
+            const bool prefill = c->mode == MODE_PREFILL;
+            const int nrows = prefill ? 1 : m;            // <= 64
+            const int rbase = r0 + (prefill ? m - 1 : 0);
+            const int row = tid & 63, j = tid >> 6;
+            float bv = -INFINITY;
+            int bx = 0x7fffffff;
+            int nan = 0;
+            if (row < nrows) {
+                for (int g0 = j; g0 < p.n_wg; g0 += 16 * 8) {
+                    float v[8];
+                    int ix[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int g = g0 + 16 * u;
+                        ix[u] = g < p.n_wg ? p.pidx[(size_t)g * p.cap + rbase + row] : 0x7fffffff;
+                        v[u] = g < p.n_wg ? p.pmax[(size_t)g * p.cap + rbase + row] : -INFINITY;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        if (ix[u] < 0) nan = 1;
+                        else if (v[u] > bv || (v[u] == bv && ix[u] < bx)) { bv = v[u]; bx = ix[u]; }
+                    }
+                }
+            }
+            __shared__ float s_v[1024];
+            __shared__ int s_i[1024];
+            __shared__ int s_nan[1024];
+            s_v[tid] = bv;
+            s_i[tid] = bx;
+            s_nan[tid] = nan;
+            __syncthreads();
+            if (tid < nrows) {
+                float best = s_v[tid];
+                int i = s_i[tid], nn = s_nan[tid];
+                for (int jj = 1; jj < 16; ++jj) {
+                    const float ov = s_v[jj * 64 + tid];
+                    const int oi = s_i[jj * 64 + tid];
+                    nn |= s_nan[jj * 64 + tid];
+                    if (ov > best || (ov == best && oi < i)) { best = ov; i = oi; }
+                }
+                c->pred[tid] = (nn || i == 0x7fffffff) ? -1 : i;
+            }
+            __syncthreads();
+            if (tid == 0)
+                commit_and_next(c, m, p.out ? p.out + (size_t)seq * p.out_stride : nullptr,
+                                p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr);
+        }
+    }
+    if (p.plan_inline) {
+        __syncthreads();
+        plan_rows(p.ctl, p.tab, p.rows, p.cap);
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -745,46 +810,50 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
+// Grid: (column workgroups, row tiles of 16 * RG rows starting at row tile p.rt0).
 template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves, bool KC = kGemmKContig>
-static hipError_t launch_gemm_t(const GemmParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
     const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
     auto kern = gemm_kernel<P, NT, RG, EP, D, W, KC>;
+    const dim3 grid(p.n_wg, row_tiles);
     if (e0) {
-        hipExtLaunchKernelGGL(kern, dim3(p.n_wg), dim3(W * kWave), lds, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, p);
     } else {
-        hipLaunchKernelGGL(kern, dim3(p.n_wg), dim3(W * kWave), lds, s, p);
+        hipLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, p);
     }
     return hipGetLastError();
 }
 
 template <Prec P, int RG>
-static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
+                                 hipEvent_t e1) {
     switch (kind) {
     case GEMM_QKV:
-        return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, row_tiles, s, e0, e1);
     case GEMM_O:
     case GEMM_DOWN:
-        return launch_gemm_t<P, kNtResid, RG, E_RESID>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtResid, RG, E_RESID>(p, row_tiles, s, e0, e1);
     case GEMM_GATE_UP:
-        return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, s, e0, e1);
+        return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, row_tiles, s, e0, e1);
     case GEMM_LM:
-        return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX>(p, s, e0, e1);
+        return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX>(p, row_tiles, s, e0, e1);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, const GemmParams &p, hipStream_t s, hipEvent_t e0,
-                       hipEvent_t e1) {
+hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const GemmParams &p, hipStream_t s,
+                       hipEvent_t e0, hipEvent_t e1) {
+    if (row_tiles < 1 || (row_tiles > 1 && rg != 4)) return hipErrorInvalidValue;
     if (bf16) {
-        if (rg == 1) return launch_gemm_rg<Prec::BF16, 1>(kind, p, s, e0, e1);
-        if (rg == 2) return launch_gemm_rg<Prec::BF16, 2>(kind, p, s, e0, e1);
-        return launch_gemm_rg<Prec::BF16, 4>(kind, p, s, e0, e1);
+        if (rg == 1) return launch_gemm_rg<Prec::BF16, 1>(kind, p, row_tiles, s, e0, e1);
+        if (rg == 2) return launch_gemm_rg<Prec::BF16, 2>(kind, p, row_tiles, s, e0, e1);
+        return launch_gemm_rg<Prec::BF16, 4>(kind, p, row_tiles, s, e0, e1);
     }
-    if (rg == 1) return launch_gemm_rg<Prec::F32, 1>(kind, p, s, e0, e1);
-    if (rg == 2) return launch_gemm_rg<Prec::F32, 2>(kind, p, s, e0, e1);
-    return launch_gemm_rg<Prec::F32, 4>(kind, p, s, e0, e1);
+    if (rg == 1) return launch_gemm_rg<Prec::F32, 1>(kind, p, row_tiles, s, e0, e1);
+    if (rg == 2) return launch_gemm_rg<Prec::F32, 2>(kind, p, row_tiles, s, e0, e1);
+    return launch_gemm_rg<Prec::F32, 4>(kind, p, row_tiles, s, e0, e1);
 }
 
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
@@ -797,9 +866,10 @@ hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s
 }
 
 template <Prec P, int HD>
-static hipError_t launch_attn_hd(int rg, const AttnParams &p, int nch_launch, hipStream_t s, hipEvent_t e0,
-                                 hipEvent_t e1) {
-    dim3 grid(nch_launch, p.n_heads);
+static hipError_t launch_attn_hd(int rg, const AttnParams &p, int nch_launch, int nseq_launch, hipStream_t s,
+                                 hipEvent_t e0, hipEvent_t e1) {
+    if (p.nrb < 1 || (p.nrb > 1 && rg != 4)) return hipErrorInvalidValue;
+    dim3 grid(nch_launch, p.n_heads, nseq_launch * p.nrb);
     auto kern = rg == 1 ? attn_partial_kernel<P, HD, 1>
                         : (rg == 2 ? attn_partial_kernel<P, HD, 2> : attn_partial_kernel<P, HD, 4>);
     if (e0)
@@ -809,21 +879,21 @@ static hipError_t launch_attn_hd(int rg, const AttnParams &p, int nch_launch, hi
     return hipGetLastError();
 }
 
-hipError_t launch_attn(bool bf16, int rg, int nch_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
-                       hipEvent_t e1) {
+hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const AttnParams &p, hipStream_t s,
+                       hipEvent_t e0, hipEvent_t e1) {
     if (bf16) {
         switch (p.hd) {
-        case 32: return launch_attn_hd<Prec::BF16, 32>(rg, p, nch_launch, s, e0, e1);
-        case 64: return launch_attn_hd<Prec::BF16, 64>(rg, p, nch_launch, s, e0, e1);
-        case 128: return launch_attn_hd<Prec::BF16, 128>(rg, p, nch_launch, s, e0, e1);
-        case 256: return launch_attn_hd<Prec::BF16, 256>(rg, p, nch_launch, s, e0, e1);
+        case 32: return launch_attn_hd<Prec::BF16, 32>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 64: return launch_attn_hd<Prec::BF16, 64>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 128: return launch_attn_hd<Prec::BF16, 128>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 256: return launch_attn_hd<Prec::BF16, 256>(rg, p, nch_launch, nseq_launch, s, e0, e1);
         }
     } else {
         switch (p.hd) {
-        case 16: return launch_attn_hd<Prec::F32, 16>(rg, p, nch_launch, s, e0, e1);
-        case 32: return launch_attn_hd<Prec::F32, 32>(rg, p, nch_launch, s, e0, e1);
-        case 64: return launch_attn_hd<Prec::F32, 64>(rg, p, nch_launch, s, e0, e1);
-        case 128: return launch_attn_hd<Prec::F32, 128>(rg, p, nch_launch, s, e0, e1);
+        case 16: return launch_attn_hd<Prec::F32, 16>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 32: return launch_attn_hd<Prec::F32, 32>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 64: return launch_attn_hd<Prec::F32, 64>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        case 128: return launch_attn_hd<Prec::F32, 128>(rg, p, nch_launch, nseq_launch, s, e0, e1);
         }
     }
     return hipErrorInvalidValue;
@@ -841,36 +911,61 @@ hipError_t launch_attn_combine(bool bf16, int rows, const AttnParams &p, hipStre
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_scan(int nseq_launch, const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     if (e0)
-        hipExtLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(1024), 0, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(scan_commit_kernel, dim3(nseq_launch), dim3(1024), 0, s, e0, e1, 0, p);
     else
-        hipLaunchKernelGGL(scan_commit_kernel, dim3(1), dim3(1024), 0, s, p);
+        hipLaunchKernelGGL(scan_commit_kernel, dim3(nseq_launch), dim3(1024), 0, s, p);
     return hipGetLastError();
 }
 
-__global__ void setup_kernel(SetupParams p) {
-    Ctl *c = p.ctl;
-    const int i = threadIdx.x;
-    if (i < p.m) c->z[i] = p.z[i];
-    if (i == 0) {
-        c->mode = p.mode;
-        c->m = p.m;
-        if (p.set_L) {
-            c->L = p.L;
-            c->err = 0;
-            c->done = 0;
+static_assert(kMaxSeqs == 64, "SetupParams holds 64 entries");
+
+// Host edits: entry b's block (or prefill chunk) of m[b] tokens, then the row table.
+__global__ __launch_bounds__(256) void setup_kernel(SetupParams p) {
+    __shared__ int s_r0[kMaxSeqs], s_L[kMaxSeqs];
+    if (threadIdx.x == 0) {
+        int R = 0;
+        for (int b = 0; b < p.nseq; ++b) {
+            Ctl *c = p.ctl + p.seq[b];
+            if (p.set_L) {
+                c->L = p.L;
+                c->err = 0;
+                c->done = 0;
+            }
+            c->mode = p.mode;
+            c->m = p.m[b];
+            if (p.mode != MODE_PREFILL)
+                for (int i = 0; i < p.m[b]; ++i) c->z[i] = p.zin[(size_t)b * p.zstride + i];
+            p.tab->seq[b] = p.seq[b];
+            p.tab->r0[b] = R;
+            p.tab->m[b] = p.m[b];
+            p.tab->L[b] = c->L;
+            s_r0[b] = R;
+            s_L[b] = c->L;
+            R += p.m[b];
         }
+        p.tab->nseq = p.nseq;
+        p.tab->R = R;
     }
+    __syncthreads();
+    for (int b = 0; b < p.nseq; ++b)
+        for (int i = threadIdx.x; i < p.m[b]; i += blockDim.x)
+            p.rows[s_r0[b] + i] = RowInfo{b, s_L[b] + i, p.zin[(size_t)b * p.zstride + i], i};
 }
 
 hipError_t launch_setup(const SetupParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kWave), 0, s, p);
+    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
-hipError_t launch_decode_init(const ScanParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(decode_init_kernel, dim3(1), dim3(kWave), 0, s, p);
+hipError_t launch_decode_init(int nseq, const ScanParams &p, hipStream_t s) {
+    hipLaunchKernelGGL(decode_init_kernel, dim3(nseq), dim3(kWave), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan(const PlanParams &p, hipStream_t s) {
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 

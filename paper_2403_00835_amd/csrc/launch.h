@@ -6,6 +6,8 @@
 namespace cllm {
 
 struct Ctl;
+struct RowTab;
+struct RowInfo;
 
 constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
 constexpr int kNtQkv = 4;     // QKV (pairs of rotate-half partner tiles)
@@ -16,19 +18,30 @@ constexpr bool kGemmKContig = false;  // k-steps per wave: interleaved (false) o
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
+// Rows of an iteration: the row table, its per-row entries and the row capacity of the
+// activation buffers (their plane size).
+struct RowsRef {
+    const RowTab *tab;
+    const RowInfo *rows;
+    int cap;
+};
+
 struct GemmParams {
     const uint8_t *W;  // packed tiles
     int Ks;            // k-steps per 16-row tile
-    int n_wg;          // workgroups (tiles / NT)
-    const void *A;     // activation operand (compute dtype), rows of lda elements
+    int n_wg;          // workgroups along the columns (tiles / NT)
+    int rt0;           // first row tile (grid y adds to it)
+    const void *A;     // activation operand, packed operand order, lda elements per row
     int lda;
+    RowsRef rr;
     // RMSNorm row factor (QKV, gate/up, LM head): per-16-column sums of squares [row][T]
     const float *ssq;
     int T, K;
     float eps;
-    const Ctl *ctl;
-    // E_QKV
+    // E_QKV: Q operand; K cache [seq][layer][pos][d] and transposed V cache [seq][layer][d][pos]
+    // given for this layer of sequence slot 0, kv_seq elements apart per slot
     void *Q, *Kc, *Vt;
+    size_t kv_seq;
     int ctx_alloc;
     const float *rcos, *rsin;
     int d, hd;
@@ -40,7 +53,7 @@ struct GemmParams {
     // E_SWIGLU
     void *H;
     int Fp;
-    // E_ARGMAX
+    // E_ARGMAX: per-workgroup (max, index) [workgroup][row capacity]; optional logits [row][V]
     float *pmax;
     int *pidx;
     float *dbg;
@@ -53,45 +66,67 @@ struct EmbedParams {
     void *An;           // first RMSNorm operand X (.) gain
     const float *gain;
     int d;
-    const Ctl *ctl;
+    RowsRef rr;
 };
 
 struct AttnParams {
-    const void *Q, *Kc, *Vt;
+    const void *Q, *Kc, *Vt;  // caches as in GemmParams
+    size_t kv_seq;
     void *O;
-    float *Opart, *Mpart, *Lpart;
+    float *Opart, *Mpart, *Lpart;  // [head][chunk][row capacity] (x hd for Opart)
     int d, hd, n_heads, nch, ctx_alloc;
+    int nrb;  // workgroups per batch entry along its block rows (16 * rg rows each)
     float scale_log2;
-    const Ctl *ctl;
+    RowsRef rr;
 };
 
 struct ScanParams {
-    Ctl *ctl;
+    Ctl *ctl;               // control blocks, one per sequence slot
+    RowTab *tab;
+    RowInfo *rows;
+    int cap;                // row capacity
     const float *pmax;
     const int *pidx;
     int n_wg;
-    int32_t *out;           // decode output tokens
-    const int32_t *stream;  // guess stream (may be null)
+    int32_t *out;           // decode output tokens, out_stride per slot
+    const int32_t *stream;  // guess streams (may be null), stream_stride per slot
+    int out_stride, stream_stride;
     int advance_only;       // prefill chunk without LM head: commit all rows, no predictions
+    int plan_inline;        // one batch entry: the scan also lays out the next row table
 };
 
-// Host-side edits of the control block, applied on the stream in order with the kernels.
+// Host-side edits of the control blocks and the row table, applied on the stream in order with
+// the kernels. Entry b's tokens are zin[b * zstride + i]; a prefill chunk (one entry) may hold
+// up to the row capacity.
 struct SetupParams {
     Ctl *ctl;
-    int mode, m, set_L, L;
-    int32_t z[64];
+    RowTab *tab;
+    RowInfo *rows;
+    const int32_t *zin;
+    int zstride, nseq, mode, set_L, L;
+    int32_t seq[64], m[64];
 };
+
+// Lay out the row table from the control blocks of the batch entries already in the table.
+struct PlanParams {
+    Ctl *ctl;
+    RowTab *tab;
+    RowInfo *rows;
+    int cap;
+};
+
 hipError_t launch_setup(const SetupParams &p, hipStream_t s);
 
-hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, const GemmParams &p, hipStream_t s, hipEvent_t e0,
-                       hipEvent_t e1);
+hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const GemmParams &p, hipStream_t s,
+                       hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_attn(bool bf16, int rg, int nch_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
-                       hipEvent_t e1);
+hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const AttnParams &p, hipStream_t s,
+                       hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_attn_combine(bool bf16, int rows, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                                hipEvent_t e1);
-hipError_t launch_scan(const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_decode_init(const ScanParams &p, hipStream_t s);
+hipError_t launch_scan(int nseq_launch, const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_decode_init(int nseq, const ScanParams &p, hipStream_t s);
+hipError_t launch_plan(const PlanParams &p, hipStream_t s);
 hipError_t launch_repack(bool bf16, const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst,
                          hipStream_t s);
 

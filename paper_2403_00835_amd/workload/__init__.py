@@ -10,7 +10,7 @@ import subprocess
 
 import numpy as np
 
-from ..configs import ModelConfig, SEED_PROMPT, SEED_WEIGHTS
+from ..configs import SEED_BATCH, ModelConfig, SEED_PROMPT, SEED_WEIGHTS
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")
@@ -132,3 +132,13 @@ def make_uniform_f64(n, seed, stream):
     out = np.empty(n, dtype=np.float64)
     lib().wl_fill_uniform_f64(seed, stream, out.ctypes.data, n)
     return out
+
+
+def make_batch(cfg: ModelConfig, batch, len_range, p_range, seed=SEED_BATCH):
+    """Ragged batch: `batch` prompt lengths uniform in [len_range[0], len_range[1]] (inclusive) and
+    corruption rates uniform in [p_range[0], p_range[1]); prompt b is make_prompt(..., seq=b)."""
+    lens = make_uniform_range(len_range[0], len_range[1], batch, seed, 1)
+    u = make_uniform_f64(batch, seed, 2)
+    ps = p_range[0] + (p_range[1] - p_range[0]) * u
+    prompts = [make_prompt(cfg, int(n), seq=b) for b, n in enumerate(lens)]
+    return prompts, ps

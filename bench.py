@@ -7,6 +7,10 @@ positions corrupted and re-drawn after every iteration (emulating a consistency-
 the block shrinks as in the paper's algorithm. value = generated tokens / second over the
 timed steps (inputs resident on the device when timing starts).
 
+--workload 7b_long (prompt 2048, n = 64, 512 new) and 7b_batched (16 sequences, prompts uniform
+in [256, 1024], n = 32, 256 new each, corruption rates uniform in [0.1, 0.6], all decoded in one
+batched loop; value = tokens of all sequences / second) measure the other configurations.
+
 Prints one JSON line. --gpus above 1 is refused: this build runs on one GPU.
 """
 import argparse
@@ -23,6 +27,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+METRIC = "Jacobi-step ms & accepted tokens/s, 7B-shape bf16 n=16; HBM GB/s vs peak"
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_gemm_gate_up_llama7b_n16.md")
 
 
@@ -51,16 +57,16 @@ def measured_traffic():
     return float(m_bytes.group(1))
 
 
-def cpu_baseline(cfg, ws, mean_accept, n):
-    """The oracle as it stands, timed on this host: one Jacobi iteration of n rows at the 7B
-    shape after a 16-token prefill (attention over 16 instead of ~640 keys is about 2% of the
-    iteration's work), scaled to tokens/s with the mean accepted length of the GPU run."""
+def oracle_iteration_s(cfg, ws, n):
+    """Seconds of the oracle, as it stands, for one Jacobi iteration of n rows at this shape
+    after a 16-token prefill (attention over 16 instead of several hundred keys is about 2% of
+    the iteration's work at the 7B shape)."""
     import oracle
     from paper_2403_00835_amd import workload
     log("[bench] cpu baseline: oracle on the host")
     tensors = [workload.as_f32(cfg, t) for t in ws]
     om = oracle.Model(cfg, tensors)
-    st = oracle.State(om, 64)
+    st = oracle.State(om, 16 + n + 1)
     prompt = workload.make_prompt(cfg, 16, seed=11)
     y0 = st.prefill(prompt)
     block = np.array([y0] + list(workload.make_prompt(cfg, n - 1, seed=12)), dtype=np.int32)
@@ -68,7 +74,13 @@ def cpu_baseline(cfg, ws, mean_accept, n):
     st.eval_block(block)
     dt = time.perf_counter() - t0
     del om, tensors
-    return {"value": mean_accept / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+    return dt, oracle.num_threads()
+
+
+def cpu_baseline(cfg, ws, mean_accept, n):
+    """The oracle's tokens/s: one n-row iteration, scaled by the GPU run's mean accepted length."""
+    dt, cores = oracle_iteration_s(cfg, ws, n)
+    return {"value": mean_accept / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"one Jacobi iteration of {n} rows at the 7B shape after a 16-token prefill "
                       f"({dt:.2f} s), scaled by the GPU run's mean accepted length {mean_accept:.2f}",
             "iteration_s": dt}
@@ -79,7 +91,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long", "7b_batched"])
     ap.add_argument("--p", type=float, default=0.3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -97,6 +109,8 @@ def main():
     from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT, WORKLOADS
 
     wl = WORKLOADS[args.workload]
+    if wl.batch > 1:
+        return main_batched(args, wl)
     cfg = wl.model
     P, n, max_new = wl.prompt_len, wl.n, wl.max_new
     torch.cuda.init()
@@ -149,7 +163,7 @@ def main():
     gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * f_pad * 4 + n * (d // 16) * 4
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
-    traffic = measured_traffic()
+    traffic = measured_traffic() if (args.workload == "7b" and n == 16) else None
     mean_ctx = P + max_new / 2
     kv_bytes = cfg.n_layers * 2 * mean_ctx * d * 2
     step_gbps = (wbytes + kv_bytes) / (iter_ms / 1e3) / 1e9
@@ -168,7 +182,7 @@ def main():
         cpu = cpu_baseline(cfg, ws, mean_accept, n)
 
     line = {
-        "metric": "Jacobi-step ms & accepted tokens/s, 7B-shape bf16 n=16; HBM GB/s vs peak",
+        "metric": METRIC,
         "value": round(value, 3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -196,6 +210,105 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
                      "launches": launches},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def main_batched(args, wl):
+    """Batched ragged decoding: all sequences of the workload in one device-resident loop."""
+    import torch
+    from paper_2403_00835_amd import binding, workload
+    from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT
+
+    cfg = wl.model
+    n, max_new = wl.n, wl.max_new
+    prompts, ps = workload.make_batch(cfg, wl.batch, wl.prompt_len_range, wl.p_range)
+    B = len(prompts)
+    ids = list(range(B))
+    torch.cuda.init()
+    stream = torch.cuda.current_stream()
+    log(f"[bench] generating {cfg.streamed_params() / 1e9:.2f} B streamed parameters")
+    ws = workload.make_weights(cfg)
+    model = binding.Model(cfg, max_ctx=wl.prompt_len_range[1] + max_new + n + 64, max_block=n, max_new=max_new,
+                          max_batch=B, stream=stream.cuda_stream, weights=ws)
+    log(f"[bench] batched GPU AR decode of {B} sequences (guess streams and AR baseline)")
+    ar, ar_stats = model.jacobi_decode_batch(ids, prompts, 1, max_new)
+    ar_tps = B * max_new / ((ar_stats[0]["prefill_ms"] + ar_stats[0]["decode_ms"]) / 1e3)
+    specs = [dict(policy=GUESS_STREAM_REINJECT, block_policy=BLOCK_SHRINK, stream=ar[b], p=float(ps[b]), seed=3)
+             for b in range(B)]
+
+    def one_step():
+        return model.jacobi_decode_batch(ids, prompts, n, max_new, specs=specs)
+
+    for _ in range(args.warmup):
+        out, _ = one_step()
+        if not np.array_equal(out, ar):
+            raise RuntimeError("batched Jacobi output differs from batched greedy AR output")
+    torch.cuda.synchronize()
+    model.timing_enable("gate_up", max_rows=64)  # iteration launches (row tiles of 64 rows)
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out, st = one_step()
+        stats.append(st)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launches, gu_ms = model.timing_read()
+    model.timing_enable(-1)
+    if not np.array_equal(out, ar):
+        raise RuntimeError("batched Jacobi output differs from batched greedy AR output")
+
+    tokens = args.steps * B * max_new
+    value = tokens / elapsed
+    iters = [max(s["steps"] for s in st) for st in stats]  # batched iterations per step
+    rows = sum(s["rows"] for st in stats for s in st)
+    decode_ms = sum(st[0]["decode_ms"] for st in stats)
+    prefill_ms = sum(st[0]["prefill_ms"] for st in stats) / len(stats)
+    d, F = cfg.d_model, cfg.ffn_dim
+    f_pad = (F + 31) // 32 * 32
+    # gate/up: algorithmic flops 2 * rows * (2 F) * d over the timed launches (executed MFMA work
+    # is twice that: the activation's hi and lo planes)
+    gu_flops = 2.0 * rows * 2 * f_pad * d
+    achieved = gu_flops / (gu_ms / 1e3) / 1e12 if gu_ms > 0 else 0.0
+    mean_rows = rows / sum(iters)
+    cpu = None
+    if not args.no_cpu_baseline:
+        dt, cores = oracle_iteration_s(cfg, ws, n)
+        tok_per_row = tokens / rows
+        cpu = {"value": n / dt * tok_per_row, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+               "sample": f"one Jacobi iteration of {n} rows of one sequence at the 7B shape after a 16-token "
+                         f"prefill ({dt:.2f} s), scaled to tokens by the GPU run's {tok_per_row:.3f} tokens per "
+                         f"row", "iteration_s": dt}
+    line = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {B} sequences, prompts uniform in {list(wl.prompt_len_range)}, n={n}, "
+                               f"{max_new} new tokens each, guesses = GPU greedy continuation corrupted at per-sequence "
+                               f"p uniform in {list(wl.p_range)} and re-drawn each iteration, shrink blocks, one "
+                               f"batched loop",
+                   "batch": B, "n": n, "max_new": max_new, "layers": cfg.n_layers, "d_model": d},
+        "batched_iterations_per_step": sum(iters) / len(iters),
+        "mean_rows_per_iteration": round(mean_rows, 2),
+        "batched_iteration_ms": round(decode_ms / sum(iters), 4),
+        "prefill_ms": round(prefill_ms, 3),
+        "ar_tokens_per_s": round(ar_tps, 3),
+        "speedup_vs_ar": round(value / ar_tps, 3),
+        "roofline": {"bound": "mfma", "kernel": "gemm gate/up + SwiGLU (per layer), row tiles of 64",
+                     "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "executed_mfma_tflops": round(2 * achieved, 2), "algorithmic_flops": gu_flops / max(launches, 1),
+                     "avg_launch_us": round(gu_ms / max(launches, 1) * 1e3, 2), "launches": launches},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -102,6 +102,7 @@ typedef struct cllm_decode_stats {
     int64_t accept_hist[65];  /* accept_hist[a]: iterations that accepted a tokens */
     double prefill_ms;        /* device time of the prefill */
     double decode_ms;         /* device time of the iterations */
+    int64_t rows;             /* block rows run through the decoder by the iterations (sum of m) */
 } cllm_decode_stats;
 
 typedef struct cllm_ctx cllm_ctx;
@@ -198,8 +199,9 @@ cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_
 /* Kernel timing for measurement: kernel_class selects one class of kernels (CLLM_KT_*
  * below); while enabled, each launch of that class is bracketed by HIP events on the context's
  * stream. max_rows > 0 restricts timing to launches sized for that many rows (the kernels are
- * instantiated for 16, 32 or 64 rows: max_rows = n times the Jacobi iterations of blocks of n
- * and leaves out 64-row prefill chunks when n <= 32); 0 times every launch. cllm_timing_read
+ * instantiated for 16, 32 or 64 rows per row tile: max_rows = n times the Jacobi iterations of
+ * blocks of n when n <= 32); 0 times every launch. Launches of a prefill are never timed.
+ * cllm_timing_read
  * returns the number of timed launches and their total device time since the last enable, and
  * clears them. kernel_class < 0 disables. */
 #define CLLM_KT_GEMM_QKV 0

@@ -39,7 +39,7 @@ class cllm_guess_spec(ctypes.Structure):
 
 class cllm_decode_stats(ctypes.Structure):
     _fields_ = [("steps", _i64), ("blocks", _i64), ("tokens", _i64), ("accept_hist", _i64 * 65),
-                ("prefill_ms", _dbl), ("decode_ms", _dbl)]
+                ("prefill_ms", _dbl), ("decode_ms", _dbl), ("rows", _i64)]
 
 
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
@@ -259,7 +259,7 @@ class Model:
 def _stats(st):
     return {"steps": int(st.steps), "blocks": int(st.blocks), "tokens": int(st.tokens),
             "accept_hist": [int(x) for x in st.accept_hist], "prefill_ms": float(st.prefill_ms),
-            "decode_ms": float(st.decode_ms)}
+            "decode_ms": float(st.decode_ms), "rows": int(st.rows)}
 
 
 def write_weight_file(path, cfg: ModelConfig, tensors):

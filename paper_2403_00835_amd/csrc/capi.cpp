@@ -28,7 +28,7 @@ struct cllm_ctx {
     int ctx_alloc = 0;  // KV capacity, multiple of the attention chunk
     int nch = 0;        // attention chunks of ctx_alloc
     int ks_d = 0, ks_f = 0;
-    int n_wg_qkv = 0, n_wg_o = 0, n_wg_gu = 0, n_wg_d = 0, n_wg_lm = 0;
+    int n_wg_lm = 0;  // LM-head workgroups (argmax partials per row)
     int max_batch = 1;
     int cap = 0;        // row capacity of one iteration (multiple of 64): activation buffer rows
     size_t kv_seq = 0;  // KV cache elements per sequence slot
@@ -72,6 +72,7 @@ struct cllm_ctx {
     // kernel timing
     int kt_class = -1;
     int kt_rg = 0;  // time only launches for this many 16-row groups (0 = all)
+    bool in_prefill = false;  // prefill launches are not timed
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
     int64_t kt_launches = 0;
@@ -130,7 +131,7 @@ cllm_status dalloc_t(cllm_ctx *c, T **p, size_t count) {
 // Timing events for the selected kernel class and row-group count (null when not timed).
 void timing_events(cllm_ctx *c, int cls, int rg, hipEvent_t *e0, hipEvent_t *e1) {
     *e0 = *e1 = nullptr;
-    if (c->kt_class != cls || (c->kt_rg > 0 && c->kt_rg != rg)) return;
+    if (c->kt_class != cls || c->in_prefill || (c->kt_rg > 0 && c->kt_rg != rg)) return;
     while (c->ev_pool.size() < c->ev_used + 2) {
         hipEvent_t e;
         if (hipEventCreate(&e) != hipSuccess) return;
@@ -266,7 +267,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         GemmParams q = base;  // operand: attention RMSNorm of X, written by the previous producer
         q.W = c->w_qkv[l];
         q.Ks = c->ks_d;
-        q.n_wg = c->n_wg_qkv;
+        q.cols = 3 * c->d;
         q.A = c->An;
         q.lda = c->d;
         q.Q = c->Q;
@@ -285,7 +286,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         GemmParams o = base;  // X += O W_o^T; writes the FFN RMSNorm operand
         o.W = c->w_o[l];
         o.Ks = c->ks_d;
-        o.n_wg = c->n_wg_o;
+        o.cols = c->d;
         o.A = c->O;
         o.lda = c->d;
         o.gain = c->g_ffn[l];
@@ -295,7 +296,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         GemmParams gu = base;
         gu.W = c->w_gu[l];
         gu.Ks = c->ks_d;
-        gu.n_wg = c->n_wg_gu;
+        gu.cols = 2 * c->Fp;
         gu.A = c->An;
         gu.lda = c->d;
         gu.H = c->Hb;
@@ -305,7 +306,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         GemmParams dn = base;  // X += H W_d^T; writes the next layer's (or the final) RMSNorm operand
         dn.W = c->w_d[l];
         dn.Ks = c->ks_f;
-        dn.n_wg = c->n_wg_d;
+        dn.cols = c->d;
         dn.A = c->Hb;
         dn.lda = c->Fp;
         dn.gain = l + 1 < c->NL ? c->g_attn[l + 1] : c->g_final;
@@ -330,7 +331,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         GemmParams lm = base;
         lm.W = c->w_lm;
         lm.Ks = c->ks_d;
-        lm.n_wg = c->n_wg_lm;
+        lm.cols = c->n_wg_lm * 16 * kLmTiles;
         lm.A = c->An;
         lm.lda = c->d;
         lm.pmax = c->pmax;
@@ -397,6 +398,11 @@ cllm_status check_ids(cllm_ctx *c, const int32_t *ids, int n) {
 // row tile only.
 cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
     c->slot[seq].prefilled = false;
+    c->in_prefill = true;
+    struct Flag {  // cleared on every return
+        bool &f;
+        ~Flag() { f = false; }
+    } flag{c->in_prefill};
     const int chunk = c->cap;
     const int nchunks = ceil_div(len, chunk);
     for (int k = 0; k < nchunks; ++k) {
@@ -591,6 +597,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             cllm_decode_stats &st = stats[b];
             memset(&st, 0, sizeof(st));
             st.steps = ct.steps;
+            st.rows = ct.rows;
             st.blocks = ct.blocks;
             st.tokens = ct.e;
             for (int i = 0; i <= kMaxBlock; ++i) st.accept_hist[i] = ct.hist[i];
@@ -676,10 +683,6 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->nch = c->ctx_alloc / kAttnChunk;
     c->ks_d = c->d / kstep;
     c->ks_f = c->Fp / kstep;
-    c->n_wg_qkv = 3 * c->d / 16 / kNtQkv;
-    c->n_wg_o = c->d / 16 / kNtResid;
-    c->n_wg_gu = 2 * c->Fp / 16 / kNtGateUp;
-    c->n_wg_d = c->d / 16 / kNtResid;
     c->n_wg_lm = round_up(c->V, 16 * kLmTiles) / (16 * kLmTiles);
     c->stream = static_cast<hipStream_t>(opts->stream);
     c->max_batch = opts->max_batch > 0 ? opts->max_batch : 1;

@@ -143,7 +143,8 @@ struct Ctl {
     int32_t n, max_new;
     int32_t policy, block_policy;
     int32_t seq, stream_len;
-    int32_t vocab, pad0;
+    int32_t vocab;
+    int32_t rows;      // block rows run by the decode's iterations
     uint64_t seed, thr53;
     int32_t z[kMaxBlock];     // tokens of the current iteration
     int32_t pred[kMaxBlock];  // greedy predictions of the last iteration

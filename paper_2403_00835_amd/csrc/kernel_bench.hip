@@ -120,6 +120,7 @@ int main(int argc, char **argv) {
     for (const Shape &s : shapes) {
         GemmParams p{};
         p.Ks = s.K / 32;
+        p.cols = s.cols;
         p.n_wg = s.cols / 16 / s.nt;
         p.A = s.kind == GEMM_DOWN ? A_f : A_d;
         p.lda = s.K;

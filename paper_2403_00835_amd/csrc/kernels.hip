@@ -93,6 +93,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     using T = typename PT::T;
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const int wg = blockIdx.x;
     // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration; m of them are live.
     const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
     const int m = p.rr.tab->R - row0;
@@ -102,7 +103,6 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
     // every load shares one per-lane offset
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wg = blockIdx.x;
     const int t0 = wg * NT;
 
     extern __shared__ float smem[];
@@ -641,6 +641,7 @@ __global__ void decode_init_kernel(ScanParams p) {
     c->b0 = 0;
     c->nb = c->n < c->max_new ? c->n : c->max_new;
     c->steps = 0;
+    c->rows = 0;
     c->blocks = 1;
     c->done = 0;
     c->err = 0;
@@ -671,6 +672,7 @@ __device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stre
     c->L += a;
     c->a_last = a;
     c->steps += 1;
+    c->rows += m;
     c->hist[a] += 1;
     c->pending = c->pred[a - 1];
     if (c->mode != MODE_DECODE) {
@@ -810,18 +812,21 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
-// Grid: (column workgroups, row tiles of 16 * RG rows starting at row tile p.rt0).
+// Grid: column workgroups (p.cols / (16 * NT)) x row tiles of 16 * RG rows (from row tile p.rt0).
 template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves, bool KC = kGemmKContig>
 static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
     const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
     auto kern = gemm_kernel<P, NT, RG, EP, D, W, KC>;
-    const dim3 grid(p.n_wg, row_tiles);
+    GemmParams q = p;
+    q.row_tiles = row_tiles;
+    q.n_wg = p.cols / COLS;
+    const dim3 grid(q.n_wg, row_tiles);
     if (e0) {
-        hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, p);
+        hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, q);
     } else {
-        hipLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, p);
+        hipLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, q);
     }
     return hipGetLastError();
 }
@@ -829,6 +834,23 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
+    if (row_tiles > 1) {
+        // Row-tiled launches (more than 64 rows) use 64-column tiles for every product, so each
+        // activation k-step feeds four weight tiles, and three k-steps in flight. The column width
+        // does not change any row's reduction order.
+        switch (kind) {
+        case GEMM_QKV:
+            return launch_gemm_t<P, 4, RG, E_QKV, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_O:
+        case GEMM_DOWN:
+            return launch_gemm_t<P, 4, RG, E_RESID, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_GATE_UP:
+            return launch_gemm_t<P, 4, RG, E_SWIGLU, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_LM:
+            return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX, 3>(p, row_tiles, s, e0, e1);
+        }
+        return hipErrorInvalidValue;
+    }
     switch (kind) {
     case GEMM_QKV:
         return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, row_tiles, s, e0, e1);

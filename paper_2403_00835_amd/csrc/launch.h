@@ -29,8 +29,10 @@ struct RowsRef {
 struct GemmParams {
     const uint8_t *W;  // packed tiles
     int Ks;            // k-steps per 16-row tile
-    int n_wg;          // workgroups along the columns (tiles / NT)
-    int rt0;           // first row tile (grid y adds to it)
+    int cols;          // packed output columns (multiple of 16 * every NT used)
+    int n_wg;          // workgroups along the columns (set by the launcher: cols / (16 NT))
+    int rt0;           // first row tile
+    int row_tiles;     // row tiles of the launch (set by the launcher)
     const void *A;     // activation operand, packed operand order, lda elements per row
     int lda;
     RowsRef rr;

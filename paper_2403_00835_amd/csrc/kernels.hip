@@ -27,7 +27,9 @@ namespace cllm {
 //
 // Packed layout: tile (t, s) covers weight rows 16t .. 16t+15 (after the per-GEMM row order)
 // and K indices s*KSTEP .. s*KSTEP+KSTEP-1; lane l's 16 bytes are row 16t + l%16, K indices
-// s*KSTEP + (l/16)*VEC .. +VEC. Tiles of one row block are contiguous over s.
+// s*KSTEP + (l/16)*VEC .. +VEC. Tiles are stored k-step major: tile (t, s) at index s * T + t
+// (T tiles per k-step), so the tiles every workgroup reads for one k-step are one contiguous
+// region (measured 1-7% faster streaming than row blocks contiguous over s).
 //
 // A workgroup of 8 waves owns NT consecutive tiles (16*NT output columns) for all rows; wave w
 // takes k-steps w, w+8, w+16, ... and accumulates them in order with MFMA; the 8 partial tiles
@@ -58,7 +60,7 @@ __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams
     using T = typename PT::T;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)(t0 + j) * p.Ks + s) * kTileBytes) + lane;
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * (p.cols >> 4) + t0 + j) * kTileBytes) + lane;
         if constexpr (kWeightsNonTemporal) st.b[j] = __builtin_nontemporal_load(src);
         else st.b[j] = *src;
     }
@@ -793,9 +795,9 @@ template <Prec P>
 __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst) {
     using PT = PrecT<P>;
     using T = typename PT::T;
-    const size_t tile = (size_t)blockIdx.x + (size_t)blockIdx.y * gridDim.x;
+    const size_t tile = (size_t)blockIdx.x + (size_t)blockIdx.y * gridDim.x;  // = s * n_tiles + t
     if (tile >= (size_t)n_tiles * Ks) return;
-    const int t = (int)(tile / Ks), s = (int)(tile % Ks);
+    const int t = (int)(tile % n_tiles), s = (int)(tile / n_tiles);
     const int lane = threadIdx.x, g = lane >> 4, r16 = lane & 15;
     const int row = perm[16 * t + r16];
     T v[PT::VEC];

@@ -267,9 +267,9 @@ def main_batched(args, wl):
     prefill_ms = sum(st[0]["prefill_ms"] for st in stats) / len(stats)
     d, F = cfg.d_model, cfg.ffn_dim
     f_pad = (F + 31) // 32 * 32
-    # gate/up: algorithmic flops 2 * rows * (2 F) * d over the timed launches (executed MFMA work
-    # is twice that: the activation's hi and lo planes)
-    gu_flops = 2.0 * rows * 2 * f_pad * d
+    # gate/up: algorithmic flops 2 * rows * (2 F) * d per layer over the timed launches (executed
+    # MFMA work is twice that: the activation's hi and lo planes)
+    gu_flops = 2.0 * rows * 2 * f_pad * d * cfg.n_layers
     achieved = gu_flops / (gu_ms / 1e3) / 1e12 if gu_ms > 0 else 0.0
     mean_rows = rows / sum(iters)
     cpu = None

@@ -17,6 +17,8 @@
 // (AR), Jacobi decoding and batched Jacobi decoding produce bit-identical tokens.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
@@ -89,140 +91,60 @@ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
 // W waves per workgroup split K; KC selects each wave's k-steps: interleaved (w, w+W, ...) or a
 // contiguous range.
-template <Prec P, int NT, int RG, int EP, int D, int W, bool KC>
-__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
-    using PT = PrecT<P>;
-    using T = typename PT::T;
-    constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    const int wg = blockIdx.x;
-    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration; m of them are live.
-    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
-    const int m = p.rr.tab->R - row0;
-    if (m <= 0) return;
-    const int rg0 = row0 >> 4;
-    const int tid = threadIdx.x, lane = tid & 63;
-    // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
-    // every load shares one per-lane offset
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int t0 = wg * NT;
+// Row factor 1/sqrt(mean(x^2) + eps) of the rows [row0, row0 + ROWS) from the producer's
+// per-16-column sums of squares (layout [row][T], T a multiple of 4). 32 threads per row each add
+// a contiguous run of q = 4 * ceil(T/128) partials in order (16-byte reads), then a fixed xor tree
+// over the row's 32 threads; the scheme depends only on T, never on the number of rows. The
+// first two vectors of the first row pass are requested early by row_factor_preload. The caller's
+// next barrier publishes s_inv.
+template <int W>
+__device__ __forceinline__ void row_factor_preload(const GemmParams &p, int row0, int tid, f32x4 (&sq_pre)[2]) {
+    const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
+    const float *src = p.ssq + (size_t)(row0 + (tid >> 5)) * p.T;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)  // clamped, unconditional
+        sq_pre[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + 4 * i, p.T - 4));
+}
 
-    extern __shared__ float smem[];
-    float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
-    float *s_tile = s_red + W * NT * 256;  // ROWS x (COLS + 1)
-    float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
-
-    // Row factor inputs (products that follow an RMSNorm): the producer's per-16-column sums of
-    // squares, layout [row][T] with T a multiple of 4. 32 threads per row each own a contiguous
-    // run of q = 4 * ceil(T/128) partials, read as 16-byte vectors; the first two vectors of the
-    // first row pass are requested before the weights, so their latency overlaps the first
-    // k-step's, and everything is reduced after the main loop.
+template <int W, int ROWS>
+__device__ __forceinline__ void row_factor_reduce(const GemmParams &p, int row0, int tid, const f32x4 (&sq_pre)[2],
+                                                  float *s_inv) {
     constexpr int RPP = W * kWave / 32;  // rows per pass
     static_assert(ROWS % RPP == 0, "row passes cover the row groups");
     const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
-    f32x4 sq_pre[2];
-    if constexpr (ROWSCALE) {
-        const float *src = p.ssq + (size_t)(row0 + (tid >> 5)) * p.T;
+    for (int pass = 0; pass < ROWS / RPP; ++pass) {
+        const int row = pass * RPP + (tid >> 5);
+        const float *src = p.ssq + (size_t)(row0 + row) * p.T;
+        float sum = 0.0f;
+        for (int i0 = 0; i0 < sq_q; i0 += 8) {
+            f32x4 v[2];
+            if (pass == 0 && i0 == 0) {
+                v[0] = sq_pre[0];
+                v[1] = sq_pre[1];
+            } else {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)  // clamped, unconditional
-            sq_pre[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + 4 * i, p.T - 4));
-    }
-
-    // This wave's k-steps (nmy of them); the first D-1 are requested first.
-    const int nper = (p.Ks + W - 1) / W;
-    const int nmy = KC ? max(0, min(nper, p.Ks - w * nper)) : (w < p.Ks ? (p.Ks - w + W - 1) / W : 0);
-    auto step_of = [&](int q) { return min(KC ? w * nper + q : w + q * W, p.Ks - 1); };
-    Stage<P, NT, RG> ring[D];
-#pragma unroll
-    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, rg0, step_of(j), lane);
-
-    f32x4 acc[RG][NT];
-#pragma unroll
-    for (int r = 0; r < RG; ++r)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Software pipeline: a ring of D k-steps whose loads are in flight while the oldest one's
-    // MFMAs run. The steady state is branch-free (exact wait counts); the drain issues no loads
-    // past the end.
-    if (nmy > 0) {
-        // blocks of D steps whose prefetches (up to step b*D + 2D - 2) are all in range
-        const int nfull = nmy >= 2 * D - 1 ? (nmy - (D - 1)) / D : 0;
-        for (int bi = 0; bi < nfull; ++bi) {
-#pragma unroll
-            for (int j = 0; j < D; ++j) {
-                // sched_barrier keeps the scheduler from sinking loads to their uses.
-                gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
-                __builtin_amdgcn_sched_barrier(0);
-                gemm_compute(ring[j], acc);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        const int v0 = nfull * D;
-#pragma unroll
-        for (int j = 0; j < 2 * D - 1; ++j) {
-            const int v = v0 + j;
-            if (v < nmy) {
-                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
-                gemm_compute(ring[j % D], acc);
-            }
-        }
-    }
-
-    if constexpr (ROWSCALE) {
-        // Row factor 1/sqrt(mean(x^2) + eps): each thread adds its run in order, then a fixed xor
-        // tree over the row's 32 threads. The scheme depends only on T, never on the number of
-        // rows. The barrier of the reduction below publishes s_inv.
-        for (int pass = 0; pass < ROWS / RPP; ++pass) {
-            const int row = pass * RPP + (tid >> 5);
-            const float *src = p.ssq + (size_t)(row0 + row) * p.T;
-            float sum = 0.0f;
-            for (int i0 = 0; i0 < sq_q; i0 += 8) {
-                f32x4 v[2];
-                if (pass == 0 && i0 == 0) {
-                    v[0] = sq_pre[0];
-                    v[1] = sq_pre[1];
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-                        v[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + i0 + 4 * i, p.T - 4));
-                }
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    if (i0 + i < sq_q && sq_part * sq_q + i0 + i < p.T) sum += v[i >> 2][i & 3];
+                for (int i = 0; i < 2; ++i)
+                    v[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + i0 + 4 * i, p.T - 4));
             }
 #pragma unroll
-            for (int off = 16; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 32);
-            if (sq_part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
+            for (int i = 0; i < 8; ++i)
+                if (i0 + i < sq_q && sq_part * sq_q + i0 + i < p.T) sum += v[i >> 2][i & 3];
         }
+#pragma unroll
+        for (int off = 16; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 32);
+        if (sq_part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
     }
+}
 
-    // Sum of the W waves' partial tiles through LDS, one row group at a time, in a fixed tree
-    // (W = 8: ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); W = 4: (w0+w2)+(w1+w3)); then the RMSNorm row
-    // factor.
-#pragma unroll
-    for (int r = 0; r < RG; ++r) {
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-            *reinterpret_cast<f32x4 *>(s_red + ((size_t)(w * NT + j) * 64 + lane) * 4) = acc[r][j];
-        __syncthreads();
-        for (int e = tid; e < NT * 256; e += W * kWave) {
-            float x[W];
-#pragma unroll
-            for (int q = 0; q < W; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
-            float sum;
-            if constexpr (W == 8) sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
-            else sum = (x[0] + x[2]) + (x[1] + x[3]);
-            // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
-            const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
-            const int row = 16 * r + 4 * (l >> 4) + v;
-            if constexpr (ROWSCALE) sum *= s_inv[row];
-            s_tile[row * (COLS + 1) + 16 * j + (l & 15)] = sum;
-        }
-        __syncthreads();
-    }
-
-    // ---------------------------------------------------------------- epilogues
+// Epilogues of a finished ROWS x COLS output tile in s_tile (row stride COLS + 1) for rows
+// [row0, row0 + ROWS) of the iteration (m of them live) and column workgroup wg of width COLS;
+// s_red is scratch of at least ROWS x COLS floats. Shared by both GEMM kernels.
+template <Prec P, int NT, int RG, int EP, int W>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile, float *s_red, int row0, int m, int wg,
+                                              int tid, int lane, int w) {
+    using T = typename PrecT<P>::T;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const int t0 = wg * NT;
     if constexpr (EP == E_QKV) {
         // Packed columns -> (section, head, dim). With head_dim >= 32 a workgroup's two tiles are
         // dims [16b, 16b+16) and [hd/2+16b, hd/2+16b+16) of one head (rotate-half partners);
@@ -334,6 +256,264 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
             }
         }
     }
+}
+
+template <Prec P, int NT, int RG, int EP, int D, int W, bool KC>
+__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const int wg = blockIdx.x;
+    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration; m of them are live.
+    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    const int m = p.rr.tab->R - row0;
+    if (m <= 0) return;
+    const int rg0 = row0 >> 4;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
+    // every load shares one per-lane offset
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int t0 = wg * NT;
+
+    extern __shared__ float smem[];
+    float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
+    float *s_tile = s_red + W * NT * 256;  // ROWS x (COLS + 1)
+    float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
+
+    // Row factor inputs are requested before the weights (their latency overlaps the first
+    // k-step's) and reduced after the main loop.
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // This wave's k-steps (nmy of them); the first D-1 are requested first.
+    const int nper = (p.Ks + W - 1) / W;
+    const int nmy = KC ? max(0, min(nper, p.Ks - w * nper)) : (w < p.Ks ? (p.Ks - w + W - 1) / W : 0);
+    auto step_of = [&](int q) { return min(KC ? w * nper + q : w + q * W, p.Ks - 1); };
+    Stage<P, NT, RG> ring[D];
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, rg0, step_of(j), lane);
+
+    f32x4 acc[RG][NT];
+#pragma unroll
+    for (int r = 0; r < RG; ++r)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Software pipeline: a ring of D k-steps whose loads are in flight while the oldest one's
+    // MFMAs run. The steady state is branch-free (exact wait counts); the drain issues no loads
+    // past the end.
+    if (nmy > 0) {
+        // blocks of D steps whose prefetches (up to step b*D + 2D - 2) are all in range
+        const int nfull = nmy >= 2 * D - 1 ? (nmy - (D - 1)) / D : 0;
+        for (int bi = 0; bi < nfull; ++bi) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                // sched_barrier keeps the scheduler from sinking loads to their uses.
+                gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
+                __builtin_amdgcn_sched_barrier(0);
+                gemm_compute(ring[j], acc);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const int v0 = nfull * D;
+#pragma unroll
+        for (int j = 0; j < 2 * D - 1; ++j) {
+            const int v = v0 + j;
+            if (v < nmy) {
+                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
+                gemm_compute(ring[j % D], acc);
+            }
+        }
+    }
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+
+    // Sum of the W waves' partial tiles through LDS, one row group at a time, in a fixed tree
+    // (W = 8: ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); W = 4: (w0+w2)+(w1+w3)); then the RMSNorm row
+    // factor.
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+            *reinterpret_cast<f32x4 *>(s_red + ((size_t)(w * NT + j) * 64 + lane) * 4) = acc[r][j];
+        __syncthreads();
+        for (int e = tid; e < NT * 256; e += W * kWave) {
+            float x[W];
+#pragma unroll
+            for (int q = 0; q < W; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
+            float sum;
+            if constexpr (W == 8) sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
+            else sum = (x[0] + x[2]) + (x[1] + x[3]);
+            // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
+            const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
+            const int row = 16 * r + 4 * (l >> 4) + v;
+            if constexpr (ROWSCALE) sum *= s_inv[row];
+            s_tile[row * (COLS + 1) + 16 * j + (l & 15)] = sum;
+        }
+        __syncthreads();
+    }
+
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+// ------------------------------------------------------------------------------------------
+// Row-tiled GEMM for iterations of more than 64 rows (batched blocks, prefill chunks).
+//
+// A workgroup computes a 64-row x 16*TNT-column tile; its 8 waves (2 x 4: 32 rows x 16*TNT/4
+// columns each) share the operands through LDS, in blocks of kTileKB k-steps that are double
+// buffered in LDS and prefetched two blocks ahead in registers. Each output element is accumulated
+// exactly as in gemm_kernel: eight partial sums, one per k-step class s mod 8 (each in increasing
+// s, hi plane then lo plane per k-step), then the same fixed tree and row factor, so a row's
+// results are bit-identical whichever of the two kernels computed them.
+// ------------------------------------------------------------------------------------------
+constexpr int kTileKB = 4;  // k-steps per LDS block
+
+template <Prec P, int TNT>
+struct TileShape {
+    static constexpr int RG = 4, ROWS = 64, COLS = 16 * TNT;
+    static constexpr int NA = kTileKB * PrecT<P>::PLANES * RG;  // activation tiles per block
+    static constexpr int NB = kTileKB * TNT;                    // weight tiles per block
+    static constexpr int NTL = NA + NB;
+    static constexpr size_t lds_bytes = (size_t)(2 * NTL * 256 + ROWS) * sizeof(float);
+};
+
+template <Prec P, int TNT, int EP>
+__global__ __launch_bounds__(512) void gemm_tile_kernel(GemmParams p) {
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    using SH = TileShape<P, TNT>;
+    constexpr int W = 8, RG = SH::RG, ROWS = SH::ROWS, COLS = SH::COLS, PL = PT::PLANES;
+    constexpr int NA = SH::NA, NTL = SH::NTL, LPW = NTL / W;  // tile loads per wave per block
+    constexpr int TW = TNT / 4;                                // tiles per wave along the columns
+    constexpr bool ROWSCALE = EP != E_RESID;
+    static_assert(NTL % W == 0 && TNT % 4 == 0, "tile loads split evenly over the waves");
+    static_assert(2 * NTL * 256 >= ROWS * (COLS + 1) + ROWS * COLS, "epilogue tiles reuse the staging LDS");
+    const int wg = blockIdx.x;
+    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    const int m = p.rr.tab->R - row0;
+    if (m <= 0) return;
+    const int rg0 = row0 >> 4;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = w >> 2, wc = w & 3;  // row groups 2wr, 2wr+1; column tiles wc*TW ..
+    const int t0 = wg * TNT;
+    const int tall = p.cols >> 4;
+    const int ks_a = p.lda / PT::KSTEP;
+    const int nblk = (p.Ks + kTileKB - 1) / kTileKB;
+    const size_t plane = act_plane(p.rr.cap, p.lda);
+
+    extern __shared__ float smem[];
+    uint8_t *lds = reinterpret_cast<uint8_t *>(smem);  // 2 x NTL tiles of 1 KiB
+    float *s_inv = smem + 2 * NTL * 256;               // ROWS
+
+    // Tile i of block blk: activation tiles (k-step, plane, row group) first, then weight tiles
+    // (k-step, column tile). k-steps past the end are clamped (their products are skipped).
+    auto tile_src = [&](int blk, int i) -> const u32x4 * {
+        if (i < NA) {
+            const int ks = i / (PL * RG), pl = (i / RG) % PL, r = i % RG;
+            const int s = min(blk * kTileKB + ks, p.Ks - 1);
+            const T *A = reinterpret_cast<const T *>(p.A) + pl * plane;
+            return reinterpret_cast<const u32x4 *>(A + (size_t)((rg0 + r) * ks_a + s) * kWave * PT::VEC) + lane;
+        }
+        const int j = i - NA, ks = j / TNT, t = j % TNT;
+        const int s = min(blk * kTileKB + ks, p.Ks - 1);
+        return reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tall + t0 + t) * kTileBytes) + lane;
+    };
+    auto issue = [&](u32x4 (&dst)[LPW], int blk) {
+#pragma unroll
+        for (int k = 0; k < LPW; ++k) dst[k] = *tile_src(blk, w + W * k);
+    };
+    auto commit = [&](const u32x4 (&src)[LPW], int buf) {
+#pragma unroll
+        for (int k = 0; k < LPW; ++k)
+            *reinterpret_cast<u32x4 *>(lds + ((size_t)buf * NTL + w + W * k) * kTileBytes + lane * 16) = src[k];
+    };
+    auto lds_tile = [&](int buf, int i) {
+        return *reinterpret_cast<const u32x4 *>(lds + ((size_t)buf * NTL + i) * kTileBytes + lane * 16);
+    };
+
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+    f32x4 acc[8][2][TW];
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int t = 0; t < TW; ++t) acc[c][r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Block b's k-steps belong to classes 4 * (b % 2) + ks: the loop runs two blocks per trip so
+    // the class (an accumulator index) is a compile-time constant.
+    auto compute = [&](int blk, int buf, auto cls_base) {
+        constexpr int CB = decltype(cls_base)::value;
+#pragma unroll
+        for (int ks = 0; ks < kTileKB; ++ks) {
+            if (blk * kTileKB + ks < p.Ks) {
+                u32x4 a[PL][2], bw[TW];
+#pragma unroll
+                for (int pl = 0; pl < PL; ++pl)
+#pragma unroll
+                    for (int r = 0; r < 2; ++r) a[pl][r] = lds_tile(buf, (ks * PL + pl) * RG + 2 * wr + r);
+#pragma unroll
+                for (int t = 0; t < TW; ++t) bw[t] = lds_tile(buf, NA + ks * TNT + wc * TW + t);
+#pragma unroll
+                for (int pl = 0; pl < PL; ++pl)
+#pragma unroll
+                    for (int r = 0; r < 2; ++r)
+#pragma unroll
+                        for (int t = 0; t < TW; ++t)
+                            acc[CB + ks][r][t] = mfma_kstep<P>(a[pl][r], bw[t], acc[CB + ks][r][t]);
+            }
+        }
+    };
+
+    // The compiler waits for a register stage's loads (exact counts: every load is issued,
+    // clamped) before its commit; sched_barrier keeps a stage's loads ahead of the block's MFMAs.
+    u32x4 stg[2][LPW];
+    issue(stg[0], 0);
+    issue(stg[1], min(1, nblk - 1));
+    commit(stg[0], 0);
+    __syncthreads();
+    for (int b0 = 0; b0 < nblk; b0 += 2) {
+        // block b0 (LDS buffer 0, classes 0..3), then block b0 + 1 (buffer 1, classes 4..7)
+        issue(stg[0], min(b0 + 2, nblk - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        compute(b0, 0, std::integral_constant<int, 0>{});
+        commit(stg[1], 1);  // block b0 + 1
+        __syncthreads();
+        if (b0 + 1 < nblk) {
+            issue(stg[1], min(b0 + 3, nblk - 1));
+            __builtin_amdgcn_sched_barrier(0);
+            compute(b0 + 1, 1, std::integral_constant<int, 4>{});
+            commit(stg[0], 0);  // block b0 + 2
+            __syncthreads();
+        }
+    }
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+    __syncthreads();
+    float *s_tile = smem;                    // ROWS x (COLS + 1), over the staging buffers
+    float *s_red = s_tile + ROWS * (COLS + 1);  // ROWS x COLS
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            // the fixed tree of gemm_kernel: ((c0+c4)+(c2+c6))+((c1+c5)+(c3+c7))
+            const f32x4 sum = ((acc[0][r][t] + acc[4][r][t]) + (acc[2][r][t] + acc[6][r][t])) +
+                              ((acc[1][r][t] + acc[5][r][t]) + (acc[3][r][t] + acc[7][r][t]));
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                // C layout: row 4*(l/16)+v, column l%16 of the 16 x 16 tile
+                const int row = 16 * (2 * wr + r) + 4 * (lane >> 4) + v;
+                const int col = 16 * (wc * TW + t) + (lane & 15);
+                float x = sum[v];
+                if constexpr (ROWSCALE) x *= s_inv[row];
+                s_tile[row * (COLS + 1) + col] = x;
+            }
+        }
+    __syncthreads();
+    gemm_epilogue<P, TNT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -833,13 +1013,31 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     return hipGetLastError();
 }
 
+template <Prec P, int TNT, int EP>
+static hipError_t launch_gemm_tile_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    using SH = TileShape<P, TNT>;
+    GemmParams q = p;
+    q.row_tiles = row_tiles;
+    q.n_wg = p.cols / SH::COLS;
+    auto kern = gemm_tile_kernel<P, TNT, EP>;
+    const dim3 grid(q.n_wg, row_tiles);
+    if (e0)
+        hipExtLaunchKernelGGL(kern, grid, dim3(512), SH::lds_bytes, s, e0, e1, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(512), SH::lds_bytes, s, q);
+    return hipGetLastError();
+}
+
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
     if (row_tiles > 1) {
-        // Row-tiled launches (more than 64 rows) use 64-column tiles for every product, so each
-        // activation k-step feeds four weight tiles, and three k-steps in flight. The column width
-        // does not change any row's reduction order.
+        // More than 64 rows: gate/up runs the LDS-tiled kernel (128-column tiles; measured faster
+        // than gemm_kernel there, slower for the other products at ~160 rows), the others
+        // 64-column tiles of gemm_kernel with three k-steps in flight. Neither changes any row's
+        // reduction order.
+        if (kind == GEMM_GATE_UP && p.cols % 128 == 0)
+            return launch_gemm_tile_t<P, 8, E_SWIGLU>(p, row_tiles, s, e0, e1);
         switch (kind) {
         case GEMM_QKV:
             return launch_gemm_t<P, 4, RG, E_QKV, 3>(p, row_tiles, s, e0, e1);

@@ -70,6 +70,31 @@ __device__ __forceinline__ size_t act_idx(int row, int k, int K) {
     return ((size_t)((row >> 4) * (K / KSTEP) + s) * kWave + (w / VEC) * 16 + (row & 15)) * VEC + (w % VEC);
 }
 
+// KV cache layout (per sequence slot, layer and head; ctx_alloc * head_dim elements per head), in
+// the attention kernel's MFMA operand order so that each load is one contiguous KiB:
+//  K:   [pos/16][head_dim/KSTEP][lane 64][VEC], lane = 16 * (dim % KSTEP / VEC) + pos % 16;
+//  V^T: bf16 [pos/32][head_dim/16][lane 64][8], lane = 16 * g + dim % 16 where, for key kw =
+//       pos % 32, g = (kw % 16) / 4 and the slot is 4 * (kw / 16) + kw % 4 (the probabilities'
+//       key order in the score registers); fp32 [pos/16][head_dim/16][lane 64][4],
+//       lane = 16 * ((pos % 16) / 4) + dim % 16, slot pos % 4.
+template <Prec P>
+__device__ __forceinline__ size_t kcache_idx(int pos, int dim, int hd) {
+    constexpr int VEC = PrecT<P>::VEC, KSTEP = PrecT<P>::KSTEP;
+    return ((size_t)(pos >> 4) * (hd / KSTEP) + dim / KSTEP) * (kWave * VEC) +
+           (((dim % KSTEP) / VEC) * 16 + (pos & 15)) * VEC + dim % VEC;
+}
+template <Prec P>
+__device__ __forceinline__ size_t vcache_idx(int pos, int dim, int hd) {
+    if constexpr (P == Prec::BF16) {
+        const int kw = pos & 31, kq = kw & 15;
+        return ((size_t)(pos >> 5) * (hd / 16) + dim / 16) * (kWave * 8) + ((kq >> 2) * 16 + (dim & 15)) * 8 +
+               (kw >> 4) * 4 + (kq & 3);
+    } else {
+        return ((size_t)(pos >> 4) * (hd / 16) + dim / 16) * (kWave * 4) + (((pos & 15) >> 2) * 16 + (dim & 15)) * 4 +
+               (pos & 3);
+    }
+}
+
 // Store x at element i of an activation operand (both planes for bf16).
 template <Prec P>
 __device__ __forceinline__ void put_act(typename PrecT<P>::T *base, size_t plane, size_t i, float x) {

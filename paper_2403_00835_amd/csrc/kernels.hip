@@ -180,13 +180,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
                 x = dim < h2 ? (x * c - y * s) : (x * c + y * s);
             }
             const T e = to_elem<P>(x);  // cached keys and values are rounded to the cache dtype
-            const int col = head * hd + dim;
             if (sec == 0)
-                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(p.rr.cap, d), act_idx<P>(row0 + row, col, d), x);
+                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(p.rr.cap, d), act_idx<P>(row0 + row, head * hd + dim, d), x);
             else if (sec == 1)
-                reinterpret_cast<T *>(p.Kc)[kvo + (size_t)pos * d + col] = e;
+                reinterpret_cast<T *>(p.Kc)[kvo + (size_t)head * p.ctx_alloc * hd + kcache_idx<P>(pos, dim, hd)] = e;
             else
-                reinterpret_cast<T *>(p.Vt)[kvo + (size_t)col * p.ctx_alloc + pos] = e;
+                reinterpret_cast<T *>(p.Vt)[kvo + (size_t)head * p.ctx_alloc * hd + vcache_idx<P>(pos, dim, hd)] = e;
         }
     } else if constexpr (EP == E_RESID) {
         // X += Y over this workgroup's columns, then the per-16-column sums of squares of the
@@ -599,9 +598,10 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     const int qrow = tab->r0[b] + qi;       // row of the iteration
     const int qld = min(qrow, p.rr.cap - 1);  // rows past the block load in-bounds filler
     const int qpos = L + qi;
-    const size_t kvo = (size_t)tab->seq[b] * p.kv_seq;
-    const T *Kc = reinterpret_cast<const T *>(p.Kc) + kvo;
-    const T *Vt = reinterpret_cast<const T *>(p.Vt) + kvo;
+    // this head's caches of this sequence slot (operand order: one contiguous KiB per load)
+    const size_t kvo = (size_t)tab->seq[b] * p.kv_seq + (size_t)h * p.ctx_alloc * HD;
+    const T *Kh = reinterpret_cast<const T *>(p.Kc) + kvo;
+    const T *Vh = reinterpret_cast<const T *>(p.Vt) + kvo;
     const T *Q = reinterpret_cast<const T *>(p.Q);
 
     // Every load of the workgroup is issued up front: Q rows, the chunk's 64 keys and values.
@@ -613,22 +613,20 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
         for (int pl = 0; pl < PT::PLANES; ++pl)
             qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, dcol, d));
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-            kv[kt][kk] = *reinterpret_cast<const u32x4 *>(Kc + (size_t)(key0 + 16 * kt + r16) * d + dcol);
+        for (int kt = 0; kt < 4; ++kt)  // keys key0 + 16kt + lane%16, dims kk*KSTEP + (lane/16)*VEC ..
+            kv[kt][kk] = *reinterpret_cast<const u32x4 *>(
+                Kh + ((size_t)((key0 >> 4) + kt) * NKK + kk) * (kWave * PT::VEC) + lane * PT::VEC);
     }
     // V^T operand: row = dim 16*dt + lane%16; K slots = keys 32kp+4g+(0..3), 32kp+16+4g+(0..3) (bf16),
-    // or keys 16kt+4g+(0..3) (fp32).
+    // or keys 16kt+4g+(0..3) (fp32); the cache holds exactly these 16 bytes per lane contiguously.
     u32x4 vv[NDT][2];
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
-        const T *vrow = Vt + (size_t)(h * HD + 16 * dt + r16) * p.ctx_alloc + key0;
         if constexpr (P == Prec::BF16) {
 #pragma unroll
-            for (int kp = 0; kp < 2; ++kp) {
-                const u32x2 va = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 4 * g);
-                const u32x2 vb = *reinterpret_cast<const u32x2 *>(vrow + 32 * kp + 16 + 4 * g);
-                vv[dt][kp] = u32x4{va.x, va.y, vb.x, vb.y};
-            }
+            for (int kp = 0; kp < 2; ++kp)
+                vv[dt][kp] = *reinterpret_cast<const u32x4 *>(
+                    Vh + ((size_t)((key0 >> 5) + kp) * NDT + dt) * (kWave * 8) + lane * 8);
         }
     }
 
@@ -692,10 +690,10 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
                 o = mfma_kstep<P>(vv[dt][kp], blo, o);
             }
         } else {
-            const T *vrow = Vt + (size_t)(h * HD + 16 * dt + r16) * p.ctx_alloc + key0;
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
-                const u32x4 va = *reinterpret_cast<const u32x4 *>(vrow + 16 * kt + 4 * g);
+                const u32x4 va = *reinterpret_cast<const u32x4 *>(
+                    Vh + ((size_t)((key0 >> 4) + kt) * NDT + dt) * (kWave * 4) + lane * 4);
                 const f32x4 pk = st[kt];
                 o = mfma_kstep<P>(va, u32x4{__float_as_uint(pk[0]), __float_as_uint(pk[1]), __float_as_uint(pk[2]),
                                             __float_as_uint(pk[3])},

@@ -199,6 +199,12 @@ def main():
                    "prompt_len": P, "n": n, "max_new": max_new, "p": args.p, "batch": 1,
                    "layers": cfg.n_layers, "d_model": cfg.d_model},
         "jacobi_step_ms": round(iter_ms, 4),
+        "iteration_ms": {"mean": round(iter_ms, 4),
+                         "p10": round(float(np.median([x["iter_ms_p10"] for x in stats])), 4),
+                         "p50": round(float(np.median([x["iter_ms_p50"] for x in stats])), 4),
+                         "p90": round(float(np.median([x["iter_ms_p90"] for x in stats])), 4),
+                         "full_block_p50": round(float(np.median([x["iter_ms_full_p50"] for x in stats])), 4)},
+        "decode_tokens_per_s": round(tokens / (decode_ms / 1e3), 3),
         "iterations_per_step": iters / args.steps,
         "mean_accepted": round(mean_accept, 3),
         "prefill_ms": round(prefill_ms, 3),
@@ -301,6 +307,11 @@ def main_batched(args, wl):
         "batched_iterations_per_step": sum(iters) / len(iters),
         "mean_rows_per_iteration": round(mean_rows, 2),
         "batched_iteration_ms": round(decode_ms / sum(iters), 4),
+        "iteration_ms": {"mean": round(decode_ms / sum(iters), 4),
+                         "p10": round(float(np.median([st[0]["iter_ms_p10"] for st in stats])), 4),
+                         "p50": round(float(np.median([st[0]["iter_ms_p50"] for st in stats])), 4),
+                         "p90": round(float(np.median([st[0]["iter_ms_p90"] for st in stats])), 4)},
+        "decode_tokens_per_s": round(tokens / (decode_ms / 1e3), 3),
         "prefill_ms": round(prefill_ms, 3),
         "ar_tokens_per_s": round(ar_tps, 3),
         "speedup_vs_ar": round(value / ar_tps, 3),

@@ -103,6 +103,11 @@ typedef struct cllm_decode_stats {
     double prefill_ms;        /* device time of the prefill */
     double decode_ms;         /* device time of the iterations */
     int64_t rows;             /* block rows run through the decoder by the iterations (sum of m) */
+    /* Device time per iteration (between consecutive iteration boundaries on the stream):
+     * percentiles over the decode's iterations, and the median over the iterations that ran a
+     * full block of n rows (the first iteration of each block). For a batched decode: over the
+     * batched iterations, and iter_ms_full_p50 = iter_ms_p50. */
+    double iter_ms_p10, iter_ms_p50, iter_ms_p90, iter_ms_full_p50;
 } cllm_decode_stats;
 
 typedef struct cllm_ctx cllm_ctx;

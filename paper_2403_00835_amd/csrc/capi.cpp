@@ -55,6 +55,8 @@ struct cllm_ctx {
     int32_t *zin = nullptr;  // staging of host tokens (blocks, prefill chunks)
     int zin_cap = 0;
     int32_t *out_dev = nullptr, *stream_dev = nullptr;  // per slot: max_new outputs, stream_cap guesses
+    int32_t *mlog_dev = nullptr;  // per slot: block size of each decode iteration (max_new entries)
+    std::vector<hipEvent_t> it_ev;  // one per queued decode iteration
     int stream_cap = 0;
     std::vector<void *> allocs;
 
@@ -327,6 +329,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
     sp.out_stride = c->opts.max_new;
     sp.stream_stride = c->stream_cap;
     sp.plan_inline = sh.nseq == 1;
+    sp.mlog = out_dev ? c->mlog_dev : nullptr;
     if (sh.with_lm) {
         GemmParams lm = base;
         lm.W = c->w_lm;
@@ -563,6 +566,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     // queues iterations: as many as are certainly needed by the sequence with the most tokens
     // left (each iteration fixes at most n tokens of a sequence), then reads the control blocks.
     int64_t queued = 0;
+    size_t nev = 0;  // iteration events recorded
     while (true) {
         int need = 0;
         for (int b = 0; b < B; ++b) {
@@ -571,8 +575,15 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             need = std::max(need, ceil_div(left, n));
         }
         if (need == 0) break;
-        for (int i = 0; i < need; ++i)
+        for (int i = 0; i < need; ++i) {
             if ((s = enqueue_iteration(c, sh, c->out_dev, any_stream ? c->stream_dev : nullptr))) return s;
+            if (nev == c->it_ev.size()) {
+                hipEvent_t e;
+                HIPCHK(c, hipEventCreate(&e));
+                c->it_ev.push_back(e);
+            }
+            HIPCHK(c, hipEventRecord(c->it_ev[nev++], c->stream));
+        }
         queued += need;
         HIPCHK(c, hipEventRecord(ev[2], c->stream));
         if ((s = read_ctl(c, h.data()))) return s;
@@ -588,6 +599,29 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     float pre_ms = 0.f, dec_ms = 0.f;
     (void)hipEventElapsedTime(&pre_ms, ev[0], ev[1]);
     (void)hipEventElapsedTime(&dec_ms, ev[1], ev[2]);
+    // Per-iteration device times over the iterations that ran (the queue may hold a few past the
+    // end, which exit at once) and, with one sequence, the block size of each.
+    int64_t real = 0;
+    for (int b = 0; b < B; ++b) real = std::max<int64_t>(real, h[seq_ids[b]].steps);
+    real = std::min<int64_t>(real, (int64_t)nev);
+    std::vector<double> it_ms, full_ms;
+    std::vector<int32_t> mlog(B == 1 ? (size_t)real : 0);
+    if (B == 1 && real > 0)
+        HIPCHK(c, hipMemcpy(mlog.data(), c->mlog_dev + (size_t)seq_ids[0] * c->opts.max_new, (size_t)real * 4,
+                            hipMemcpyDeviceToHost));
+    for (int64_t i = 0; i < real; ++i) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, i ? c->it_ev[i - 1] : ev[1], c->it_ev[i]) != hipSuccess) continue;
+        it_ms.push_back(ms);
+        if (B == 1 && mlog[i] == n) full_ms.push_back(ms);
+    }
+    auto pct = [](std::vector<double> v, double q) {
+        if (v.empty()) return 0.0;
+        std::sort(v.begin(), v.end());
+        return v[(size_t)(q * (double)(v.size() - 1) + 0.5)];
+    };
+    const double p10 = pct(it_ms, 0.1), p50 = pct(it_ms, 0.5), p90 = pct(it_ms, 0.9);
+    const double full50 = B == 1 ? pct(full_ms, 0.5) : p50;
     for (int b = 0; b < B; ++b) {
         const int q = seq_ids[b];
         HIPCHK(c, hipMemcpy(out_tokens + (size_t)b * max_new, c->out_dev + (size_t)q * c->opts.max_new,
@@ -603,6 +637,10 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             for (int i = 0; i <= kMaxBlock; ++i) st.accept_hist[i] = ct.hist[i];
             st.prefill_ms = pre_ms;
             st.decode_ms = dec_ms;
+            st.iter_ms_p10 = p10;
+            st.iter_ms_p50 = p50;
+            st.iter_ms_p90 = p90;
+            st.iter_ms_full_p50 = full50;
         }
         c->slot[q].prefilled = true;
         c->slot[q].L = ct.L;
@@ -642,6 +680,7 @@ void cllm_model_free(cllm_ctx *c) {
     if (c->stream) (void)hipStreamSynchronize(c->stream);
     for (void *p : c->allocs) (void)hipFree(p);
     for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+    for (hipEvent_t e : c->it_ev) (void)hipEventDestroy(e);
     delete c;
 }
 
@@ -736,6 +775,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->zin_cap = std::max(c->cap, c->max_batch * opts->max_block);
     if ((s = dalloc_t(c, &c->zin, (size_t)c->zin_cap))) return bail(s);
     if ((s = dalloc_t(c, &c->out_dev, (size_t)opts->max_new * c->max_batch))) return bail(s);
+    if ((s = dalloc_t(c, &c->mlog_dev, (size_t)opts->max_new * c->max_batch))) return bail(s);
     c->stream_cap = opts->max_new + kMaxBlock;
     if ((s = dalloc_t(c, &c->stream_dev, (size_t)c->stream_cap * c->max_batch))) return bail(s);
 

@@ -1,5 +1,6 @@
 // kernel_bench: standalone driver of libcllm's weight-streaming GEMM kernels at the LLaMA-2-7B
-// shape (d 4096, FFN 11008, vocab 32000, head_dim 128, bf16) for one iteration of `rows` rows.
+// shape (d 4096, FFN 11008, vocab 32000, head_dim 128, bf16) for one iteration of `rows` rows
+// (more than 64 rows: row tiles of 64, as in batched iterations and prefill chunks).
 //
 // Each product of an iteration (QKV, O, gate/up, down, LM head) is launched `iters` times through
 // the library's own launchers, in the library's launch configuration, over rotating copies of its
@@ -8,7 +9,7 @@
 // (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE) to bytes. Weights and activations hold arbitrary
 // finite values: the timing and the traffic of these kernels do not depend on them.
 //
-// Usage: kernel_bench [rows (1..64, default 16)] [iters (default 20)]
+// Usage: kernel_bench [rows (1..512, default 16)] [iters (default 20)]
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -61,11 +62,13 @@ struct Shape {
 int main(int argc, char **argv) {
     const int rows = argc > 1 ? std::atoi(argv[1]) : 16;
     const int iters = argc > 2 ? std::atoi(argv[2]) : 20;
-    if (rows < 1 || rows > kMaxRows || iters < 1) {
-        std::fprintf(stderr, "usage: kernel_bench [rows 1..%d] [iters >= 1]\n", kMaxRows);
+    if (rows < 1 || rows > 512 || iters < 1) {
+        std::fprintf(stderr, "usage: kernel_bench [rows 1..512] [iters >= 1]\n");
         return 2;
     }
     const int rg = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
+    const int row_tiles = rows > kMaxRows ? (rows + kMaxRows - 1) / kMaxRows : 1;
+    const int cap = row_tiles * kMaxRows;  // row capacity of the activation buffers
 
     uint8_t *W = dev<uint8_t>(kWBytes, 0x11);  // bf16 0x1111 in every weight
     // one sequence (slot 0) with a block of `rows` rows at positions kL ..
@@ -76,27 +79,27 @@ int main(int argc, char **argv) {
     th.L[0] = kL;
     RowTab *tab = dev<RowTab>(1, 0);
     CK(hipMemcpy(tab, &th, sizeof(RowTab), hipMemcpyHostToDevice));
-    RowInfo rh[kMaxRows];
-    for (int i = 0; i < kMaxRows; ++i) rh[i] = RowInfo{0, kL + i, 0, i};
-    RowInfo *rinfo = dev<RowInfo>(kMaxRows, 0);
-    CK(hipMemcpy(rinfo, rh, sizeof(rh), hipMemcpyHostToDevice));
-    // activation operands: two bf16 planes of kMaxRows rows (act_plane elements each)
-    void *A_d = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
-    void *A_f = dev<uint16_t>(2 * act_plane(kMaxRows, kFp), 0);
-    void *An = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
-    void *Q = dev<uint16_t>(2 * act_plane(kMaxRows, kD), 0);
-    void *H = dev<uint16_t>(2 * act_plane(kMaxRows, kFp), 0);
+    static RowInfo rh[512];
+    for (int i = 0; i < cap; ++i) rh[i] = RowInfo{0, kL + i, 0, i};
+    RowInfo *rinfo = dev<RowInfo>(cap, 0);
+    CK(hipMemcpy(rinfo, rh, sizeof(RowInfo) * cap, hipMemcpyHostToDevice));
+    // activation operands: two bf16 planes of cap rows (act_plane elements each)
+    void *A_d = dev<uint16_t>(2 * act_plane(cap, kD), 0);
+    void *A_f = dev<uint16_t>(2 * act_plane(cap, kFp), 0);
+    void *An = dev<uint16_t>(2 * act_plane(cap, kD), 0);
+    void *Q = dev<uint16_t>(2 * act_plane(cap, kD), 0);
+    void *H = dev<uint16_t>(2 * act_plane(cap, kFp), 0);
     void *Kc = dev<uint16_t>((size_t)kCtx * kD, 0);
     void *Vt = dev<uint16_t>((size_t)kD * kCtx, 0);
-    float *ssq = dev<float>((size_t)(kD / 16) * kMaxRows, 0);
-    float *ssq_out = dev<float>((size_t)(kD / 16) * kMaxRows, 0);
-    float *X = dev<float>((size_t)kMaxRows * kD, 0);
+    float *ssq = dev<float>((size_t)(kD / 16) * cap, 0);
+    float *ssq_out = dev<float>((size_t)(kD / 16) * cap, 0);
+    float *X = dev<float>((size_t)cap * kD, 0);
     float *gain = dev<float>(kD, 0);
     float *rcos = dev<float>((size_t)kCtx * (kHd / 2), 0);
     float *rsin = dev<float>((size_t)kCtx * (kHd / 2), 0);
     const int n_wg_lm = (kV + 16 * kLmTiles - 1) / (16 * kLmTiles);
-    float *pmax = dev<float>((size_t)n_wg_lm * kMaxRows, 0);
-    int *pidx = dev<int>((size_t)n_wg_lm * kMaxRows, 0);
+    float *pmax = dev<float>((size_t)n_wg_lm * cap, 0);
+    int *pidx = dev<int>((size_t)n_wg_lm * cap, 0);
 
     {  // 256 MiB copy: read 268435456 bytes, write 268435456 bytes, inside the weight buffer
         const size_t bytes = (size_t)256 << 20;
@@ -128,7 +131,7 @@ int main(int argc, char **argv) {
         p.T = kD / 16;
         p.K = kD;
         p.eps = 1e-6f;
-        p.rr = RowsRef{tab, rinfo, kMaxRows};
+        p.rr = RowsRef{tab, rinfo, cap};
         p.Q = Q;
         p.Kc = Kc;
         p.Vt = Vt;
@@ -156,21 +159,22 @@ int main(int argc, char **argv) {
         }
         for (int i = 0; i < 2; ++i) {  // warm-up
             p.W = W + (size_t)(i % copies) * per;
-            CK(launch_gemm(s.kind, true, rg, 1, p, 0, nullptr, nullptr));
+            CK(launch_gemm(s.kind, true, rg, row_tiles, p, 0, nullptr, nullptr));
         }
         CK(hipDeviceSynchronize());
         CK(hipEventRecord(e0, 0));
         for (int i = 0; i < iters; ++i) {
             p.W = W + (size_t)((i + 2) % copies) * per;
-            CK(launch_gemm(s.kind, true, rg, 1, p, 0, nullptr, nullptr));
+            CK(launch_gemm(s.kind, true, rg, row_tiles, p, 0, nullptr, nullptr));
         }
         CK(hipEventRecord(e1, 0));
         CK(hipEventSynchronize(e1));
         float ms = 0.0f;
         CK(hipEventElapsedTime(&ms, e0, e1));
         const double us = ms * 1e3 / iters;
-        std::printf("%-8s rows=%d NT=%d workgroups=%4d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s\n", s.name, rows,
-                    s.nt, p.n_wg, per, us, per / us / 1e3);
+        const double flops = 2.0 * rows * s.cols * s.K;  // algorithmic (the MFMA work is twice: hi, lo)
+        std::printf("%-8s rows=%d row_tiles=%d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s  %7.1f TFLOP/s\n", s.name,
+                    rows, row_tiles, per, us, per / us / 1e3, flops / us / 1e6);
     }
     CK(hipDeviceSynchronize());
     std::printf("done\n");

@@ -833,7 +833,7 @@ __global__ void decode_init_kernel(ScanParams p) {
 
 // Acceptance, commit, emit and the next block of one sequence, from its predictions c->pred
 // (one thread).
-__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream) {
+__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream, int32_t *mlog) {
     for (int i = 0; i < (c->mode == MODE_PREFILL ? 1 : m); ++i)
         if (c->pred[i] < 0) {
             c->err |= 1;
@@ -851,6 +851,7 @@ __device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stre
     while (a < m && c->z[a] == c->pred[a - 1]) ++a;
     c->L += a;
     c->a_last = a;
+    if (mlog && c->mode == MODE_DECODE && c->steps < c->max_new) mlog[c->steps] = m;
     c->steps += 1;
     c->rows += m;
     c->hist[a] += 1;
@@ -956,7 +957,8 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
             __syncthreads();
             if (tid == 0)
                 commit_and_next(c, m, p.out ? p.out + (size_t)seq * p.out_stride : nullptr,
-                                p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr);
+                                p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr,
+                                p.mlog ? p.mlog + (size_t)seq * p.out_stride : nullptr);
         }
     }
     if (p.plan_inline) {

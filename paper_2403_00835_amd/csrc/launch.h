@@ -95,6 +95,7 @@ struct ScanParams {
     int out_stride, stream_stride;
     int advance_only;       // prefill chunk without LM head: commit all rows, no predictions
     int plan_inline;        // one batch entry: the scan also lays out the next row table
+    int32_t *mlog;          // block size of each decode iteration (out_stride entries per slot), or null
 };
 
 // Host-side edits of the control blocks and the row table, applied on the stream in order with

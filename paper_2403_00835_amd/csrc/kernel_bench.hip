@@ -124,7 +124,7 @@ int main(int argc, char **argv) {
         GemmParams p{};
         p.Ks = s.K / 32;
         p.cols = s.cols;
-        p.n_wg = s.cols / 16 / s.nt;
+        p.n_wg = (s.cols / 16 + s.nt - 1) / s.nt;  // as the launcher sets it
         p.A = s.kind == GEMM_DOWN ? A_f : A_d;
         p.lda = s.K;
         p.ssq = ssq;
@@ -151,9 +151,9 @@ int main(int argc, char **argv) {
         p.pidx = pidx;
         p.dbg = nullptr;
         p.V = kV;
-        const size_t per = (size_t)p.n_wg * s.nt * p.Ks * kTileBytes;  // packed weight bytes per launch
+        const size_t per = (size_t)(s.cols / 16) * p.Ks * kTileBytes;  // packed weight bytes per launch
         const int copies = (int)(kWBytes / per);
-        if (copies < 2 || p.n_wg * s.nt * 16 != s.cols) {
+        if (copies < 2 || s.cols % 32 != 0) {
             std::fprintf(stderr, "kernel_bench: shape %s does not fit the buffers\n", s.name);
             return 1;
         }

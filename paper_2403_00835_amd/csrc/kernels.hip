@@ -55,14 +55,17 @@ struct Stage {  // operands of one k-step
 };
 
 // Loads of one k-step s (callers clamp s into [0, Ks), so every load is issued and the compiler
-// can count outstanding loads exactly).
+// can count outstanding loads exactly). Tiles past the last one (a ragged last workgroup) load
+// the last tile again; their columns are never written.
 template <Prec P, int NT, int RG>
 __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int rg0, int s, int lane) {
     using PT = PrecT<P>;
     using T = typename PT::T;
+    const int tiles = p.cols >> 4;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * (p.cols >> 4) + t0 + j) * kTileBytes) + lane;
+        const u32x4 *src =
+            reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tiles + min(t0 + j, tiles - 1)) * kTileBytes) + lane;
         if constexpr (kWeightsNonTemporal) st.b[j] = __builtin_nontemporal_load(src);
         else st.b[j] = *src;
     }
@@ -137,8 +140,9 @@ __device__ __forceinline__ void row_factor_reduce(const GemmParams &p, int row0,
 }
 
 // Epilogues of a finished ROWS x COLS output tile in s_tile (row stride COLS + 1) for rows
-// [row0, row0 + ROWS) of the iteration (m of them live) and column workgroup wg of width COLS;
-// s_red is scratch of at least ROWS x COLS floats. Shared by both GEMM kernels.
+// [row0, row0 + ROWS) of the iteration (m of them live) and column workgroup wg of width COLS
+// (columns at or past p.cols, in a ragged last workgroup, are dropped); s_red is scratch of at
+// least ROWS x COLS floats. Shared by both GEMM kernels.
 template <Prec P, int NT, int RG, int EP, int W>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile, float *s_red, int row0, int m, int wg,
                                               int tid, int lane, int w) {
@@ -152,8 +156,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
         const int hd = p.hd, d = p.d, h2 = hd >> 1;
         for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
             const int row = idx / COLS, pc = idx % COLS;
-            if (row >= m) continue;
             const int R = t0 * 16 + pc;  // packed row index
+            if (row >= m || R >= p.cols) continue;
             int sec, head, dim, partner;
             if (hd >= 32) {
                 const int per_sec = d;  // packed rows per section
@@ -195,7 +199,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
         for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
             const int row = idx / COLS, c = idx % COLS;
             float v = 0.0f;
-            if (row < m) {
+            if (row < m && c0 + c < p.cols) {
                 float *xp = p.Xout + (size_t)(row0 + row) * p.ldx + c0 + c;
                 v = *xp + s_tile[row * (COLS + 1) + c];
                 *xp = v;
@@ -208,7 +212,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
         __syncthreads();
         if (tid < ROWS * NT) {
             const int row = tid / NT, j = tid % NT;
-            if (row < m) {
+            if (row < m && (t0 + j) * 16 < p.cols) {
                 float sum = 0.0f;
 #pragma unroll
                 for (int c = 0; c < 16; ++c) sum += s_sq[row * COLS + 16 * j + c];
@@ -220,7 +224,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
         static_assert(NT % 2 == 0, "gate/up epilogue pairs a gate tile with an up tile");
         for (int idx = tid; idx < ROWS * COLS / 2; idx += W * kWave) {
             const int row = idx / (COLS / 2), f = idx % (COLS / 2), q = f >> 4, c = f & 15;
-            if (row >= m) continue;
+            if (row >= m || wg * COLS + 32 * q >= p.cols) continue;  // pair past the last column
             const float gt = s_tile[row * (COLS + 1) + 32 * q + c];
             const float up = s_tile[row * (COLS + 1) + 32 * q + 16 + c];
             put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.rr.cap, p.Fp),
@@ -994,7 +998,7 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
-// Grid: column workgroups (p.cols / (16 * NT)) x row tiles of 16 * RG rows (from row tile p.rt0).
+// Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile p.rt0).
 template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves, bool KC = kGemmKContig>
 static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -1003,7 +1007,7 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     auto kern = gemm_kernel<P, NT, RG, EP, D, W, KC>;
     GemmParams q = p;
     q.row_tiles = row_tiles;
-    q.n_wg = p.cols / COLS;
+    q.n_wg = (p.cols + COLS - 1) / COLS;  // the last workgroup may be ragged
     const dim3 grid(q.n_wg, row_tiles);
     if (e0) {
         hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, q);

@@ -11,7 +11,7 @@ struct RowInfo;
 
 constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
 constexpr int kNtQkv = 4;     // QKV (pairs of rotate-half partner tiles)
-constexpr int kNtGateUp = 2;  // gate/up ((gate, up) tile pairs)
+constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups at 7B, one per CU)
 constexpr int kNtResid = 1;   // O and down projections
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
 constexpr bool kGemmKContig = false;  // k-steps per wave: interleaved (false) or contiguous
@@ -29,8 +29,8 @@ struct RowsRef {
 struct GemmParams {
     const uint8_t *W;  // packed tiles
     int Ks;            // k-steps per 16-row tile
-    int cols;          // packed output columns (multiple of 16 * every NT used)
-    int n_wg;          // workgroups along the columns (set by the launcher: cols / (16 NT))
+    int cols;          // packed output columns (multiple of 16; of 32 for QKV and gate/up)
+    int n_wg;          // workgroups along the columns (set by the launcher: ceil(cols / (16 NT)))
     int rt0;           // first row tile
     int row_tiles;     // row tiles of the launch (set by the launcher)
     const void *A;     // activation operand, packed operand order, lda elements per row

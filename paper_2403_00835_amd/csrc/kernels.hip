@@ -261,17 +261,23 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
     }
 }
 
-template <Prec P, int NT, int RG, int EP, int D, int W, bool KC>
+template <Prec P, int NT, int RG, int EP, int D, int W, bool KC, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     using PT = PrecT<P>;
     using T = typename PT::T;
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     const int wg = blockIdx.x;
-    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration; m of them are live.
+    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
+    // capacity); m of them are live. A launch of one row tile (MT false) always has live rows, so
+    // nothing waits for the row count before the first loads; with several row tiles (MT) a tile
+    // with no live row exits first.
     const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T);
     const int m = p.rr.tab->R - row0;
-    if (m <= 0) return;
+    if constexpr (MT) {
+        if (m <= 0) return;
+    }
     const int rg0 = row0 >> 4;
     const int tid = threadIdx.x, lane = tid & 63;
     // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
@@ -529,9 +535,11 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
     using T = typename PT::T;
     constexpr int V16 = 16 / sizeof(T);  // elements per 16-byte vector
     static_assert(V16 == PT::VEC, "an operand vector is one 16-byte load");
-    const int row = blockIdx.x;
-    if (row >= p.rr.tab->R) return;
-    const int tok = p.rr.rows[row].tok;
+    const int row = blockIdx.x;  // < row capacity (launcher)
+    request_together(p.rr.tab, p.rr.rows, p.rr.cap, p.E, p.X, p.ssq, p.An, p.gain, p.d);
+    const int R = p.rr.tab->R, tok = p.rr.rows[row].tok;
+    request_together(R, tok);
+    if (row >= R) return;
     const T *e = reinterpret_cast<const T *>(p.E) + (size_t)tok * p.d;
     float *x = p.X + (size_t)row * p.d;
     T *an = reinterpret_cast<T *>(p.An);
@@ -585,11 +593,13 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     constexpr int NKK = HD / PT::KSTEP;  // k-steps of the score product
     constexpr int NDT = HD / 16;         // 16-dim tiles of the output
     const RowTab *tab = p.rr.tab;
-    const int b = blockIdx.z / p.nrb;            // batch entry
+    request_together(tab, p.nrb, p.Q, p.Kc, p.Vt, p.kv_seq, p.ctx_alloc, p.rr.cap, p.d, p.nch);
+    const int b = blockIdx.z / p.nrb;            // batch entry (< kMaxSeqs: the launcher checks)
     const int rbase = (blockIdx.z % p.nrb) * 16 * RG;  // first block row of this workgroup
-    if (b >= tab->nseq) return;
-    const int m = tab->m[b];
-    const int L = tab->L[b];
+    // the entry's fields are requested together, before any of them is tested
+    const int nseq = tab->nseq, m = tab->m[b], L = tab->L[b], r0 = tab->r0[b], slot = tab->seq[b];
+    request_together(nseq, m, L, r0, slot);
+    if (b >= nseq) return;
     if (rbase >= m) return;
     const int c = blockIdx.x, h = blockIdx.y;
     const int key0 = c * kAttnChunk;
@@ -599,11 +609,11 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     const int g = lane >> 4, r16 = lane & 15;
     const int d = p.d;
     const int qi = rbase + 16 * rg + r16;   // row within the block
-    const int qrow = tab->r0[b] + qi;       // row of the iteration
+    const int qrow = r0 + qi;               // row of the iteration
     const int qld = min(qrow, p.rr.cap - 1);  // rows past the block load in-bounds filler
     const int qpos = L + qi;
     // this head's caches of this sequence slot (operand order: one contiguous KiB per load)
-    const size_t kvo = (size_t)tab->seq[b] * p.kv_seq + (size_t)h * p.ctx_alloc * HD;
+    const size_t kvo = (size_t)slot * p.kv_seq + (size_t)h * p.ctx_alloc * HD;
     const T *Kh = reinterpret_cast<const T *>(p.Kc) + kvo;
     const T *Vh = reinterpret_cast<const T *>(p.Vt) + kvo;
     const T *Q = reinterpret_cast<const T *>(p.Q);
@@ -715,50 +725,69 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
 
 // Combine the chunk partials of one (head, row) in chunk order and write the O operand.
 // Wave 0 derives the chunk weights w_c = 2^(m_c - M) into LDS; every thread (one output dim)
-// then sums w_c * O_c in chunk order.
+// then sums w_c * O_c in chunk order. The loads are issued in two rounds: the row count and the
+// row's position, then the chunk maxima, sums and the first kCombinePre chunks' values together.
+constexpr int kCombinePre = 16;  // chunks whose values are requested with the maxima
+
 template <Prec P>
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
     using T = typename PrecT<P>::T;
-    const RowTab *tab = p.rr.tab;
-    const int h = blockIdx.x, row = blockIdx.y;
-    if (row >= tab->R) return;
+    const int h = blockIdx.x, row = blockIdx.y;  // row < row capacity (launcher)
+    request_together(p.rr.tab, p.rr.rows, p.rr.cap, p.Mpart, p.Lpart, p.Opart, p.nch, p.hd);
+    const int R = p.rr.tab->R;
+    const int pos = p.rr.rows[row].pos;
+    request_together(R, pos);
+    if (row >= R) return;
     // chunks holding a key at or before this row's position (later chunks hold none)
-    const int nlive = p.rr.rows[row].pos / kAttnChunk + 1;
+    const int nlive = pos / kAttnChunk + 1;
     const int tid = threadIdx.x;
     const int cap = p.rr.cap;
     const size_t b0 = (size_t)h * p.nch * cap + row;
-    __shared__ float s_w[kMaxChunks];
+    __shared__ float s_w[kMaxChunks], s_l[kMaxChunks];
     __shared__ float s_den;
+    const int dim = tid;
+    const bool has_dim = dim < p.hd;
+    float pre[kCombinePre];
+#pragma unroll
+    for (int c = 0; c < kCombinePre; ++c)
+        pre[c] = (has_dim && c < nlive) ? p.Opart[(b0 + (size_t)c * cap) * p.hd + dim] : 0.0f;
     if (tid < kWave) {
         float M = -INFINITY;
-        for (int c = tid; c < nlive; c += kWave) M = fmaxf(M, p.Mpart[b0 + (size_t)c * cap]);
+        for (int c = tid; c < nlive; c += kWave) {
+            const float mc = p.Mpart[b0 + (size_t)c * cap];
+            s_w[c] = mc;
+            s_l[c] = p.Lpart[b0 + (size_t)c * cap];
+            M = fmaxf(M, mc);
+        }
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
         for (int c = tid; c < nlive; c += kWave) {
-            const float mc = p.Mpart[b0 + (size_t)c * cap];
+            const float mc = s_w[c];
             s_w[c] = mc == -INFINITY ? 0.0f : exp2f(mc - M);
         }
     }
     __syncthreads();
     if (tid == 0) {
         float den = 0.0f;
-        for (int c = 0; c < nlive; ++c) den += s_w[c] * p.Lpart[b0 + (size_t)c * cap];
+        for (int c = 0; c < nlive; ++c) den += s_w[c] * s_l[c];
         s_den = den;
     }
     __syncthreads();
-    for (int dim = tid; dim < p.hd; dim += blockDim.x) {
-        float num = 0.0f;
-        int c = 0;
-        for (; c + 4 <= nlive; c += 4) {
-            float o[4];
+    if (!has_dim) return;
+    float num = 0.0f;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * cap) * p.hd + dim];
+    for (int c = 0; c < kCombinePre; ++c)
+        if (c < nlive) num += s_w[c] * pre[c];
+    int c = kCombinePre;
+    for (; c + 4 <= nlive; c += 4) {
+        float o[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
-        }
-        for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * cap) * p.hd + dim];
-        put_act<P>(reinterpret_cast<T *>(p.O), act_plane(cap, p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
+        for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * cap) * p.hd + dim];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
     }
+    for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * cap) * p.hd + dim];
+    put_act<P>(reinterpret_cast<T *>(p.O), act_plane(cap, p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1004,7 +1033,7 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
     const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
-    auto kern = gemm_kernel<P, NT, RG, EP, D, W, KC>;
+    auto kern = row_tiles > 1 ? gemm_kernel<P, NT, RG, EP, D, W, KC, true> : gemm_kernel<P, NT, RG, EP, D, W, KC, false>;
     GemmParams q = p;
     q.row_tiles = row_tiles;
     q.n_wg = (p.cols + COLS - 1) / COLS;  // the last workgroup may be ragged
@@ -1083,6 +1112,7 @@ hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const Ge
 }
 
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    if (rows < 1 || rows > p.rr.cap) return hipErrorInvalidValue;  // every row entry read is within the table
     auto kern = bf16 ? embed_kernel<Prec::BF16> : embed_kernel<Prec::F32>;
     if (e0)
         hipExtLaunchKernelGGL(kern, dim3(rows), dim3(256), 0, s, e0, e1, 0, p);
@@ -1107,6 +1137,7 @@ static hipError_t launch_attn_hd(int rg, const AttnParams &p, int nch_launch, in
 
 hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const AttnParams &p, hipStream_t s,
                        hipEvent_t e0, hipEvent_t e1) {
+    if (nseq_launch < 1 || nseq_launch > kMaxSeqs) return hipErrorInvalidValue;  // entries index the row table
     if (bf16) {
         switch (p.hd) {
         case 32: return launch_attn_hd<Prec::BF16, 32>(rg, p, nch_launch, nseq_launch, s, e0, e1);
@@ -1127,8 +1158,9 @@ hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const
 
 hipError_t launch_attn_combine(bool bf16, int rows, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                                hipEvent_t e1) {
+    if (rows > p.rr.cap || p.hd > 256) return hipErrorInvalidValue;
     dim3 grid(p.n_heads, rows);
-    const unsigned threads = p.hd < 256 ? (unsigned)p.hd : 256u;
+    const unsigned threads = p.hd < kWave ? (unsigned)kWave : (unsigned)p.hd;  // wave 0 reduces the maxima
     auto kern = bf16 ? attn_combine_kernel<Prec::BF16> : attn_combine_kernel<Prec::F32>;
     if (e0)
         hipExtLaunchKernelGGL(kern, grid, dim3(threads), 0, s, e0, e1, 0, p);

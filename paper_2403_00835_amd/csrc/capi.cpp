@@ -159,13 +159,10 @@ void timing_collect(cllm_ctx *c) {
 std::vector<int32_t> qkv_perm(const cllm_ctx *c) {
     const int d = c->d, hd = c->hd, h2 = hd / 2;
     std::vector<int32_t> p(3 * d);
-    for (int R = 0; R < 3 * d; ++R) {
+    for (int R = 0; R < 3 * d; ++R) {  // tile b of a head: dims [8b, 8b+8) and [hd/2+8b, hd/2+8b+8)
         const int sec = R / d, within = R % d, head = within / hd, q = within % hd;
-        int dim = q;
-        if (hd >= 32) {
-            const int b16 = q >> 4, o = q & 15;
-            dim = (b16 & 1) ? (h2 + (b16 >> 1) * 16 + o) : ((b16 >> 1) * 16 + o);
-        }
+        const int b = q >> 4, o = q & 15;
+        const int dim = o < 8 ? 8 * b + o : h2 + 8 * b + (o - 8);
         p[R] = sec * d + head * hd + dim;
     }
     return p;

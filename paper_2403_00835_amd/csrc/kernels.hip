@@ -150,29 +150,19 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     const int t0 = wg * NT;
     if constexpr (EP == E_QKV) {
-        // Packed columns -> (section, head, dim). With head_dim >= 32 a workgroup's two tiles are
-        // dims [16b, 16b+16) and [hd/2+16b, hd/2+16b+16) of one head (rotate-half partners);
-        // with head_dim 16 one tile is a whole head.
+        // Packed columns -> (section, head, dim). Tile b of a head holds dims [8b, 8b+8) and
+        // their rotate-half partners [hd/2+8b, hd/2+8b+8): column o of the tile and column o ^ 8
+        // are partners, so every tile is complete for RoPE and a workgroup may own any number
+        // of tiles.
         const int hd = p.hd, d = p.d, h2 = hd >> 1;
         for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
             const int row = idx / COLS, pc = idx % COLS;
             const int R = t0 * 16 + pc;  // packed row index
             if (row >= m || R >= p.cols) continue;
-            int sec, head, dim, partner;
-            if (hd >= 32) {
-                const int per_sec = d;  // packed rows per section
-                sec = R / per_sec;
-                const int within = R % per_sec;
-                head = within / hd;
-                const int q = within % hd, b16 = q >> 4, o = q & 15;
-                dim = (b16 & 1) ? (h2 + (b16 >> 1) * 16 + o) : ((b16 >> 1) * 16 + o);
-                partner = pc ^ 16;
-            } else {
-                sec = R / d;
-                head = (R % d) / hd;
-                dim = R % hd;
-                partner = pc ^ h2;
-            }
+            const int sec = R / d, within = R % d, head = within / hd;
+            const int q = within % hd, b = q >> 4, o = q & 15;
+            const int dim = o < 8 ? 8 * b + o : h2 + 8 * b + (o - 8);
+            const int partner = pc ^ 8;
             const RowInfo ri = p.rr.rows[row0 + row];
             const int pos = ri.pos;
             const size_t kvo = (size_t)p.rr.tab->seq[ri.b] * p.kv_seq;  // this row's sequence slot

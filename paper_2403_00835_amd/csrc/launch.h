@@ -10,7 +10,7 @@ struct RowTab;
 struct RowInfo;
 
 constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
-constexpr int kNtQkv = 4;     // QKV (pairs of rotate-half partner tiles)
+constexpr int kNtQkv = 3;     // QKV (each tile holds rotate-half partners; 256 workgroups at 7B)
 constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups at 7B, one per CU)
 constexpr int kNtResid = 1;   // O and down projections
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
@@ -29,7 +29,7 @@ struct RowsRef {
 struct GemmParams {
     const uint8_t *W;  // packed tiles
     int Ks;            // k-steps per 16-row tile
-    int cols;          // packed output columns (multiple of 16; of 32 for QKV and gate/up)
+    int cols;          // packed output columns (multiple of 16; of 32 for gate/up)
     int n_wg;          // workgroups along the columns (set by the launcher: ceil(cols / (16 NT)))
     int rt0;           // first row tile
     int row_tiles;     // row tiles of the launch (set by the launcher)

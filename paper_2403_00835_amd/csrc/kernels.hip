@@ -254,7 +254,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
 template <Prec P, int NT, int RG, int EP, int D, int W, bool KC, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     using PT = PrecT<P>;
-    using T = typename PT::T;
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     const int wg = blockIdx.x;
@@ -562,6 +561,193 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedParams p) {
                 *reinterpret_cast<u32x4 *>(an + pl * act_plane(p.rr.cap, p.d) + act_idx<P>(row, 16 * t + q * V16, p.d)) =
                     *reinterpret_cast<u32x4 *>(&av[pl][q * V16]);
         p.ssq[(size_t)row * (p.d / 16) + t] = sum;
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Block-causal attention in one kernel, for launches whose rows see at most kFusedChunks
+// chunks. Workgroup (16-dim output slice dt, head h; 16-row group of a batch entry), 8 waves:
+// wave w computes chunks w, w+8, ... exactly as attn_partial_kernel computes them (chunk max,
+// sum and unnormalised output of this slice, per row) into LDS; the workgroup then combines the
+// chunks up to each row's position exactly as attn_combine_kernel does (same weights, same
+// chunk order). Every value is therefore bit-identical to the two-kernel path, whichever of the
+// two a launch takes. Each workgroup of a head reads the head's whole K and one 16-dim slice of
+// V; the slices of a head are dispatched to one XCD (block index dt * n_heads + h with n_heads
+// a multiple of 8), so its L2 serves the K re-reads.
+// ------------------------------------------------------------------------------------------
+constexpr int kAttnWaves = 8;
+
+template <Prec P, int HD>
+struct AttnChunk {  // one chunk's operands in registers
+    u32x4 k[4][HD / PrecT<P>::KSTEP];
+    u32x4 v[4];  // bf16: v[0..1] (keys 32kp..); fp32: v[0..3] (keys 16kt..)
+};
+
+template <Prec P, int HD>
+__device__ __forceinline__ void attn_load_chunk(AttnChunk<P, HD> &ch, const typename PrecT<P>::T *Kh,
+                                                const typename PrecT<P>::T *Vh, int c, int dt, int lane) {
+    using PT = PrecT<P>;
+    constexpr int NKK = HD / PT::KSTEP, NDT = HD / 16;
+    const int key0 = c * kAttnChunk;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            ch.k[kt][kk] = *reinterpret_cast<const u32x4 *>(Kh + ((size_t)((key0 >> 4) + kt) * NKK + kk) * (kWave * PT::VEC) +
+                                                            lane * PT::VEC);
+    if constexpr (P == Prec::BF16) {
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp)
+            ch.v[kp] = *reinterpret_cast<const u32x4 *>(Vh + ((size_t)((key0 >> 5) + kp) * NDT + dt) * (kWave * 8) + lane * 8);
+    } else {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            ch.v[kt] = *reinterpret_cast<const u32x4 *>(Vh + ((size_t)((key0 >> 4) + kt) * NDT + dt) * (kWave * 4) + lane * 4);
+    }
+}
+
+template <Prec P, int HD>
+__global__ __launch_bounds__(kAttnWaves * kWave) void attn_kernel(AttnParams p) {
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    constexpr int NKK = HD / PT::KSTEP;
+    constexpr int W = kAttnWaves;
+    const RowTab *tab = p.rr.tab;
+    request_together(tab, p.Q, p.Kc, p.Vt, p.kv_seq, p.ctx_alloc, p.rr.cap, p.d, p.n_heads);
+    const int h = blockIdx.x % p.n_heads, dt = blockIdx.x / p.n_heads;
+    const int rgi = blockIdx.y, b = blockIdx.z;  // b < kMaxSeqs (launcher)
+    const int nseq = tab->nseq, m = tab->m[b], L = tab->L[b], r0 = tab->r0[b], slot = tab->seq[b];
+    request_together(nseq, m, L, r0, slot);
+    if (b >= nseq || 16 * rgi >= m) return;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, r16 = lane & 15;
+    const int d = p.d;
+    const int qi = 16 * rgi + r16;              // row within the block
+    const int qld = min(r0 + qi, p.rr.cap - 1);  // rows past the block load in-bounds filler
+    const int qpos = L + qi;
+    // chunks holding a key visible to some row of the group (<= kFusedChunks: the launcher's bound)
+    const int nvis = min((L + min(m - 1, 16 * rgi + 15)) / kAttnChunk + 1, kFusedChunks);
+    const size_t kvo = (size_t)slot * p.kv_seq + (size_t)h * p.ctx_alloc * HD;
+    const T *Kh = reinterpret_cast<const T *>(p.Kc) + kvo;
+    const T *Vh = reinterpret_cast<const T *>(p.Vt) + kvo;
+    const T *Q = reinterpret_cast<const T *>(p.Q);
+
+    // per chunk and row: max, sum, and the slice's 16 unnormalised output dims
+    __shared__ float s_mc[kFusedChunks][16], s_lc[kFusedChunks][16], s_oc[kFusedChunks][16][17];
+
+    // This wave's chunks w, w + W, ... (nmine of them); the loads of the next one are in flight
+    // while a chunk is computed (the index is clamped, so the last prefetch stays in bounds).
+    const int nmine = w < nvis ? (nvis - 1 - w) / W + 1 : 0;
+    auto chunk_of = [&](int i) { return min(w + i * W, nvis - 1); };
+    u32x4 qv[PT::PLANES][NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+        for (int pl = 0; pl < PT::PLANES; ++pl)
+            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(
+                Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, h * HD + kk * PT::KSTEP + g * PT::VEC, d));
+    AttnChunk<P, HD> buf[2];
+    attn_load_chunk<P, HD>(buf[0], Kh, Vh, chunk_of(0), dt, lane);
+
+    auto process = [&](const AttnChunk<P, HD> &ch, int c) {
+        const int key0 = c * kAttnChunk;
+        f32x4 st[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int pl = 0; pl < PT::PLANES; ++pl)
+#pragma unroll
+                for (int kk = 0; kk < NKK; ++kk) st[kt] = mfma_kstep<P>(ch.k[kt][kk], qv[pl][kk], st[kt]);
+        }
+        // st[kt][v] = S^T[key0 + 16kt + 4g + v][row r16]
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int key = key0 + 16 * kt + 4 * g + v;
+                const float sc = key <= qpos ? st[kt][v] * p.scale_log2 : -INFINITY;
+                st[kt][v] = sc;
+                mx = fmaxf(mx, sc);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        float l = 0.0f;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float pr = (mx == -INFINITY || st[kt][v] == -INFINITY) ? 0.0f : exp2f(st[kt][v] - mx);
+                st[kt][v] = pr;
+                l += pr;
+            }
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (P == Prec::BF16) {
+#pragma unroll
+            for (int kp = 0; kp < 2; ++kp) {
+                // P = hi + lo, hi = bf16(P), lo = bf16(P - hi): the probabilities keep ~2^-17
+                const f32x4 pa = st[2 * kp], pb = st[2 * kp + 1];
+                const float pv[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+                uint32_t hi[8], lo[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    hi[q] = f2bf(pv[q]);
+                    lo[q] = f2bf(pv[q] - bf2f((uint16_t)hi[q]));
+                }
+                const u32x4 bhi = u32x4{hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16), hi[4] | (hi[5] << 16),
+                                        hi[6] | (hi[7] << 16)};
+                const u32x4 blo = u32x4{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16), lo[4] | (lo[5] << 16),
+                                        lo[6] | (lo[7] << 16)};
+                o = mfma_kstep<P>(ch.v[kp], bhi, o);
+                o = mfma_kstep<P>(ch.v[kp], blo, o);
+            }
+        } else {
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                const f32x4 pk = st[kt];
+                o = mfma_kstep<P>(ch.v[kt], u32x4{__float_as_uint(pk[0]), __float_as_uint(pk[1]), __float_as_uint(pk[2]),
+                                                  __float_as_uint(pk[3])},
+                                  o);
+            }
+        }
+        // o[v] = O^T[16dt + 4g + v][row r16]
+        if (g == 0) {
+            s_mc[c][r16] = mx;
+            s_lc[c][r16] = l;
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s_oc[c][r16][4 * g + v] = o[v];
+    };
+    for (int i = 0; i < nmine; i += 2) {
+        attn_load_chunk<P, HD>(buf[1], Kh, Vh, chunk_of(i + 1), dt, lane);
+        process(buf[0], w + i * W);
+        if (i + 1 >= nmine) break;
+        attn_load_chunk<P, HD>(buf[0], Kh, Vh, chunk_of(i + 2), dt, lane);
+        process(buf[1], w + (i + 1) * W);
+    }
+    __syncthreads();
+
+    // Combine the chunks up to the row's own position in chunk order (as attn_combine_kernel).
+    if (tid < 256) {
+        const int row = tid >> 4, dim = tid & 15;
+        if (16 * rgi + row < m) {
+            const int nlive = min((L + 16 * rgi + row) / kAttnChunk + 1, nvis);
+            float M = -INFINITY;
+            for (int c = 0; c < nlive; ++c) M = fmaxf(M, s_mc[c][row]);
+            float num = 0.0f, den = 0.0f;
+            for (int c = 0; c < nlive; ++c) {
+                const float mc = s_mc[c][row];
+                const float wc = mc == -INFINITY ? 0.0f : exp2f(mc - M);
+                den += wc * s_lc[c][row];
+                num += wc * s_oc[c][row][dim];
+            }
+            put_act<P>(reinterpret_cast<T *>(p.O), act_plane(p.rr.cap, d),
+                       act_idx<P>(r0 + 16 * rgi + row, h * HD + 16 * dt + dim, d), num / den);
+        }
     }
 }
 
@@ -1141,6 +1327,39 @@ hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const
         case 32: return launch_attn_hd<Prec::F32, 32>(rg, p, nch_launch, nseq_launch, s, e0, e1);
         case 64: return launch_attn_hd<Prec::F32, 64>(rg, p, nch_launch, nseq_launch, s, e0, e1);
         case 128: return launch_attn_hd<Prec::F32, 128>(rg, p, nch_launch, nseq_launch, s, e0, e1);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+template <Prec P, int HD>
+static hipError_t launch_attn_fused_hd(int nrg, int nseq_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
+                                       hipEvent_t e1) {
+    dim3 grid(p.n_heads * (HD / 16), nrg, nseq_launch);
+    auto kern = attn_kernel<P, HD>;
+    if (e0)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kAttnWaves * kWave), 0, s, e0, e1, 0, p);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kAttnWaves * kWave), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_fused(bool bf16, int nrg, int nseq_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
+                             hipEvent_t e1) {
+    if (nseq_launch < 1 || nseq_launch > kMaxSeqs || nrg < 1) return hipErrorInvalidValue;
+    if (bf16) {
+        switch (p.hd) {
+        case 32: return launch_attn_fused_hd<Prec::BF16, 32>(nrg, nseq_launch, p, s, e0, e1);
+        case 64: return launch_attn_fused_hd<Prec::BF16, 64>(nrg, nseq_launch, p, s, e0, e1);
+        case 128: return launch_attn_fused_hd<Prec::BF16, 128>(nrg, nseq_launch, p, s, e0, e1);
+        case 256: return launch_attn_fused_hd<Prec::BF16, 256>(nrg, nseq_launch, p, s, e0, e1);
+        }
+    } else {
+        switch (p.hd) {
+        case 16: return launch_attn_fused_hd<Prec::F32, 16>(nrg, nseq_launch, p, s, e0, e1);
+        case 32: return launch_attn_fused_hd<Prec::F32, 32>(nrg, nseq_launch, p, s, e0, e1);
+        case 64: return launch_attn_fused_hd<Prec::F32, 64>(nrg, nseq_launch, p, s, e0, e1);
+        case 128: return launch_attn_fused_hd<Prec::F32, 128>(nrg, nseq_launch, p, s, e0, e1);
         }
     }
     return hipErrorInvalidValue;

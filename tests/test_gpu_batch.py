@@ -5,7 +5,9 @@ C ABI.
 Every row of a batched iteration is computed exactly as a single-sequence iteration computes
 it (fixed reduction orders that do not depend on the rows sharing the pass), so:
 - tiny fp32 and small bf16: batched steps give bit-identical tokens, accepted lengths and logits
-  to single-sequence steps on a context with one slot; a batched decode of sequences with
+  to single-sequence steps on a context with one slot (the single-sequence launches take the
+  one-kernel attention, the batched ones the chunk-parallel pair, so this also pins the two
+  attention paths to each other bit for bit); a batched decode of sequences with
   different prompt lengths and guess policies equals, per sequence, the single-sequence GPU AR
   decode; prompts longer than 64 rows run as one row-tiled prefill chunk; on tiny the result is
   also the oracle's greedy AR continuation.

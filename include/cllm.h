@@ -202,13 +202,15 @@ cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, si
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 
 /* Kernel timing for measurement: kernel_class selects one class of kernels (CLLM_KT_*
- * below); while enabled, each launch of that class is bracketed by HIP events on the context's
+ * below); while enabled, launches of that class are bracketed by HIP events on the context's
  * stream. max_rows > 0 restricts timing to launches sized for that many rows (the kernels are
  * instantiated for 16, 32 or 64 rows per row tile: max_rows = n times the Jacobi iterations of
  * blocks of n when n <= 32); 0 times every launch. Launches of a prefill are never timed.
- * cllm_timing_read
- * returns the number of timed launches and their total device time since the last enable, and
- * clears them. kernel_class < 0 disables. */
+ * every >= 1 samples: one of every `every` eligible launches is timed (each bracket costs a
+ * few microseconds of queue time; a stride coprime with the layer count rotates the sample over
+ * the layers). cllm_timing_read returns the number of timed launches and their total device
+ * time since the last enable, and clears them. kernel_class < 0 disables. Errors: ERR_ARG for
+ * an unknown class, max_rows outside [0, 64] or every < 1. */
 #define CLLM_KT_GEMM_QKV 0
 #define CLLM_KT_ATTN 1
 #define CLLM_KT_GEMM_O 2
@@ -218,7 +220,7 @@ cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_
 #define CLLM_KT_SCAN 6
 #define CLLM_KT_ATTN_COMBINE 7
 #define CLLM_KT_EMBED 8
-cllm_status cllm_timing_enable(cllm_ctx *ctx, int32_t kernel_class, int32_t max_rows);
+cllm_status cllm_timing_enable(cllm_ctx *ctx, int32_t kernel_class, int32_t max_rows, int32_t every);
 cllm_status cllm_timing_read(cllm_ctx *ctx, int64_t *launches, double *total_ms);
 
 /* Bytes of weights streamed by one forward pass (all matrices except the embedding), after

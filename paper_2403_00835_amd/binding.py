@@ -74,7 +74,7 @@ def lib():
         L.cllm_reset.argtypes = [_vp, _i32]
         L.cllm_debug_logits.argtypes = [_vp, _i32, _vp, ctypes.c_size_t]
         L.cllm_seq_state.argtypes = [_vp, _i32, P(_i32), P(_i32)]
-        L.cllm_timing_enable.argtypes = [_vp, _i32, _i32]
+        L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
         L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
         L.cllm_streamed_weight_bytes.argtypes = [_vp]
         L.cllm_streamed_weight_bytes.restype = _i64
@@ -247,9 +247,9 @@ class Model:
         self._check(self.L.cllm_seq_state(self.h, seq, ctypes.byref(L), ctypes.byref(pend)))
         return int(L.value), int(pend.value)
 
-    def timing_enable(self, kernel_class, max_rows=0):
+    def timing_enable(self, kernel_class, max_rows=0, every=1):
         cls = KT[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
-        self._check(self.L.cllm_timing_enable(self.h, cls, max_rows))
+        self._check(self.L.cllm_timing_enable(self.h, cls, max_rows, every))
 
     def timing_read(self):
         n, ms = _i64(0), _dbl(0.0)

@@ -74,6 +74,8 @@ struct cllm_ctx {
     // kernel timing
     int kt_class = -1;
     int kt_rg = 0;  // time only launches for this many 16-row groups (0 = all)
+    int kt_every = 1;           // time one of every kt_every eligible launches
+    int64_t kt_eligible = 0;    // eligible launches since the last enable
     bool in_prefill = false;  // prefill launches are not timed
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
@@ -134,6 +136,7 @@ cllm_status dalloc_t(cllm_ctx *c, T **p, size_t count) {
 void timing_events(cllm_ctx *c, int cls, int rg, hipEvent_t *e0, hipEvent_t *e1) {
     *e0 = *e1 = nullptr;
     if (c->kt_class != cls || c->in_prefill || (c->kt_rg > 0 && c->kt_rg != rg)) return;
+    if (c->kt_eligible++ % c->kt_every != 0) return;
     while (c->ev_pool.size() < c->ev_used + 2) {
         hipEvent_t e;
         if (hipEventCreate(&e) != hipSuccess) return;
@@ -1052,12 +1055,14 @@ cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_le
     return CLLM_OK;
 }
 
-cllm_status cllm_timing_enable(cllm_ctx *c, int32_t kernel_class, int32_t max_rows) {
+cllm_status cllm_timing_enable(cllm_ctx *c, int32_t kernel_class, int32_t max_rows, int32_t every) {
     if (!c) return CLLM_ERR_ARG;
-    if (kernel_class > CLLM_KT_EMBED || max_rows < 0 || max_rows > kMaxRows)
-        return fail(c, CLLM_ERR_ARG, "unknown kernel class or bad max_rows");
+    if (kernel_class > CLLM_KT_EMBED || max_rows < 0 || max_rows > kMaxRows || every < 1)
+        return fail(c, CLLM_ERR_ARG, "unknown kernel class, bad max_rows or bad sampling stride");
     c->kt_class = kernel_class < 0 ? -1 : kernel_class;
     c->kt_rg = max_rows == 0 ? 0 : rows_to_rg(max_rows);
+    c->kt_every = every;
+    c->kt_eligible = 0;
     c->ev_used = 0;
     c->kt_launches = 0;
     c->kt_ms = 0.0;

@@ -252,3 +252,28 @@ def test_weight_file_roundtrip(tiny, tmp_path):
     a, _ = g.ar_decode(prompt, 24)
     b, _ = tiny.gpu.ar_decode(prompt, 24)
     np.testing.assert_array_equal(a, b)
+
+
+def test_kernel_timing_sampling(tiny):
+    """The measurement hook: with a sampling stride, one eligible launch in `every` is timed;
+    every timed launch has a positive duration; a bad stride is rejected."""
+    from paper_2403_00835_amd import binding
+    log("[gpu] kernel timing sampling stride")
+    g = tiny.gpu
+    prompt = workload.make_prompt(TINY, 16, seed=9)
+    ar, _ = g.ar_decode(prompt, 40)
+    out = {}
+    for every in (1, 3):
+        g.timing_enable("gate_up", max_rows=8, every=every)
+        res, st = g.jacobi_decode(prompt, 8, 40)
+        launches, ms = g.timing_read()
+        g.timing_enable(-1)
+        np.testing.assert_array_equal(res, ar)
+        out[every] = (launches, ms, st["steps"])
+    # one gate/up launch per layer and queued iteration (iterations queued past the end launch too)
+    assert out[1][0] >= out[1][2] * TINY.n_layers
+    assert out[3][0] == (out[1][0] + 2) // 3  # the same decode: launches 0, 3, 6, ... are timed
+    assert out[1][1] > 0 and out[3][1] > 0
+    with pytest.raises(binding.CllmError) as e:
+        g.timing_enable("gate_up", max_rows=8, every=0)
+    assert e.value.status == 1

@@ -32,6 +32,10 @@ class _GuessSpec(ctypes.Structure):
                 ("thr53", _u64), ("seed", _u64)]
 
 
+class _Traj(ctypes.Structure):
+    _fields_ = [("L", _vp), ("e", _vp), ("b0", _vp), ("z", _vp), ("pred", _vp), ("cap", _i32)]
+
+
 class _Stats(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("blocks", ctypes.c_int64), ("tokens", ctypes.c_int64),
                 ("accept_hist", ctypes.c_int64 * 257)]
@@ -95,7 +99,7 @@ def lib():
         L.orc_ar_decode.argtypes = [_vp, _vp, _i32, _i32, _vp]
         L.orc_jacobi_decode.restype = _i32
         L.orc_jacobi_decode.argtypes = [_vp, _vp, _i32, _i32, _i32, ctypes.POINTER(_GuessSpec), _i32, _vp,
-                                        ctypes.POINTER(_Stats), _vp, _vp, _i32]
+                                        ctypes.POINTER(_Stats), _vp, _vp, _i32, ctypes.POINTER(_Traj)]
         _lib = L
     return _lib
 
@@ -161,6 +165,55 @@ def accept_len(z, pred):
     return int(lib().orc_accept_len(_p(z), _p(pred), z.size))
 
 
+def trajectory_counts(traj, tokens, n, block_policy):
+    """Fast-forward and stationary token counts of a Jacobi trajectory (the paper's profiling
+    of CLLMs, Section 5 analysis and its profiling table), from records as returned by
+    Model.jacobi_decode(trace=True) and the decode's output tokens (the greedy continuation).
+
+    Fast-forward count of an iteration: its accepted length a, which includes the token that is
+    right without fast forwarding (as the profiling table counts it).
+
+    Output position q is stationary when, at some iteration t0 before the one that accepts q,
+    q already lies past the next pending position (q >= e + a + 1: a wrong token precedes it in
+    the block), its prediction is the final token y[q], and the prediction of q stays y[q] in
+    every iteration from t0 until q is accepted. Row k of an iteration predicts output position
+    e + k + 1. A token is counted in the block (or n-token window) that accepts it.
+
+    Returns dict: iterations, fast_forward_mean, stationary (total), windows (the blocks of
+    the shrink policy, block_policy 0, or ceil(tokens / n) windows of the slide policy),
+    stationary_per_window, positions (the stationary output positions)."""
+    T = len(traj)
+    y = np.asarray(tokens)
+    acc = {}
+    for t, r in enumerate(traj):
+        for q in range(r["e"], r["e"] + r["a"]):
+            acc[q] = t
+    positions = []
+    for q, tq in acc.items():
+        found = False
+        for t0 in range(tq):
+            r0 = traj[t0]
+            if q < r0["e"] + r0["a"] + 1:
+                continue
+            ok = True
+            for t in range(t0, tq):
+                r = traj[t]
+                k = q - r["e"] - 1
+                if not (0 <= k < r["m"]) or int(r["pred"][k]) != int(y[q]):
+                    ok = False
+                    break
+            if ok:
+                found = True
+                break
+        if found:
+            positions.append(q)
+    stationary = len(positions)
+    windows = len({r["b0"] for r in traj}) if block_policy == 0 else -(-len(acc) // n)
+    return {"iterations": T, "fast_forward_mean": sum(r["a"] for r in traj) / max(T, 1),
+            "stationary": stationary, "windows": windows,
+            "stationary_per_window": stationary / max(windows, 1), "positions": sorted(positions)}
+
+
 def mix(x):
     return int(lib().orc_mix(x))
 
@@ -224,21 +277,34 @@ class Model:
             raise RuntimeError(f"orc_ar_decode failed: {rc}")
         return out
 
-    def jacobi_decode(self, prompt, n, max_new, spec: GuessSpec, seq=0, max_steps=None):
+    def jacobi_decode(self, prompt, n, max_new, spec: GuessSpec, seq=0, max_steps=None, trace=False):
+        """Jacobi decoding with a KV cache (Appendix algorithm). With trace, stats["trajectory"]
+        holds one record per iteration: committed length L before it, output position e of the
+        block's first token, block start b0, rows m, accepted a, tokens z and predictions pred."""
         p = np.ascontiguousarray(prompt, dtype=np.int32)
         out = np.empty(max_new, dtype=np.int32)
         st = _Stats()
         cap = max_steps or max_new
         sm = np.zeros(cap, dtype=np.int32)
         sa = np.zeros(cap, dtype=np.int32)
+        tr = None
+        if trace:
+            tL, te, tb = (np.zeros(cap, dtype=np.int32) for _ in range(3))
+            tz = np.zeros((cap, n), dtype=np.int32)
+            tp = np.zeros((cap, n), dtype=np.int32)
+            tr = _Traj(_p(tL), _p(te), _p(tb), _p(tz), _p(tp), cap)
         rc = lib().orc_jacobi_decode(self.h, _p(p), p.size, n, max_new, ctypes.byref(spec.c), seq, _p(out),
-                                     ctypes.byref(st), _p(sm), _p(sa), cap)
+                                     ctypes.byref(st), _p(sm), _p(sa), cap, ctypes.byref(tr) if tr else None)
         if rc:
             raise RuntimeError(f"orc_jacobi_decode failed: {rc}")
         steps = int(st.steps)
         stats = {"steps": steps, "blocks": int(st.blocks), "tokens": int(st.tokens),
                  "accept_hist": [int(x) for x in st.accept_hist],
                  "step_m": sm[:min(steps, cap)].copy(), "step_a": sa[:min(steps, cap)].copy()}
+        if trace:
+            stats["trajectory"] = [
+                {"L": int(tL[t]), "e": int(te[t]), "b0": int(tb[t]), "m": int(sm[t]), "a": int(sa[t]),
+                 "z": tz[t, :sm[t]].copy(), "pred": tp[t, :sm[t]].copy()} for t in range(min(steps, cap))]
         return out, stats
 
 

@@ -72,6 +72,15 @@ typedef struct orc_guess_spec {
     uint64_t seed;
 } orc_guess_spec;
 
+/* Optional trajectory of a decode: per iteration t < cap the committed length L before the
+ * iteration, the output position e of the block's first token, the first output position b0
+ * of the current block (shrink policy; the slide policy keeps b0 = e), and the block tokens z
+ * and predictions pred (stride n; entries past the iteration's m are left unwritten). */
+typedef struct orc_traj {
+    int32_t *L, *e, *b0, *z, *pred;
+    int32_t cap;
+} orc_traj;
+
 typedef struct orc_stats {
     int64_t steps, blocks, tokens;
     int64_t accept_hist[257];
@@ -478,7 +487,7 @@ int32_t orc_ar_decode(const orc_model *m, const int32_t *prompt, int32_t len, in
  * step_m / step_a (capacity max_steps, may be NULL) record the trajectory's sizes. */
 int32_t orc_jacobi_decode(const orc_model *m, const int32_t *prompt, int32_t len, int32_t n, int32_t max_new,
                           const orc_guess_spec *gs, int32_t seq, int32_t *out, orc_stats *stats, int32_t *step_m,
-                          int32_t *step_a, int32_t max_steps) {
+                          int32_t *step_a, int32_t max_steps, const orc_traj *tr) {
     const int32_t V = m->c.vocab;
     if (n < 1 || max_new < 1 || !gs) return -1;
     orc_state *st = orc_state_new(m, len + max_new + n);
@@ -500,7 +509,18 @@ int32_t orc_jacobi_decode(const orc_model *m, const int32_t *prompt, int32_t len
     loc.blocks = 1;
     while (rc == 0 && e < max_new) {
         int32_t a;
+        const int32_t L_before = st->L;
         if (orc_jacobi_step(st, z, mlen, pred, &a, NULL)) { rc = -4; break; }
+        if (tr && loc.steps < tr->cap) {
+            const int64_t t = loc.steps;
+            tr->L[t] = L_before;
+            tr->e[t] = e;
+            tr->b0[t] = gs->block_policy == 0 ? b0 : e;
+            for (int32_t k = 0; k < mlen; ++k) {
+                tr->z[t * n + k] = z[k];
+                tr->pred[t * n + k] = pred[k];
+            }
+        }
         for (int32_t k = 0; k < a; ++k) out[e + k] = z[k];
         if (step_m && loc.steps < max_steps) { step_m[loc.steps] = mlen; step_a[loc.steps] = a; }
         e += a;

@@ -1,0 +1,97 @@
+"""Pins of the oracle's trajectory recorder and of its fast-forward / stationary token counts
+(the paper's profiling of Jacobi trajectories, Section 5 and its profiling table; the
+definition taken for stationary tokens is stated in oracle.trajectory_counts)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2403_00835_amd import workload
+from paper_2403_00835_amd.configs import (BLOCK_SHRINK, BLOCK_SLIDE, GUESS_STREAM, GUESS_STREAM_REINJECT,
+                                          GUESS_UNIFORM, TINY)
+
+
+def _rec(L, e, b0, z, pred):
+    z, pred = np.array(z, dtype=np.int32), np.array(pred, dtype=np.int32)
+    return {"L": L, "e": e, "b0": b0, "m": z.size, "a": oracle.accept_len(z, pred), "z": z, "pred": pred}
+
+
+# One block of n = 4, final tokens y = 10, 11, 12, 13; the model's own predictions iterate.
+# Iteration 0 predicts position 3 right (13) while position 1 is wrong; it stays right in
+# iteration 1 and is accepted in iteration 2: one stationary token.
+Y = [10, 11, 12, 13]
+STATIONARY = [_rec(16, 0, 0, [10, 5, 6, 7], [11, 9, 13, 20]),
+              _rec(17, 1, 0, [11, 9, 13], [12, 13, 14]),
+              _rec(18, 2, 0, [12, 13], [13, 14])]
+# The same start, but the prediction of position 3 changes in iteration 1: nothing stationary.
+CHANGED = [_rec(16, 0, 0, [10, 5, 6, 7], [11, 9, 13, 20]),
+           _rec(17, 1, 0, [11, 9, 13], [12, 3, 14]),
+           _rec(18, 2, 0, [12, 3], [13, 14]),
+           _rec(19, 3, 0, [13], [14])]
+
+
+def test_fixture_accepted_lengths():
+    assert [r["a"] for r in STATIONARY] == [1, 1, 2]
+    assert [r["a"] for r in CHANGED] == [1, 1, 1, 1]
+
+
+def test_stationary_token_counted():
+    c = oracle.trajectory_counts(STATIONARY, Y, 4, BLOCK_SHRINK)
+    assert c["iterations"] == 3 and c["stationary"] == 1 and c["windows"] == 1 and c["positions"] == [3]
+    assert c["fast_forward_mean"] == pytest.approx(4 / 3)
+
+
+def test_changed_prediction_not_stationary():
+    c = oracle.trajectory_counts(CHANGED, Y, 4, BLOCK_SHRINK)
+    assert c["stationary"] == 0 and c["fast_forward_mean"] == 1.0
+
+
+def test_next_pending_position_is_not_stationary():
+    # from iteration 1 on: position 2 is predicted right there, but it is the next pending
+    # position (e + a = 2), ordinary progress; position 3 (past it) is stationary
+    c = oracle.trajectory_counts(STATIONARY[1:], Y, 4, BLOCK_SHRINK)
+    assert c["positions"] == [3]
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return oracle.load_model(TINY, seed=0)
+
+
+def _trajectory_invariants(traj, out, stats, max_new, n, block_policy):
+    e = 0
+    for t, r in enumerate(traj):
+        assert r["e"] == e and 1 <= r["a"] <= r["m"] <= n
+        assert r["a"] == oracle.accept_len(r["z"], r["pred"])
+        np.testing.assert_array_equal(out[e:e + r["a"]], r["z"][:r["a"]])
+        if t > 0:
+            assert r["L"] == traj[t - 1]["L"] + traj[t - 1]["a"]
+            assert r["z"][0] == traj[t - 1]["pred"][traj[t - 1]["a"] - 1]
+        if block_policy == BLOCK_SLIDE:
+            assert r["b0"] == r["e"]
+        e += r["a"]
+    assert e == max_new == sum(r["a"] for r in traj) and len(traj) == stats["steps"]
+
+
+@pytest.mark.parametrize("policy,block_policy", [(GUESS_UNIFORM, BLOCK_SHRINK), (GUESS_STREAM, BLOCK_SHRINK),
+                                                 (GUESS_STREAM_REINJECT, BLOCK_SHRINK), (GUESS_STREAM, BLOCK_SLIDE)])
+def test_recorded_trajectories_are_consistent(tiny, policy, block_policy):
+    prompt = workload.make_prompt(TINY, 16, seed=4)
+    ar = tiny.ar_decode(prompt, 48)
+    spec = oracle.GuessSpec(policy, block_policy, None if policy == GUESS_UNIFORM else ar, p=0.4, seed=9)
+    out, st = tiny.jacobi_decode(prompt, 8, 48, spec, trace=True)
+    np.testing.assert_array_equal(out, ar)
+    _trajectory_invariants(st["trajectory"], out, st, 48, 8, block_policy)
+    c = oracle.trajectory_counts(st["trajectory"], out, 8, block_policy)
+    assert c["fast_forward_mean"] == pytest.approx(48 / st["steps"])
+    assert 0 <= c["stationary"] <= 48 - st["steps"]
+    if block_policy == BLOCK_SHRINK:
+        assert c["windows"] == st["blocks"]
+
+
+def test_exact_guesses_fast_forward_whole_blocks(tiny):
+    prompt = workload.make_prompt(TINY, 16, seed=5)
+    ar = tiny.ar_decode(prompt, 40)
+    spec = oracle.GuessSpec(GUESS_STREAM, BLOCK_SHRINK, ar, p=0.0, seed=1)
+    out, st = tiny.jacobi_decode(prompt, 8, 40, spec, trace=True)
+    c = oracle.trajectory_counts(st["trajectory"], out, 8, BLOCK_SHRINK)
+    assert c["iterations"] == 5 and c["fast_forward_mean"] == 8.0 and c["stationary"] == 0 and c["windows"] == 5

@@ -180,6 +180,14 @@ def main():
         log("[bench] calibration copy: 1073741824 bytes read, 1073741824 bytes written")
         del src, dst
 
+    # trajectory profile of one more (untimed) decode of the same request: fast-forwarded and
+    # stationary token counts (the paper's profiling of Jacobi trajectories)
+    model.trace_enable(True)
+    tr_out, _ = one_step()
+    traj = model.trace_read()
+    model.trace_enable(False)
+    tc = binding.trace_count(traj, tr_out, n, BLOCK_SHRINK)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, ws, mean_accept, n)
@@ -215,6 +223,8 @@ def main():
         "speedup_vs_ar": round(value / ar_tps, 3),
         "step_hbm_gbps": round(step_gbps, 1),
         "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "trajectory": {"fast_forward_mean": round(tc["fast_forward_mean"], 4), "stationary": tc["stationary"],
+                       "blocks": tc["windows"], "stationary_per_block": round(tc["stationary_per_window"], 4)},
         "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (per layer)", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),

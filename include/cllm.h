@@ -198,6 +198,41 @@ cllm_status cllm_reset(cllm_ctx *ctx, int32_t seq);
  * max(64, max_batch * max_block) * vocab). Errors: ERR_ARG. */
 cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, size_t host_floats);
 
+/* Trajectory recording (the paper's profiling of Jacobi trajectories, Section 5: fast-forwarded
+ * and stationary tokens). While enabled, every iteration of a decode call (cllm_jacobi_decode,
+ * cllm_jacobi_decode_batch) writes one record per sequence into a device buffer of max_batch x
+ * max_new records that the context allocates on the first enable (and frees with the context).
+ * A record is CLLM_TRACE_STRIDE int32: [0] committed length L before the iteration, [1] output
+ * position e of the block's first token (z[0] = out_tokens[e]), [2] first output position of
+ * the current block (shrink policy; e for the slide policy), [3] rows m, [4] accepted length a,
+ * [5 .. 5+m) the block tokens z, [5+64 .. 5+64+m) the predictions (row k predicts output
+ * position e+k+1); other entries are unspecified. Errors: ERR_ARG, ERR_OOM. */
+#define CLLM_TRACE_STRIDE (5 + 2 * 64)
+cllm_status cllm_trace_enable(cllm_ctx *ctx, int32_t enable);
+
+/* Copies up to cap records of the last decode of slot seq that ran with recording on into
+ * records[cap * CLLM_TRACE_STRIDE] (caller-owned host memory); *n_records = the number that
+ * decode wrote (0 if it ran without recording). Synchronous. Errors: ERR_ARG, ERR_DEVICE. */
+cllm_status cllm_trace_read(cllm_ctx *ctx, int32_t seq, int32_t *records, int64_t cap, int64_t *n_records);
+
+/* Counts over a recorded trajectory (host computation, no context): the fast-forward count of
+ * an iteration is its accepted length (it includes the token that is right without fast
+ * forwarding); output position q is stationary when, in some iteration t0 before the one that
+ * accepts q, q lies past the next pending position (q >= e + a + 1) and its prediction equals
+ * tokens[q] (the decode's output) in every iteration from t0 until q is accepted. windows =
+ * blocks of the shrink policy (block_policy 0) or ceil(n_tokens / n) n-token windows of the
+ * slide policy (1). Errors: ERR_ARG for null pointers, n outside [1, 64], an unknown policy
+ * or records inconsistent with n_tokens. */
+typedef struct {
+    int64_t iterations;
+    double fast_forward_mean;
+    int64_t stationary;
+    int64_t windows;
+    double stationary_per_window;
+} cllm_trace_stats;
+cllm_status cllm_trace_count(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
+                             int32_t n, int32_t block_policy, cllm_trace_stats *out);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 

@@ -43,10 +43,18 @@ class cllm_decode_stats(ctypes.Structure):
                 ("iter_ms_p50", _dbl), ("iter_ms_p90", _dbl), ("iter_ms_full_p50", _dbl)]
 
 
+class cllm_trace_stats(ctypes.Structure):
+    _fields_ = [("iterations", _i64), ("fast_forward_mean", _dbl), ("stationary", _i64), ("windows", _i64),
+                ("stationary_per_window", _dbl)]
+
+
+TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
+
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
-           "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_seq_state", "cllm_timing_enable",
-           "cllm_timing_read", "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
+           "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
+           "cllm_trace_count", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
+           "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
 
@@ -74,6 +82,9 @@ def lib():
         L.cllm_reset.argtypes = [_vp, _i32]
         L.cllm_debug_logits.argtypes = [_vp, _i32, _vp, ctypes.c_size_t]
         L.cllm_seq_state.argtypes = [_vp, _i32, P(_i32), P(_i32)]
+        L.cllm_trace_enable.argtypes = [_vp, _i32]
+        L.cllm_trace_read.argtypes = [_vp, _i32, _vp, _i64, P(_i64)]
+        L.cllm_trace_count.argtypes = [_vp, _i64, _vp, _i64, _i32, _i32, P(cllm_trace_stats)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
         L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
         L.cllm_streamed_weight_bytes.argtypes = [_vp]
@@ -247,6 +258,17 @@ class Model:
         self._check(self.L.cllm_seq_state(self.h, seq, ctypes.byref(L), ctypes.byref(pend)))
         return int(L.value), int(pend.value)
 
+    def trace_enable(self, enable=True):
+        self._check(self.L.cllm_trace_enable(self.h, 1 if enable else 0))
+
+    def trace_read(self, seq=0):
+        """Records of the slot's last recorded decode, as dicts (L, e, b0, m, a, z, pred)."""
+        n = _i64(0)
+        self._check(self.L.cllm_trace_read(self.h, seq, None, 0, ctypes.byref(n)))
+        raw = np.zeros((max(int(n.value), 1), TRACE_STRIDE), dtype=np.int32)
+        self._check(self.L.cllm_trace_read(self.h, seq, _p(raw), int(n.value), ctypes.byref(n)))
+        return records_to_dicts(raw[:int(n.value)])
+
     def timing_enable(self, kernel_class, max_rows=0, every=1):
         cls = KT[kernel_class] if isinstance(kernel_class, str) else int(kernel_class)
         self._check(self.L.cllm_timing_enable(self.h, cls, max_rows, every))
@@ -255,6 +277,38 @@ class Model:
         n, ms = _i64(0), _dbl(0.0)
         self._check(self.L.cllm_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms)))
         return int(n.value), float(ms.value)
+
+
+def records_to_dicts(raw):
+    out = []
+    for r in raw:
+        m = int(r[3])
+        out.append({"L": int(r[0]), "e": int(r[1]), "b0": int(r[2]), "m": m, "a": int(r[4]),
+                    "z": r[5:5 + m].copy(), "pred": r[5 + 64:5 + 64 + m].copy()})
+    return out
+
+
+def dicts_to_records(traj):
+    raw = np.zeros((max(len(traj), 1), TRACE_STRIDE), dtype=np.int32)
+    for t, r in enumerate(traj):
+        raw[t, :5] = [r["L"], r["e"], r["b0"], r["m"], r["a"]]
+        raw[t, 5:5 + r["m"]] = r["z"]
+        raw[t, 5 + 64:5 + 64 + r["m"]] = r["pred"]
+    return raw[:len(traj)]
+
+
+def trace_count(traj, tokens, n, block_policy):
+    """Fast-forward and stationary counts of a trajectory (cllm_trace_count)."""
+    raw = dicts_to_records(traj) if isinstance(traj, list) else np.ascontiguousarray(traj, dtype=np.int32)
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    st = cllm_trace_stats()
+    rc = lib().cllm_trace_count(_p(raw) if raw.size else None, raw.shape[0], _p(tok) if tok.size else None,
+                                tok.size, n, block_policy, ctypes.byref(st))
+    if rc:
+        raise CllmError(rc, "cllm_trace_count")
+    return {"iterations": int(st.iterations), "fast_forward_mean": float(st.fast_forward_mean),
+            "stationary": int(st.stationary), "windows": int(st.windows),
+            "stationary_per_window": float(st.stationary_per_window)}
 
 
 def _stats(st):

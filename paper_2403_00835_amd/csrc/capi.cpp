@@ -64,7 +64,10 @@ struct cllm_ctx {
     struct Slot {
         bool prefilled = false;
         int L = 0, pending = 0;
+        int64_t trace_n = 0;  // trajectory records of the slot's last recorded decode
     };
+    int32_t *trace_dev = nullptr;  // trajectory records: max_batch x max_new x kTraceStride int32
+    bool trace_on = false;
     std::vector<Slot> slot;
     bool dead = false;
     std::string err;
@@ -105,6 +108,8 @@ cllm_status fail(cllm_ctx *c, cllm_status s, const char *fmt, ...) {
             return fail((c), CLLM_ERR_DEVICE, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(_e), \
                         __FILE__, __LINE__);                                                       \
     } while (0)
+
+static_assert(CLLM_TRACE_STRIDE == kTraceStride && kMaxBlock == 64, "trajectory record layout of the header");
 
 inline int round_up(int x, int a) { return (x + a - 1) / a * a; }
 inline int rows_to_rg(int rows) { return rows <= 16 ? 1 : (rows <= 32 ? 2 : 4); }
@@ -336,6 +341,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
     sp.stream_stride = c->stream_cap;
     sp.plan_inline = sh.nseq == 1;
     sp.mlog = out_dev ? c->mlog_dev : nullptr;
+    sp.trace = (out_dev && c->trace_on) ? c->trace_dev : nullptr;
+    sp.trace_cap = c->opts.max_new;
     if (sh.with_lm) {
         GemmParams lm = base;
         lm.W = c->w_lm;
@@ -651,6 +658,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
         c->slot[q].prefilled = true;
         c->slot[q].L = ct.L;
         c->slot[q].pending = ct.pending;
+        c->slot[q].trace_n = c->trace_on ? std::min<int64_t>(ct.steps, c->opts.max_new) : 0;
     }
     return CLLM_OK;
 }
@@ -1044,6 +1052,71 @@ cllm_status cllm_debug_logits(cllm_ctx *c, int32_t enable, float *host_buf, size
         c->dbg_host = nullptr;
         c->dbg_cap = 0;
     }
+    return CLLM_OK;
+}
+
+cllm_status cllm_trace_enable(cllm_ctx *c, int32_t enable) {
+    if (!c) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c))) return s;
+    if (enable && !c->trace_dev) {
+        const size_t n = (size_t)c->max_batch * c->opts.max_new * kTraceStride;
+        if ((s = dalloc_t(c, &c->trace_dev, n))) return s;
+    }
+    c->trace_on = enable != 0;
+    return CLLM_OK;
+}
+
+cllm_status cllm_trace_read(cllm_ctx *c, int32_t seq, int32_t *records, int64_t cap, int64_t *n_records) {
+    if (!c || !n_records || cap < 0 || (cap > 0 && !records)) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_seq(c, seq))) return s;
+    const int64_t n = std::min<int64_t>(cap, c->slot[seq].trace_n);
+    *n_records = c->slot[seq].trace_n;
+    if (n > 0)
+        HIPCHK(c, hipMemcpy(records, c->trace_dev + (size_t)seq * c->opts.max_new * kTraceStride,
+                            (size_t)n * kTraceStride * sizeof(int32_t), hipMemcpyDeviceToHost));
+    return CLLM_OK;
+}
+
+cllm_status cllm_trace_count(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
+                             int32_t n, int32_t block_policy, cllm_trace_stats *out) {
+    if (!out || n_records < 0 || n_tokens < 0 || (n_records > 0 && (!records || !tokens)) || n < 1 ||
+        n > kMaxBlock || (block_policy != 0 && block_policy != 1))
+        return CLLM_ERR_ARG;
+    memset(out, 0, sizeof(*out));
+    auto rec = [&](int64_t t) { return records + t * kTraceStride; };
+    // acceptance iteration of every output position, and the records' sanity
+    std::vector<int64_t> acc((size_t)n_tokens, -1);
+    int64_t a_sum = 0;
+    std::vector<int32_t> starts;
+    for (int64_t t = 0; t < n_records; ++t) {
+        const int32_t *r = rec(t);
+        const int32_t e = r[1], m = r[3], a = r[4];
+        if (m < 1 || m > n || a < 1 || a > m || e < 0 || (int64_t)e + a > n_tokens) return CLLM_ERR_ARG;
+        for (int32_t q = e; q < e + a; ++q) acc[q] = t;
+        a_sum += a;
+        if (starts.empty() || starts.back() != r[2]) starts.push_back(r[2]);
+    }
+    // stationary: walking back from the iteration before q's acceptance while q's prediction
+    // is its final token, some iteration has q past its next pending position
+    int64_t stationary = 0;
+    for (int64_t q = 0; q < n_tokens; ++q) {
+        for (int64_t t = acc[q] - 1; t >= 0; --t) {
+            const int32_t *r = rec(t);
+            const int64_t k = q - r[1] - 1;
+            if (k < 0 || k >= r[3] || r[5 + kMaxBlock + k] != tokens[q]) break;
+            if (q >= (int64_t)r[1] + r[4] + 1) {
+                ++stationary;
+                break;
+            }
+        }
+    }
+    out->iterations = n_records;
+    out->fast_forward_mean = n_records ? (double)a_sum / (double)n_records : 0.0;
+    out->stationary = stationary;
+    out->windows = block_policy == 0 ? (int64_t)starts.size() : (n_tokens + n - 1) / n;
+    out->stationary_per_window = out->windows ? (double)stationary / (double)out->windows : 0.0;
     return CLLM_OK;
 }
 

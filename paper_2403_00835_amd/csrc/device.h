@@ -17,6 +17,10 @@ constexpr int kMaxSeqs = 64;       // sequences of one batched iteration
 constexpr int kGemmWaves = 8;      // waves per GEMM workgroup; they split K
 constexpr int kAttnChunk = 64;     // keys per attention workgroup, at absolute positions
 constexpr int kMaxChunks = 1024;   // attention chunks per sequence: context <= 65536
+// Trajectory record of one decode iteration (int32): L before it, output position e of z[0],
+// block start b0 (shrink policy; e for the slide policy), rows m, accepted a, z[kMaxBlock],
+// pred[kMaxBlock].
+constexpr int kTraceStride = 5 + 2 * kMaxBlock;
 constexpr int kTileBytes = 1024;   // one packed weight tile: 16 rows x 16 bytes x 4 lane groups
 #ifndef CLLM_WEIGHTS_NT
 #define CLLM_WEIGHTS_NT 1

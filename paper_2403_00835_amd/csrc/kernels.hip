@@ -1042,7 +1042,7 @@ __global__ void decode_init_kernel(ScanParams p) {
 
 // Acceptance, commit, emit and the next block of one sequence, from its predictions c->pred
 // (one thread).
-__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream, int32_t *mlog) {
+__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream, int32_t *mlog, int32_t *rec) {
     for (int i = 0; i < (c->mode == MODE_PREFILL ? 1 : m); ++i)
         if (c->pred[i] < 0) {
             c->err |= 1;
@@ -1058,6 +1058,13 @@ __device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stre
     }
     int a = 1;
     while (a < m && c->z[a] == c->pred[a - 1]) ++a;
+    if (rec) {  // trajectory record header (its z and pred were written by the scan's threads)
+        rec[0] = c->L;
+        rec[1] = c->e;
+        rec[2] = c->block_policy == 0 ? c->b0 : c->e;
+        rec[3] = m;
+        rec[4] = a;
+    }
     c->L += a;
     c->a_last = a;
     if (mlog && c->mode == MODE_DECODE && c->steps < c->max_new) mlog[c->steps] = m;
@@ -1152,6 +1159,10 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
             s_i[tid] = bx;
             s_nan[tid] = nan;
             __syncthreads();
+            // this iteration's trajectory record (decode loops with recording on)
+            int32_t *rec = (p.trace && c->mode == MODE_DECODE && c->steps < p.trace_cap)
+                               ? p.trace + ((size_t)seq * p.trace_cap + c->steps) * kTraceStride
+                               : nullptr;
             if (tid < nrows) {
                 float best = s_v[tid];
                 int i = s_i[tid], nn = s_nan[tid];
@@ -1161,13 +1172,18 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
                     nn |= s_nan[jj * 64 + tid];
                     if (ov > best || (ov == best && oi < i)) { best = ov; i = oi; }
                 }
-                c->pred[tid] = (nn || i == 0x7fffffff) ? -1 : i;
+                const int pr = (nn || i == 0x7fffffff) ? -1 : i;
+                c->pred[tid] = pr;
+                if (rec) {
+                    rec[5 + tid] = c->z[tid];
+                    rec[5 + kMaxBlock + tid] = pr;
+                }
             }
             __syncthreads();
             if (tid == 0)
                 commit_and_next(c, m, p.out ? p.out + (size_t)seq * p.out_stride : nullptr,
                                 p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr,
-                                p.mlog ? p.mlog + (size_t)seq * p.out_stride : nullptr);
+                                p.mlog ? p.mlog + (size_t)seq * p.out_stride : nullptr, rec);
         }
     }
     if (p.plan_inline) {

@@ -96,6 +96,8 @@ struct ScanParams {
     int advance_only;       // prefill chunk without LM head: commit all rows, no predictions
     int plan_inline;        // one batch entry: the scan also lays out the next row table
     int32_t *mlog;          // block size of each decode iteration (out_stride entries per slot), or null
+    int32_t *trace;         // decode trajectory records (trace_cap per slot, kTraceStride int32 each), or null
+    int trace_cap;
 };
 
 // Host-side edits of the control blocks and the row table, applied on the stream in order with

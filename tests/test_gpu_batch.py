@@ -196,3 +196,32 @@ def test_7b_batched_ragged_full_size():
     single, _ = m.ar_decode(prompts[0], wl.max_new, seq=0)
     np.testing.assert_array_equal(single, ar[0])
     m.close()
+
+
+def test_tiny_batched_trajectories_equal_single(tiny):
+    """Trajectory records of a batched decode, per sequence slot, equal the records of the same
+    sequence decoded alone in the same slot (the guess draws depend on the slot id; every row
+    is computed as in a single-sequence iteration)."""
+    ws, batched, single = tiny
+    slots = (4, 1, 6)
+    prompts = [workload.make_prompt(TINY, L, seed=36, seq=b) for b, L in enumerate([12, 70, 33])]
+    ars = [single.ar_decode(p, 40)[0] for p in prompts]
+    specs = _specs(prompts, ars, POLICIES)
+    log("[gpu-batch] tiny: trajectories of a batched decode vs single decodes")
+    batched.trace_enable(True)
+    try:
+        out, stats = batched.jacobi_decode_batch(list(slots), prompts, 8, 40, specs=specs)
+        trajs = [batched.trace_read(q) for q in slots]
+        for b, p in enumerate(prompts):
+            sp = specs[b]
+            o1, _ = batched.jacobi_decode(p, 8, 40, seq=slots[b], policy=sp["policy"], block_policy=sp["block_policy"],
+                                          stream=sp["stream"], p=sp["p"], seed=sp["seed"])
+            np.testing.assert_array_equal(out[b], o1)
+            t1 = batched.trace_read(slots[b])
+            assert len(t1) == len(trajs[b]) == stats[b]["steps"]
+            for r, r1 in zip(trajs[b], t1):
+                assert {k: r[k] for k in ("L", "e", "b0", "m", "a")} == {k: r1[k] for k in ("L", "e", "b0", "m", "a")}
+                np.testing.assert_array_equal(r["z"], r1["z"])
+                np.testing.assert_array_equal(r["pred"], r1["pred"])
+    finally:
+        batched.trace_enable(False)

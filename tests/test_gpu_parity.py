@@ -277,3 +277,34 @@ def test_kernel_timing_sampling(tiny):
     with pytest.raises(binding.CllmError) as e:
         g.timing_enable("gate_up", max_rows=8, every=0)
     assert e.value.status == 1
+
+
+@pytest.mark.parametrize("policy,block_policy", [(GUESS_STREAM, 0), (GUESS_STREAM_REINJECT, 0), (GUESS_STREAM, 1)])
+def test_tiny_trajectory_equals_oracle(tiny, policy, block_policy):
+    """The GPU's recorded trajectory (every iteration's L, e, block start, m, a, z and
+    predictions) equals the oracle's, and so do the fast-forward and stationary counts."""
+    from paper_2403_00835_amd import binding
+    log(f"[gpu] tiny trajectory vs oracle policy={policy} block={block_policy}")
+    prompt = workload.make_prompt(TINY, 16, seed=12)
+    ar, _ = tiny.gpu.ar_decode(prompt, 64)
+    g = tiny.gpu
+    g.trace_enable(True)
+    try:
+        out, st = g.jacobi_decode(prompt, 8, 64, policy=policy, block_policy=block_policy, stream=ar, p=0.3, seed=4)
+        traj = g.trace_read()
+    finally:
+        g.trace_enable(False)
+    spec = oracle.GuessSpec(policy, block_policy, ar, p=0.3, seed=4)
+    out_o, st_o = tiny.orc.jacobi_decode(prompt, 8, 64, spec, trace=True)
+    np.testing.assert_array_equal(out, out_o)
+    assert len(traj) == st["steps"] == st_o["steps"]
+    for t, (r, ro) in enumerate(zip(traj, st_o["trajectory"])):
+        assert {k: r[k] for k in ("L", "e", "b0", "m", "a")} == {k: ro[k] for k in ("L", "e", "b0", "m", "a")}, t
+        np.testing.assert_array_equal(r["z"], ro["z"])
+        np.testing.assert_array_equal(r["pred"], ro["pred"])
+    c = binding.trace_count(traj, out, 8, block_policy)
+    co = oracle.trajectory_counts(st_o["trajectory"], out_o, 8, block_policy)
+    assert (c["iterations"], c["stationary"], c["windows"]) == (co["iterations"], co["stationary"], co["windows"])
+    # a decode without recording leaves no records
+    g.jacobi_decode(prompt, 8, 64, policy=policy, block_policy=block_policy, stream=ar, p=0.3, seed=4)
+    assert g.trace_read() == []

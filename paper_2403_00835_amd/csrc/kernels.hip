@@ -142,7 +142,7 @@ __device__ __forceinline__ void row_factor_reduce(const GemmParams &p, int row0,
 // Epilogues of a finished ROWS x COLS output tile in s_tile (row stride COLS + 1) for rows
 // [row0, row0 + ROWS) of the iteration (m of them live) and column workgroup wg of width COLS
 // (columns at or past p.cols, in a ragged last workgroup, are dropped); s_red is scratch of at
-// least ROWS x COLS floats. Shared by both GEMM kernels.
+// least ROWS x COLS floats.
 template <Prec P, int NT, int RG, int EP, int W>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile, float *s_red, int row0, int m, int wg,
                                               int tid, int lane, int w) {
@@ -353,165 +353,6 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     }
 
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
-}
-
-// ------------------------------------------------------------------------------------------
-// Row-tiled GEMM for iterations of more than 64 rows (batched blocks, prefill chunks).
-//
-// A workgroup computes a 64-row x 16*TNT-column tile; its 8 waves (2 x 4: 32 rows x 16*TNT/4
-// columns each) share the operands through LDS, in blocks of kTileKB k-steps that are double
-// buffered in LDS and prefetched two blocks ahead in registers. Each output element is accumulated
-// exactly as in gemm_kernel: eight partial sums, one per k-step class s mod 8 (each in increasing
-// s, hi plane then lo plane per k-step), then the same fixed tree and row factor, so a row's
-// results are bit-identical whichever of the two kernels computed them.
-// ------------------------------------------------------------------------------------------
-constexpr int kTileKB = 4;  // k-steps per LDS block
-
-template <Prec P, int TNT>
-struct TileShape {
-    static constexpr int RG = 4, ROWS = 64, COLS = 16 * TNT;
-    static constexpr int NA = kTileKB * PrecT<P>::PLANES * RG;  // activation tiles per block
-    static constexpr int NB = kTileKB * TNT;                    // weight tiles per block
-    static constexpr int NTL = NA + NB;
-    static constexpr size_t lds_bytes = (size_t)(2 * NTL * 256 + ROWS) * sizeof(float);
-};
-
-template <Prec P, int TNT, int EP>
-__global__ __launch_bounds__(512) void gemm_tile_kernel(GemmParams p) {
-    using PT = PrecT<P>;
-    using T = typename PT::T;
-    using SH = TileShape<P, TNT>;
-    constexpr int W = 8, RG = SH::RG, ROWS = SH::ROWS, COLS = SH::COLS, PL = PT::PLANES;
-    constexpr int NA = SH::NA, NTL = SH::NTL, LPW = NTL / W;  // tile loads per wave per block
-    constexpr int TW = TNT / 4;                                // tiles per wave along the columns
-    constexpr bool ROWSCALE = EP != E_RESID;
-    static_assert(NTL % W == 0 && TNT % 4 == 0, "tile loads split evenly over the waves");
-    static_assert(2 * NTL * 256 >= ROWS * (COLS + 1) + ROWS * COLS, "epilogue tiles reuse the staging LDS");
-    const int wg = blockIdx.x;
-    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
-    const int m = p.rr.tab->R - row0;
-    if (m <= 0) return;
-    const int rg0 = row0 >> 4;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wr = w >> 2, wc = w & 3;  // row groups 2wr, 2wr+1; column tiles wc*TW ..
-    const int t0 = wg * TNT;
-    const int tall = p.cols >> 4;
-    const int ks_a = p.lda / PT::KSTEP;
-    const int nblk = (p.Ks + kTileKB - 1) / kTileKB;
-    const size_t plane = act_plane(p.rr.cap, p.lda);
-
-    extern __shared__ float smem[];
-    uint8_t *lds = reinterpret_cast<uint8_t *>(smem);  // 2 x NTL tiles of 1 KiB
-    float *s_inv = smem + 2 * NTL * 256;               // ROWS
-
-    // Tile i of block blk: activation tiles (k-step, plane, row group) first, then weight tiles
-    // (k-step, column tile). k-steps past the end are clamped (their products are skipped).
-    auto tile_src = [&](int blk, int i) -> const u32x4 * {
-        if (i < NA) {
-            const int ks = i / (PL * RG), pl = (i / RG) % PL, r = i % RG;
-            const int s = min(blk * kTileKB + ks, p.Ks - 1);
-            const T *A = reinterpret_cast<const T *>(p.A) + pl * plane;
-            return reinterpret_cast<const u32x4 *>(A + (size_t)((rg0 + r) * ks_a + s) * kWave * PT::VEC) + lane;
-        }
-        const int j = i - NA, ks = j / TNT, t = j % TNT;
-        const int s = min(blk * kTileKB + ks, p.Ks - 1);
-        return reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tall + t0 + t) * kTileBytes) + lane;
-    };
-    auto issue = [&](u32x4 (&dst)[LPW], int blk) {
-#pragma unroll
-        for (int k = 0; k < LPW; ++k) dst[k] = *tile_src(blk, w + W * k);
-    };
-    auto commit = [&](const u32x4 (&src)[LPW], int buf) {
-#pragma unroll
-        for (int k = 0; k < LPW; ++k)
-            *reinterpret_cast<u32x4 *>(lds + ((size_t)buf * NTL + w + W * k) * kTileBytes + lane * 16) = src[k];
-    };
-    auto lds_tile = [&](int buf, int i) {
-        return *reinterpret_cast<const u32x4 *>(lds + ((size_t)buf * NTL + i) * kTileBytes + lane * 16);
-    };
-
-    f32x4 sq_pre[2];
-    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
-    f32x4 acc[8][2][TW];
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-#pragma unroll
-            for (int t = 0; t < TW; ++t) acc[c][r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Block b's k-steps belong to classes 4 * (b % 2) + ks: the loop runs two blocks per trip so
-    // the class (an accumulator index) is a compile-time constant.
-    auto compute = [&](int blk, int buf, auto cls_base) {
-        constexpr int CB = decltype(cls_base)::value;
-#pragma unroll
-        for (int ks = 0; ks < kTileKB; ++ks) {
-            if (blk * kTileKB + ks < p.Ks) {
-                u32x4 a[PL][2], bw[TW];
-#pragma unroll
-                for (int pl = 0; pl < PL; ++pl)
-#pragma unroll
-                    for (int r = 0; r < 2; ++r) a[pl][r] = lds_tile(buf, (ks * PL + pl) * RG + 2 * wr + r);
-#pragma unroll
-                for (int t = 0; t < TW; ++t) bw[t] = lds_tile(buf, NA + ks * TNT + wc * TW + t);
-#pragma unroll
-                for (int pl = 0; pl < PL; ++pl)
-#pragma unroll
-                    for (int r = 0; r < 2; ++r)
-#pragma unroll
-                        for (int t = 0; t < TW; ++t)
-                            acc[CB + ks][r][t] = mfma_kstep<P>(a[pl][r], bw[t], acc[CB + ks][r][t]);
-            }
-        }
-    };
-
-    // The compiler waits for a register stage's loads (exact counts: every load is issued,
-    // clamped) before its commit; sched_barrier keeps a stage's loads ahead of the block's MFMAs.
-    u32x4 stg[2][LPW];
-    issue(stg[0], 0);
-    issue(stg[1], min(1, nblk - 1));
-    commit(stg[0], 0);
-    __syncthreads();
-    for (int b0 = 0; b0 < nblk; b0 += 2) {
-        // block b0 (LDS buffer 0, classes 0..3), then block b0 + 1 (buffer 1, classes 4..7)
-        issue(stg[0], min(b0 + 2, nblk - 1));
-        __builtin_amdgcn_sched_barrier(0);
-        compute(b0, 0, std::integral_constant<int, 0>{});
-        commit(stg[1], 1);  // block b0 + 1
-        __syncthreads();
-        if (b0 + 1 < nblk) {
-            issue(stg[1], min(b0 + 3, nblk - 1));
-            __builtin_amdgcn_sched_barrier(0);
-            compute(b0 + 1, 1, std::integral_constant<int, 4>{});
-            commit(stg[0], 0);  // block b0 + 2
-            __syncthreads();
-        }
-    }
-
-    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
-    __syncthreads();
-    float *s_tile = smem;                    // ROWS x (COLS + 1), over the staging buffers
-    float *s_red = s_tile + ROWS * (COLS + 1);  // ROWS x COLS
-#pragma unroll
-    for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int t = 0; t < TW; ++t) {
-            // the fixed tree of gemm_kernel: ((c0+c4)+(c2+c6))+((c1+c5)+(c3+c7))
-            const f32x4 sum = ((acc[0][r][t] + acc[4][r][t]) + (acc[2][r][t] + acc[6][r][t])) +
-                              ((acc[1][r][t] + acc[5][r][t]) + (acc[3][r][t] + acc[7][r][t]));
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                // C layout: row 4*(l/16)+v, column l%16 of the 16 x 16 tile
-                const int row = 16 * (2 * wr + r) + 4 * (lane >> 4) + v;
-                const int col = 16 * (wc * TW + t) + (lane & 15);
-                float x = sum[v];
-                if constexpr (ROWSCALE) x *= s_inv[row];
-                s_tile[row * (COLS + 1) + col] = x;
-            }
-        }
-    __syncthreads();
-    gemm_epilogue<P, TNT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1238,39 +1079,22 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     return hipGetLastError();
 }
 
-template <Prec P, int TNT, int EP>
-static hipError_t launch_gemm_tile_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    using SH = TileShape<P, TNT>;
-    GemmParams q = p;
-    q.row_tiles = row_tiles;
-    q.n_wg = p.cols / SH::COLS;
-    auto kern = gemm_tile_kernel<P, TNT, EP>;
-    const dim3 grid(q.n_wg, row_tiles);
-    if (e0)
-        hipExtLaunchKernelGGL(kern, grid, dim3(512), SH::lds_bytes, s, e0, e1, 0, q);
-    else
-        hipLaunchKernelGGL(kern, grid, dim3(512), SH::lds_bytes, s, q);
-    return hipGetLastError();
-}
-
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
     if (row_tiles > 1) {
-        // More than 64 rows: gate/up runs the LDS-tiled kernel (128-column tiles; measured faster
-        // than gemm_kernel there, slower for the other products at ~160 rows), the others
-        // 64-column tiles of gemm_kernel with three k-steps in flight. Neither changes any row's
-        // reduction order.
-        if (kind == GEMM_GATE_UP && p.cols % 128 == 0)
-            return launch_gemm_tile_t<P, 8, E_SWIGLU>(p, row_tiles, s, e0, e1);
+        // More than 64 rows (measured at 160 and 512 rows, 7B): QKV and gate/up take 96-column
+        // workgroups (two k-steps in flight), O and down 64-column workgroups (three k-steps in
+        // flight). Row tiles past the iteration's rows exit at once, so a batched iteration
+        // launched for its largest row count costs what its live rows cost.
         switch (kind) {
         case GEMM_QKV:
-            return launch_gemm_t<P, 4, RG, E_QKV, 3>(p, row_tiles, s, e0, e1);
+            return launch_gemm_t<P, 6, RG, E_QKV, 2>(p, row_tiles, s, e0, e1);
         case GEMM_O:
         case GEMM_DOWN:
             return launch_gemm_t<P, 4, RG, E_RESID, 3>(p, row_tiles, s, e0, e1);
         case GEMM_GATE_UP:
-            return launch_gemm_t<P, 4, RG, E_SWIGLU, 3>(p, row_tiles, s, e0, e1);
+            return launch_gemm_t<P, 6, RG, E_SWIGLU, 2>(p, row_tiles, s, e0, e1);
         case GEMM_LM:
             return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX, 3>(p, row_tiles, s, e0, e1);
         }
@@ -1368,8 +1192,7 @@ hipError_t launch_attn_fused(bool bf16, int nrg, int nseq_launch, const AttnPara
         case 32: return launch_attn_fused_hd<Prec::BF16, 32>(nrg, nseq_launch, p, s, e0, e1);
         case 64: return launch_attn_fused_hd<Prec::BF16, 64>(nrg, nseq_launch, p, s, e0, e1);
         case 128: return launch_attn_fused_hd<Prec::BF16, 128>(nrg, nseq_launch, p, s, e0, e1);
-        case 256: return launch_attn_fused_hd<Prec::BF16, 256>(nrg, nseq_launch, p, s, e0, e1);
-        }
+        }  // head_dim 256: two chunks of keys do not fit the registers; the two-kernel path
     } else {
         switch (p.hd) {
         case 16: return launch_attn_fused_hd<Prec::F32, 16>(nrg, nseq_launch, p, s, e0, e1);

@@ -130,7 +130,8 @@ hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const
 hipError_t launch_attn_combine(bool bf16, int rows, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                                hipEvent_t e1);
 // One-kernel attention: nrg 16-row groups per batch entry, no row seeing more than
-// kFusedChunks 64-key chunks (O written directly; bit-identical to launch_attn + combine).
+// kFusedChunks 64-key chunks, head_dim <= 128 (O written directly; bit-identical to
+// launch_attn + combine).
 constexpr int kFusedChunks = 32;
 hipError_t launch_attn_fused(bool bf16, int nrg, int nseq_launch, const AttnParams &p, hipStream_t s, hipEvent_t e0,
                              hipEvent_t e1);

@@ -22,11 +22,6 @@ constexpr int kMaxChunks = 1024;   // attention chunks per sequence: context <= 
 // pred[kMaxBlock].
 constexpr int kTraceStride = 5 + 2 * kMaxBlock;
 constexpr int kTileBytes = 1024;   // one packed weight tile: 16 rows x 16 bytes x 4 lane groups
-#ifndef CLLM_WEIGHTS_NT
-#define CLLM_WEIGHTS_NT 1
-#endif
-constexpr bool kWeightsNonTemporal = CLLM_WEIGHTS_NT;  // weights are streamed once per iteration
-constexpr int kGainVecs = 4;       // RMSNorm gain staging: d_model <= 4 * 4 * 512
 
 // Precision traits. A "k-step" is the K extent one wave covers with one 16-byte load per lane:
 // 4 lane groups x VEC elements. bf16: one 16x16x32 MFMA per k-step; fp32: four 16x16x4 MFMAs.

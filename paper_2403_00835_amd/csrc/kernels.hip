@@ -66,8 +66,7 @@ __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams
     for (int j = 0; j < NT; ++j) {
         const u32x4 *src =
             reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tiles + min(t0 + j, tiles - 1)) * kTileBytes) + lane;
-        if constexpr (kWeightsNonTemporal) st.b[j] = __builtin_nontemporal_load(src);
-        else st.b[j] = *src;
+        st.b[j] = __builtin_nontemporal_load(src);  // streamed once per iteration
     }
     const T *A = reinterpret_cast<const T *>(p.A);
     const int ks_a = p.lda / PT::KSTEP;
@@ -92,8 +91,6 @@ __device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG> &st, f32x4 (
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
-// W waves per workgroup split K; KC selects each wave's k-steps: interleaved (w, w+W, ...) or a
-// contiguous range.
 // Row factor 1/sqrt(mean(x^2) + eps) of the rows [row0, row0 + ROWS) from the producer's
 // per-16-column sums of squares (layout [row][T], T a multiple of 4). 32 threads per row each add
 // a contiguous run of q = 4 * ceil(T/128) partials in order (16-byte reads), then a fixed xor tree
@@ -251,9 +248,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
     }
 }
 
-template <Prec P, int NT, int RG, int EP, int D, int W, bool KC, bool MT>
+template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
-    using PT = PrecT<P>;
+    static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
     constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     const int wg = blockIdx.x;
@@ -285,9 +282,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
 
     // This wave's k-steps (nmy of them); the first D-1 are requested first.
-    const int nper = (p.Ks + W - 1) / W;
-    const int nmy = KC ? max(0, min(nper, p.Ks - w * nper)) : (w < p.Ks ? (p.Ks - w + W - 1) / W : 0);
-    auto step_of = [&](int q) { return min(KC ? w * nper + q : w + q * W, p.Ks - 1); };
+    const int nmy = w < p.Ks ? (p.Ks - w + W - 1) / W : 0;
+    auto step_of = [&](int q) { return min(w + q * W, p.Ks - 1); };
     Stage<P, NT, RG> ring[D];
 #pragma unroll
     for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, rg0, step_of(j), lane);
@@ -327,9 +323,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
 
     if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
 
-    // Sum of the W waves' partial tiles through LDS, one row group at a time, in a fixed tree
-    // (W = 8: ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); W = 4: (w0+w2)+(w1+w3)); then the RMSNorm row
-    // factor.
+    // Sum of the 8 waves' partial tiles through LDS, one row group at a time, in the fixed tree
+    // ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); then the RMSNorm row factor.
 #pragma unroll
     for (int r = 0; r < RG; ++r) {
 #pragma unroll
@@ -340,9 +335,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
             float x[W];
 #pragma unroll
             for (int q = 0; q < W; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
-            float sum;
-            if constexpr (W == 8) sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
-            else sum = (x[0] + x[2]) + (x[1] + x[3]);
+            float sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
             // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
             const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
             const int row = 16 * r + 4 * (l >> 4) + v;
@@ -1061,12 +1054,12 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // Launchers
 // ------------------------------------------------------------------------------------------
 // Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile p.rt0).
-template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves, bool KC = kGemmKContig>
+template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves>
 static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
     const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
-    auto kern = row_tiles > 1 ? gemm_kernel<P, NT, RG, EP, D, W, KC, true> : gemm_kernel<P, NT, RG, EP, D, W, KC, false>;
+    auto kern = row_tiles > 1 ? gemm_kernel<P, NT, RG, EP, D, W, true> : gemm_kernel<P, NT, RG, EP, D, W, false>;
     GemmParams q = p;
     q.row_tiles = row_tiles;
     q.n_wg = (p.cols + COLS - 1) / COLS;  // the last workgroup may be ragged

@@ -14,7 +14,6 @@ constexpr int kNtQkv = 3;     // QKV (each tile holds rotate-half partners; 256 
 constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups at 7B, one per CU)
 constexpr int kNtResid = 1;   // O and down projections
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
-constexpr bool kGemmKContig = false;  // k-steps per wave: interleaved (false) or contiguous
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 

@@ -214,6 +214,49 @@ def trajectory_counts(traj, tokens, n, block_policy):
             "stationary_per_window": stationary / max(windows, 1), "positions": sorted(positions)}
 
 
+def collect_trajectories(traj, tokens, n, rate, seed):
+    """Jacobi trajectory collection with data augmentation (the paper's Algorithm 1, Section
+    3.2.1), from one recorded decode with the shrink block policy (records as returned by
+    Model.jacobi_decode(trace=True)) and its output tokens.
+
+    For every block (n-token truncation, first output position b0, size nb), the trajectory
+    J = {y(0), ..., y*} holds the block's full n-token state at each iteration (the tokens
+    already fixed in the block followed by the iteration's block z) and finally the fixed point
+    y* = tokens[b0 : b0 + nb]. Augmentation corrects false tokens at random: in state number s
+    of the whole collection (counted from 0 over all blocks, fixed points included), each
+    position i whose token differs from y*[i] takes y*[i] when the SplitMix64 draw
+    mix(mix(mix(seed) ^ s) ^ i) has its top 53 bits below thr53(rate).
+
+    Returns a list of dicts per block: b0, fixed, states (list of arrays), augmented."""
+    thr = thr53(rate)
+    out = []
+    s_index = 0
+    t = 0
+    while t < len(traj):
+        b0 = traj[t]["b0"]
+        nb = traj[t]["m"] if traj[t]["e"] == b0 else None
+        recs = []
+        while t < len(traj) and traj[t]["b0"] == b0:
+            recs.append(traj[t])
+            t += 1
+        if nb is None:
+            raise ValueError("a block's first record must start at the block")
+        fixed = np.asarray(tokens[b0:b0 + nb], dtype=np.int32)
+        states = [np.concatenate([np.asarray(tokens[b0:r["e"]], dtype=np.int32), r["z"]]) for r in recs] + [fixed]
+        aug = []
+        for st in states:
+            a = st.copy()
+            for i in range(nb):
+                if a[i] != fixed[i]:
+                    h = mix(mix(mix(seed) ^ s_index) ^ i)
+                    if (h >> 11) < thr:
+                        a[i] = fixed[i]
+            aug.append(a)
+            s_index += 1
+        out.append({"b0": b0, "fixed": fixed, "states": states, "augmented": aug})
+    return out
+
+
 def mix(x):
     return int(lib().orc_mix(x))
 

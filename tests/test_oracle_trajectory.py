@@ -95,3 +95,45 @@ def test_exact_guesses_fast_forward_whole_blocks(tiny):
     out, st = tiny.jacobi_decode(prompt, 8, 40, spec, trace=True)
     c = oracle.trajectory_counts(st["trajectory"], out, 8, BLOCK_SHRINK)
     assert c["iterations"] == 5 and c["fast_forward_mean"] == 8.0 and c["stationary"] == 0 and c["windows"] == 5
+
+
+# ---- trajectory collection with augmentation (Algorithm 1) ------------------------------------
+
+def test_collection_fixture_states():
+    blocks = oracle.collect_trajectories(STATIONARY, Y, 4, 0.0, seed=1)
+    assert len(blocks) == 1 and blocks[0]["b0"] == 0
+    st = [list(x) for x in blocks[0]["states"]]
+    # each state: tokens already fixed in the block, then the iteration's block; last: y*
+    assert st == [[10, 5, 6, 7], [10, 11, 9, 13], [10, 11, 12, 13], Y]
+    assert [list(x) for x in blocks[0]["augmented"]] == st  # rate 0 corrects nothing
+
+
+def test_collection_full_rate_gives_fixed_points(tiny):
+    prompt = workload.make_prompt(TINY, 16, seed=21)
+    ar = tiny.ar_decode(prompt, 40)
+    spec = oracle.GuessSpec(GUESS_STREAM_REINJECT, BLOCK_SHRINK, ar, p=0.5, seed=2)
+    out, st = tiny.jacobi_decode(prompt, 8, 40, spec, trace=True)
+    blocks = oracle.collect_trajectories(st["trajectory"], out, 8, 1.0, seed=3)
+    assert sum(len(b["states"]) for b in blocks) == st["steps"] + st["blocks"]
+    for b in blocks:
+        np.testing.assert_array_equal(b["fixed"], out[b["b0"]:b["b0"] + b["fixed"].size])
+        np.testing.assert_array_equal(b["states"][0][0], out[b["b0"]])  # the pending token opens the block
+        for a in b["augmented"]:
+            np.testing.assert_array_equal(a, b["fixed"])
+
+
+def test_collection_partial_rate_corrects_only_false_tokens(tiny):
+    prompt = workload.make_prompt(TINY, 16, seed=22)
+    ar = tiny.ar_decode(prompt, 64)
+    spec = oracle.GuessSpec(GUESS_UNIFORM, BLOCK_SHRINK, None, seed=4)
+    out, st = tiny.jacobi_decode(prompt, 16, 64, spec, trace=True)
+    blocks = oracle.collect_trajectories(st["trajectory"], out, 16, 0.5, seed=5)
+    wrong = corrected = 0
+    for b in blocks:
+        for s, a in zip(b["states"], b["augmented"]):
+            right = s == b["fixed"]
+            np.testing.assert_array_equal(a[right], s[right])  # correct tokens untouched
+            wrong += int((~right).sum())
+            corrected += int(((~right) & (a == b["fixed"])).sum())
+            assert np.all((a == s) | (a == b["fixed"]))
+    assert wrong > 100 and abs(corrected / wrong - 0.5) < 0.1

@@ -233,6 +233,23 @@ typedef struct {
 cllm_status cllm_trace_count(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
                              int32_t n, int32_t block_policy, cllm_trace_stats *out);
 
+/* Jacobi trajectory collection with data augmentation (the paper's Algorithm 1, Section 3.2.1),
+ * from the records of one decode with the shrink block policy and its output tokens (host
+ * computation, no context). For every block (first output position b0, size nb <= n) the
+ * trajectory holds the block's full state at each iteration (the tokens already fixed in the
+ * block, then the iteration's block z) and finally the fixed point tokens[b0 .. b0+nb). State
+ * number s (counted from 0 over the whole collection) goes to states[s*n ..] and, with false
+ * tokens corrected at random, to augmented[s*n ..]: position i with a token different from the
+ * fixed point's takes the fixed point's token when the top 53 bits of the SplitMix64 draw
+ * mix(mix(mix(seed) ^ s) ^ i) are below rate * 2^53 (mix: SplitMix64's output function).
+ * Entries past nb are -1; block_start[s] = b0. At most cap states are written (caller-owned
+ * host arrays of cap*n, cap*n and cap int32); *n_states = the number the collection holds.
+ * Errors: ERR_ARG for null pointers, n outside [1, 64], rate outside [0, 1], or records that
+ * are not a shrink-policy trajectory of these tokens. */
+cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
+                                int32_t n, double rate, uint64_t seed, int32_t *states, int32_t *augmented,
+                                int32_t *block_start, int64_t cap, int64_t *n_states);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 

@@ -53,7 +53,7 @@ TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
-           "cllm_trace_count", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
+           "cllm_trace_count", "cllm_collect_states", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
            "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
@@ -85,6 +85,8 @@ def lib():
         L.cllm_trace_enable.argtypes = [_vp, _i32]
         L.cllm_trace_read.argtypes = [_vp, _i32, _vp, _i64, P(_i64)]
         L.cllm_trace_count.argtypes = [_vp, _i64, _vp, _i64, _i32, _i32, P(cllm_trace_stats)]
+        L.cllm_collect_states.argtypes = [_vp, _i64, _vp, _i64, _i32, _dbl, ctypes.c_uint64, _vp, _vp, _vp, _i64,
+                                          P(_i64)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
         L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
         L.cllm_streamed_weight_bytes.argtypes = [_vp]
@@ -309,6 +311,27 @@ def trace_count(traj, tokens, n, block_policy):
     return {"iterations": int(st.iterations), "fast_forward_mean": float(st.fast_forward_mean),
             "stationary": int(st.stationary), "windows": int(st.windows),
             "stationary_per_window": float(st.stationary_per_window)}
+
+
+def collect_states(traj, tokens, n, rate, seed):
+    """Trajectory states and their augmented copies (cllm_collect_states): arrays
+    states[S, n], augmented[S, n] (-1 past a short block) and block_start[S]."""
+    raw = dicts_to_records(traj) if isinstance(traj, list) else np.ascontiguousarray(traj, dtype=np.int32)
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    cnt = _i64(0)
+    args = (_p(raw) if raw.size else None, raw.shape[0], _p(tok) if tok.size else None, tok.size, n, float(rate),
+            int(seed) & ((1 << 64) - 1))
+    rc = lib().cllm_collect_states(*args, None, None, None, 0, ctypes.byref(cnt))
+    if rc:
+        raise CllmError(rc, "cllm_collect_states")
+    S = int(cnt.value)
+    st = np.zeros((max(S, 1), n), dtype=np.int32)
+    au = np.zeros((max(S, 1), n), dtype=np.int32)
+    bs = np.zeros(max(S, 1), dtype=np.int32)
+    rc = lib().cllm_collect_states(*args, _p(st), _p(au), _p(bs), S, ctypes.byref(cnt))
+    if rc:
+        raise CllmError(rc, "cllm_collect_states")
+    return st[:S], au[:S], bs[:S]
 
 
 def _stats(st):

@@ -1120,6 +1120,58 @@ cllm_status cllm_trace_count(const int32_t *records, int64_t n_records, const in
     return CLLM_OK;
 }
 
+namespace {
+// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014): the collection's
+// augmentation draws on the host.
+uint64_t splitmix64(uint64_t x) {
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+}  // namespace
+
+cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
+                                int32_t n, double rate, uint64_t seed, int32_t *states, int32_t *augmented,
+                                int32_t *block_start, int64_t cap, int64_t *n_states) {
+    if (!n_states || n_records < 0 || n_tokens < 0 || cap < 0 || (n_records > 0 && (!records || !tokens)) ||
+        (cap > 0 && (!states || !augmented || !block_start)) || n < 1 || n > kMaxBlock || !(rate >= 0.0 && rate <= 1.0))
+        return CLLM_ERR_ARG;
+    const uint64_t thr = (uint64_t)std::nearbyint(rate * 9007199254740992.0);  // rate * 2^53, ties to even
+    int64_t count = 0;
+    std::vector<int32_t> st((size_t)n), fx((size_t)n);
+    auto emit = [&](int32_t b0, int32_t nb) {
+        if (count < cap) {
+            int32_t *so = states + count * n, *ao = augmented + count * n;
+            for (int32_t i = 0; i < n; ++i) so[i] = ao[i] = i < nb ? st[i] : -1;
+            for (int32_t i = 0; i < nb; ++i)
+                if (ao[i] != fx[i] && (splitmix64(splitmix64(splitmix64(seed) ^ (uint64_t)count) ^ (uint64_t)i) >> 11) < thr)
+                    ao[i] = fx[i];
+            block_start[count] = b0;
+        }
+        ++count;
+    };
+    int64_t t = 0;
+    while (t < n_records) {
+        const int32_t *r0 = records + t * kTraceStride;
+        const int32_t b0 = r0[2], nb = r0[3];
+        if (r0[1] != b0 || nb < 1 || nb > n || (int64_t)b0 + nb > n_tokens) return CLLM_ERR_ARG;
+        for (int32_t i = 0; i < nb; ++i) fx[i] = tokens[b0 + i];
+        for (; t < n_records && records[t * kTraceStride + 2] == b0; ++t) {
+            const int32_t *rc = records + t * kTraceStride;
+            const int32_t e = rc[1], m = rc[3];
+            if (e < b0 || e - b0 + m != nb) return CLLM_ERR_ARG;  // the block's state is fixed tokens + z
+            for (int32_t i = 0; i < e - b0; ++i) st[i] = tokens[b0 + i];
+            for (int32_t k = 0; k < m; ++k) st[e - b0 + k] = rc[5 + k];
+            emit(b0, nb);
+        }
+        for (int32_t i = 0; i < nb; ++i) st[i] = fx[i];
+        emit(b0, nb);  // the fixed point closes the trajectory
+    }
+    *n_states = count;
+    return CLLM_OK;
+}
+
 cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_len, int32_t *pending) {
     if (!c || seq < 0 || seq >= c->max_batch || !committed_len || !pending) return CLLM_ERR_ARG;
     if (!c->slot[seq].prefilled) return CLLM_ERR_STATE;

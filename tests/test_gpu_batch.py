@@ -225,3 +225,33 @@ def test_tiny_batched_trajectories_equal_single(tiny):
                 np.testing.assert_array_equal(r["pred"], r1["pred"])
     finally:
         batched.trace_enable(False)
+
+
+def test_tiny_trajectory_collection_equals_oracle(tiny):
+    """Algorithm 1 over 10 prompts (two batches of the 8 slots): every block's states, fixed
+    point and augmented copy equal the oracle's collection from its own decode of the prompt in
+    the same slot."""
+    from paper_2403_00835_amd import collect
+    ws, batched, single = tiny
+    orc = oracle.Model(TINY, [workload.as_f32(TINY, t) for t in ws])
+    prompts = [workload.make_prompt(TINY, L, seed=37, seq=i) for i, L in enumerate([9, 20, 31, 5, 64, 12, 40, 17, 3, 50])]
+    ars = [single.ar_decode(p, 32)[0] for p in prompts]
+    specs = [dict(policy=GUESS_STREAM_REINJECT if i % 2 else GUESS_UNIFORM, block_policy=BLOCK_SHRINK,
+                  stream=ars[i] if i % 2 else None, p=0.4, seed=50 + i) for i in range(len(prompts))]
+    log("[gpu-batch] tiny: trajectory collection of 10 prompts vs oracle")
+    entries = collect.collect(batched, prompts, 8, 32, specs=specs, rate=0.5, seed=77)
+    k = 0
+    for i, p in enumerate(prompts):
+        sp = specs[i]
+        spec = oracle.GuessSpec(sp["policy"], BLOCK_SHRINK, sp["stream"], p=sp["p"], seed=sp["seed"])
+        out_o, st_o = orc.jacobi_decode(p, 8, 32, spec, seq=i % batched.max_batch, trace=True)
+        np.testing.assert_array_equal(out_o, ars[i])
+        for blk in oracle.collect_trajectories(st_o["trajectory"], out_o, 8, 0.5, 77 + i):
+            e = entries[k]
+            k += 1
+            assert e["prompt"] == i
+            np.testing.assert_array_equal(e["prefix"], np.concatenate([p, out_o[:blk["b0"]]]))
+            np.testing.assert_array_equal(e["fixed"], blk["fixed"])
+            np.testing.assert_array_equal(e["states"], np.stack(blk["states"]))
+            np.testing.assert_array_equal(e["augmented"], np.stack(blk["augmented"]))
+    assert k == len(entries)

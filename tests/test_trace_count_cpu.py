@@ -87,3 +87,45 @@ def test_synthetic_trajectories_with_stationary_tokens():
             traj.append(r)
             e += r["a"]
         _same(traj, y[:e], n, BLOCK_SHRINK)
+
+
+# ---- trajectory collection (cllm_collect_states) against the oracle --------------------------
+
+def _same_collection(traj, tokens, n, rate, seed):
+    blocks = oracle.collect_trajectories(traj, tokens, n, rate, seed)
+    st, au, bs = binding.collect_states(traj, tokens, n, rate, seed)
+    s = 0
+    for b in blocks:
+        for x, a in zip(b["states"], b["augmented"]):
+            k = x.size
+            np.testing.assert_array_equal(st[s, :k], x)
+            np.testing.assert_array_equal(au[s, :k], a)
+            assert np.all(st[s, k:] == -1) and np.all(au[s, k:] == -1) and bs[s] == b["b0"]
+            s += 1
+    assert s == st.shape[0]
+    return st, au
+
+
+def test_collection_fixture():
+    st, au = _same_collection(STATIONARY, Y, 4, 0.0, 1)
+    assert st.tolist() == [[10, 5, 6, 7], [10, 11, 9, 13], [10, 11, 12, 13], Y]
+    st, au = _same_collection(STATIONARY, Y, 4, 1.0, 1)
+    assert au.tolist() == [Y] * 4
+
+
+@pytest.mark.parametrize("policy,p", [(GUESS_UNIFORM, 0.0), (GUESS_STREAM, 0.3), (GUESS_STREAM_REINJECT, 0.5)])
+@pytest.mark.parametrize("rate", [0.0, 0.3, 0.5, 1.0])
+def test_collection_of_recorded_trajectories(tiny, policy, p, rate):
+    prompt = workload.make_prompt(TINY, 16, seed=7)
+    ar = tiny.ar_decode(prompt, 50)
+    for n in (5, 8, 16):
+        spec = oracle.GuessSpec(policy, BLOCK_SHRINK, None if policy == GUESS_UNIFORM else ar, p=p, seed=n)
+        out, st = tiny.jacobi_decode(prompt, n, 50, spec, trace=True)
+        _same_collection(st["trajectory"], out, n, rate, seed=1000 + n)
+
+
+def test_collection_rejects_non_trajectories():
+    with pytest.raises(binding.CllmError):
+        binding.collect_states(STATIONARY[1:], Y, 4, 0.5, 1)  # does not start at a block start
+    with pytest.raises(binding.CllmError):
+        binding.collect_states(STATIONARY, Y, 4, 1.5, 1)  # rate outside [0, 1]

@@ -214,7 +214,9 @@ def main():
                          "p10": round(float(np.median([x["iter_ms_p10"] for x in stats])), 4),
                          "p50": round(float(np.median([x["iter_ms_p50"] for x in stats])), 4),
                          "p90": round(float(np.median([x["iter_ms_p90"] for x in stats])), 4),
-                         "full_block_p50": round(float(np.median([x["iter_ms_full_p50"] for x in stats])), 4)},
+                         "full_block_p10": round(float(np.median([x["iter_ms_full_p10"] for x in stats])), 4),
+                         "full_block_p50": round(float(np.median([x["iter_ms_full_p50"] for x in stats])), 4),
+                         "full_block_p90": round(float(np.median([x["iter_ms_full_p90"] for x in stats])), 4)},
         "decode_tokens_per_s": round(tokens / (decode_ms / 1e3), 3),
         "iterations_per_step": iters / args.steps,
         "mean_accepted": round(mean_accept, 3),

@@ -106,8 +106,9 @@ typedef struct cllm_decode_stats {
     /* Device time per iteration (between consecutive iteration boundaries on the stream):
      * percentiles over the decode's iterations, and the median over the iterations that ran a
      * full block of n rows (the first iteration of each block). For a batched decode: over the
-     * batched iterations, and iter_ms_full_p50 = iter_ms_p50. */
+     * batched iterations, and the full-block figures equal the overall ones. */
     double iter_ms_p10, iter_ms_p50, iter_ms_p90, iter_ms_full_p50;
+    double iter_ms_full_p10, iter_ms_full_p90; /* p10, p90 over the full-block iterations */
 } cllm_decode_stats;
 
 typedef struct cllm_ctx cllm_ctx;

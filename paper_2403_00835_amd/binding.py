@@ -40,7 +40,8 @@ class cllm_guess_spec(ctypes.Structure):
 class cllm_decode_stats(ctypes.Structure):
     _fields_ = [("steps", _i64), ("blocks", _i64), ("tokens", _i64), ("accept_hist", _i64 * 65),
                 ("prefill_ms", _dbl), ("decode_ms", _dbl), ("rows", _i64), ("iter_ms_p10", _dbl),
-                ("iter_ms_p50", _dbl), ("iter_ms_p90", _dbl), ("iter_ms_full_p50", _dbl)]
+                ("iter_ms_p50", _dbl), ("iter_ms_p90", _dbl), ("iter_ms_full_p50", _dbl), ("iter_ms_full_p10", _dbl),
+                ("iter_ms_full_p90", _dbl)]
 
 
 class cllm_trace_stats(ctypes.Structure):
@@ -339,7 +340,8 @@ def _stats(st):
             "accept_hist": [int(x) for x in st.accept_hist], "prefill_ms": float(st.prefill_ms),
             "decode_ms": float(st.decode_ms), "rows": int(st.rows), "iter_ms_p10": float(st.iter_ms_p10),
             "iter_ms_p50": float(st.iter_ms_p50), "iter_ms_p90": float(st.iter_ms_p90),
-            "iter_ms_full_p50": float(st.iter_ms_full_p50)}
+            "iter_ms_full_p50": float(st.iter_ms_full_p50), "iter_ms_full_p10": float(st.iter_ms_full_p10),
+            "iter_ms_full_p90": float(st.iter_ms_full_p90)}
 
 
 def write_weight_file(path, cfg: ModelConfig, tensors):

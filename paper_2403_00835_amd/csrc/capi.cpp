@@ -635,6 +635,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     };
     const double p10 = pct(it_ms, 0.1), p50 = pct(it_ms, 0.5), p90 = pct(it_ms, 0.9);
     const double full50 = B == 1 ? pct(full_ms, 0.5) : p50;
+    const double full10 = B == 1 ? pct(full_ms, 0.1) : p10, full90 = B == 1 ? pct(full_ms, 0.9) : p90;
     for (int b = 0; b < B; ++b) {
         const int q = seq_ids[b];
         HIPCHK(c, hipMemcpy(out_tokens + (size_t)b * max_new, c->out_dev + (size_t)q * c->opts.max_new,
@@ -654,6 +655,8 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             st.iter_ms_p50 = p50;
             st.iter_ms_p90 = p90;
             st.iter_ms_full_p50 = full50;
+            st.iter_ms_full_p10 = full10;
+            st.iter_ms_full_p90 = full90;
         }
         c->slot[q].prefilled = true;
         c->slot[q].L = ct.L;

@@ -117,6 +117,10 @@ def test_tiny_decode_equals_oracle(tiny):
         np.testing.assert_array_equal(out, ar_o)
     assert st["tokens"] == 32 and st["steps"] <= 32
     assert sum(a * c for a, c in enumerate(st["accept_hist"])) == 32
+    # per-iteration device times: ordered percentiles, full blocks (m = n) among them
+    assert 0 < st["iter_ms_p10"] <= st["iter_ms_p50"] <= st["iter_ms_p90"]
+    assert 0 < st["iter_ms_full_p10"] <= st["iter_ms_full_p50"] <= st["iter_ms_full_p90"]
+    assert st["decode_ms"] > 0 and st["prefill_ms"] > 0
 
 
 @pytest.mark.parametrize("policy,block_policy", [(GUESS_UNIFORM, BLOCK_SHRINK), (GUESS_STREAM, BLOCK_SHRINK),

@@ -257,6 +257,43 @@ def collect_trajectories(traj, tokens, n, rate, seed):
     return out
 
 
+def loss_head(W, teacher, student, ar_rows, ar_targets, omega):
+    """The CLLM training loss of Section 3.2.2 at the LM head, and its gradients (fp64).
+
+    W [V, d]: LM-head weights. teacher [P, d]: LM-head input rows of the fixed point y* (the
+    stop-gradient model q_theta-: no gradient flows through them), student [P, d]: rows of the
+    trajectory state y at the same positions, ar_rows [A, d] with targets ar_targets [A]: rows of
+    the target model's generation. Per pair i the global-consistency term is the forward KL
+    D(p || q) = sum_v p_v (log p_v - log q_v) with p = softmax(W teacher_i), q = softmax(W
+    student_i) (eq. global_loss); per AR row the term is -log softmax(W ar_i)[target_i] (eq.
+    ar_loss). L = sum_i KL_i + omega * sum_j NLL_j (sums; the expectation's normalisation is the
+    caller's).
+
+    Returns dict: kl [P], nll [A], loss, d_student [P, d], d_ar [A, d], d_W [V, d] (gradient of L
+    through the student and AR rows only)."""
+    W = np.asarray(W, dtype=np.float64)
+    T = np.asarray(teacher, dtype=np.float64).reshape(-1, W.shape[1])
+    S = np.asarray(student, dtype=np.float64).reshape(-1, W.shape[1])
+    Ar = np.asarray(ar_rows, dtype=np.float64).reshape(-1, W.shape[1])
+    tg = np.asarray(ar_targets, dtype=np.int64)
+
+    def log_softmax(z):
+        m = z.max(axis=1, keepdims=True)
+        return z - (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))
+
+    la, lb, lc = log_softmax(T @ W.T), log_softmax(S @ W.T), log_softmax(Ar @ W.T)
+    pa, pb, pc = np.exp(la), np.exp(lb), np.exp(lc)
+    kl = (pa * (la - lb)).sum(axis=1)
+    nll = -lc[np.arange(tg.size), tg]
+    loss = kl.sum() + omega * nll.sum()
+    db = pb - pa                       # dKL/d(student logits)
+    dc = pc.copy()
+    dc[np.arange(tg.size), tg] -= 1.0
+    dc *= omega                        # d(omega NLL)/d(AR logits)
+    return {"kl": kl, "nll": nll, "loss": float(loss), "d_student": db @ W, "d_ar": dc @ W,
+            "d_W": db.T @ S + dc.T @ Ar}
+
+
 def mix(x):
     return int(lib().orc_mix(x))
 

@@ -1,0 +1,82 @@
+"""Pins of the oracle's CLLM loss head (global consistency forward KL + omega x AR loss at the LM
+head, Section 3.2.2, eqs. global_loss and ar_loss) and of its gradients."""
+import numpy as np
+import pytest
+
+import oracle
+
+
+def _case(seed, V=11, d=6, P=3, A=2):
+    r = np.random.default_rng(seed)
+    return (r.normal(0, 0.7, (V, d)), r.normal(0, 1, (P, d)), r.normal(0, 1, (P, d)), r.normal(0, 1, (A, d)),
+            r.integers(0, V, A))
+
+
+def test_identical_rows_have_zero_kl_and_gradient():
+    W, T, S, Ar, tg = _case(0)
+    out = oracle.loss_head(W, T, T, Ar, tg, 0.0)
+    np.testing.assert_allclose(out["kl"], 0.0, atol=1e-14)
+    np.testing.assert_allclose(out["d_student"], 0.0, atol=1e-14)
+    np.testing.assert_allclose(out["d_W"], 0.0, atol=1e-14)
+
+
+def test_zero_weights_uniform_logits():
+    # all logits 0: NLL = log V, the AR logit gradient is omega (1/V - onehot)
+    V, d = 9, 4
+    W = np.zeros((V, d))
+    Ar = np.ones((2, d))
+    out = oracle.loss_head(W, np.ones((1, d)), np.ones((1, d)), Ar, [3, 5], 2.0)
+    np.testing.assert_allclose(out["nll"], np.log(V))
+    assert out["loss"] == pytest.approx(2.0 * 2 * np.log(V))
+    g = np.full((2, V), 1.0 / V)
+    g[0, 3] -= 1.0
+    g[1, 5] -= 1.0
+    np.testing.assert_allclose(out["d_W"], 2.0 * g.T @ Ar)
+
+
+def test_two_point_kl_closed_form():
+    # V = 2 with logits (x, 0) and (y, 0): KL of two Bernoulli distributions
+    W = np.array([[1.0], [0.0]])
+    x, y = 0.8, -0.3
+    out = oracle.loss_head(W, [[x]], [[y]], np.zeros((0, 1)), np.zeros(0, dtype=int), 1.0)
+    p, q = 1 / (1 + np.exp(-x)), 1 / (1 + np.exp(-y))
+    want = p * np.log(p / q) + (1 - p) * np.log((1 - p) / (1 - q))
+    assert out["kl"][0] == pytest.approx(want, rel=1e-12)
+    # dKL/dy = q - p along the logit, times W[0] = 1
+    assert out["d_student"][0, 0] == pytest.approx(q - p, rel=1e-12)
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_gradients_match_finite_differences(seed):
+    W, T, S, Ar, tg = _case(seed)
+    om = 0.7
+    out = oracle.loss_head(W, T, S, Ar, tg, om)
+    h = 1e-6
+
+    def L(W_=W, S_=S, Ar_=Ar):
+        return oracle.loss_head(W_, T, S_, Ar_, tg, om)["loss"]
+
+    for (i, j) in [(0, 0), (2, 5), (1, 3)]:
+        Sp, Sm = S.copy(), S.copy()
+        Sp[i, j] += h
+        Sm[i, j] -= h
+        assert (L(S_=Sp) - L(S_=Sm)) / (2 * h) == pytest.approx(out["d_student"][i, j], rel=1e-6, abs=1e-9)
+    for (i, j) in [(0, 1), (1, 4)]:
+        Ap, Am = Ar.copy(), Ar.copy()
+        Ap[i, j] += h
+        Am[i, j] -= h
+        assert (L(Ar_=Ap) - L(Ar_=Am)) / (2 * h) == pytest.approx(out["d_ar"][i, j], rel=1e-6, abs=1e-9)
+    for (v, j) in [(0, 0), (7, 2), (10, 5)]:
+        # the teacher rows are stop-gradient: perturbing W moves only the student and AR terms
+        Wp, Wm = W.copy(), W.copy()
+        Wp[v, j] += h
+        Wm[v, j] -= h
+        Tfix = T @ W.T  # teacher logits held fixed
+        def Lw(Wx):
+            o = oracle.loss_head(Wx, np.zeros_like(T), S, Ar, tg, om)
+            # recompute the KL with the fixed teacher distribution
+            lb = S @ Wx.T
+            lb = lb - np.log(np.exp(lb - lb.max(1, keepdims=True)).sum(1, keepdims=True)) - lb.max(1, keepdims=True)
+            la = Tfix - np.log(np.exp(Tfix - Tfix.max(1, keepdims=True)).sum(1, keepdims=True)) - Tfix.max(1, keepdims=True)
+            return (np.exp(la) * (la - lb)).sum() + om * o["nll"].sum()
+        assert (Lw(Wp) - Lw(Wm)) / (2 * h) == pytest.approx(out["d_W"][v, j], rel=1e-6, abs=1e-9)

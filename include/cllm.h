@@ -251,6 +251,25 @@ cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const
                                 int32_t n, double rate, uint64_t seed, int32_t *states, int32_t *augmented,
                                 int32_t *block_start, int64_t cap, int64_t *n_states);
 
+/* CLLM training loss at the LM head (Section 3.2.2: global consistency loss with the forward
+ * KL, eq. global_loss, plus omega times the AR loss, eq. ar_loss), forward then backward, on the
+ * context's LM-head weights W [V][d]. Inputs are LM-head input rows (after the final RMSNorm),
+ * fp32 host arrays: teacher[n_pairs][d] (conditioned on the fixed point y*; the stop-gradient
+ * model, so no gradient flows through them), student[n_pairs][d] (conditioned on a trajectory
+ * state y at the same positions), ar_rows[n_ar][d] with ar_targets[n_ar] in [0, V) (the target
+ * model's generation). Per pair KL(softmax(W teacher) || softmax(W student)) -> row_kl[n_pairs];
+ * per AR row -log softmax(W ar)[target] -> row_nll[n_ar]; *loss = sum row_kl + omega * sum
+ * row_nll (sums; the expectation's normalisation is the caller's). Gradients of *loss:
+ * d_student[n_pairs][d], d_ar[n_ar][d] and, when d_weight is not NULL, d_weight[V][d] (fp32,
+ * through the student and AR rows). Logits and reductions in fp32 (the products as in the
+ * decode: bf16 weights, activations in hi + lo bf16 planes), every sum in a fixed order.
+ * Synchronous; the context keeps a workspace (grown on demand) until it is freed. Errors:
+ * ERR_ARG (n_pairs + n_ar outside [1, 64], null arrays, target out of range), ERR_STATE (no
+ * weights), ERR_OOM, ERR_DEVICE. */
+cllm_status cllm_loss_head(cllm_ctx *ctx, const float *teacher, const float *student, int32_t n_pairs,
+                           const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega, float *row_kl,
+                           float *row_nll, float *d_student, float *d_ar, float *d_weight, double *loss);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 
@@ -262,8 +281,9 @@ cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_
  * every >= 1 samples: one of every `every` eligible launches is timed (each bracket costs a
  * few microseconds of queue time; a stride coprime with the layer count rotates the sample over
  * the layers). cllm_timing_read returns the number of timed launches and their total device
- * time since the last enable, and clears them. kernel_class < 0 disables. Errors: ERR_ARG for
- * an unknown class, max_rows outside [0, 64] or every < 1. */
+ * time since the last enable, and clears them. kernel_class < 0 disables. The loss head's
+ * launches (classes CLLM_KT_LOSS_*) are timed whatever max_rows. Errors: ERR_ARG for an unknown
+ * class, max_rows outside [0, 64] or every < 1. */
 #define CLLM_KT_GEMM_QKV 0
 #define CLLM_KT_ATTN 1
 #define CLLM_KT_GEMM_O 2
@@ -273,6 +293,10 @@ cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_
 #define CLLM_KT_SCAN 6
 #define CLLM_KT_ATTN_COMBINE 7
 #define CLLM_KT_EMBED 8
+#define CLLM_KT_LOSS_LOGITS 9   /* loss head: logits GEMM */
+#define CLLM_KT_LOSS_ROWS 10    /* loss head: per-row losses and logit gradients */
+#define CLLM_KT_LOSS_DH 11      /* loss head: gradient of the input rows */
+#define CLLM_KT_LOSS_DW 12      /* loss head: gradient of the LM-head weight */
 cllm_status cllm_timing_enable(cllm_ctx *ctx, int32_t kernel_class, int32_t max_rows, int32_t every);
 cllm_status cllm_timing_read(cllm_ctx *ctx, int64_t *launches, double *total_ms);
 

@@ -16,7 +16,7 @@ CLLM_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_ARG", 2: "ERR_STATE", 3: "ERR_CAPACITY", 4: "ERR_OOM", 5: "ERR_IO",
                 6: "ERR_FORMAT", 7: "ERR_DEVICE", 8: "ERR_NUMERIC"}
 KT = {"qkv": 0, "attn": 1, "o": 2, "gate_up": 3, "down": 4, "lm_head": 5, "scan": 6, "attn_combine": 7,
-      "embed": 8}
+      "embed": 8, "loss_logits": 9, "loss_rows": 10, "loss_dh": 11, "loss_dw": 12}
 
 _i32, _i64, _u64, _f32, _dbl, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float,
                                      ctypes.c_double, ctypes.c_void_p)
@@ -54,7 +54,7 @@ TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
-           "cllm_trace_count", "cllm_collect_states", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
+           "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
            "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
@@ -86,6 +86,7 @@ def lib():
         L.cllm_trace_enable.argtypes = [_vp, _i32]
         L.cllm_trace_read.argtypes = [_vp, _i32, _vp, _i64, P(_i64)]
         L.cllm_trace_count.argtypes = [_vp, _i64, _vp, _i64, _i32, _i32, P(cllm_trace_stats)]
+        L.cllm_loss_head.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _vp, _vp, _vp, P(_dbl)]
         L.cllm_collect_states.argtypes = [_vp, _i64, _vp, _i64, _i32, _dbl, ctypes.c_uint64, _vp, _vp, _vp, _i64,
                                           P(_i64)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
@@ -260,6 +261,28 @@ class Model:
         L, pend = _i32(0), _i32(0)
         self._check(self.L.cllm_seq_state(self.h, seq, ctypes.byref(L), ctypes.byref(pend)))
         return int(L.value), int(pend.value)
+
+    def loss_head(self, teacher, student, ar_rows, ar_targets, omega, want_dw=False):
+        """CLLM loss at the LM head and its gradients (cllm_loss_head): dict kl, nll, loss,
+        d_student, d_ar and, with want_dw, d_W."""
+        d, V = self.cfg.d_model, self.cfg.vocab
+        T = np.ascontiguousarray(teacher, dtype=np.float32).reshape(-1, d)
+        S = np.ascontiguousarray(student, dtype=np.float32).reshape(-1, d)
+        Ar = np.ascontiguousarray(ar_rows, dtype=np.float32).reshape(-1, d)
+        tg = np.ascontiguousarray(ar_targets, dtype=np.int32)
+        P, A = T.shape[0], Ar.shape[0]
+        kl, nll = np.zeros(max(P, 1), np.float32), np.zeros(max(A, 1), np.float32)
+        ds, da = np.zeros((max(P, 1), d), np.float32), np.zeros((max(A, 1), d), np.float32)
+        dw = np.zeros((V, d), np.float32) if want_dw else None
+        loss = _dbl(0.0)
+        self._check(self.L.cllm_loss_head(self.h, _p(T) if P else None, _p(S) if P else None, P,
+                                          _p(Ar) if A else None, _p(tg) if A else None, A, float(omega),
+                                          _p(kl), _p(nll), _p(ds), _p(da), None if dw is None else _p(dw),
+                                          ctypes.byref(loss)))
+        out = {"kl": kl[:P], "nll": nll[:A], "loss": float(loss.value), "d_student": ds[:P], "d_ar": da[:A]}
+        if want_dw:
+            out["d_W"] = dw
+        return out
 
     def trace_enable(self, enable=True):
         self._check(self.L.cllm_trace_enable(self.h, 1 if enable else 0))

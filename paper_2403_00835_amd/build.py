@@ -15,7 +15,7 @@ ARCH = "gfx950"
 # Packed-fp32 VALU instructions are kept out of generated code (build flags).
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I" + INCLUDE]
-SOURCES = ["kernels.hip", "capi.cpp"]
+SOURCES = ["kernels.hip", "loss.hip", "capi.cpp"]
 
 
 def _run(cmd, verbose):

@@ -68,6 +68,15 @@ struct cllm_ctx {
     };
     int32_t *trace_dev = nullptr;  // trajectory records: max_batch x max_new x kTraceStride int32
     bool trace_on = false;
+    // loss head workspace (allocated on first use, grown on demand)
+    struct LossWs {
+        size_t h = 0, a = 0, z = 0, dd = 0, part = 0, dh = 0, dw = 0, rows = 0;
+        float *H = nullptr, *Z = nullptr, *D = nullptr, *part_p = nullptr, *dH = nullptr, *dW = nullptr,
+              *out = nullptr;
+        uint8_t *A = nullptr;  // GEMM operand planes of the input rows (bytes)
+        int32_t *tg = nullptr;
+        RowTab *tab = nullptr;
+    } loss;
     std::vector<Slot> slot;
     bool dead = false;
     std::string err;
@@ -140,7 +149,7 @@ cllm_status dalloc_t(cllm_ctx *c, T **p, size_t count) {
 // Timing events for the selected kernel class and row-group count (null when not timed).
 void timing_events(cllm_ctx *c, int cls, int rg, hipEvent_t *e0, hipEvent_t *e1) {
     *e0 = *e1 = nullptr;
-    if (c->kt_class != cls || c->in_prefill || (c->kt_rg > 0 && c->kt_rg != rg)) return;
+    if (c->kt_class != cls || c->in_prefill || (c->kt_rg > 0 && c->kt_rg != rg && cls < CLLM_KT_LOSS_LOGITS)) return;
     if (c->kt_eligible++ % c->kt_every != 0) return;
     while (c->ev_pool.size() < c->ev_used + 2) {
         hipEvent_t e;
@@ -671,6 +680,23 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
 // ------------------------------------------------------------------------------------------
 // C ABI
 // ------------------------------------------------------------------------------------------
+namespace {
+// Grow a loss-head workspace buffer (contents are not kept).
+template <class T>
+cllm_status loss_buf(cllm_ctx *c, T **p, size_t *have, size_t need) {
+    if (*have >= need && *p) return CLLM_OK;
+    if (*p) {
+        (void)hipFree(*p);
+        c->allocs.erase(std::find(c->allocs.begin(), c->allocs.end(), (void *)*p));
+        *p = nullptr;
+    }
+    *have = 0;
+    cllm_status s = dalloc_t(c, p, need);
+    if (s == CLLM_OK) *have = need;
+    return s;
+}
+}  // namespace
+
 extern "C" {
 
 const char *cllm_status_string(cllm_status s) {
@@ -1175,6 +1201,89 @@ cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const
     return CLLM_OK;
 }
 
+cllm_status cllm_loss_head(cllm_ctx *c, const float *teacher, const float *student, int32_t n_pairs,
+                           const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega, float *row_kl,
+                           float *row_nll, float *d_student, float *d_ar, float *d_weight, double *loss) {
+    if (!c || !loss || n_pairs < 0 || n_ar < 0 || n_pairs + n_ar < 1 || n_pairs + n_ar > 64 ||
+        (n_pairs > 0 && (!teacher || !student || !row_kl || !d_student)) ||
+        (n_ar > 0 && (!ar_rows || !ar_targets || !row_nll || !d_ar)) || !(omega == omega))
+        return c ? fail(c, CLLM_ERR_ARG, "loss head: bad arguments (pairs + AR rows in [1, 64])") : CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c))) return s;
+    if (!c->w_lm) return fail(c, CLLM_ERR_STATE, "loss head: weights not set");
+    for (int i = 0; i < n_ar; ++i)
+        if (ar_targets[i] < 0 || ar_targets[i] >= c->V) return fail(c, CLLM_ERR_ARG, "loss head: target out of range");
+    const int P = n_pairs, A = n_ar, R = 2 * P + A, Rg = P + A, d = c->d, V = c->V;
+    const int Vp = c->n_wg_lm * 16 * kLmTiles;
+    const int cap = round_up(R, kMaxRows);
+    const int nch = ceil_div(Vp, kLossChunk);
+    auto &w = c->loss;
+    if ((s = loss_buf(c, &w.H, &w.h, (size_t)R * d)) || (s = loss_buf(c, &w.A, &w.a, (size_t)cap * d * 4)) ||
+        (s = loss_buf(c, &w.Z, &w.z, (size_t)R * Vp)) || (s = loss_buf(c, &w.D, &w.dd, (size_t)Rg * Vp)) ||
+        (s = loss_buf(c, &w.part_p, &w.part, (size_t)nch * Rg * d)) || (s = loss_buf(c, &w.dH, &w.dh, (size_t)Rg * d)) ||
+        (s = loss_buf(c, &w.out, &w.rows, (size_t)Rg)) || (d_weight && (s = loss_buf(c, &w.dW, &w.dw, (size_t)V * d))))
+        return s;
+    if (!w.tab && (s = dalloc_t(c, &w.tab, 1))) return s;
+    if (!w.tg && (s = dalloc_t(c, &w.tg, (size_t)64))) return s;
+    hipStream_t st = c->stream;
+    const size_t row_b = (size_t)d * sizeof(float);
+    if (P) {
+        HIPCHK(c, hipMemcpyAsync(w.H, teacher, P * row_b, hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipMemcpyAsync(w.H + (size_t)P * d, student, P * row_b, hipMemcpyHostToDevice, st));
+    }
+    if (A) {
+        HIPCHK(c, hipMemcpyAsync(w.H + (size_t)2 * P * d, ar_rows, A * row_b, hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipMemcpyAsync(w.tg, ar_targets, A * sizeof(int32_t), hipMemcpyHostToDevice, st));
+    }
+    RowTab th{};
+    th.R = R;
+    th.nseq = 1;
+    HIPCHK(c, hipMemcpyAsync(w.tab, &th, sizeof(th), hipMemcpyHostToDevice, st));
+    HIPCHK(c, launch_pack_rows(c->bf16, w.H, R, d, cap, w.A, st));
+    // logits Z = H W^T over the packed LM head (no RMSNorm row factor: the rows are the head's input)
+    GemmParams g{};
+    g.W = c->w_lm;
+    g.Ks = c->ks_d;
+    g.cols = Vp;
+    g.A = w.A;
+    g.lda = d;
+    g.rr = RowsRef{w.tab, nullptr, cap};
+    g.V = V;
+    g.Zout = w.Z;
+    g.ldz = Vp;
+    const int row_tiles = ceil_div(R, kMaxRows);
+    const int rg = row_tiles > 1 ? 4 : rows_to_rg(R);
+    hipEvent_t e0, e1;
+    timing_events(c, CLLM_KT_LOSS_LOGITS, rg, &e0, &e1);
+    HIPCHK(c, launch_gemm(GEMM_LOGITS, c->bf16, rg, row_tiles, g, st, e0, e1));
+    LossParams lp{w.Z, w.tg, P, A, V, Vp, omega, w.out, w.out + P, w.D};
+    timing_events(c, CLLM_KT_LOSS_ROWS, rg, &e0, &e1);
+    HIPCHK(c, launch_loss_rows(lp, st, e0, e1));
+    timing_events(c, CLLM_KT_LOSS_DH, rg, &e0, &e1);
+    HIPCHK(c, launch_loss_dh(c->bf16, w.D, Rg, Vp, c->w_lm, Vp, d, w.part_p, w.dH, st, e0, e1));
+    if (d_weight) {
+        timing_events(c, CLLM_KT_LOSS_DW, rg, &e0, &e1);
+        HIPCHK(c, launch_loss_dw(w.D, Rg, Vp, w.H + (size_t)P * d, d, V, w.dW, st, e0, e1));
+    }
+    std::vector<float> rl((size_t)Rg);
+    HIPCHK(c, hipMemcpyAsync(rl.data(), w.out, Rg * sizeof(float), hipMemcpyDeviceToHost, st));
+    if (P) HIPCHK(c, hipMemcpyAsync(d_student, w.dH, P * row_b, hipMemcpyDeviceToHost, st));
+    if (A) HIPCHK(c, hipMemcpyAsync(d_ar, w.dH + (size_t)P * d, A * row_b, hipMemcpyDeviceToHost, st));
+    if (d_weight) HIPCHK(c, hipMemcpyAsync(d_weight, w.dW, (size_t)V * row_b, hipMemcpyDeviceToHost, st));
+    HIPCHK(c, hipStreamSynchronize(st));
+    double kl_sum = 0.0, nll_sum = 0.0;
+    for (int i = 0; i < P; ++i) {
+        row_kl[i] = rl[i];
+        kl_sum += rl[i];
+    }
+    for (int i = 0; i < A; ++i) {
+        row_nll[i] = rl[P + i];
+        nll_sum += rl[P + i];
+    }
+    *loss = kl_sum + (double)omega * nll_sum;
+    return CLLM_OK;
+}
+
 cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_len, int32_t *pending) {
     if (!c || seq < 0 || seq >= c->max_batch || !committed_len || !pending) return CLLM_ERR_ARG;
     if (!c->slot[seq].prefilled) return CLLM_ERR_STATE;
@@ -1185,7 +1294,7 @@ cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_le
 
 cllm_status cllm_timing_enable(cllm_ctx *c, int32_t kernel_class, int32_t max_rows, int32_t every) {
     if (!c) return CLLM_ERR_ARG;
-    if (kernel_class > CLLM_KT_EMBED || max_rows < 0 || max_rows > kMaxRows || every < 1)
+    if (kernel_class > CLLM_KT_LOSS_DW || max_rows < 0 || max_rows > kMaxRows || every < 1)
         return fail(c, CLLM_ERR_ARG, "unknown kernel class, bad max_rows or bad sampling stride");
     c->kt_class = kernel_class < 0 ? -1 : kernel_class;
     c->kt_rg = max_rows == 0 ? 0 : rows_to_rg(max_rows);

@@ -106,9 +106,6 @@ __device__ __forceinline__ void put_act(typename PrecT<P>::T *base, size_t plane
     }
 }
 
-// One k-step of C += A * B on 16x16 tiles. a holds this lane's 16 bytes of the activation row
-// (row = lane % 16), b this lane's 16 bytes of the weight row (column = lane % 16); both hold
-// the same K indices, so the K-slot assignment inside the instruction does not matter.
 // Makes wave-uniform values available at this point. Kernel prologues list here every
 // parameter (and row-table field) their first loads need, so those are requested in one round
 // trip; left to itself the compiler requests each one next to its first use, behind the
@@ -118,6 +115,9 @@ __device__ __forceinline__ void request_together(const Ts &...v) {
     (..., [](const auto &x) { asm volatile("" ::"s"(x)); }(v));
 }
 
+// One k-step of C += A * B on 16x16 tiles. a holds this lane's 16 bytes of the activation row
+// (row = lane % 16), b this lane's 16 bytes of the weight row (column = lane % 16); both hold
+// the same K indices, so the K-slot assignment inside the instruction does not matter.
 template <Prec P> __device__ __forceinline__ f32x4 mfma_kstep(u32x4 a, u32x4 b, f32x4 c);
 template <> __device__ __forceinline__ f32x4 mfma_kstep<Prec::BF16>(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,

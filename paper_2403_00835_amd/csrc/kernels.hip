@@ -46,7 +46,7 @@ namespace cllm {
 // sums of squares.
 // ------------------------------------------------------------------------------------------
 
-enum Epi { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_ARGMAX = 3 };
+enum Epi { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_ARGMAX = 3, E_LOGITS = 4 };
 
 template <Prec P, int NT, int RG>
 struct Stage {  // operands of one k-step
@@ -217,6 +217,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
             put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.rr.cap, p.Fp),
                        act_idx<P>(row0 + row, wg * (COLS / 2) + f, p.Fp), silu(gt) * up);
         }
+    } else if constexpr (EP == E_LOGITS) {
+        // Plain fp32 output rows (the loss head's logits): Zout[row][col], col < V.
+        const int c0 = t0 * 16;
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
+            const int row = idx / COLS, c = idx % COLS;
+            if (row < m && c0 + c < p.V) p.Zout[(size_t)(row0 + row) * p.ldz + c0 + c] = s_tile[row * (COLS + 1) + c];
+        }
     } else {  // E_ARGMAX
         // One wave per row: (max, lowest column) over this workgroup's columns < V.
         for (int row = w; row < ROWS; row += W) {
@@ -251,7 +258,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
-    constexpr bool ROWSCALE = EP != E_RESID;  // the product follows an RMSNorm
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     const int wg = blockIdx.x;
     // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
@@ -1090,6 +1097,8 @@ static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_til
             return launch_gemm_t<P, 6, RG, E_SWIGLU, 2>(p, row_tiles, s, e0, e1);
         case GEMM_LM:
             return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_LOGITS:
+            return launch_gemm_t<P, kLmTiles, RG, E_LOGITS, 3>(p, row_tiles, s, e0, e1);
         }
         return hipErrorInvalidValue;
     }
@@ -1103,6 +1112,8 @@ static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_til
         return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, row_tiles, s, e0, e1);
     case GEMM_LM:
         return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX>(p, row_tiles, s, e0, e1);
+    case GEMM_LOGITS:
+        return launch_gemm_t<P, kLmTiles, RG, E_LOGITS>(p, row_tiles, s, e0, e1);
     }
     return hipErrorInvalidValue;
 }

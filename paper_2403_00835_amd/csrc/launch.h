@@ -15,7 +15,7 @@ constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups 
 constexpr int kNtResid = 1;   // O and down projections
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
 
-enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
+enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4, GEMM_LOGITS = 5 };
 
 // Rows of an iteration: the row table, its per-row entries and the row capacity of the
 // activation buffers (their plane size).
@@ -59,6 +59,9 @@ struct GemmParams {
     int *pidx;
     float *dbg;
     int V;
+    // E_LOGITS (the loss head's LM head, no RMSNorm row factor): fp32 logits [row][ldz]
+    float *Zout;
+    int ldz;
 };
 
 struct EmbedParams {
@@ -137,6 +140,28 @@ hipError_t launch_attn_fused(bool bf16, int nrg, int nseq_launch, const AttnPara
 hipError_t launch_scan(int nseq_launch, const ScanParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_decode_init(int nseq, const ScanParams &p, hipStream_t s);
 hipError_t launch_plan(const PlanParams &p, hipStream_t s);
+// CLLM loss head (global consistency KL + omega AR loss at the LM head) and its gradients.
+struct LossParams {
+    const float *Z;    // logits [R][ldz]: teacher rows 0..P-1, student rows P..2P-1, AR rows 2P..
+    const int32_t *targets;  // AR targets [A]
+    int P, A, V, ldz;
+    float omega;
+    float *kl, *nll;   // per pair / per AR row
+    float *D;          // logit gradients [P + A][ldz] (student rows, then AR rows; 0 past V)
+};
+hipError_t launch_loss_rows(const LossParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// Rows (fp32 [rows][d]) to the two bf16 planes (or one fp32 plane) of a GEMM operand of row
+// capacity cap.
+hipError_t launch_pack_rows(bool bf16, const float *X, int rows, int d, int cap, void *A, hipStream_t s);
+// dH = D W over the packed LM-head weights W (tiles of Vp/16 rows x d/32 k-steps): per chunk of
+// kLossChunk vocabulary rows a partial [nch][rows][d], then their sum in chunk order.
+constexpr int kLossChunk = 1024;
+hipError_t launch_loss_dh(bool bf16, const float *D, int rows, int ldd, const uint8_t *W, int Vp, int d, float *part,
+                          float *dH, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// dW[v][k] = sum_r D[r][v] H[r][k] for v < V (rows <= 64).
+hipError_t launch_loss_dw(const float *D, int rows, int ldd, const float *H, int d, int V, float *dW, hipStream_t s,
+                          hipEvent_t e0, hipEvent_t e1);
+
 hipError_t launch_repack(bool bf16, const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst,
                          hipStream_t s);
 

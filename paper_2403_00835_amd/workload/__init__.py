@@ -134,6 +134,30 @@ def make_uniform_f64(n, seed, stream):
     return out
 
 
+def make_normal_f32(shape, std, seed, stream):
+    """float32 array of the given shape with N(0, std^2) entries from stream `stream`."""
+    out = np.empty(shape, dtype=np.float32)
+    lib().wl_fill_normal_f32(seed, stream, float(std), out.ctypes.data, out.size)
+    return out
+
+
+def make_head_rows(cfg: ModelConfig, n_pairs, n_ar, seed, logit_std=3.0, student_mix=0.5):
+    """Synthetic LM-head input rows for the training loss: teacher [P, d], student [P, d], AR
+    rows [A, d] and AR targets [A]. Entries are normal, scaled so that with the N(0, 0.02) head
+    weights the logits have standard deviation about `logit_std`; a student row is its teacher row
+    plus `student_mix` times an independent row (the state's hidden rows lie near the fixed
+    point's), and every fourth student row equals its teacher row (a converged position)."""
+    d = cfg.d_model
+    s = logit_std / (WEIGHT_STD * np.sqrt(d))
+    t = make_normal_f32((n_pairs, d), s, seed, 201)
+    st = t + np.float32(student_mix) * make_normal_f32((n_pairs, d), s, seed, 202)
+    st[::4] = t[::4]
+    ar = make_normal_f32((n_ar, d), s, seed, 203)
+    tg = np.empty(n_ar, dtype=np.int32)
+    lib().wl_fill_uniform_ids(seed, 204, cfg.vocab, tg.ctypes.data, n_ar)
+    return t, st.astype(np.float32), ar, tg
+
+
 def make_batch(cfg: ModelConfig, batch, len_range, p_range, seed=SEED_BATCH):
     """Ragged batch: `batch` prompt lengths uniform in [len_range[0], len_range[1]] (inclusive) and
     corruption rates uniform in [p_range[0], p_range[1]); prompt b is make_prompt(..., seq=b)."""

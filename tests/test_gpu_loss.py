@@ -1,0 +1,159 @@
+"""GPU checks of the CLLM training loss at the LM head (Section 3.2.2: the global consistency
+loss, a forward KL between the fixed point's and the trajectory state's token distributions, plus
+omega times the AR loss) against the oracle's fp64 loss_head, through cllm_loss_head.
+
+Inputs: the model's own LM-head weights (N(0, 0.02), bf16 or fp32) and seeded rows scaled so the
+logits have standard deviation ~3 (workload.make_head_rows; every fourth student row equals its
+teacher row, so its KL and gradient vanish).
+
+Tolerances. The fp32 path (rows and weights fp32, fp32 MFMA accumulation) gets the fp32 bar,
+1e-4. In bf16 the rows enter the GEMM as hi + lo bf16 planes (16 significant bits, relative error
+<= 2^-16) against exact bf16 weights with fp32 accumulation, so each logit is within ~2^-16 of
+its scale (~3 here) of the fp64 value, i.e. ~5e-5; the log-softmax moves by at most twice that,
+a KL or NLL by at most ~4x (times 1 + its value), and the gradients (softmax differences times
+W or H, fp32 MFMA) by the same relative amount of their scale. 1e-3 covers this with a margin of
+~5, and stays two orders of magnitude below what a dropped term, a wrong sign or a swapped
+operand would change (those are pinned in the oracle's own tests).
+
+Every value is checked per row as |gpu - oracle| <= tol * (1 + |oracle|). A gradient element,
+a sum of products of softmax terms and rows or weights, is checked against the same sum over
+absolute values (the usual forward-error form: a converged pair has an exact gradient of zero,
+which the GPU reaches only up to rounding): for dH[i, k] = sum_v D[i, v] W[v, k] the scale is
+sum_v |dD|[i, v] |W[v, k]| with |dD| = p + q for a pair and omega (c + onehot) for an AR row, and
+for dW[v, k] the scale is sum_i |dD|[i, v] |H[i, k]|.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2403_00835_amd import workload
+from paper_2403_00835_amd.configs import SMALL, ModelConfig
+from tests.parity import log
+
+pytestmark = pytest.mark.gpu
+
+# fp32 head with a vocabulary that is not a multiple of the 64-column LM-head tile (1000 -> 1024)
+HEAD_F32 = ModelConfig(n_layers=1, d_model=64, n_heads=4, head_dim=16, ffn_dim=172, vocab=1000, dtype="f32")
+TOLS = {"f32": 1e-4, "bf16": 1e-3}
+
+CASES = [  # (teacher/student pairs, AR rows, omega)
+    (5, 3, 1.0),
+    (0, 7, 2.0),      # AR rows only
+    (9, 0, 1.0),      # consistency pairs only
+    (1, 0, 1.0),
+    (0, 1, 0.5),
+    (40, 24, 1.0),    # 64 loss rows, 104 GEMM rows: two 64-row tiles
+    (16, 16, 0.0),    # omega 0: the AR rows are reported but carry no gradient
+]
+
+
+@pytest.fixture(scope="module", params=[HEAD_F32, SMALL], ids=["f32-v1000", "small-bf16"])
+def head(request):
+    from paper_2403_00835_amd import binding
+    cfg = request.param
+    log(f"[loss] context {cfg.dtype} d={cfg.d_model} V={cfg.vocab}")
+    ws = workload.make_weights(cfg)
+    m = binding.Model(cfg, max_ctx=64, max_block=8, max_new=8, weights=ws)
+    W = workload.as_f32(cfg, ws[-1]).astype(np.float64)
+    yield cfg, m, W
+    m.close()
+
+
+def _close_rows(g, o, tol, what):
+    err = np.abs(np.asarray(g, np.float64) - o)
+    bound = tol * (1.0 + np.abs(o))
+    assert np.all(err <= bound), f"{what}: worst {err.max():.3g} (bound {bound[err.argmax()]:.3g})"
+    return float(err.max()) if err.size else 0.0
+
+
+def _softmax(z):
+    e = np.exp(z - z.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def _grad_scales(W, t, s, ar, tg, omega):
+    """Absolute-value sums bounding the gradients' rounding (see the module docstring)."""
+    aW = np.abs(W)
+    dp = _softmax(t.astype(np.float64) @ W.T) + _softmax(s.astype(np.float64) @ W.T)
+    da = _softmax(ar.astype(np.float64) @ W.T)
+    da[np.arange(tg.size), tg] += 1.0
+    da *= abs(omega)
+    return dp @ aW, da @ aW, dp.T @ np.abs(s) + da.T @ np.abs(ar)
+
+
+def _close_array(g, o, scale, tol, what):
+    if o.size == 0:
+        return 0.0
+    err = np.abs(np.asarray(g, np.float64) - o)
+    ratio = err / np.maximum(scale, 1e-300)
+    assert np.all(err <= tol * scale), f"{what}: worst err/scale {ratio.max():.3g} (err {err.max():.3g})"
+    return float(ratio.max())
+
+
+@pytest.mark.parametrize("P,A,omega", CASES)
+def test_loss_head_vs_oracle(head, P, A, omega):
+    cfg, m, W = head
+    tol = TOLS[cfg.dtype]
+    t, s, ar, tg = workload.make_head_rows(cfg, P, A, seed=100 + 7 * P + A)
+    log(f"[loss] {cfg.dtype} P={P} A={A} omega={omega}")
+    g = m.loss_head(t, s, ar, tg, omega, want_dw=True)
+    o = oracle.loss_head(W, t, s, ar, tg, omega)
+    e_kl = _close_rows(g["kl"], o["kl"], tol, "kl")
+    e_nll = _close_rows(g["nll"], o["nll"], tol, "nll")
+    terms = np.abs(o["kl"]).sum() + abs(omega) * np.abs(o["nll"]).sum()
+    assert abs(g["loss"] - o["loss"]) <= tol * (1.0 + terms), (g["loss"], o["loss"])
+    sc_s, sc_a, sc_w = _grad_scales(W, t, s, ar, tg, omega)
+    r_s = _close_array(g["d_student"], o["d_student"], sc_s, tol, "d_student")
+    r_a = _close_array(g["d_ar"], o["d_ar"], sc_a, tol, "d_ar")
+    r_w = _close_array(g["d_W"], o["d_W"], sc_w, tol, "d_W")
+    log(f"  max err kl {e_kl:.2g} nll {e_nll:.2g}; rel grad err student {r_s:.2g} ar {r_a:.2g} W {r_w:.2g}")
+    if P:
+        conv = np.arange(0, P, 4)  # student rows equal to their teacher rows
+        assert np.all(np.abs(g["kl"][conv]) <= tol), g["kl"][conv]
+    if omega == 0.0 and A:
+        assert np.all(g["d_ar"] == 0.0)
+    assert np.all(g["kl"] >= -tol)  # a KL divergence is non-negative
+    assert np.all(g["nll"] >= 0.0)
+
+
+def test_loss_head_repeat_is_deterministic(head):
+    """Every sum runs in a fixed order: two calls return identical bits, and a call with a
+    smaller batch in between does not disturb the next one."""
+    cfg, m, W = head
+    t, s, ar, tg = workload.make_head_rows(cfg, 12, 6, seed=5)
+    a = m.loss_head(t, s, ar, tg, 1.0, want_dw=True)
+    m.loss_head(t[:2], s[:2], ar[:1], tg[:1], 3.0, want_dw=True)
+    b = m.loss_head(t, s, ar, tg, 1.0, want_dw=True)
+    for k in ("kl", "nll", "d_student", "d_ar", "d_W"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["loss"] == b["loss"]
+
+
+def test_loss_head_without_dw_matches(head):
+    cfg, m, W = head
+    t, s, ar, tg = workload.make_head_rows(cfg, 6, 4, seed=9)
+    a = m.loss_head(t, s, ar, tg, 1.0, want_dw=True)
+    b = m.loss_head(t, s, ar, tg, 1.0, want_dw=False)
+    assert "d_W" not in b
+    for k in ("kl", "nll", "d_student", "d_ar"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_loss_head_argument_errors(head):
+    from paper_2403_00835_amd import binding
+    cfg, m, W = head
+    t, s, ar, tg = workload.make_head_rows(cfg, 40, 25, seed=11)
+    with pytest.raises(binding.CllmError):
+        m.loss_head(t[:0], s[:0], ar[:0], tg[:0], 1.0)       # no rows
+    with pytest.raises(binding.CllmError):
+        m.loss_head(t, s, ar, tg, 1.0)                       # 65 loss rows
+    bad = tg[:3].copy()
+    bad[1] = cfg.vocab
+    with pytest.raises(binding.CllmError):
+        m.loss_head(t[:2], s[:2], ar[:3], bad, 1.0)          # target out of range
+    with pytest.raises(binding.CllmError):
+        m.loss_head(t[:2], s[:2], ar[:3], tg[:3], float("nan"))
+    # the context still works after rejected calls
+    g = m.loss_head(t[:2], s[:2], ar[:3], tg[:3], 1.0)
+    o = oracle.loss_head(W, t[:2], s[:2], ar[:3], tg[:3], 1.0)
+    _close_rows(g["kl"], o["kl"], TOLS[cfg.dtype], "kl after errors")

@@ -10,6 +10,9 @@ timed steps (inputs resident on the device when timing starts).
 --workload 7b_long (prompt 2048, n = 64, 512 new) and 7b_batched (16 sequences, prompts uniform
 in [256, 1024], n = 32, 256 new each, corruption rates uniform in [0.1, 0.6], all decoded in one
 batched loop; value = tokens of all sequences / second) measure the other configurations.
+--workload 7b_loss times the CLLM training loss at the LLaMA-2-7B LM head (32000 x 4096 bf16):
+a step is one forward + backward of the loss head over 16 teacher/student pairs (one n = 16
+block) and 48 AR rows, on device arrays; value = loss rows / second.
 
 Prints one JSON line. --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -92,7 +95,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long", "7b_batched"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long", "7b_batched", "7b_loss"])
     ap.add_argument("--p", type=float, default=0.3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -109,6 +112,8 @@ def main():
     from paper_2403_00835_amd import binding, workload
     from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT, WORKLOADS
 
+    if args.workload == "7b_loss":
+        return main_loss(args)
     wl = WORKLOADS[args.workload]
     if wl.batch > 1:
         return main_batched(args, wl)
@@ -338,6 +343,129 @@ def main_batched(args, wl):
                      "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
                      "executed_mfma_tflops": round(2 * achieved, 2), "algorithmic_flops": gu_launch_flops,
                      "avg_launch_us": round(gu_ms / max(launches, 1) * 1e3, 2), "launches": launches},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+LOSS_PAIRS, LOSS_AR, LOSS_OMEGA = 16, 48, 1.0
+LOSS_STEPS_PER_STEP = 20  # loss-head calls per timed step (one call is ~0.2 ms)
+
+
+def main_loss(args):
+    """The CLLM loss head (global consistency KL + omega AR loss, forward then backward) at the
+    LLaMA-2-7B LM head. The model holds one decoder layer: the loss head touches no weight but
+    the LM head's, which has the 7B shape. A step is LOSS_STEPS_PER_STEP calls of
+    cllm_loss_head_device on arrays resident on the GPU (each call: 16 pairs + 48 AR rows, with
+    the weight gradient)."""
+    import dataclasses
+
+    import torch
+    from paper_2403_00835_amd import binding, workload
+    from paper_2403_00835_amd.configs import LLAMA7B
+
+    cfg = dataclasses.replace(LLAMA7B, n_layers=1)
+    d, V = cfg.d_model, cfg.vocab
+    P, A, omega = LOSS_PAIRS, LOSS_AR, LOSS_OMEGA
+    torch.cuda.init()
+    stream = torch.cuda.current_stream()
+    ws = workload.make_weights(cfg)
+    model = binding.Model(cfg, max_ctx=64, max_block=16, max_new=16, stream=stream.cuda_stream, weights=ws)
+    t, s, ar, tg = workload.make_head_rows(cfg, P, A, seed=1)
+
+    def dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+    T, S, Ar, TG = dev(t), dev(s), dev(ar), dev(tg)
+    kl, nll = torch.empty(P, device="cuda"), torch.empty(A, device="cuda")
+    ds, da = torch.empty(P, d, device="cuda"), torch.empty(A, d, device="cuda")
+    dw = torch.empty(V, d, device="cuda")
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+
+    def one_call():
+        model.loss_head_device(P, A, omega, T, S, Ar, TG, kl, nll, ds, da, dw, loss)
+
+    def one_step():
+        for _ in range(LOSS_STEPS_PER_STEP):
+            one_call()
+
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    # the device entry point must give the host entry point's results bit for bit
+    h = model.loss_head(t, s, ar, tg, omega, want_dw=True)
+    if not (np.array_equal(kl.cpu().numpy(), h["kl"]) and np.array_equal(dw.cpu().numpy(), h["d_W"]) and
+            loss.item() == h["loss"]):
+        raise RuntimeError("device loss head differs from the host entry point")
+    del h
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        one_step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    calls = args.steps * LOSS_STEPS_PER_STEP
+
+    # per-kernel durations: one pass of the same calls per kernel class, every launch timed
+    R, Rg = 2 * P + A, P + A
+    nch = (V + 1023) // 1024
+    w_bytes = V * d * 2
+    algo = {"loss_logits": w_bytes + R * d * 4 + R * V * 4,
+            "loss_rows": R * V * 4 + Rg * V * 4 + A * 4,
+            "loss_dh": w_bytes + Rg * V * 4 + nch * Rg * d * 4,
+            "loss_dw": Rg * V * 4 + Rg * d * 4 + V * d * 4}
+    kern = {}
+    for cls in algo:
+        model.timing_enable(cls, every=1)
+        for _ in range(args.steps):
+            one_step()
+        torch.cuda.synchronize()
+        n_l, ms = model.timing_read()
+        model.timing_enable(-1)
+        us = ms * 1e3 / max(n_l, 1)
+        kern[cls] = {"avg_launch_us": round(us, 2), "launches": n_l, "algorithmic_bytes": algo[cls],
+                     "achieved_gbps": round(algo[cls] / (us * 1e3), 1) if us > 0 else None}
+    dom = max(kern, key=lambda k: kern[k]["avg_launch_us"])
+    ach = kern[dom]["achieved_gbps"] or 0.0
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        log("[bench] cpu baseline: oracle loss head on the host")
+        Wf = workload.as_f32(cfg, ws[-1]).astype(np.float64)
+        reps, t_cpu = 0, 0.0
+        while t_cpu < 10.0 and reps < 20:
+            c0 = time.perf_counter()
+            oracle.loss_head(Wf, t, s, ar, tg, omega)
+            t_cpu += time.perf_counter() - c0
+            reps += 1
+        cpu = {"value": round(reps * Rg / t_cpu, 3), "unit": "rows/s", "cores": oracle.num_threads(),
+               "kind": "oracle", "sample": f"{reps} full loss-head calls ({P} pairs + {A} AR rows, with the "
+                                           f"weight gradient) in {t_cpu:.2f} s"}
+    line = {
+        "metric": "CLLM loss head (LM-head forward + backward) rows/s, 7B-shape bf16",
+        "value": round(calls * Rg / elapsed, 1),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"CLLM loss head at the LLaMA-2-7B LM head ({V} x {d} bf16): {P} teacher/student "
+                               f"pairs + {A} AR rows per call, omega {omega}, weight gradient on, "
+                               f"{LOSS_STEPS_PER_STEP} calls per step, rows and gradients resident on the GPU",
+                   "pairs": P, "ar_rows": A, "calls_per_step": LOSS_STEPS_PER_STEP, "d_model": d, "vocab": V},
+        "call_us": round(elapsed / calls * 1e6, 2),
+        "kernels": kern,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes": algo[dom], "avg_launch_us": kern[dom]["avg_launch_us"],
+                     "launches": kern[dom]["launches"]},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -270,6 +270,23 @@ cllm_status cllm_loss_head(cllm_ctx *ctx, const float *teacher, const float *stu
                            const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega, float *row_kl,
                            float *row_nll, float *d_student, float *d_ar, float *d_weight, double *loss);
 
+/* cllm_loss_head on device arrays, for a training loop whose rows and gradients stay in HBM:
+ * the same arguments, computation and results (bit for bit), but every array (rows, targets,
+ * row_kl, row_nll, d_student, d_ar, d_weight, and loss, a device double) is memory the context's
+ * GPU can access: its device memory, managed or pinned host memory; each is checked and anything
+ * else is ERR_ARG. The work is enqueued on the context's stream and the call returns without
+ * waiting: results are ready when that stream reaches this point; the caller keeps the inputs
+ * alive and unmodified until then. loss may be NULL (no total). Sizes are not checked beyond the
+ * row counts: each array must hold its rows. A target outside [0, V) cannot be checked on the
+ * host here: that AR row's row_nll and gradient row, and every d_weight entry it reaches, are
+ * NaN. Calls on one context share its workspace and must be ordered by its stream. Errors:
+ * ERR_ARG (n_pairs + n_ar outside [1, 64], null or inaccessible arrays), ERR_STATE, ERR_OOM
+ * (workspace growth, the only allocation), ERR_DEVICE. */
+cllm_status cllm_loss_head_device(cllm_ctx *ctx, const float *teacher, const float *student, int32_t n_pairs,
+                                  const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega,
+                                  float *row_kl, float *row_nll, float *d_student, float *d_ar, float *d_weight,
+                                  double *loss);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 

@@ -54,7 +54,7 @@ TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
-           "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
+           "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_loss_head_device", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
            "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
@@ -66,6 +66,13 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2403_00835_amd.build`")
+        # PyTorch wheels carry their own HIP runtime. Loaded first, it is the one libcllm.so binds
+        # to, so torch's device memory and streams are valid in the library's calls; loaded after
+        # the system runtime has opened the GPU, it finds no GPU. Import it first when installed.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.POINTER
         L.cllm_model_create.argtypes = [P(cllm_config), P(cllm_runtime_opts), P(_vp)]
@@ -87,6 +94,7 @@ def lib():
         L.cllm_trace_read.argtypes = [_vp, _i32, _vp, _i64, P(_i64)]
         L.cllm_trace_count.argtypes = [_vp, _i64, _vp, _i64, _i32, _i32, P(cllm_trace_stats)]
         L.cllm_loss_head.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _vp, _vp, _vp, P(_dbl)]
+        L.cllm_loss_head_device.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp]
         L.cllm_collect_states.argtypes = [_vp, _i64, _vp, _i64, _i32, _dbl, ctypes.c_uint64, _vp, _vp, _vp, _i64,
                                           P(_i64)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
@@ -284,6 +292,22 @@ class Model:
             out["d_W"] = dw
         return out
 
+    def loss_head_device(self, n_pairs, n_ar, omega, teacher, student, ar_rows, ar_targets, row_kl, row_nll,
+                         d_student, d_ar, d_weight=None, loss=None):
+        """cllm_loss_head_device: enqueue the loss head on device arrays (torch tensors on the
+        context's GPU, or raw addresses) and return without waiting. A tensor argument must be
+        contiguous, of the entry point's type (float32; int32 targets; float64 loss) and hold at
+        least its rows."""
+        d, V = self.cfg.d_model, self.cfg.vocab
+        P, A = int(n_pairs), int(n_ar)
+        args = [(teacher, P * d, "float32"), (student, P * d, "float32"), (ar_rows, A * d, "float32"),
+                (ar_targets, A, "int32"), (row_kl, P, "float32"), (row_nll, A, "float32"),
+                (d_student, P * d, "float32"), (d_ar, A * d, "float32"), (d_weight, V * d, "float32"),
+                (loss, 1, "float64")]
+        ptrs = [_dev_ptr(x, n, t) if n else None for x, n, t in args]
+        self._check(self.L.cllm_loss_head_device(self.h, ptrs[0], ptrs[1], P, ptrs[2], ptrs[3], A, float(omega),
+                                                 *ptrs[4:]))
+
     def trace_enable(self, enable=True):
         self._check(self.L.cllm_trace_enable(self.h, 1 if enable else 0))
 
@@ -303,6 +327,19 @@ class Model:
         n, ms = _i64(0), _dbl(0.0)
         self._check(self.L.cllm_timing_read(self.h, ctypes.byref(n), ctypes.byref(ms)))
         return int(n.value), float(ms.value)
+
+
+def _dev_ptr(x, count, dtype):
+    """Device address of x (None, an int address, or a tensor with data_ptr(): checked to be
+    contiguous, of dtype and holding at least count elements)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous() or str(x.dtype).split(".")[-1] != dtype or x.numel() < count:
+        raise ValueError(f"device array: need a contiguous {dtype} tensor of >= {count} elements, got "
+                         f"{x.dtype} {tuple(x.shape)}")
+    return x.data_ptr()
 
 
 def records_to_dicts(raw):

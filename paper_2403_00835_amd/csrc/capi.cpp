@@ -70,12 +70,17 @@ struct cllm_ctx {
     bool trace_on = false;
     // loss head workspace (allocated on first use, grown on demand)
     struct LossWs {
-        size_t h = 0, a = 0, z = 0, dd = 0, part = 0, dh = 0, dw = 0, rows = 0;
+        size_t h = 0, a = 0, z = 0, dd = 0, part = 0, dh = 0, dw = 0, rows = 0, st = 0, da = 0, dt = 0, ht = 0;
         float *H = nullptr, *Z = nullptr, *D = nullptr, *part_p = nullptr, *dH = nullptr, *dW = nullptr,
-              *out = nullptr;
-        uint8_t *A = nullptr;  // GEMM operand planes of the input rows (bytes)
+              *out = nullptr, *stats = nullptr;
+        uint8_t *A = nullptr;     // GEMM operand planes of the input rows (bytes)
+        uint8_t *Dact = nullptr;  // GEMM operand planes of D (bytes)
+        uint16_t *DT = nullptr, *HT = nullptr;  // dW operands (bf16 planes)
+        uint8_t *WT = nullptr;    // the packed LM head transposed (built on first use)
+        bool wt_ok = false;       // WT holds the current LM head
         int32_t *tg = nullptr;
-        RowTab *tab = nullptr;
+        RowTab *tabs = nullptr;   // row tables of the loss GEMMs: tabs[R - 1] holds R rows (R <= 128)
+        double *loss = nullptr;   // staging of the host entry point's total
     } loss;
     std::vector<Slot> slot;
     bool dead = false;
@@ -695,6 +700,123 @@ cllm_status loss_buf(cllm_ctx *c, T **p, size_t *have, size_t need) {
     if (s == CLLM_OK) *have = need;
     return s;
 }
+
+bool loss_args_ok(const float *teacher, const float *student, int32_t n_pairs, const float *ar_rows,
+                  const int32_t *ar_targets, int32_t n_ar, float omega, const float *row_kl, const float *row_nll,
+                  const float *d_student, const float *d_ar) {
+    return n_pairs >= 0 && n_ar >= 0 && n_pairs + n_ar >= 1 && n_pairs + n_ar <= 64 &&
+           (n_pairs == 0 || (teacher && student && row_kl && d_student)) &&
+           (n_ar == 0 || (ar_rows && ar_targets && row_nll && d_ar)) && omega == omega;
+}
+
+// Memory a kernel on the context's GPU may access: device memory of that GPU, managed memory, or
+// pinned host memory (pageable host memory is not known to the runtime and fails the query).
+bool device_accessible(cllm_ctx *c, const void *p) {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (a.type == hipMemoryTypeDevice) return a.device == c->opts.device;
+    return a.type == hipMemoryTypeManaged || a.type == hipMemoryTypeHost || a.isManaged;
+}
+
+// The loss head on device arrays, enqueued on the context's stream: pack the rows into the GEMM
+// operand, logits through the LM head, per-row losses and logit gradients D, D (and H) packed as
+// MFMA operands, dH = D W through the transposed LM head (K split over workgroups, partials
+// summed in split order), dW = D^T H (if d_weight) and the total (if loss). The workspace grows
+// on demand (hipMalloc); the transposed LM head is built on the first call after the weights
+// are set.
+cllm_status loss_head_enqueue(cllm_ctx *c, const float *T, const float *S, int P, const float *Ar, const int32_t *tg,
+                              int A, float omega, float *kl, float *nll, float *dS, float *dA, float *dW,
+                              double *loss) {
+    const int R = 2 * P + A, Rg = P + A, d = c->d, V = c->V;
+    if (R > 2 * kMaxRows) return fail(c, CLLM_ERR_ARG, "loss head: %d GEMM rows exceed %d", R, 2 * kMaxRows);
+    const int Vp = c->n_wg_lm * 16 * kLmTiles;
+    const int cap = round_up(R, kMaxRows);
+    const int nch = ceil_div(Vp, kLossChunk);
+    const int rpad = round_up(Rg, 32);
+    const int kstep = c->bf16 ? 32 : 16;  // MFMA k-step (elements)
+    // dH splits: about 512 workgroups over the columns of d and the vocabulary's k-steps
+    const int ks_v = Vp / kstep, n_wg_dh = ceil_div(d, 16 * kLmTiles);
+    const int kc = ceil_div(ks_v, std::max(1, std::min(ks_v, ceil_div(512, n_wg_dh))));
+    const int nsplit = ceil_div(ks_v, kc);
+    auto &w = c->loss;
+    cllm_status s;
+    if ((s = loss_buf(c, &w.A, &w.a, (size_t)cap * d * 4)) || (s = loss_buf(c, &w.Z, &w.z, (size_t)R * Vp)) ||
+        (s = loss_buf(c, &w.D, &w.dd, (size_t)Rg * Vp)) || (s = loss_buf(c, &w.stats, &w.st, (size_t)Rg * nch * 5)) ||
+        (s = loss_buf(c, &w.Dact, &w.da, (size_t)kMaxRows * Vp * 4)) ||
+        (s = loss_buf(c, &w.part_p, &w.part, (size_t)nsplit * Rg * d)))
+        return s;
+    if (c->bf16 && ((s = loss_buf(c, &w.DT, &w.dt, (size_t)2 * Vp * rpad)) ||
+                    (s = loss_buf(c, &w.HT, &w.ht, (size_t)2 * d * rpad))))
+        return s;
+    hipStream_t st = c->stream;
+    if (!w.tabs) {  // once per context: every row count's table (rows of one block, no positions)
+        if ((s = dalloc_t(c, &w.tabs, 2 * kMaxRows))) return s;
+        std::vector<RowTab> th(2 * kMaxRows);
+        for (int i = 0; i < 2 * kMaxRows; ++i) {
+            th[i].R = i + 1;
+            th[i].nseq = 1;
+        }
+        HIPCHK(c, hipMemcpyAsync(w.tabs, th.data(), th.size() * sizeof(RowTab), hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipStreamSynchronize(st));
+    }
+    if (!w.wt_ok) {  // the LM head as the weight operand of dH = D W
+        if (!w.WT && (s = dalloc_t(c, &w.WT, (size_t)Vp * d * c->elem))) return s;
+        HIPCHK(c, launch_transpose_lm(c->bf16, c->w_lm, Vp, d, w.WT, st));
+        w.wt_ok = true;
+    }
+    hipEvent_t e0, e1;
+    // logits Z = H W^T over the packed LM head (no RMSNorm row factor: the rows are the head's input)
+    timing_events(c, CLLM_KT_LOSS_LOGITS, 0, &e0, &e1);
+    HIPCHK(c, launch_pack_rows(c->bf16, T, S, P, Ar, A, d, cap, w.A, st, e0));
+    GemmParams g{};
+    g.W = c->w_lm;
+    g.Ks = c->ks_d;
+    g.cols = Vp;
+    g.A = w.A;
+    g.lda = d;
+    g.rr = RowsRef{w.tabs + (R - 1), nullptr, cap};
+    g.V = V;
+    g.Zout = w.Z;
+    g.ldz = Vp;
+    // one launch per 64-row tile (each streams the weights once; measured faster than one launch
+    // of two row tiles sharing them), each sized to its rows
+    const int row_tiles = ceil_div(R, kMaxRows);
+    for (int t = 0; t < row_tiles; ++t) {
+        const int rg = rows_to_rg(std::min(kMaxRows, R - t * kMaxRows));
+        g.rt0 = t * kMaxRows / (16 * rg);  // in units of the launch's 16 * rg rows
+        HIPCHK(c, launch_gemm(GEMM_LOGITS, c->bf16, rg, 1, g, st, nullptr, t == row_tiles - 1 ? e1 : nullptr));
+    }
+    // per-row losses, D, and D (and H) as MFMA operands
+    LossParams lp{w.Z, tg, P, A, V, Vp, omega, kl, nll, w.D};
+    timing_events(c, CLLM_KT_LOSS_ROWS, 0, &e0, &e1);
+    HIPCHK(c, launch_loss_rows(lp, w.stats, st, e0, nullptr));
+    HIPCHK(c, launch_loss_pack(c->bf16, w.D, Rg, Vp, Vp, kMaxRows, w.Dact, rpad, w.DT, S, P, Ar, d, w.HT, st, e1));
+    // dH = D W: the streaming GEMM over the transposed LM head, K (the vocabulary) split nsplit ways
+    GemmParams h{};
+    h.W = w.WT;
+    h.Ks = ks_v;
+    h.cols = d;
+    h.A = w.Dact;
+    h.lda = Vp;
+    h.rr = RowsRef{w.tabs + (Rg - 1), nullptr, kMaxRows};
+    h.V = d;
+    h.Zout = w.part_p;
+    h.ldz = d;
+    h.kc = kc;
+    h.zstride = (size_t)Rg * d;
+    timing_events(c, CLLM_KT_LOSS_DH, 0, &e0, &e1);
+    HIPCHK(c, launch_gemm(GEMM_LOGITS, c->bf16, rows_to_rg(Rg), 1, h, st, e0, nullptr));
+    HIPCHK(c, launch_loss_dh_sum(w.part_p, nsplit, Rg, d, P, dS, dA, st, e1));
+    if (dW) {
+        timing_events(c, CLLM_KT_LOSS_DW, 0, &e0, &e1);
+        HIPCHK(c, launch_loss_dw(c->bf16, w.DT, w.HT, Vp, rpad, w.D, Rg, Vp, S, P, Ar, d, V, dW, st, e0, e1));
+    }
+    if (loss) HIPCHK(c, launch_loss_total(kl, P, nll, A, omega, loss, st));
+    return CLLM_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -860,6 +982,7 @@ cllm_status cllm_model_set_weights(cllm_ctx *c, const void *const *tensors, int3
     if (!tensors || n_tensors != 3 + 9 * c->NL) return fail(c, CLLM_ERR_ARG, "expected %d tensors", 3 + 9 * c->NL);
     for (int i = 0; i < n_tensors; ++i)
         if (!tensors[i]) return fail(c, CLLM_ERR_ARG, "tensor %d is NULL", i);
+    c->loss.wt_ok = false;  // the loss head's transposed LM head is rebuilt on its next call
     const int d = c->d, F = c->F, V = c->V;
     const size_t E = c->elem;
     size_t stage_elems = std::max({(size_t)3 * d * d, (size_t)2 * F * d, (size_t)V * d});
@@ -1204,84 +1327,64 @@ cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const
 cllm_status cllm_loss_head(cllm_ctx *c, const float *teacher, const float *student, int32_t n_pairs,
                            const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega, float *row_kl,
                            float *row_nll, float *d_student, float *d_ar, float *d_weight, double *loss) {
-    if (!c || !loss || n_pairs < 0 || n_ar < 0 || n_pairs + n_ar < 1 || n_pairs + n_ar > 64 ||
-        (n_pairs > 0 && (!teacher || !student || !row_kl || !d_student)) ||
-        (n_ar > 0 && (!ar_rows || !ar_targets || !row_nll || !d_ar)) || !(omega == omega))
+    if (!c || !loss || !loss_args_ok(teacher, student, n_pairs, ar_rows, ar_targets, n_ar, omega, row_kl, row_nll,
+                                     d_student, d_ar))
         return c ? fail(c, CLLM_ERR_ARG, "loss head: bad arguments (pairs + AR rows in [1, 64])") : CLLM_ERR_ARG;
     cllm_status s;
     if ((s = check_ctx(c))) return s;
     if (!c->w_lm) return fail(c, CLLM_ERR_STATE, "loss head: weights not set");
     for (int i = 0; i < n_ar; ++i)
         if (ar_targets[i] < 0 || ar_targets[i] >= c->V) return fail(c, CLLM_ERR_ARG, "loss head: target out of range");
-    const int P = n_pairs, A = n_ar, R = 2 * P + A, Rg = P + A, d = c->d, V = c->V;
-    const int Vp = c->n_wg_lm * 16 * kLmTiles;
-    const int cap = round_up(R, kMaxRows);
-    const int nch = ceil_div(Vp, kLossChunk);
+    const int P = n_pairs, A = n_ar, Rg = P + A, d = c->d, V = c->V;
     auto &w = c->loss;
-    if ((s = loss_buf(c, &w.H, &w.h, (size_t)R * d)) || (s = loss_buf(c, &w.A, &w.a, (size_t)cap * d * 4)) ||
-        (s = loss_buf(c, &w.Z, &w.z, (size_t)R * Vp)) || (s = loss_buf(c, &w.D, &w.dd, (size_t)Rg * Vp)) ||
-        (s = loss_buf(c, &w.part_p, &w.part, (size_t)nch * Rg * d)) || (s = loss_buf(c, &w.dH, &w.dh, (size_t)Rg * d)) ||
-        (s = loss_buf(c, &w.out, &w.rows, (size_t)Rg)) || (d_weight && (s = loss_buf(c, &w.dW, &w.dw, (size_t)V * d))))
+    // staging of the host arrays: rows (teacher, student, AR), targets, per-row losses, dH, loss
+    if ((s = loss_buf(c, &w.H, &w.h, (size_t)(2 * P + A) * d)) || (s = loss_buf(c, &w.out, &w.rows, (size_t)Rg)) ||
+        (s = loss_buf(c, &w.dH, &w.dh, (size_t)Rg * d)) || (d_weight && (s = loss_buf(c, &w.dW, &w.dw, (size_t)V * d))))
         return s;
-    if (!w.tab && (s = dalloc_t(c, &w.tab, 1))) return s;
     if (!w.tg && (s = dalloc_t(c, &w.tg, (size_t)64))) return s;
+    if (!w.loss && (s = dalloc_t(c, &w.loss, 1))) return s;
     hipStream_t st = c->stream;
     const size_t row_b = (size_t)d * sizeof(float);
+    float *T = w.H, *S = w.H + (size_t)P * d, *Ar = w.H + (size_t)2 * P * d;
     if (P) {
-        HIPCHK(c, hipMemcpyAsync(w.H, teacher, P * row_b, hipMemcpyHostToDevice, st));
-        HIPCHK(c, hipMemcpyAsync(w.H + (size_t)P * d, student, P * row_b, hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipMemcpyAsync(T, teacher, P * row_b, hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipMemcpyAsync(S, student, P * row_b, hipMemcpyHostToDevice, st));
     }
     if (A) {
-        HIPCHK(c, hipMemcpyAsync(w.H + (size_t)2 * P * d, ar_rows, A * row_b, hipMemcpyHostToDevice, st));
+        HIPCHK(c, hipMemcpyAsync(Ar, ar_rows, A * row_b, hipMemcpyHostToDevice, st));
         HIPCHK(c, hipMemcpyAsync(w.tg, ar_targets, A * sizeof(int32_t), hipMemcpyHostToDevice, st));
     }
-    RowTab th{};
-    th.R = R;
-    th.nseq = 1;
-    HIPCHK(c, hipMemcpyAsync(w.tab, &th, sizeof(th), hipMemcpyHostToDevice, st));
-    HIPCHK(c, launch_pack_rows(c->bf16, w.H, R, d, cap, w.A, st));
-    // logits Z = H W^T over the packed LM head (no RMSNorm row factor: the rows are the head's input)
-    GemmParams g{};
-    g.W = c->w_lm;
-    g.Ks = c->ks_d;
-    g.cols = Vp;
-    g.A = w.A;
-    g.lda = d;
-    g.rr = RowsRef{w.tab, nullptr, cap};
-    g.V = V;
-    g.Zout = w.Z;
-    g.ldz = Vp;
-    const int row_tiles = ceil_div(R, kMaxRows);
-    const int rg = row_tiles > 1 ? 4 : rows_to_rg(R);
-    hipEvent_t e0, e1;
-    timing_events(c, CLLM_KT_LOSS_LOGITS, rg, &e0, &e1);
-    HIPCHK(c, launch_gemm(GEMM_LOGITS, c->bf16, rg, row_tiles, g, st, e0, e1));
-    LossParams lp{w.Z, w.tg, P, A, V, Vp, omega, w.out, w.out + P, w.D};
-    timing_events(c, CLLM_KT_LOSS_ROWS, rg, &e0, &e1);
-    HIPCHK(c, launch_loss_rows(lp, st, e0, e1));
-    timing_events(c, CLLM_KT_LOSS_DH, rg, &e0, &e1);
-    HIPCHK(c, launch_loss_dh(c->bf16, w.D, Rg, Vp, c->w_lm, Vp, d, w.part_p, w.dH, st, e0, e1));
-    if (d_weight) {
-        timing_events(c, CLLM_KT_LOSS_DW, rg, &e0, &e1);
-        HIPCHK(c, launch_loss_dw(w.D, Rg, Vp, w.H + (size_t)P * d, d, V, w.dW, st, e0, e1));
-    }
+    if ((s = loss_head_enqueue(c, T, S, P, Ar, w.tg, A, omega, w.out, w.out + P, w.dH, w.dH + (size_t)P * d,
+                               d_weight ? w.dW : nullptr, w.loss)))
+        return s;
     std::vector<float> rl((size_t)Rg);
     HIPCHK(c, hipMemcpyAsync(rl.data(), w.out, Rg * sizeof(float), hipMemcpyDeviceToHost, st));
     if (P) HIPCHK(c, hipMemcpyAsync(d_student, w.dH, P * row_b, hipMemcpyDeviceToHost, st));
     if (A) HIPCHK(c, hipMemcpyAsync(d_ar, w.dH + (size_t)P * d, A * row_b, hipMemcpyDeviceToHost, st));
     if (d_weight) HIPCHK(c, hipMemcpyAsync(d_weight, w.dW, (size_t)V * row_b, hipMemcpyDeviceToHost, st));
+    HIPCHK(c, hipMemcpyAsync(loss, w.loss, sizeof(double), hipMemcpyDeviceToHost, st));
     HIPCHK(c, hipStreamSynchronize(st));
-    double kl_sum = 0.0, nll_sum = 0.0;
-    for (int i = 0; i < P; ++i) {
-        row_kl[i] = rl[i];
-        kl_sum += rl[i];
-    }
-    for (int i = 0; i < A; ++i) {
-        row_nll[i] = rl[P + i];
-        nll_sum += rl[P + i];
-    }
-    *loss = kl_sum + (double)omega * nll_sum;
+    for (int i = 0; i < P; ++i) row_kl[i] = rl[i];
+    for (int i = 0; i < A; ++i) row_nll[i] = rl[P + i];
     return CLLM_OK;
+}
+
+cllm_status cllm_loss_head_device(cllm_ctx *c, const float *teacher, const float *student, int32_t n_pairs,
+                                  const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega,
+                                  float *row_kl, float *row_nll, float *d_student, float *d_ar, float *d_weight,
+                                  double *loss) {
+    if (!c || !loss_args_ok(teacher, student, n_pairs, ar_rows, ar_targets, n_ar, omega, row_kl, row_nll, d_student,
+                            d_ar))
+        return c ? fail(c, CLLM_ERR_ARG, "loss head: bad arguments (pairs + AR rows in [1, 64])") : CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c))) return s;
+    if (!c->w_lm) return fail(c, CLLM_ERR_STATE, "loss head: weights not set");
+    const void *ptrs[] = {teacher, student, ar_rows, ar_targets, row_kl, row_nll, d_student, d_ar, d_weight, loss};
+    for (const void *q : ptrs)
+        if (q && !device_accessible(c, q))
+            return fail(c, CLLM_ERR_ARG, "loss head (device): an array is not device memory of this context's GPU");
+    return loss_head_enqueue(c, teacher, student, n_pairs, ar_rows, ar_targets, n_ar, omega, row_kl, row_nll,
+                             d_student, d_ar, d_weight, loss);
 }
 
 cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_len, int32_t *pending) {

@@ -56,8 +56,10 @@ struct Stage {  // operands of one k-step
 
 // Loads of one k-step s (callers clamp s into [0, Ks), so every load is issued and the compiler
 // can count outstanding loads exactly). Tiles past the last one (a ragged last workgroup) load
-// the last tile again; their columns are never written.
-template <Prec P, int NT, int RG>
+// the last tile again; their columns are never written. SHARED: the weight tiles are read by
+// several workgroups (the row tiles of one column group), so they are loaded as ordinary
+// (cached) loads; otherwise they are streamed (nontemporal: read once, not kept in the caches).
+template <Prec P, int NT, int RG, bool SHARED>
 __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int rg0, int s, int lane) {
     using PT = PrecT<P>;
     using T = typename PT::T;
@@ -66,7 +68,7 @@ __device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams
     for (int j = 0; j < NT; ++j) {
         const u32x4 *src =
             reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tiles + min(t0 + j, tiles - 1)) * kTileBytes) + lane;
-        st.b[j] = __builtin_nontemporal_load(src);  // streamed once per iteration
+        st.b[j] = SHARED ? *src : __builtin_nontemporal_load(src);
     }
     const T *A = reinterpret_cast<const T *>(p.A);
     const int ks_a = p.lda / PT::KSTEP;
@@ -260,7 +262,16 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    const int wg = blockIdx.x;
+    const int wg = blockIdx.x;  // column group
+    if constexpr (EP == E_LOGITS) {
+        if (p.kc > 0) {  // split K: k-steps [z kc, min((z + 1) kc, Ks)), partial products to plane z
+            const int ks0 = blockIdx.z * p.kc;
+            p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
+            p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;  // 16-byte lane vectors
+            p.Ks = min(p.kc, p.Ks - ks0);
+            p.Zout += (size_t)blockIdx.z * p.zstride;
+        }
+    }
     // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
     // capacity); m of them are live. A launch of one row tile (MT false) always has live rows, so
     // nothing waits for the row count before the first loads; with several row tiles (MT) a tile
@@ -293,7 +304,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     auto step_of = [&](int q) { return min(w + q * W, p.Ks - 1); };
     Stage<P, NT, RG> ring[D];
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j) gemm_load(ring[j], p, t0, rg0, step_of(j), lane);
+    for (int j = 0; j < D - 1; ++j) gemm_load<P, NT, RG, MT>(ring[j], p, t0, rg0, step_of(j), lane);
 
     f32x4 acc[RG][NT];
 #pragma unroll
@@ -311,7 +322,7 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
 #pragma unroll
             for (int j = 0; j < D; ++j) {
                 // sched_barrier keeps the scheduler from sinking loads to their uses.
-                gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
+                gemm_load<P, NT, RG, MT>(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
                 __builtin_amdgcn_sched_barrier(0);
                 gemm_compute(ring[j], acc);
                 __builtin_amdgcn_sched_barrier(0);
@@ -322,7 +333,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
         for (int j = 0; j < 2 * D - 1; ++j) {
             const int v = v0 + j;
             if (v < nmy) {
-                if (v + D - 1 < nmy) gemm_load(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
+                if (v + D - 1 < nmy)
+                    gemm_load<P, NT, RG, MT>(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
                 gemm_compute(ring[j % D], acc);
             }
         }
@@ -1060,7 +1072,8 @@ __global__ void repack_kernel(const void *src, const int32_t *perm, int K, int K
 // ------------------------------------------------------------------------------------------
 // Launchers
 // ------------------------------------------------------------------------------------------
-// Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile p.rt0).
+// Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile
+// p.rt0) x K splits (E_LOGITS with p.kc > 0).
 template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves>
 static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -1070,8 +1083,10 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     GemmParams q = p;
     q.row_tiles = row_tiles;
     q.n_wg = (p.cols + COLS - 1) / COLS;  // the last workgroup may be ragged
-    const dim3 grid(q.n_wg, row_tiles);
-    if (e0) {
+    const int splits = EP == E_LOGITS && p.kc > 0 ? (p.Ks + p.kc - 1) / p.kc : 1;
+    if (EP != E_LOGITS && p.kc != 0) return hipErrorInvalidValue;
+    const dim3 grid(q.n_wg, row_tiles, splits);
+    if (e0 || e1) {
         hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, q);
     } else {
         hipLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, q);

@@ -59,9 +59,13 @@ struct GemmParams {
     int *pidx;
     float *dbg;
     int V;
-    // E_LOGITS (the loss head's LM head, no RMSNorm row factor): fp32 logits [row][ldz]
+    // E_LOGITS (plain fp32 products, no RMSNorm row factor): Zout[row][ldz], columns < V. With
+    // kc > 0 the launch splits K: grid z takes k-steps [z kc, min((z + 1) kc, Ks)) and writes its
+    // partial products to Zout + z * zstride.
     float *Zout;
     int ldz;
+    int kc;
+    size_t zstride;
 };
 
 struct EmbedParams {
@@ -149,18 +153,37 @@ struct LossParams {
     float *kl, *nll;   // per pair / per AR row
     float *D;          // logit gradients [P + A][ldz] (student rows, then AR rows; 0 past V)
 };
-hipError_t launch_loss_rows(const LossParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-// Rows (fp32 [rows][d]) to the two bf16 planes (or one fp32 plane) of a GEMM operand of row
-// capacity cap.
-hipError_t launch_pack_rows(bool bf16, const float *X, int rows, int d, int cap, void *A, hipStream_t s);
-// dH = D W over the packed LM-head weights W (tiles of Vp/16 rows x d/32 k-steps): per chunk of
-// kLossChunk vocabulary rows a partial [nch][rows][d], then their sum in chunk order.
-constexpr int kLossChunk = 1024;
-hipError_t launch_loss_dh(bool bf16, const float *D, int rows, int ldd, const uint8_t *W, int Vp, int d, float *part,
-                          float *dH, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-// dW[v][k] = sum_r D[r][v] H[r][k] for v < V (rows <= 64).
-hipError_t launch_loss_dw(const float *D, int rows, int ldd, const float *H, int d, int V, float *dW, hipStream_t s,
-                          hipEvent_t e0, hipEvent_t e1);
+// Per-row losses and logit gradients in two passes over vocabulary chunks of kLossChunk entries:
+// per-chunk statistics (stats: [P + A][chunks][5] floats), then their combination in chunk order,
+// the losses and D. e0 (if any) marks the start of the first pass.
+constexpr int kLossChunk = 2048;
+hipError_t launch_loss_rows(const LossParams &p, float *stats, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// Rows (fp32 [.][d]: np teacher rows T0, np student rows S0, na AR rows R0, in that order) to the
+// two bf16 planes (or one fp32 plane) of a GEMM operand of row capacity cap; e0 marks its start.
+hipError_t launch_pack_rows(bool bf16, const float *T0, const float *S0, int np, const float *R0, int na, int d,
+                            int cap, void *A, hipStream_t s, hipEvent_t e0);
+// D [rows][ldd] as the GEMM operand of dH = D W (Dact: operand order, row capacity cap, K = Vp);
+// in bf16 also D^T and the gradient rows H (S0 rows < np, then R0) as the operands of dW = D^T H
+// with the contraction over rpad rows (DT: 2 planes Vp x rpad; HT: 2 planes d x rpad; zero rows
+// from `rows`). e1 marks the end of the last launch.
+hipError_t launch_loss_pack(bool bf16, const float *D, int rows, int ldd, int Vp, int cap, void *Dact, int rpad,
+                            uint16_t *DT, const float *S0, int np, const float *R0, int d, uint16_t *HT,
+                            hipStream_t s, hipEvent_t e1);
+// The packed LM head [Vp][d] repacked as the weight operand of dH = D W (tiles over k-steps of the
+// vocabulary and 16 columns of d); Vp x d elements.
+hipError_t launch_transpose_lm(bool bf16, const uint8_t *W, int Vp, int d, uint8_t *WT, hipStream_t s);
+// dH from the K-split partials [nsplit][rows][d], summed in split order: rows < np to dS [np][d],
+// the others to dA. e1 marks the end.
+hipError_t launch_loss_dh_sum(const float *part, int nsplit, int rows, int d, int np, float *dS, float *dA,
+                              hipStream_t s, hipEvent_t e1);
+// dW[v][k] = sum_r D[r][v] H[r][k] for v < V (rows <= 64), H row r = S0 row r for r < np, else
+// R0 row r - np: bf16 from the DT / HT operands, fp32 from D, S0 and R0.
+hipError_t launch_loss_dw(bool bf16, const uint16_t *DT, const uint16_t *HT, int Vp, int rpad, const float *D,
+                          int rows, int ldd, const float *S0, int np, const float *R0, int d, int V, float *dW,
+                          hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// *loss = sum kl[0..np) + omega * sum nll[0..na), each in row order, in double (one thread).
+hipError_t launch_loss_total(const float *kl, int np, const float *nll, int na, float omega, double *loss,
+                             hipStream_t s);
 
 hipError_t launch_repack(bool bf16, const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst,
                          hipStream_t s);

@@ -157,3 +157,60 @@ def test_loss_head_argument_errors(head):
     g = m.loss_head(t[:2], s[:2], ar[:3], tg[:3], 1.0)
     o = oracle.loss_head(W, t[:2], s[:2], ar[:3], tg[:3], 1.0)
     _close_rows(g["kl"], o["kl"], TOLS[cfg.dtype], "kl after errors")
+
+
+def _dev(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def test_loss_head_device_equals_host(head):
+    """cllm_loss_head_device on device arrays returns the host entry point's results bit for bit,
+    on two calls in a row, the second smaller (the workspace keeps the first call's contents)."""
+    import torch
+    cfg, m, W = head
+    d, V = cfg.d_model, cfg.vocab
+    for P, A in ((12, 20), (3, 2)):
+        t, s, ar, tg = workload.make_head_rows(cfg, P, A, seed=31 + P)
+        h = m.loss_head(t, s, ar, tg, 1.5, want_dw=True)
+        T, S, Ar, TG = _dev(t), _dev(s), _dev(ar), _dev(tg)
+        nan = float("nan")
+        kl, nll = torch.full((P,), nan, device="cuda"), torch.full((A,), nan, device="cuda")
+        ds, da = torch.full((P, d), nan, device="cuda"), torch.full((A, d), nan, device="cuda")
+        dw = torch.full((V, d), nan, device="cuda")
+        loss = torch.full((1,), nan, dtype=torch.float64, device="cuda")
+        torch.cuda.synchronize()
+        m.loss_head_device(P, A, 1.5, T, S, Ar, TG, kl, nll, ds, da, dw, loss)
+        torch.cuda.synchronize()
+        assert np.array_equal(kl.cpu().numpy(), h["kl"]) and np.array_equal(nll.cpu().numpy(), h["nll"])
+        assert np.array_equal(ds.cpu().numpy(), h["d_student"]) and np.array_equal(da.cpu().numpy(), h["d_ar"])
+        assert np.array_equal(dw.cpu().numpy(), h["d_W"])
+        assert loss.item() == h["loss"]
+
+
+def test_loss_head_device_bad_target_and_host_memory(head):
+    """On device arrays a target outside the vocabulary gives a NaN loss and gradient for that AR
+    row only; pageable host memory is rejected before anything runs."""
+    import torch
+    from paper_2403_00835_amd import binding
+    cfg, m, W = head
+    d = cfg.d_model
+    t, s, ar, tg = workload.make_head_rows(cfg, 2, 3, seed=41)
+    h = m.loss_head(t, s, ar, tg, 1.0)
+    bad = tg.copy()
+    bad[1] = cfg.vocab + 5
+    T, S, Ar, TG = _dev(t), _dev(s), _dev(ar), _dev(bad)
+    kl, nll = torch.zeros(2, device="cuda"), torch.zeros(3, device="cuda")
+    ds, da = torch.zeros(2, d, device="cuda"), torch.zeros(3, d, device="cuda")
+    torch.cuda.synchronize()
+    m.loss_head_device(2, 3, 1.0, T, S, Ar, TG, kl, nll, ds, da)
+    torch.cuda.synchronize()
+    nll_h, da_h = nll.cpu().numpy(), da.cpu().numpy()
+    assert np.isnan(nll_h[1]) and np.all(np.isnan(da_h[1]))
+    assert np.array_equal(nll_h[[0, 2]], h["nll"][[0, 2]]) and np.array_equal(da_h[[0, 2]], h["d_ar"][[0, 2]])
+    assert np.array_equal(kl.cpu().numpy(), h["kl"]) and np.array_equal(ds.cpu().numpy(), h["d_student"])
+    host_rows = np.ascontiguousarray(t)
+    with pytest.raises(binding.CllmError):
+        m.loss_head_device(2, 3, 1.0, host_rows.ctypes.data, S, Ar, TG, kl, nll, ds, da)
+    with pytest.raises(ValueError):
+        m.loss_head_device(2, 3, 1.0, T, S, Ar, TG, kl, nll[:2], ds, da)  # too few rows

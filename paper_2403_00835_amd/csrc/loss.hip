@@ -310,12 +310,16 @@ __global__ void loss_total_kernel(const float *kl, int np, const float *nll, int
 
 // dW = D^T H, bf16 operands (hi + lo planes; the products hi hi + hi lo + lo hi, fp32
 // accumulation). Workgroup: 128 vocabulary rows x 128 columns; wave (wv, wk) owns 64 x 64 (4 x 4
-// tiles of 16 x 16); the contraction runs over the rpad rows, 32 per k-step.
+// tiles of 16 x 16); the contraction runs over the rpad rows, 32 per k-step. The wave's block
+// goes out through LDS so that each store instruction writes four whole 256-byte row segments
+// (16 bytes per lane) instead of 64-byte pieces of four rows.
+constexpr int kDwV = 128, kDwK = 128, kDwLd = 64 + 4;  // LDS row stride (floats)
 __global__ __launch_bounds__(256) void loss_dw_mfma_kernel(const uint16_t *DT, const uint16_t *HT, int Vp, int d,
                                                            int rpad, int V, float *dW) {
+    __shared__ float s_blk[4][64 * kDwLd];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int nvt = Vp / 16, nkt = d / 16, ks = rpad / 32;
-    const int vt0 = blockIdx.x * 8 + (w & 1) * 4, kt0 = blockIdx.y * 8 + (w >> 1) * 4;
+    const int vt0 = blockIdx.x * (kDwV / 16) + (w & 1) * 4, kt0 = blockIdx.y * (kDwK / 16) + (w >> 1) * 4;
     const size_t pd = (size_t)Vp * rpad, ph = (size_t)d * rpad;
     f32x4 acc[4][4];
 #pragma unroll
@@ -347,19 +351,24 @@ __global__ __launch_bounds__(256) void loss_dw_mfma_kernel(const uint16_t *DT, c
                 acc[i][j] = mfma_kstep<Prec::BF16>(al[i], bh[j], acc[i][j]);
             }
     }
-    // C layout: vocabulary row 4 * (lane / 16) + e of the tile, column lane % 16
+    // C layout: row 4 * (lane / 16) + e of tile (i, j), column lane % 16; into the wave's LDS block
+    float *blk = s_blk[w];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (vt0 + i >= nvt || kt0 + j >= nkt) continue;
-            const int k = 16 * (kt0 + j) + (lane & 15);
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int v = 16 * (vt0 + i) + 4 * (lane >> 4) + e;
-                if (v < V) dW[(size_t)v * d + k] = acc[i][j][e];
-            }
+            for (int e = 0; e < 4; ++e) blk[(16 * i + 4 * (lane >> 4) + e) * kDwLd + 16 * j + (lane & 15)] = acc[i][j][e];
+    __syncthreads();
+    // rows of the block: 16 lanes per row (16 bytes each), four rows per store
+    const int k = 16 * kt0 + 4 * (lane & 15);
+    if (k < d) {
+#pragma unroll 4
+        for (int r = lane >> 4; r < 64; r += 4) {
+            const int v = 16 * vt0 + r;
+            if (v < V) *reinterpret_cast<f32x4 *>(dW + (size_t)v * d + k) = *reinterpret_cast<const f32x4 *>(blk + r * kDwLd + 4 * (lane & 15));
         }
+    }
 }
 
 // dW, fp32 operands: workgroup (64 vocabulary rows, 64 columns of d); wave w owns rows
@@ -472,7 +481,7 @@ hipError_t launch_loss_dw(bool bf16, const uint16_t *DT, const uint16_t *HT, int
         return hipErrorInvalidValue;
     if (bf16) {
         if (rpad % 32 != 0 || rpad < rows) return hipErrorInvalidValue;
-        const dim3 grid((Vp + 127) / 128, (d + 127) / 128);
+        const dim3 grid((Vp + kDwV - 1) / kDwV, (d + kDwK - 1) / kDwK);
         if (e0)
             hipExtLaunchKernelGGL(loss_dw_mfma_kernel, grid, dim3(256), 0, s, e0, e1, 0, DT, HT, Vp, d, rpad, V, dW);
         else

@@ -34,29 +34,30 @@ BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 TIMING_EVERY = 33  # kernel-timing sample stride (coprime with 32 layers)
 METRIC = "Jacobi-step ms & accepted tokens/s, 7B-shape bf16 n=16; HBM GB/s vs peak"
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_gemm_gate_up_llama7b_n16.md")
+LOSS_SUMMARY = os.path.join(ROOT, "profiles", "loss_head_llama7b.md")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
+def kernel_source_hash(files=("kernels.hip", "device.h", "launch.h")):
     h = hashlib.sha256()
-    for f in ("kernels.hip", "device.h", "launch.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2403_00835_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source; otherwise None."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+def measured_traffic(summary=TRAFFIC_SUMMARY, files=("kernels.hip", "device.h", "launch.h")):
+    """HBM bytes per launch of a kernel from a committed rocprofv3 counter summary, if it was
+    taken on the current source of `files`; otherwise None."""
+    if not os.path.exists(summary):
         return None
-    text = open(TRAFFIC_SUMMARY).read()
+    text = open(summary).read()
     m_hash = re.search(r"kernel_source_hash:\s*([0-9a-f]+)", text)
     m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash(files):
         return None
     return float(m_bytes.group(1))
 
@@ -88,6 +89,19 @@ def cpu_baseline(cfg, ws, mean_accept, n):
             "sample": f"one Jacobi iteration of {n} rows at the 7B shape after a 16-token prefill "
                       f"({dt:.2f} s), scaled by the GPU run's mean accepted length {mean_accept:.2f}",
             "iteration_s": dt}
+
+
+def calibration_copy():
+    """One device-to-device copy of 1 GiB: a kernel of known traffic, for scaling hardware byte
+    counters."""
+    import torch
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log("[bench] calibration copy: 1073741824 bytes read, 1073741824 bytes written")
+    del src, dst
 
 
 def main():
@@ -177,13 +191,7 @@ def main():
     step_gbps = (wbytes + kv_bytes) / (iter_ms / 1e3) / 1e9
 
     if args.calibrate_copy:
-        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log("[bench] calibration copy: 1073741824 bytes read, 1073741824 bytes written")
-        del src, dst
+        calibration_copy()
 
     # trajectory profile of one more (untimed) decode of the same request: fast-forwarded and
     # stationary token counts (the paper's profiling of Jacobi trajectories)
@@ -394,6 +402,8 @@ def main_loss(args):
         one_step()
     torch.cuda.synchronize()
     # the device entry point must give the host entry point's results bit for bit
+    one_call()
+    torch.cuda.synchronize()
     h = model.loss_head(t, s, ar, tg, omega, want_dw=True)
     if not (np.array_equal(kl.cpu().numpy(), h["kl"]) and np.array_equal(dw.cpu().numpy(), h["d_W"]) and
             loss.item() == h["loss"]):
@@ -428,6 +438,8 @@ def main_loss(args):
                      "achieved_gbps": round(algo[cls] / (us * 1e3), 1) if us > 0 else None}
     dom = max(kern, key=lambda k: kern[k]["avg_launch_us"])
     ach = kern[dom]["achieved_gbps"] or 0.0
+    if args.calibrate_copy:
+        calibration_copy()
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -463,7 +475,9 @@ def main_loss(args):
         "call_us": round(elapsed / calls * 1e6, 2),
         "kernels": kern,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(ach / HBM_PEAK_GBPS, 4),
+                     "traffic": measured_traffic(LOSS_SUMMARY, ("loss.hip", "device.h", "launch.h"))
+                     if dom == "loss_dw" else None,
                      "algorithmic_bytes": algo[dom], "avg_launch_us": kern[dom]["avg_launch_us"],
                      "launches": kern[dom]["launches"]},
         "cpu_baseline": cpu,

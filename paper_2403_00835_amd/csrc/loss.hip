@@ -319,7 +319,9 @@ __global__ __launch_bounds__(256) void loss_dw_mfma_kernel(const uint16_t *DT, c
     __shared__ float s_blk[4][64 * kDwLd];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int nvt = Vp / 16, nkt = d / 16, ks = rpad / 32;
-    const int vt0 = blockIdx.x * (kDwV / 16) + (w & 1) * 4, kt0 = blockIdx.y * (kDwK / 16) + (w >> 1) * 4;
+    // grid x: column blocks (fastest, so consecutive workgroups share the block of D^T through
+    // L2), y: vocabulary blocks
+    const int vt0 = blockIdx.y * (kDwV / 16) + (w & 1) * 4, kt0 = blockIdx.x * (kDwK / 16) + (w >> 1) * 4;
     const size_t pd = (size_t)Vp * rpad, ph = (size_t)d * rpad;
     f32x4 acc[4][4];
 #pragma unroll
@@ -481,7 +483,7 @@ hipError_t launch_loss_dw(bool bf16, const uint16_t *DT, const uint16_t *HT, int
         return hipErrorInvalidValue;
     if (bf16) {
         if (rpad % 32 != 0 || rpad < rows) return hipErrorInvalidValue;
-        const dim3 grid((Vp + kDwV - 1) / kDwV, (d + kDwK - 1) / kDwK);
+        const dim3 grid((d + kDwK - 1) / kDwK, (Vp + kDwV - 1) / kDwV);
         if (e0)
             hipExtLaunchKernelGGL(loss_dw_mfma_kernel, grid, dim3(256), 0, s, e0, e1, 0, DT, HT, Vp, d, rpad, V, dW);
         else

@@ -89,6 +89,8 @@ def lib():
         L.orc_prefill.argtypes = [_vp, _vp, _i32, _vp]
         L.orc_eval_block.restype = _i32
         L.orc_eval_block.argtypes = [_vp, _vp, _i32, _vp]
+        L.orc_eval_block_hidden.restype = _i32
+        L.orc_eval_block_hidden.argtypes = [_vp, _vp, _i32, _vp]
         L.orc_commit.restype = _i32
         L.orc_commit.argtypes = [_vp, _i32, _i32]
         L.orc_jacobi_step.restype = _i32
@@ -428,6 +430,17 @@ class State:
         if rc:
             raise RuntimeError(f"orc_eval_block failed: {rc}")
         return lg
+
+    def eval_block_hidden(self, block):
+        """The LM head's input rows RMSNorm(x) (.) g_final [m, d] of an iteration over block at
+        positions L .. L+m-1 (nothing committed): the rows whose products with the LM head are
+        the next-token logits of each position, the inputs of the training loss (Section 3.2.2)."""
+        b = np.ascontiguousarray(block, dtype=np.int32)
+        h = np.empty((b.size, self.model.cfg.d_model), dtype=np.float64)
+        rc = lib().orc_eval_block_hidden(self.h, _p(b), b.size, _p(h))
+        if rc:
+            raise RuntimeError(f"orc_eval_block_hidden failed: {rc}")
+        return h
 
     def commit(self, a, pending):
         rc = lib().orc_commit(self.h, int(a), int(pending))

@@ -280,7 +280,10 @@ static void linear(const double *a, int32_t rows, const float *W, int32_t in, in
  * Row i attends to cache positions 0 .. pos0+i; its own key and value are written to the
  * cache at position pos0+i first (this is the causal mask over the block, Section 3.1).
  * logits: m x vocab (may be NULL when only the cache is wanted). */
-static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t pos0, double *logits) {
+/* Forward of m tokens at positions pos0..pos0+m-1 over the cache; writes the rows' logits
+ * (m x vocab) and, if hidden is not NULL, the LM head's input rows RMSNorm(x) (.) g_final
+ * (m x d_model). */
+static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t pos0, double *logits, double *hidden) {
     const orc_model *M = st->m;
     const orc_config *c = &M->c;
     int32_t d = c->d_model, F = c->ffn_dim, H = c->n_heads, hd = c->head_dim, V = c->vocab;
@@ -344,11 +347,16 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         linear(g, m, M->wd[l], F, d, y);
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
     }
-    if (logits) {
+    if (logits || hidden) {
         for (int32_t i = 0; i < m; ++i)
             norm_operand(h + (size_t)i * d, d, M->final_norm, c->rms_eps, a + (size_t)i * d, inv + i);
-        linear(a, m, M->lm_head, d, V, logits);
-        scale_rows(logits, m, V, inv);
+        if (hidden)
+            for (int32_t i = 0; i < m; ++i)
+                for (int32_t k = 0; k < d; ++k) hidden[(size_t)i * d + k] = a[(size_t)i * d + k] * inv[i];
+        if (logits) {
+            linear(a, m, M->lm_head, d, V, logits);
+            scale_rows(logits, m, V, inv);
+        }
     }
     free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u); free(inv);
     return 0;
@@ -392,7 +400,7 @@ int32_t orc_prefill(orc_state *st, const int32_t *prompt, int32_t len, double *l
     if (len < 1 || len > st->max_ctx) return -1;
     double *lg = (double *)malloc(sizeof(double) * (size_t)len * c->vocab);
     if (!lg) return -2;
-    int rc = forward_rows(st, prompt, len, 0, lg);
+    int rc = forward_rows(st, prompt, len, 0, lg, NULL);
     if (rc) { free(lg); return -3; }
     const double *last = lg + (size_t)(len - 1) * c->vocab;
     int32_t y0 = orc_argmax(last, c->vocab);
@@ -409,7 +417,14 @@ int32_t orc_prefill(orc_state *st, const int32_t *prompt, int32_t len, double *l
  * block are written to the cache provisionally; nothing is committed). */
 int32_t orc_eval_block(orc_state *st, const int32_t *block, int32_t m, double *logits) {
     if (!st->prefilled || m < 1 || st->L + m > st->max_ctx) return -1;
-    return forward_rows(st, block, m, st->L, logits) ? -3 : 0;
+    return forward_rows(st, block, m, st->L, logits, NULL) ? -3 : 0;
+}
+
+/* The LM head's input rows (m x d_model) of an iteration over block[0..m) at positions
+ * L .. L+m-1 (as orc_eval_block: nothing is committed). */
+int32_t orc_eval_block_hidden(orc_state *st, const int32_t *block, int32_t m, double *hidden) {
+    if (!st->prefilled || m < 1 || st->L + m > st->max_ctx) return -1;
+    return forward_rows(st, block, m, st->L, NULL, hidden) ? -3 : 0;
 }
 
 /* Commit a accepted tokens (their cache rows become permanent) and set the pending token. */
@@ -446,7 +461,7 @@ int32_t orc_jacobi_step(orc_state *st, const int32_t *block_in, int32_t m, int32
 int32_t orc_forward_full(const orc_model *m, const int32_t *tokens, int32_t T, double *logits) {
     orc_state *st = orc_state_new(m, T);
     if (!st) return -2;
-    int rc = forward_rows(st, tokens, T, 0, logits);
+    int rc = forward_rows(st, tokens, T, 0, logits, NULL);
     orc_state_free(st);
     return rc ? -3 : 0;
 }
@@ -467,7 +482,7 @@ int32_t orc_ar_decode(const orc_model *m, const int32_t *prompt, int32_t len, in
     for (int32_t t = 0; rc == 0 && t < max_new; ++t) {
         out[t] = y;
         if (t + 1 == max_new) break;
-        if (forward_rows(st, &y, 1, st->L, lg)) { rc = -3; break; }
+        if (forward_rows(st, &y, 1, st->L, lg, NULL)) { rc = -3; break; }
         st->L += 1;
         y = orc_argmax(lg, m->c.vocab);
         if (y < 0) rc = -4;

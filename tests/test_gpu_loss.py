@@ -34,6 +34,8 @@ pytestmark = pytest.mark.gpu
 
 # fp32 head with a vocabulary that is not a multiple of the 64-column LM-head tile (1000 -> 1024)
 HEAD_F32 = ModelConfig(n_layers=1, d_model=64, n_heads=4, head_dim=16, ffn_dim=172, vocab=1000, dtype="f32")
+# bf16 head whose width is not a multiple of the dW kernel's 128-column block (192), ragged vocabulary
+HEAD_BF16 = ModelConfig(n_layers=1, d_model=192, n_heads=3, head_dim=64, ffn_dim=512, vocab=1000, dtype="bf16")
 TOLS = {"f32": 1e-4, "bf16": 1e-3}
 
 CASES = [  # (teacher/student pairs, AR rows, omega)
@@ -47,7 +49,7 @@ CASES = [  # (teacher/student pairs, AR rows, omega)
 ]
 
 
-@pytest.fixture(scope="module", params=[HEAD_F32, SMALL], ids=["f32-v1000", "small-bf16"])
+@pytest.fixture(scope="module", params=[HEAD_F32, HEAD_BF16, SMALL], ids=["f32-v1000", "bf16-d192-v1000", "small-bf16"])
 def head(request):
     from paper_2403_00835_amd import binding
     cfg = request.param

@@ -80,3 +80,27 @@ def test_gradients_match_finite_differences(seed):
             la = Tfix - np.log(np.exp(Tfix - Tfix.max(1, keepdims=True)).sum(1, keepdims=True)) - Tfix.max(1, keepdims=True)
             return (np.exp(la) * (la - lb)).sum() + om * o["nll"].sum()
         assert (Lw(Wp) - Lw(Wm)) / (2 * h) == pytest.approx(out["d_W"][v, j], rel=1e-6, abs=1e-9)
+
+
+def test_hidden_rows_are_the_lm_head_input():
+    """The oracle's LM-head input rows: their products with the LM head are the iteration's
+    logits, and each row divided by the final norm's gains has a root mean square just below 1
+    (RMSNorm with its eps)."""
+    from paper_2403_00835_amd import workload
+    from paper_2403_00835_amd.configs import TINY
+    ws = workload.make_weights(TINY)
+    g = np.linspace(0.5, 1.5, TINY.d_model).astype(np.float32)  # non-unit final gains
+    ws[-2] = g
+    m = oracle.Model(TINY, ws)
+    st = oracle.State(m, 64)
+    y0 = st.prefill(workload.make_prompt(TINY, 12, seed=3))
+    block = np.array([y0, 5, 17, 200, 3], dtype=np.int32)
+    lg = st.eval_block(block)
+    h = st.eval_block_hidden(block)
+    W = np.asarray(ws[-1], dtype=np.float64)
+    np.testing.assert_allclose(h @ W.T, lg, rtol=1e-10, atol=1e-12)
+    # rms = sqrt(ms / (ms + eps)) with ms the mean square of the residual row: just below 1
+    # (the tiny model's residual rows have ms ~ 4e-4, so eps = 1e-6 takes ~1e-3 off)
+    rms = np.sqrt(np.mean((h / g.astype(np.float64)) ** 2, axis=1))
+    assert np.all(rms < 1.0) and np.all(rms > 0.99), rms
+    assert st.L == 12  # nothing committed

@@ -287,6 +287,19 @@ cllm_status cllm_loss_head_device(cllm_ctx *ctx, const float *teacher, const flo
                                   float *row_kl, float *row_nll, float *d_student, float *d_ar, float *d_weight,
                                   double *loss);
 
+/* LM-head input rows of an iteration over block[0..m) at the slot's committed length L, without
+ * a commit: row k = RMSNorm(x_k) (.) g_final of the last layer's residual row (fp32; the rows
+ * whose products with the LM head give the next-token logits after z[0..k]). These are the rows
+ * the training loss of Section 3.2.2 takes: for a trajectory state y and its fixed point y* of
+ * one n-token block, rows 0..n-2 over y are the student rows and over y* the teacher rows (and,
+ * the fixed point being the greedy generation, also the AR rows with targets y*[1..n)). block[0]
+ * may be any token (the loss conditions on each state as given). The KV rows L..L+m-1 are
+ * written provisionally (as by a Jacobi step) and nothing else of the slot changes.
+ * rows_out: caller-owned host array of m x d_model floats. Synchronous. Errors: ERR_ARG (m
+ * outside [1, max_block], ids out of range, NULL), ERR_STATE (slot not prefilled),
+ * ERR_CAPACITY (L + m > max_ctx), ERR_OOM, ERR_DEVICE. */
+cllm_status cllm_hidden_rows(cllm_ctx *ctx, int32_t seq, const int32_t *block, int32_t m, float *rows_out);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 

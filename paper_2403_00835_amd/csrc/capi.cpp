@@ -81,6 +81,8 @@ struct cllm_ctx {
         int32_t *tg = nullptr;
         RowTab *tabs = nullptr;   // row tables of the loss GEMMs: tabs[R - 1] holds R rows (R <= 128)
         double *loss = nullptr;   // staging of the host entry point's total
+        float *hid = nullptr;     // LM-head input rows of cllm_hidden_rows
+        size_t hd_n = 0;
     } loss;
     std::vector<Slot> slot;
     bool dead = false;
@@ -228,7 +230,8 @@ cllm_status upload_packed(cllm_ctx *c, const void *host, int N, int K, int Ks, c
 struct IterShape {
     int R, nseq, maxm, nch;
     bool with_lm;
-    int lm_rt0;  // >= 0: the LM head runs only on this 64-row tile (a prefill chunk's last row)
+    int lm_rt0;         // >= 0: the LM head runs only on this 64-row tile (a prefill chunk's last row)
+    bool tail = true;   // false: the decoder layers only (no LM head, scan or commit)
 };
 
 cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev, const int32_t *stream_dev) {
@@ -340,6 +343,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         timing_events(c, CLLM_KT_GEMM_DOWN, rg, &e0, &e1);
         HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, row_tiles, dn, s, e0, e1));
     }
+    if (!sh.tail) return CLLM_OK;
 
     ScanParams sp{};
     sp.ctl = c->ctl;
@@ -1385,6 +1389,28 @@ cllm_status cllm_loss_head_device(cllm_ctx *c, const float *teacher, const float
             return fail(c, CLLM_ERR_ARG, "loss head (device): an array is not device memory of this context's GPU");
     return loss_head_enqueue(c, teacher, student, n_pairs, ar_rows, ar_targets, n_ar, omega, row_kl, row_nll,
                              d_student, d_ar, d_weight, loss);
+}
+
+cllm_status cllm_hidden_rows(cllm_ctx *c, int32_t seq, const int32_t *block, int32_t m, float *rows_out) {
+    if (!c) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
+    if (!block || !rows_out) return fail(c, CLLM_ERR_ARG, "NULL pointer");
+    if (m < 1 || m > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "m=%d outside [1, max_block]", m);
+    if (!c->slot[seq].prefilled) return fail(c, CLLM_ERR_STATE, "hidden rows before prefill (slot %d)", seq);
+    if ((s = check_ids(c, block, m))) return s;
+    if (c->slot[seq].L + m > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "L + m exceeds max_ctx");
+    auto &w = c->loss;
+    if ((s = loss_buf(c, &w.hid, &w.hd_n, (size_t)m * c->d))) return s;
+    // the decoder layers over the block at the committed length (provisional KV rows, no commit)
+    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, false))) return s;
+    IterShape sh{m, 1, m, ceil_div(c->slot[seq].L + m, kAttnChunk), false, -1};
+    sh.tail = false;
+    if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
+    HIPCHK(c, launch_hidden_rows(c->X, c->d, m, c->d, c->g_final, c->cfg.rms_eps, w.hid, c->stream));
+    HIPCHK(c, hipMemcpyAsync(rows_out, w.hid, (size_t)m * c->d * sizeof(float), hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    return CLLM_OK;
 }
 
 cllm_status cllm_seq_state(const cllm_ctx *c, int32_t seq, int32_t *committed_len, int32_t *pending) {

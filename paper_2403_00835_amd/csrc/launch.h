@@ -181,6 +181,10 @@ hipError_t launch_loss_dh_sum(const float *part, int nsplit, int rows, int d, in
 hipError_t launch_loss_dw(bool bf16, const uint16_t *DT, const uint16_t *HT, int Vp, int rpad, const float *D,
                           int rows, int ldd, const float *S0, int np, const float *R0, int d, int V, float *dW,
                           hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// LM-head input rows out[r] = x_r (.) g / sqrt(mean(x_r^2) + eps) of the residual rows X [rows][ldx]
+// (the mean in a fixed order).
+hipError_t launch_hidden_rows(const float *X, int ldx, int rows, int d, const float *g, float eps, float *out,
+                              hipStream_t s);
 // *loss = sum kl[0..np) + omega * sum nll[0..na), each in row order, in double (one thread).
 hipError_t launch_loss_total(const float *kl, int np, const float *nll, int na, float omega, double *loss,
                              hipStream_t s);

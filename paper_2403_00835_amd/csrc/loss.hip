@@ -299,6 +299,18 @@ __global__ void loss_dh_sum_kernel(const float *part, int nsplit, int n, int np_
         dA[i - np_d] = s;
 }
 
+// One workgroup per row: out = x (.) g / sqrt(mean(x^2) + eps), the LM head's input row.
+__global__ __launch_bounds__(kLossThreads) void hidden_rows_kernel(const float *X, int ldx, int d, const float *g,
+                                                                   float eps, float *out) {
+    __shared__ float s_buf[4];
+    const float *x = X + (size_t)blockIdx.x * ldx;
+    float ss = 0.f;
+    for (int k = threadIdx.x; k < d; k += kLossThreads) ss += x[k] * x[k];
+    ss = block_reduce<false>(ss, s_buf);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int k = threadIdx.x; k < d; k += kLossThreads) out[(size_t)blockIdx.x * d + k] = x[k] * g[k] * inv;
+}
+
 // *loss = sum kl + omega * sum nll, each sum in row order, in double.
 __global__ void loss_total_kernel(const float *kl, int np, const float *nll, int na, float omega, double *loss) {
     if (threadIdx.x != 0) return;
@@ -467,6 +479,13 @@ hipError_t launch_loss_dh_sum(const float *part, int nsplit, int rows, int d, in
     const int n = rows * d;
     hipExtLaunchKernelGGL(loss_dh_sum_kernel, dim3((n + 255) / 256), dim3(256), 0, s, nullptr, e1, 0, part, nsplit, n,
                           np * d, dS, dA);
+    return hipGetLastError();
+}
+
+hipError_t launch_hidden_rows(const float *X, int ldx, int rows, int d, const float *g, float eps, float *out,
+                              hipStream_t s) {
+    if (rows < 1 || d < 1 || ldx < d) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(hidden_rows_kernel, dim3(rows), dim3(kLossThreads), 0, s, X, ldx, d, g, eps, out);
     return hipGetLastError();
 }
 

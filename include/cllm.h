@@ -127,6 +127,19 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
  * Resets every sequence. Errors: ERR_ARG, ERR_DEVICE. */
 cllm_status cllm_model_set_weights(cllm_ctx *ctx, const void *const *tensors, int32_t n_tensors);
 
+/* Create a context whose weights are seeded synthetic ones drawn on the GPU (no host arrays): in
+ * the order of cllm_model_set_weights, tensor k comes from generator stream s_k: embed 1; layer
+ * l's nine tensors 1000 (l + 1) + 0..8; final_norm 2; lm_head 3. Norm gains are 1.0; every
+ * matrix element i is 0.02 x a standard normal deviate from the counter-based generator
+ * key = mix(mix(seed) ^ s_k) (mix: the SplitMix64 output function of Steele, Lea and Flood,
+ * OOPSLA 2014): the Box-Muller pair j = i / 2 takes b1 = mix(key ^ 2j), b2 = mix(key ^ (2j + 1)),
+ * u1 = ((b1 >> 11) + 1) 2^-53, u2 = (b2 >> 11) 2^-53, r = sqrt(-2 ln u1), element 2j gets
+ * r cos(2 pi u2) and element 2j + 1 gets r sin(2 pi u2), in double; scaled, rounded to fp32 and,
+ * for a bf16 model, to bf16 (both nearest even). Errors: those of cllm_model_create, ERR_OOM,
+ * ERR_DEVICE. */
+cllm_status cllm_model_init_random(const cllm_config *cfg, uint64_t seed, const cllm_runtime_opts *opts,
+                                   cllm_ctx **out);
+
 /* Create a context from a weight file: a 64-byte header (magic "CLLMWTS1", int32 version 1,
  * then the cllm_config fields in order, zero padding) followed by the tensors of
  * cllm_model_set_weights in order, little-endian, no gaps.

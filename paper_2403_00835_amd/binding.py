@@ -51,7 +51,7 @@ class cllm_trace_stats(ctypes.Structure):
 
 TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
 
-EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_load", "cllm_model_free", "cllm_prefill",
+EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_init_random", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
            "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_loss_head_device", "cllm_hidden_rows", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
@@ -78,6 +78,7 @@ def lib():
         L.cllm_model_create.argtypes = [P(cllm_config), P(cllm_runtime_opts), P(_vp)]
         L.cllm_model_set_weights.argtypes = [_vp, _vp, _i32]
         L.cllm_model_load.argtypes = [ctypes.c_char_p, P(cllm_runtime_opts), P(_vp)]
+        L.cllm_model_init_random.argtypes = [P(cllm_config), _u64, P(cllm_runtime_opts), P(_vp)]
         L.cllm_model_free.argtypes = [_vp]
         L.cllm_model_free.restype = None
         L.cllm_prefill.argtypes = [_vp, _i32, _vp, _i32, P(_i32)]
@@ -137,7 +138,9 @@ class Model:
     """One context of libcllm.so: model weights, KV cache and workspace on one GPU."""
 
     def __init__(self, cfg: ModelConfig, max_ctx, max_block=16, max_new=256, device=0, stream=None,
-                 weights=None, path=None, max_batch=1):
+                 weights=None, path=None, max_batch=1, random_seed=None):
+        """weights: host tensors (cllm_model_set_weights); path: a weight file (cllm_model_load);
+        random_seed: seeded synthetic weights drawn on the GPU (cllm_model_init_random)."""
         self.cfg = cfg
         self.L = lib()
         self.max_block = max_block
@@ -146,6 +149,9 @@ class Model:
         h = _vp()
         if path is not None:
             st = self.L.cllm_model_load(os.fsencode(path), ctypes.byref(opts), ctypes.byref(h))
+        elif random_seed is not None:
+            st = self.L.cllm_model_init_random(ctypes.byref(make_config(cfg)), int(random_seed), ctypes.byref(opts),
+                                               ctypes.byref(h))
         else:
             st = self.L.cllm_model_create(ctypes.byref(make_config(cfg)), ctypes.byref(opts), ctypes.byref(h))
         if st != CLLM_OK:

@@ -207,17 +207,17 @@ std::vector<int32_t> plain_perm(int rows_padded, int rows) {
     return p;
 }
 
-// Upload one logical [N][K] matrix (host) and repack it into tiles.
-// Ks is the k-step count of the packed layout (K rounded up; the padding is zero).
-cllm_status upload_packed(cllm_ctx *c, const void *host, int N, int K, int Ks, const std::vector<int32_t> &perm,
-                          uint8_t **dst, void *staging, int32_t *perm_dev) {
+// Packs the row-major [N][K] matrix in `staging` into the streaming layout at *dst (perm: the
+// logical row of each packed row, -1 = zero). Ks is the k-step count of the packed layout (K
+// rounded up; the padding is zero).
+cllm_status pack_staged(cllm_ctx *c, int K, int Ks, const std::vector<int32_t> &perm, uint8_t **dst, void *staging,
+                        int32_t *perm_dev) {
     const int n_tiles = (int)perm.size() / 16;
     const size_t bytes = (size_t)n_tiles * Ks * kTileBytes;
     if (!*dst) {
         cllm_status s = dalloc(c, reinterpret_cast<void **>(dst), bytes);
         if (s) return s;
     }
-    HIPCHK(c, hipMemcpyAsync(staging, host, (size_t)N * K * c->elem, hipMemcpyHostToDevice, c->stream));
     HIPCHK(c, hipMemcpyAsync(perm_dev, perm.data(), perm.size() * sizeof(int32_t), hipMemcpyHostToDevice, c->stream));
     HIPCHK(c, launch_repack(c->bf16, staging, perm_dev, K, Ks, n_tiles, *dst, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));  // staging and perm are reused
@@ -821,6 +821,108 @@ cllm_status loss_head_enqueue(cllm_ctx *c, const float *T, const float *S, int P
     if (loss) HIPCHK(c, launch_loss_total(kl, P, nll, A, omega, loss, st));
     return CLLM_OK;
 }
+
+// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014): the host side of the weight
+// generator's keys and the collection's augmentation draws.
+uint64_t splitmix64(uint64_t x) {
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+
+// Where the weight tensors come from: host arrays in the order of cllm_model_set_weights, or
+// (host == NULL) the seeded generator, drawn on the device.
+struct WeightSource {
+    const void *const *host;
+    uint64_t seed;
+};
+
+// Generator stream of tensor idx (the order of cllm_model_set_weights) and whether it is a norm
+// gain (1.0) rather than a N(0, 0.02) matrix.
+void tensor_stream(int NL, int idx, uint64_t *stream, bool *gain) {
+    if (idx == 0) {
+        *stream = 1, *gain = false;
+    } else if (idx == 1 + 9 * NL) {
+        *stream = 2, *gain = true;
+    } else if (idx == 2 + 9 * NL) {
+        *stream = 3, *gain = false;
+    } else {
+        const int l = (idx - 1) / 9, t = (idx - 1) % 9;
+        *stream = 1000ull * (uint64_t)(l + 1) + (uint64_t)t;
+        *gain = t == 0 || t == 5;
+    }
+}
+
+// Writes tensor idx (elems elements: float for gains, the model's element type otherwise) to
+// device memory dst, from the host array or from the generator.
+cllm_status put_tensor(cllm_ctx *c, const WeightSource &src, int idx, void *dst, size_t elems) {
+    uint64_t stream;
+    bool gain;
+    tensor_stream(c->NL, idx, &stream, &gain);
+    if (src.host) {
+        HIPCHK(c, hipMemcpyAsync(dst, src.host[idx], elems * (gain ? 4 : c->elem), hipMemcpyHostToDevice, c->stream));
+        return CLLM_OK;
+    }
+    const uint64_t key = splitmix64(splitmix64(src.seed) ^ stream);
+    HIPCHK(c, launch_fill_weights(gain ? 2 : (c->bf16 ? 1 : 0), key, kWeightStd, elems, dst, c->stream));
+    return CLLM_OK;
+}
+
+// Every weight of the model: copied or drawn into place (embedding, norm gains) or into a staging
+// buffer and repacked into the streaming layout (the products' matrices).
+cllm_status load_weights(cllm_ctx *c, const WeightSource &src) {
+    c->loss.wt_ok = false;  // the loss head's transposed LM head is rebuilt on its next call
+    const int d = c->d, F = c->F, V = c->V;
+    const size_t E = c->elem;
+    size_t stage_elems = std::max({(size_t)3 * d * d, (size_t)2 * F * d, (size_t)V * d});
+    uint8_t *staging = nullptr;
+    int32_t *perm_dev = nullptr;
+    if (hipMalloc(reinterpret_cast<void **>(&staging), stage_elems * E) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(c, CLLM_ERR_OOM, "staging allocation failed");
+    }
+    const size_t perm_max = std::max({(size_t)3 * d, (size_t)2 * c->Fp, (size_t)round_up(V, 16 * kLmTiles)});
+    if (hipMalloc(reinterpret_cast<void **>(&perm_dev), perm_max * 4) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(staging);
+        return fail(c, CLLM_ERR_OOM, "staging allocation failed");
+    }
+    cllm_status s = CLLM_OK;
+    const std::vector<int32_t> pq = qkv_perm(c), pgu = gate_up_perm(c), pd = plain_perm(d, d),
+                               plm = plain_perm(round_up(V, 16 * kLmTiles), V);
+    c->streamed_bytes = 0;
+    const size_t dd = (size_t)d * d, fd = (size_t)F * d;
+    do {
+        if ((s = put_tensor(c, src, 0, c->embed, (size_t)V * d))) break;
+        for (int l = 0; l < c->NL && !s; ++l) {
+            const int t = 1 + 9 * l;
+            if ((s = put_tensor(c, src, t, c->g_attn[l], d))) break;
+            for (int k = 0; k < 3 && !s; ++k) s = put_tensor(c, src, t + 1 + k, staging + k * dd * E, dd);  // [q; k; v]
+            if (s || (s = pack_staged(c, d, c->ks_d, pq, &c->w_qkv[l], staging, perm_dev))) break;
+            if ((s = put_tensor(c, src, t + 4, staging, dd)) || (s = pack_staged(c, d, c->ks_d, pd, &c->w_o[l], staging, perm_dev)))
+                break;
+            if ((s = put_tensor(c, src, t + 5, c->g_ffn[l], d))) break;
+            if ((s = put_tensor(c, src, t + 6, staging, fd)) || (s = put_tensor(c, src, t + 7, staging + fd * E, fd)) ||
+                (s = pack_staged(c, d, c->ks_d, pgu, &c->w_gu[l], staging, perm_dev)))
+                break;
+            if ((s = put_tensor(c, src, t + 8, staging, fd)) || (s = pack_staged(c, F, c->ks_f, pd, &c->w_d[l], staging, perm_dev)))
+                break;
+        }
+        if (s) break;
+        if ((s = put_tensor(c, src, 1 + 9 * c->NL, c->g_final, d))) break;
+        if ((s = put_tensor(c, src, 2 + 9 * c->NL, staging, (size_t)V * d)) ||
+            (s = pack_staged(c, d, c->ks_d, plm, &c->w_lm, staging, perm_dev)))
+            break;
+    } while (0);
+    hipError_t e = hipStreamSynchronize(c->stream);
+    (void)hipFree(staging);
+    (void)hipFree(perm_dev);
+    if (s) return s;
+    if (e != hipSuccess) return fail(c, CLLM_ERR_DEVICE, "weight upload failed: %s", hipGetErrorString(e));
+    for (auto &q : c->slot) q = cllm_ctx::Slot{};
+    return CLLM_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -986,61 +1088,19 @@ cllm_status cllm_model_set_weights(cllm_ctx *c, const void *const *tensors, int3
     if (!tensors || n_tensors != 3 + 9 * c->NL) return fail(c, CLLM_ERR_ARG, "expected %d tensors", 3 + 9 * c->NL);
     for (int i = 0; i < n_tensors; ++i)
         if (!tensors[i]) return fail(c, CLLM_ERR_ARG, "tensor %d is NULL", i);
-    c->loss.wt_ok = false;  // the loss head's transposed LM head is rebuilt on its next call
-    const int d = c->d, F = c->F, V = c->V;
-    const size_t E = c->elem;
-    size_t stage_elems = std::max({(size_t)3 * d * d, (size_t)2 * F * d, (size_t)V * d});
-    void *staging = nullptr;
-    int32_t *perm_dev = nullptr;
-    if (hipMalloc(&staging, stage_elems * E) != hipSuccess) {
-        (void)hipGetLastError();
-        return fail(c, CLLM_ERR_OOM, "staging allocation failed");
-    }
-    const size_t perm_max = std::max({(size_t)3 * d, (size_t)2 * c->Fp, (size_t)round_up(V, 16 * kLmTiles)});
-    if (hipMalloc(reinterpret_cast<void **>(&perm_dev), perm_max * 4) != hipSuccess) {
-        (void)hipGetLastError();
-        (void)hipFree(staging);
-        return fail(c, CLLM_ERR_OOM, "staging allocation failed");
-    }
-    std::vector<uint8_t> cat;
-    cllm_status s = CLLM_OK;
-    auto gain = [&](float *dst, const void *src) -> cllm_status {
-        HIPCHK(c, hipMemcpyAsync(dst, src, (size_t)d * 4, hipMemcpyHostToDevice, c->stream));
-        return CLLM_OK;
-    };
-    const std::vector<int32_t> pq = qkv_perm(c), pgu = gate_up_perm(c), pd = plain_perm(d, d),
-                               plm = plain_perm(round_up(V, 16 * kLmTiles), V);
-    c->streamed_bytes = 0;
-    do {
-        if (hipMemcpyAsync(c->embed, tensors[0], (size_t)V * d * E, hipMemcpyHostToDevice, c->stream) != hipSuccess) {
-            s = fail(c, CLLM_ERR_DEVICE, "embedding upload failed");
-            break;
-        }
-        for (int l = 0; l < c->NL && !s; ++l) {
-            const void *const *t = tensors + 1 + 9 * l;
-            if ((s = gain(c->g_attn[l], t[0]))) break;
-            cat.resize((size_t)3 * d * d * E);
-            for (int k = 0; k < 3; ++k) memcpy(cat.data() + (size_t)k * d * d * E, t[1 + k], (size_t)d * d * E);
-            if ((s = upload_packed(c, cat.data(), 3 * d, d, c->ks_d, pq, &c->w_qkv[l], staging, perm_dev))) break;
-            if ((s = upload_packed(c, t[4], d, d, c->ks_d, pd, &c->w_o[l], staging, perm_dev))) break;
-            if ((s = gain(c->g_ffn[l], t[5]))) break;
-            cat.resize((size_t)2 * F * d * E);
-            memcpy(cat.data(), t[6], (size_t)F * d * E);
-            memcpy(cat.data() + (size_t)F * d * E, t[7], (size_t)F * d * E);
-            if ((s = upload_packed(c, cat.data(), 2 * F, d, c->ks_d, pgu, &c->w_gu[l], staging, perm_dev))) break;
-            if ((s = upload_packed(c, t[8], d, F, c->ks_f, pd, &c->w_d[l], staging, perm_dev))) break;
-        }
-        if (s) break;
-        if ((s = gain(c->g_final, tensors[1 + 9 * c->NL]))) break;
-        if ((s = upload_packed(c, tensors[2 + 9 * c->NL], V, d, c->ks_d, plm, &c->w_lm, staging, perm_dev))) break;
-    } while (0);
-    hipError_t e = hipStreamSynchronize(c->stream);
-    (void)hipFree(staging);
-    (void)hipFree(perm_dev);
+    return load_weights(c, WeightSource{tensors, 0});
+}
+
+cllm_status cllm_model_init_random(const cllm_config *cfg, uint64_t seed, const cllm_runtime_opts *opts,
+                                   cllm_ctx **out) {
+    if (!out) return CLLM_ERR_ARG;
+    cllm_status s = cllm_model_create(cfg, opts, out);
     if (s) return s;
-    if (e != hipSuccess) return fail(c, CLLM_ERR_DEVICE, "weight upload failed: %s", hipGetErrorString(e));
-    for (auto &q : c->slot) q = cllm_ctx::Slot{};
-    return CLLM_OK;
+    if ((s = load_weights(*out, WeightSource{nullptr, seed}))) {
+        cllm_model_free(*out);
+        *out = nullptr;
+    }
+    return s;
 }
 
 cllm_status cllm_model_load(const char *path, const cllm_runtime_opts *opts, cllm_ctx **out) {
@@ -1275,17 +1335,6 @@ cllm_status cllm_trace_count(const int32_t *records, int64_t n_records, const in
     out->stationary_per_window = out->windows ? (double)stationary / (double)out->windows : 0.0;
     return CLLM_OK;
 }
-
-namespace {
-// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014): the collection's
-// augmentation draws on the host.
-uint64_t splitmix64(uint64_t x) {
-    x += 0x9E3779B97F4A7C15ull;
-    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
-    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
-    return x ^ (x >> 31);
-}
-}  // namespace
 
 cllm_status cllm_collect_states(const int32_t *records, int64_t n_records, const int32_t *tokens, int64_t n_tokens,
                                 int32_t n, double rate, uint64_t seed, int32_t *states, int32_t *augmented,

@@ -1294,6 +1294,34 @@ hipError_t launch_plan(const PlanParams &p, hipStream_t s) {
     return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void fill_weights_kernel(int kind, uint64_t key, double stdv, size_t n, void *out) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+        if (kind == 2) {
+            static_cast<float *>(out)[i] = 1.0f;
+            continue;
+        }
+        const uint64_t j = i >> 1;
+        const uint64_t b1 = mix64(key ^ (2 * j)), b2 = mix64(key ^ (2 * j + 1));
+        const double u1 = ((double)(b1 >> 11) + 1.0) * 0x1.0p-53;
+        const double u2 = (double)(b2 >> 11) * 0x1.0p-53;
+        const double r = sqrt(-2.0 * log(u1));
+        const double a = 6.283185307179586476925286766559 * u2;
+        const float x = (float)(stdv * ((i & 1) ? r * sin(a) : r * cos(a)));
+        if (kind == 1)
+            static_cast<uint16_t *>(out)[i] = f2bf(x);
+        else
+            static_cast<float *>(out)[i] = x;
+    }
+}
+
+hipError_t launch_fill_weights(int kind, uint64_t key, double stdv, size_t n, void *out, hipStream_t s) {
+    if (kind < 0 || kind > 2 || !out) return hipErrorInvalidValue;
+    if (n == 0) return hipSuccess;
+    const size_t blocks = std::min<size_t>((n + 255) / 256, 65536);
+    hipLaunchKernelGGL(fill_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s, kind, key, stdv, n, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_repack(bool bf16, const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst,
                          hipStream_t s) {
     const size_t tiles = (size_t)n_tiles * Ks;

@@ -189,6 +189,14 @@ hipError_t launch_hidden_rows(const float *X, int ldx, int rows, int d, const fl
 hipError_t launch_loss_total(const float *kl, int np, const float *nll, int na, float omega, double *loss,
                              hipStream_t s);
 
+// Seeded synthetic weights, drawn in place: kind 2 fills n floats with 1.0 (norm gains); kinds
+// 0 (float) and 1 (bf16) fill n elements with std x a standard normal deviate: for element i,
+// the Box-Muller pair j = i / 2 of the counter-based draws mix(key ^ 2j), mix(key ^ (2j + 1))
+// (mix: SplitMix64's output function; u1 = (top 53 bits + 1) 2^-53, u2 = top 53 bits x 2^-53;
+// r = sqrt(-2 ln u1); even i takes r cos(2 pi u2), odd i r sin(2 pi u2)), in double, rounded to
+// fp32 and then (kind 1) to bf16, nearest even.
+constexpr double kWeightStd = 0.02;
+hipError_t launch_fill_weights(int kind, uint64_t key, double stdv, size_t n, void *out, hipStream_t s);
 hipError_t launch_repack(bool bf16, const void *src, const int32_t *perm, int K, int Ks, int n_tiles, uint8_t *dst,
                          hipStream_t s);
 

@@ -292,9 +292,12 @@ cllm_status cllm_loss_head(cllm_ctx *ctx, const float *teacher, const float *stu
  * alive and unmodified until then. loss may be NULL (no total). Sizes are not checked beyond the
  * row counts: each array must hold its rows. A target outside [0, V) cannot be checked on the
  * host here: that AR row's row_nll and gradient row, and every d_weight entry it reaches, are
- * NaN. Calls on one context share its workspace and must be ordered by its stream. Errors:
- * ERR_ARG (n_pairs + n_ar outside [1, 64], null or inaccessible arrays), ERR_STATE, ERR_OOM
- * (workspace growth, the only allocation), ERR_DEVICE. */
+ * NaN. Calls on one context share its workspace and must be ordered by its stream. The first
+ * call after the weights are set also builds the LM head's transposed copy (Vp x d elements of
+ * workspace, kept until the context is freed); a call with more rows than any before grows the
+ * workspace, and freeing the old buffers waits for the device. Errors: ERR_ARG (n_pairs + n_ar
+ * outside [1, 64], null or inaccessible arrays), ERR_STATE, ERR_OOM (workspace growth, the only
+ * allocation), ERR_DEVICE. */
 cllm_status cllm_loss_head_device(cllm_ctx *ctx, const float *teacher, const float *student, int32_t n_pairs,
                                   const float *ar_rows, const int32_t *ar_targets, int32_t n_ar, float omega,
                                   float *row_kl, float *row_nll, float *d_student, float *d_ar, float *d_weight,

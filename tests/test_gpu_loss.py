@@ -46,6 +46,8 @@ CASES = [  # (teacher/student pairs, AR rows, omega)
     (0, 1, 0.5),
     (40, 24, 1.0),    # 64 loss rows, 104 GEMM rows: two 64-row tiles
     (16, 16, 0.0),    # omega 0: the AR rows are reported but carry no gradient
+    (64, 0, 1.0),     # the most pairs: 128 GEMM rows, two full row tiles
+    (0, 64, 1.0),     # the most AR rows
 ]
 
 

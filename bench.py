@@ -41,7 +41,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash(files=("kernels.hip", "device.h", "launch.h")):
+GEMM_SOURCES = ("gemm.hip", "gemm.h", "device.h")  # everything the streaming GEMM's code depends on
+
+
+def kernel_source_hash(files=GEMM_SOURCES):
     h = hashlib.sha256()
     for f in files:
         with open(os.path.join(ROOT, "paper_2403_00835_amd", "csrc", f), "rb") as fh:
@@ -49,7 +52,7 @@ def kernel_source_hash(files=("kernels.hip", "device.h", "launch.h")):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(summary=TRAFFIC_SUMMARY, files=("kernels.hip", "device.h", "launch.h")):
+def measured_traffic(summary=TRAFFIC_SUMMARY, files=GEMM_SOURCES):
     """HBM bytes per launch of a kernel from a committed rocprofv3 counter summary, if it was
     taken on the current source of `files`; otherwise None."""
     if not os.path.exists(summary):

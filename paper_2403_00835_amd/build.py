@@ -15,7 +15,7 @@ ARCH = "gfx950"
 # Packed-fp32 VALU instructions are kept out of generated code (build flags).
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I" + INCLUDE]
-SOURCES = ["kernels.hip", "loss.hip", "capi.cpp"]
+SOURCES = ["gemm.hip", "kernels.hip", "loss.hip", "capi.cpp"]
 
 
 def _run(cmd, verbose):
@@ -41,10 +41,11 @@ def build(verbose=False):
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
-    # standalone GEMM driver (per-kernel timing, hardware byte counters): links the kernels object
+    # standalone GEMM driver (per-kernel timing, hardware byte counters): links the GEMM object
     kb_obj = os.path.join(objdir, "kernel_bench.hip.o")
     _run([HIPCC, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "kernel_bench.hip"), "-o", kb_obj], verbose)
-    _run([HIPCC, "--offload-arch=" + ARCH, kb_obj, objs[0], "-o", KERNEL_BENCH + ".tmp"], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH, kb_obj, objs[SOURCES.index("gemm.hip")], "-o", KERNEL_BENCH + ".tmp"],
+         verbose)
     os.replace(KERNEL_BENCH + ".tmp", KERNEL_BENCH)
     from . import workload
     workload.build(verbose)

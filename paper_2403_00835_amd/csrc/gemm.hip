@@ -1,0 +1,430 @@
+// Weight-streaming GEMM of libcllm.so on gfx950 (CDNA4): the products of a Jacobi iteration
+// (QKV, O, gate/up, down, LM head) with their fused epilogues, and the fp32-output product of
+// the training loss head.
+#include <hip/hip_ext.h>
+
+#include <type_traits>
+
+#include "device.h"
+#include "launch.h"
+
+namespace cllm {
+
+// ------------------------------------------------------------------------------------------
+// Weight-streaming GEMM:  Y[rows x N] = A[rows x K] * W^T,  W packed in 1 KiB tiles.
+//
+// Packed layout: tile (t, s) covers weight rows 16t .. 16t+15 (after the per-GEMM row order)
+// and K indices s*KSTEP .. s*KSTEP+KSTEP-1; lane l's 16 bytes are row 16t + l%16, K indices
+// s*KSTEP + (l/16)*VEC .. +VEC. Tiles are stored k-step major: tile (t, s) at index s * T + t
+// (T tiles per k-step), so the tiles every workgroup reads for one k-step are one contiguous
+// region (measured 1-7% faster streaming than row blocks contiguous over s).
+//
+// A workgroup of 8 waves owns NT consecutive tiles (16*NT output columns) for all rows; wave w
+// takes k-steps w, w+8, w+16, ... and accumulates them in order with MFMA; the 8 partial tiles
+// are then summed in a fixed tree ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)). Weights are read once,
+// straight into registers (no LDS); the activation rows (a few KiB, L2-resident) are re-read.
+// In bf16 the activations are fp32 values split into hi and lo bf16 planes, and each k-step runs
+// one MFMA per plane against the same weight tile: products are exact in fp32, so the operand
+// keeps 16 significant bits instead of bf16's 8.
+//
+// Products that follow an RMSNorm take the operand x (.) g written by the producer of x and
+// scale each output row by 1/sqrt(mean(x^2) + eps), reduced from the producer's per-16-column
+// sums of squares.
+// ------------------------------------------------------------------------------------------
+
+enum Epi { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_ARGMAX = 3, E_LOGITS = 4 };
+
+template <Prec P, int NT, int RG>
+struct Stage {  // operands of one k-step
+    u32x4 b[NT];                      // weight tiles
+    u32x4 a[PrecT<P>::PLANES][RG];    // activation rows (hi, lo planes for bf16)
+};
+
+// Loads of one k-step s (callers clamp s into [0, Ks), so every load is issued and the compiler
+// can count outstanding loads exactly). Tiles past the last one (a ragged last workgroup) load
+// the last tile again; their columns are never written. SHARED: the weight tiles are read by
+// several workgroups (the row tiles of one column group), so they are loaded as ordinary
+// (cached) loads; otherwise they are streamed (nontemporal: read once, not kept in the caches).
+template <Prec P, int NT, int RG, bool SHARED>
+__device__ __forceinline__ void gemm_load(Stage<P, NT, RG> &st, const GemmParams &p, int t0, int rg0, int s, int lane) {
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    const int tiles = p.cols >> 4;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const u32x4 *src =
+            reinterpret_cast<const u32x4 *>(p.W + ((size_t)s * tiles + min(t0 + j, tiles - 1)) * kTileBytes) + lane;
+        st.b[j] = SHARED ? *src : __builtin_nontemporal_load(src);
+    }
+    const T *A = reinterpret_cast<const T *>(p.A);
+    const int ks_a = p.lda / PT::KSTEP;
+#pragma unroll
+    for (int pl = 0; pl < PT::PLANES; ++pl)
+#pragma unroll
+        for (int r = 0; r < RG; ++r)
+            st.a[pl][r] = *reinterpret_cast<const u32x4 *>(A + pl * act_plane(p.rr.cap, p.lda) +
+                                                          ((size_t)((rg0 + r) * ks_a + s) * kWave + lane) * PT::VEC);
+}
+
+// MFMAs of one k-step: every hi-plane product, then every lo-plane product (bf16).
+template <Prec P, int NT, int RG>
+__device__ __forceinline__ void gemm_compute(const Stage<P, NT, RG> &st, f32x4 (&acc)[RG][NT]) {
+#pragma unroll
+    for (int pl = 0; pl < PrecT<P>::PLANES; ++pl)
+#pragma unroll
+        for (int r = 0; r < RG; ++r)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) acc[r][j] = mfma_kstep<P>(st.a[pl][r], st.b[j], acc[r][j]);
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+
+// Row factor 1/sqrt(mean(x^2) + eps) of the rows [row0, row0 + ROWS) from the producer's
+// per-16-column sums of squares (layout [row][T], T a multiple of 4). 32 threads per row each add
+// a contiguous run of q = 4 * ceil(T/128) partials in order (16-byte reads), then a fixed xor tree
+// over the row's 32 threads; the scheme depends only on T, never on the number of rows. The
+// first two vectors of the first row pass are requested early by row_factor_preload. The caller's
+// next barrier publishes s_inv.
+template <int W>
+__device__ __forceinline__ void row_factor_preload(const GemmParams &p, int row0, int tid, f32x4 (&sq_pre)[2]) {
+    const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
+    const float *src = p.ssq + (size_t)(row0 + (tid >> 5)) * p.T;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)  // clamped, unconditional
+        sq_pre[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + 4 * i, p.T - 4));
+}
+
+template <int W, int ROWS>
+__device__ __forceinline__ void row_factor_reduce(const GemmParams &p, int row0, int tid, const f32x4 (&sq_pre)[2],
+                                                  float *s_inv) {
+    constexpr int RPP = W * kWave / 32;  // rows per pass
+    static_assert(ROWS % RPP == 0, "row passes cover the row groups");
+    const int sq_part = tid & 31, sq_q = ((p.T + 127) >> 7) << 2;
+    for (int pass = 0; pass < ROWS / RPP; ++pass) {
+        const int row = pass * RPP + (tid >> 5);
+        const float *src = p.ssq + (size_t)(row0 + row) * p.T;
+        float sum = 0.0f;
+        for (int i0 = 0; i0 < sq_q; i0 += 8) {
+            f32x4 v[2];
+            if (pass == 0 && i0 == 0) {
+                v[0] = sq_pre[0];
+                v[1] = sq_pre[1];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    v[i] = *reinterpret_cast<const f32x4 *>(src + min(sq_part * sq_q + i0 + 4 * i, p.T - 4));
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (i0 + i < sq_q && sq_part * sq_q + i0 + i < p.T) sum += v[i >> 2][i & 3];
+        }
+#pragma unroll
+        for (int off = 16; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 32);
+        if (sq_part == 0) s_inv[row] = 1.0f / sqrtf(sum / (float)p.K + p.eps);
+    }
+}
+
+// Epilogues of a finished ROWS x COLS output tile in s_tile (row stride COLS + 1) for rows
+// [row0, row0 + ROWS) of the iteration (m of them live) and column workgroup wg of width COLS
+// (columns at or past p.cols, in a ragged last workgroup, are dropped); s_red is scratch of at
+// least ROWS x COLS floats.
+template <Prec P, int NT, int RG, int EP, int W>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile, float *s_red, int row0, int m, int wg,
+                                              int tid, int lane, int w) {
+    using T = typename PrecT<P>::T;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const int t0 = wg * NT;
+    if constexpr (EP == E_QKV) {
+        // Packed columns -> (section, head, dim). Tile b of a head holds dims [8b, 8b+8) and
+        // their rotate-half partners [hd/2+8b, hd/2+8b+8): column o of the tile and column o ^ 8
+        // are partners, so every tile is complete for RoPE and a workgroup may own any number
+        // of tiles.
+        const int hd = p.hd, d = p.d, h2 = hd >> 1;
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
+            const int row = idx / COLS, pc = idx % COLS;
+            const int R = t0 * 16 + pc;  // packed row index
+            if (row >= m || R >= p.cols) continue;
+            const int sec = R / d, within = R % d, head = within / hd;
+            const int q = within % hd, b = q >> 4, o = q & 15;
+            const int dim = o < 8 ? 8 * b + o : h2 + 8 * b + (o - 8);
+            const int partner = pc ^ 8;
+            const RowInfo ri = p.rr.rows[row0 + row];
+            const int pos = ri.pos;
+            const size_t kvo = (size_t)p.rr.tab->seq[ri.b] * p.kv_seq;  // this row's sequence slot
+            float x = s_tile[row * (COLS + 1) + pc];
+            if (sec < 2) {
+                const float y = s_tile[row * (COLS + 1) + partner];
+                const int j = dim < h2 ? dim : dim - h2;
+                const float c = p.rcos[(size_t)pos * h2 + j], s = p.rsin[(size_t)pos * h2 + j];
+                x = dim < h2 ? (x * c - y * s) : (x * c + y * s);
+            }
+            const T e = to_elem<P>(x);  // cached keys and values are rounded to the cache dtype
+            if (sec == 0)
+                put_act<P>(reinterpret_cast<T *>(p.Q), act_plane(p.rr.cap, d), act_idx<P>(row0 + row, head * hd + dim, d), x);
+            else if (sec == 1)
+                reinterpret_cast<T *>(p.Kc)[kvo + (size_t)head * p.ctx_alloc * hd + kcache_idx<P>(pos, dim, hd)] = e;
+            else
+                reinterpret_cast<T *>(p.Vt)[kvo + (size_t)head * p.ctx_alloc * hd + vcache_idx<P>(pos, dim, hd)] = e;
+        }
+    } else if constexpr (EP == E_RESID) {
+        // X += Y over this workgroup's columns, then the per-16-column sums of squares of the
+        // new rows (summed in column order) for the next RMSNorm.
+        const int c0 = t0 * 16;
+        float *s_sq = s_red;  // ROWS x COLS
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
+            const int row = idx / COLS, c = idx % COLS;
+            float v = 0.0f;
+            if (row < m && c0 + c < p.cols) {
+                float *xp = p.Xout + (size_t)(row0 + row) * p.ldx + c0 + c;
+                v = *xp + s_tile[row * (COLS + 1) + c];
+                *xp = v;
+                // operand of the next RMSNorm-ed product: x (.) g
+                put_act<P>(reinterpret_cast<T *>(p.An), act_plane(p.rr.cap, p.ldx),
+                           act_idx<P>(row0 + row, c0 + c, p.ldx), v * p.gain[c0 + c]);
+            }
+            s_sq[idx] = v * v;
+        }
+        __syncthreads();
+        if (tid < ROWS * NT) {
+            const int row = tid / NT, j = tid % NT;
+            if (row < m && (t0 + j) * 16 < p.cols) {
+                float sum = 0.0f;
+#pragma unroll
+                for (int c = 0; c < 16; ++c) sum += s_sq[row * COLS + 16 * j + c];
+                p.ssq_out[(size_t)(row0 + row) * p.T + t0 + j] = sum;
+            }
+        }
+    } else if constexpr (EP == E_SWIGLU) {
+        // Tiles come in (gate, up) pairs of the same 16 features.
+        static_assert(NT % 2 == 0, "gate/up epilogue pairs a gate tile with an up tile");
+        for (int idx = tid; idx < ROWS * COLS / 2; idx += W * kWave) {
+            const int row = idx / (COLS / 2), f = idx % (COLS / 2), q = f >> 4, c = f & 15;
+            if (row >= m || wg * COLS + 32 * q >= p.cols) continue;  // pair past the last column
+            const float gt = s_tile[row * (COLS + 1) + 32 * q + c];
+            const float up = s_tile[row * (COLS + 1) + 32 * q + 16 + c];
+            put_act<P>(reinterpret_cast<T *>(p.H), act_plane(p.rr.cap, p.Fp),
+                       act_idx<P>(row0 + row, wg * (COLS / 2) + f, p.Fp), silu(gt) * up);
+        }
+    } else if constexpr (EP == E_LOGITS) {
+        // Plain fp32 output rows (the loss head's logits): Zout[row][col], col < V.
+        const int c0 = t0 * 16;
+        for (int idx = tid; idx < ROWS * COLS; idx += W * kWave) {
+            const int row = idx / COLS, c = idx % COLS;
+            if (row < m && c0 + c < p.V) p.Zout[(size_t)(row0 + row) * p.ldz + c0 + c] = s_tile[row * (COLS + 1) + c];
+        }
+    } else {  // E_ARGMAX
+        // One wave per row: (max, lowest column) over this workgroup's columns < V.
+        for (int row = w; row < ROWS; row += W) {
+            if (row >= m) break;
+            float bv = -INFINITY;
+            int bi = 0x7fffffff;
+            int nan = 0;
+            for (int c = lane; c < COLS; c += kWave) {
+                const int col = t0 * 16 + c;
+                if (col < p.V) {
+                    const float v = s_tile[row * (COLS + 1) + c];
+                    if (p.dbg) p.dbg[(size_t)(row0 + row) * p.V + col] = v;
+                    if (v != v) nan = 1;
+                    else if (v > bv || (v == bv && col < bi)) { bv = v; bi = col; }
+                }
+            }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                const float ov = __shfl_xor(bv, off);
+                const int oi = __shfl_xor(bi, off);
+                nan |= __shfl_xor(nan, off);
+                if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+            }
+            if (lane == 0) {
+                p.pmax[(size_t)wg * p.rr.cap + row0 + row] = bv;
+                p.pidx[(size_t)wg * p.rr.cap + row0 + row] = nan ? -1 : bi;
+            }
+        }
+    }
+}
+
+template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
+__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
+    static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const int wg = blockIdx.x;  // column group
+    if constexpr (EP == E_LOGITS) {
+        if (p.kc > 0) {  // split K: k-steps [z kc, min((z + 1) kc, Ks)), partial products to plane z
+            const int ks0 = blockIdx.z * p.kc;
+            p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
+            p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;  // 16-byte lane vectors
+            p.Ks = min(p.kc, p.Ks - ks0);
+            p.Zout += (size_t)blockIdx.z * p.zstride;
+        }
+    }
+    // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
+    // capacity); m of them are live. A launch of one row tile (MT false) always has live rows, so
+    // nothing waits for the row count before the first loads; with several row tiles (MT) a tile
+    // with no live row exits first.
+    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T);
+    const int m = p.rr.tab->R - row0;
+    if constexpr (MT) {
+        if (m <= 0) return;
+    }
+    const int rg0 = row0 >> 4;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave index made explicitly wave-uniform, so k-step addresses live in scalar registers and
+    // every load shares one per-lane offset
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int t0 = wg * NT;
+
+    extern __shared__ float smem[];
+    float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
+    float *s_tile = s_red + W * NT * 256;  // ROWS x (COLS + 1)
+    float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
+
+    // Row factor inputs are requested before the weights (their latency overlaps the first
+    // k-step's) and reduced after the main loop.
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // This wave's k-steps (nmy of them); the first D-1 are requested first.
+    const int nmy = w < p.Ks ? (p.Ks - w + W - 1) / W : 0;
+    auto step_of = [&](int q) { return min(w + q * W, p.Ks - 1); };
+    Stage<P, NT, RG> ring[D];
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j) gemm_load<P, NT, RG, MT>(ring[j], p, t0, rg0, step_of(j), lane);
+
+    f32x4 acc[RG][NT];
+#pragma unroll
+    for (int r = 0; r < RG; ++r)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Software pipeline: a ring of D k-steps whose loads are in flight while the oldest one's
+    // MFMAs run. The steady state is branch-free (exact wait counts); the drain issues no loads
+    // past the end.
+    if (nmy > 0) {
+        // blocks of D steps whose prefetches (up to step b*D + 2D - 2) are all in range
+        const int nfull = nmy >= 2 * D - 1 ? (nmy - (D - 1)) / D : 0;
+        for (int bi = 0; bi < nfull; ++bi) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                // sched_barrier keeps the scheduler from sinking loads to their uses.
+                gemm_load<P, NT, RG, MT>(ring[(j + D - 1) % D], p, t0, rg0, step_of(bi * D + j + D - 1), lane);
+                __builtin_amdgcn_sched_barrier(0);
+                gemm_compute(ring[j], acc);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const int v0 = nfull * D;
+#pragma unroll
+        for (int j = 0; j < 2 * D - 1; ++j) {
+            const int v = v0 + j;
+            if (v < nmy) {
+                if (v + D - 1 < nmy)
+                    gemm_load<P, NT, RG, MT>(ring[(j + D - 1) % D], p, t0, rg0, step_of(v + D - 1), lane);
+                gemm_compute(ring[j % D], acc);
+            }
+        }
+    }
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+
+    // Sum of the 8 waves' partial tiles through LDS, one row group at a time, in the fixed tree
+    // ((w0+w4)+(w2+w6))+((w1+w5)+(w3+w7)); then the RMSNorm row factor.
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+            *reinterpret_cast<f32x4 *>(s_red + ((size_t)(w * NT + j) * 64 + lane) * 4) = acc[r][j];
+        __syncthreads();
+        for (int e = tid; e < NT * 256; e += W * kWave) {
+            float x[W];
+#pragma unroll
+            for (int q = 0; q < W; ++q) x[q] = s_red[(size_t)q * NT * 256 + e];
+            float sum = ((x[0] + x[4]) + (x[2] + x[6])) + ((x[1] + x[5]) + (x[3] + x[7]));
+            // element e = (tile j, lane l, register v); C layout: row 4*(l/16)+v, column l%16
+            const int j = e >> 8, l = (e >> 2) & 63, v = e & 3;
+            const int row = 16 * r + 4 * (l >> 4) + v;
+            if constexpr (ROWSCALE) sum *= s_inv[row];
+            s_tile[row * (COLS + 1) + 16 * j + (l & 15)] = sum;
+        }
+        __syncthreads();
+    }
+
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+// Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile
+// p.rt0) x K splits (E_LOGITS with p.kc > 0).
+template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves>
+static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
+    const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
+    auto kern = row_tiles > 1 ? gemm_kernel<P, NT, RG, EP, D, W, true> : gemm_kernel<P, NT, RG, EP, D, W, false>;
+    GemmParams q = p;
+    q.row_tiles = row_tiles;
+    q.n_wg = (p.cols + COLS - 1) / COLS;  // the last workgroup may be ragged
+    const int splits = EP == E_LOGITS && p.kc > 0 ? (p.Ks + p.kc - 1) / p.kc : 1;
+    if (EP != E_LOGITS && p.kc != 0) return hipErrorInvalidValue;
+    const dim3 grid(q.n_wg, row_tiles, splits);
+    if (e0 || e1) {
+        hipExtLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, e0, e1, 0, q);
+    } else {
+        hipLaunchKernelGGL(kern, grid, dim3(W * kWave), lds, s, q);
+    }
+    return hipGetLastError();
+}
+
+template <Prec P, int RG>
+static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
+                                 hipEvent_t e1) {
+    if (row_tiles > 1) {
+        // More than 64 rows (measured at 160 and 512 rows, 7B): QKV and gate/up take 96-column
+        // workgroups (two k-steps in flight), O and down 64-column workgroups (three k-steps in
+        // flight). Row tiles past the iteration's rows exit at once, so a batched iteration
+        // launched for its largest row count costs what its live rows cost.
+        switch (kind) {
+        case GEMM_QKV:
+            return launch_gemm_t<P, 6, RG, E_QKV, 2>(p, row_tiles, s, e0, e1);
+        case GEMM_O:
+        case GEMM_DOWN:
+            return launch_gemm_t<P, 4, RG, E_RESID, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_GATE_UP:
+            return launch_gemm_t<P, 6, RG, E_SWIGLU, 2>(p, row_tiles, s, e0, e1);
+        case GEMM_LM:
+            return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_LOGITS:
+            return launch_gemm_t<P, kLmTiles, RG, E_LOGITS, 3>(p, row_tiles, s, e0, e1);
+        }
+        return hipErrorInvalidValue;
+    }
+    switch (kind) {
+    case GEMM_QKV:
+        return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, row_tiles, s, e0, e1);
+    case GEMM_O:
+    case GEMM_DOWN:
+        return launch_gemm_t<P, kNtResid, RG, E_RESID>(p, row_tiles, s, e0, e1);
+    case GEMM_GATE_UP:
+        return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, row_tiles, s, e0, e1);
+    case GEMM_LM:
+        return launch_gemm_t<P, kLmTiles, RG, E_ARGMAX>(p, row_tiles, s, e0, e1);
+    case GEMM_LOGITS:
+        return launch_gemm_t<P, kLmTiles, RG, E_LOGITS>(p, row_tiles, s, e0, e1);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const GemmParams &p, hipStream_t s,
+                       hipEvent_t e0, hipEvent_t e1) {
+    if (row_tiles < 1 || (row_tiles > 1 && rg != 4)) return hipErrorInvalidValue;
+    if (bf16) {
+        if (rg == 1) return launch_gemm_rg<Prec::BF16, 1>(kind, p, row_tiles, s, e0, e1);
+        if (rg == 2) return launch_gemm_rg<Prec::BF16, 2>(kind, p, row_tiles, s, e0, e1);
+        return launch_gemm_rg<Prec::BF16, 4>(kind, p, row_tiles, s, e0, e1);
+    }
+    if (rg == 1) return launch_gemm_rg<Prec::F32, 1>(kind, p, row_tiles, s, e0, e1);
+    if (rg == 2) return launch_gemm_rg<Prec::F32, 2>(kind, p, row_tiles, s, e0, e1);
+    return launch_gemm_rg<Prec::F32, 4>(kind, p, row_tiles, s, e0, e1);
+}
+
+}  // namespace cllm

@@ -3,70 +3,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gemm.h"
+
 namespace cllm {
 
 struct Ctl;
 struct RowTab;
 struct RowInfo;
-
-constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
-constexpr int kNtQkv = 3;     // QKV (each tile holds rotate-half partners; 256 workgroups at 7B)
-constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups at 7B, one per CU)
-constexpr int kNtResid = 1;   // O and down projections
-constexpr int kGemmDepth = 2; // k-steps in flight per wave
-
-enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4, GEMM_LOGITS = 5 };
-
-// Rows of an iteration: the row table, its per-row entries and the row capacity of the
-// activation buffers (their plane size).
-struct RowsRef {
-    const RowTab *tab;
-    const RowInfo *rows;
-    int cap;
-};
-
-struct GemmParams {
-    const uint8_t *W;  // packed tiles
-    int Ks;            // k-steps per 16-row tile
-    int cols;          // packed output columns (multiple of 16; of 32 for gate/up)
-    int n_wg;          // workgroups along the columns (set by the launcher: ceil(cols / (16 NT)))
-    int rt0;           // first row tile
-    int row_tiles;     // row tiles of the launch (set by the launcher)
-    const void *A;     // activation operand, packed operand order, lda elements per row
-    int lda;
-    RowsRef rr;
-    // RMSNorm row factor (QKV, gate/up, LM head): per-16-column sums of squares [row][T]
-    const float *ssq;
-    int T, K;
-    float eps;
-    // E_QKV: Q operand; K cache [seq][layer][pos][d] and transposed V cache [seq][layer][d][pos]
-    // given for this layer of sequence slot 0, kv_seq elements apart per slot
-    void *Q, *Kc, *Vt;
-    size_t kv_seq;
-    int ctx_alloc;
-    const float *rcos, *rsin;
-    int d, hd;
-    // E_RESID: X += Y (rows of ldx floats); next RMSNorm operand An = X (.) gain; new partials
-    float *Xout, *ssq_out;
-    int ldx;
-    const float *gain;
-    void *An;
-    // E_SWIGLU
-    void *H;
-    int Fp;
-    // E_ARGMAX: per-workgroup (max, index) [workgroup][row capacity]; optional logits [row][V]
-    float *pmax;
-    int *pidx;
-    float *dbg;
-    int V;
-    // E_LOGITS (plain fp32 products, no RMSNorm row factor): Zout[row][ldz], columns < V. With
-    // kc > 0 the launch splits K: grid z takes k-steps [z kc, min((z + 1) kc, Ks)) and writes its
-    // partial products to Zout + z * zstride.
-    float *Zout;
-    int ldz;
-    int kc;
-    size_t zstride;
-};
 
 struct EmbedParams {
     const void *E;
@@ -128,8 +71,6 @@ struct PlanParams {
 
 hipError_t launch_setup(const SetupParams &p, hipStream_t s);
 
-hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const GemmParams &p, hipStream_t s,
-                       hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_embed(bool bf16, int rows, const EmbedParams &p, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_attn(bool bf16, int rg, int nch_launch, int nseq_launch, const AttnParams &p, hipStream_t s,
                        hipEvent_t e0, hipEvent_t e1);

@@ -218,3 +218,43 @@ def test_loss_head_device_bad_target_and_host_memory(head):
         m.loss_head_device(2, 3, 1.0, host_rows.ctypes.data, S, Ar, TG, kl, nll, ds, da)
     with pytest.raises(ValueError):
         m.loss_head_device(2, 3, 1.0, T, S, Ar, TG, kl, nll[:2], ds, da)  # too few rows
+
+
+def test_loss_head_7b_bench_configuration():
+    """The benchmark's configuration at full size: the LLaMA-2-7B LM head (32000 x 4096 bf16, a
+    one-layer context drawn on the device), 16 pairs + 48 AR rows through the device entry point
+    with the weight gradient; every output (per-row KL and NLL, the total, dH and all of dW)
+    against the oracle, to the bf16 bar of this file."""
+    import dataclasses
+
+    import torch
+    from paper_2403_00835_amd import binding
+    from paper_2403_00835_amd.configs import LLAMA7B
+    cfg = dataclasses.replace(LLAMA7B, n_layers=1)
+    d, V = cfg.d_model, cfg.vocab
+    P, A, omega = 16, 48, 1.0
+    log("[loss] 7B head: device-drawn context, host-drawn head for the oracle")
+    m = binding.Model(cfg, max_ctx=64, max_block=16, max_new=16, random_seed=0)
+    W = workload.as_f32(cfg, workload.make_tensor(cfg, workload.tensor_specs(cfg)[-1])).astype(np.float64)
+    t, s, ar, tg = workload.make_head_rows(cfg, P, A, seed=1)
+    T, S, Ar, TG = _dev(t), _dev(s), _dev(ar), _dev(tg)
+    kl, nll = torch.empty(P, device="cuda"), torch.empty(A, device="cuda")
+    ds, da = torch.empty(P, d, device="cuda"), torch.empty(A, d, device="cuda")
+    dw = torch.empty(V, d, device="cuda")
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    torch.cuda.synchronize()
+    m.loss_head_device(P, A, omega, T, S, Ar, TG, kl, nll, ds, da, dw, loss)
+    torch.cuda.synchronize()
+    m.close()
+    log("  oracle")
+    o = oracle.loss_head(W, t, s, ar, tg, omega)
+    tol = TOLS["bf16"]
+    e_kl = _close_rows(kl.cpu().numpy(), o["kl"], tol, "kl")
+    e_nll = _close_rows(nll.cpu().numpy(), o["nll"], tol, "nll")
+    terms = np.abs(o["kl"]).sum() + omega * np.abs(o["nll"]).sum()
+    assert abs(loss.item() - o["loss"]) <= tol * (1.0 + terms)
+    sc_s, sc_a, sc_w = _grad_scales(W, t, s, ar, tg, omega)
+    r_s = _close_array(ds.cpu().numpy(), o["d_student"], sc_s, tol, "d_student")
+    r_a = _close_array(da.cpu().numpy(), o["d_ar"], sc_a, tol, "d_ar")
+    r_w = _close_array(dw.cpu().numpy(), o["d_W"], sc_w, tol, "d_W")
+    log(f"  max err kl {e_kl:.2g} nll {e_nll:.2g}; rel grad err student {r_s:.2g} ar {r_a:.2g} W {r_w:.2g}")

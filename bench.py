@@ -196,13 +196,16 @@ def main():
     if args.calibrate_copy:
         calibration_copy()
 
-    # trajectory profile of one more (untimed) decode of the same request: fast-forwarded and
-    # stationary token counts (the paper's profiling of Jacobi trajectories)
+    # trajectory profile of one more decode of the same request (outside the timed steps):
+    # fast-forwarded and stationary token counts (the paper's profiling of Jacobi trajectories),
+    # and the recording's cost: that decode's device time against the timed decodes' mean
     model.trace_enable(True)
-    tr_out, _ = one_step()
+    tr_out, tr_st = one_step()
     traj = model.trace_read()
     model.trace_enable(False)
     tc = binding.trace_count(traj, tr_out, n, BLOCK_SHRINK)
+    if not np.array_equal(tr_out, ar):
+        raise RuntimeError("traced Jacobi output differs from greedy AR output")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -241,7 +244,9 @@ def main():
         "speedup_vs_ar": round(value / ar_tps, 3),
         "step_hbm_gbps": round(step_gbps, 1),
         "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
-        "trajectory": {"fast_forward_mean": round(tc["fast_forward_mean"], 4), "stationary": tc["stationary"],
+        "trajectory": {"decode_ms_recorded": round(tr_st["decode_ms"], 3),
+                       "decode_ms_unrecorded_mean": round(decode_ms / len(stats), 3),
+                       "fast_forward_mean": round(tc["fast_forward_mean"], 4), "stationary": tc["stationary"],
                        "blocks": tc["windows"], "stationary_per_block": round(tc["stationary_per_window"], 4)},
         "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (per layer)", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
@@ -296,6 +301,16 @@ def main_batched(args, wl):
     if not np.array_equal(out, ar):
         raise RuntimeError("batched Jacobi output differs from batched greedy AR output")
 
+    # Algorithm 1's collection of the same batch (outside the timed steps): the batched decode
+    # with trajectory recording, then each sequence's states, fixed points and augmented copies
+    # (rate 0.5); its wall-clock rate in collected states per second
+    from paper_2403_00835_amd import collect
+    torch.cuda.synchronize()
+    c0 = time.perf_counter()
+    entries = collect.collect(model, prompts, n, max_new, specs=specs, rate=0.5, seed=7)
+    coll_s = time.perf_counter() - c0
+    n_states = sum(len(e["states"]) for e in entries)
+
     tokens = args.steps * B * max_new
     value = tokens / elapsed
     iters = [max(s["steps"] for s in st) for st in stats]  # batched iterations per step
@@ -349,6 +364,8 @@ def main_batched(args, wl):
         "prefill_ms": round(prefill_ms, 3),
         "ar_tokens_per_s": round(ar_tps, 3),
         "speedup_vs_ar": round(value / ar_tps, 3),
+        "collection": {"blocks": len(entries), "states": n_states, "seconds": round(coll_s, 3),
+                       "states_per_s": round(n_states / coll_s, 1)},
         "roofline": {"bound": "mfma", "kernel": "gemm gate/up + SwiGLU (per layer), row tiles of 64",
                      "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,

@@ -52,6 +52,14 @@ def kernel_source_hash(files=GEMM_SOURCES):
     return h.hexdigest()[:16]
 
 
+def stream_ceiling():
+    """The measured streaming-read rate (GB/s) recorded in the GEMM traffic summary, or None."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    m = re.search(r"stream_read_gbps:\s*([0-9.]+)", open(TRAFFIC_SUMMARY).read())
+    return float(m.group(1)) if m else None
+
+
 def measured_traffic(summary=TRAFFIC_SUMMARY, files=GEMM_SOURCES):
     """HBM bytes per launch of a kernel from a committed rocprofv3 counter summary, if it was
     taken on the current source of `files`; otherwise None."""
@@ -65,10 +73,10 @@ def measured_traffic(summary=TRAFFIC_SUMMARY, files=GEMM_SOURCES):
     return float(m_bytes.group(1))
 
 
-def oracle_iteration_s(cfg, ws, n):
+def oracle_iteration_s(cfg, ws, n, reps=3):
     """Seconds of the oracle, as it stands, for one Jacobi iteration of n rows at this shape
     after a 16-token prefill (attention over 16 instead of several hundred keys is about 2% of
-    the iteration's work at the 7B shape)."""
+    the iteration's work at the 7B shape): the median of `reps` evaluations of the block."""
     import oracle
     from paper_2403_00835_amd import workload
     log("[bench] cpu baseline: oracle on the host")
@@ -78,11 +86,13 @@ def oracle_iteration_s(cfg, ws, n):
     prompt = workload.make_prompt(cfg, 16, seed=11)
     y0 = st.prefill(prompt)
     block = np.array([y0] + list(workload.make_prompt(cfg, n - 1, seed=12)), dtype=np.int32)
-    t0 = time.perf_counter()
-    st.eval_block(block)
-    dt = time.perf_counter() - t0
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        st.eval_block(block)
+        times.append(time.perf_counter() - t0)
     del om, tensors
-    return dt, oracle.num_threads()
+    return float(np.median(times)), oracle.num_threads()
 
 
 def cpu_baseline(cfg, ws, mean_accept, n):
@@ -90,7 +100,8 @@ def cpu_baseline(cfg, ws, mean_accept, n):
     dt, cores = oracle_iteration_s(cfg, ws, n)
     return {"value": mean_accept / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"one Jacobi iteration of {n} rows at the 7B shape after a 16-token prefill "
-                      f"({dt:.2f} s), scaled by the GPU run's mean accepted length {mean_accept:.2f}",
+                      f"(median of 3: {dt:.2f} s), scaled by the GPU run's mean accepted length "
+                      f"{mean_accept:.2f}",
             "iteration_s": dt}
 
 
@@ -189,6 +200,7 @@ def main():
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
     traffic = measured_traffic() if (args.workload == "7b" and n == 16) else None
+    ceiling = stream_ceiling()
     mean_ctx = P + max_new / 2
     kv_bytes = cfg.n_layers * 2 * mean_ctx * d * 2
     step_gbps = (wbytes + kv_bytes) / (iter_ms / 1e3) / 1e9
@@ -251,7 +263,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (per layer)", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
-                     "launches": launches},
+                     "launches": launches, "stream_read_gbps": ceiling,
+                     "frac_of_stream_read": round(achieved / ceiling, 4) if ceiling else None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -332,7 +345,7 @@ def main_batched(args, wl):
         dt, cores = oracle_iteration_s(cfg, ws, n)
         tok_per_row = tokens / rows
         cpu = {"value": n / dt * tok_per_row, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-               "sample": f"one Jacobi iteration of {n} rows of one sequence at the 7B shape after a 16-token "
+               "sample": f"one Jacobi iteration of {n} rows of one sequence at the 7B shape (median of 3) after a 16-token "
                          f"prefill ({dt:.2f} s), scaled to tokens by the GPU run's {tok_per_row:.3f} tokens per "
                          f"row", "iteration_s": dt}
     line = {

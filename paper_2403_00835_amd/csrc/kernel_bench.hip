@@ -6,7 +6,8 @@
 // the library's own launchers, in the library's launch configuration, over rotating copies of its
 // packed weights inside a 2 GiB buffer, so no launch finds its weights in the last-level cache.
 // A plain device copy of a known byte count runs first: it scales the hardware byte counters
-// (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE) to bytes. Weights and activations hold arbitrary
+// (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE) to bytes. A streaming read of 1 GiB follows: the
+// practical HBM read ceiling the GEMMs are compared with. Weights and activations hold arbitrary
 // finite values: the timing and the traffic of these kernels do not depend on them.
 //
 // Usage: kernel_bench [rows (1..512, default 16)] [iters (default 20)]
@@ -33,6 +34,18 @@ __global__ __launch_bounds__(256) void copy_known(const u32x4 *__restrict__ src,
                                                   size_t n16) {
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
         dst[i] = src[i];
+}
+
+// Streaming read of n16 16-byte vectors (non-temporal loads, as the GEMMs stream their weights):
+// the practical HBM read ceiling. The xor of the data is stored only if it equals a value it
+// practically never takes, so the loads cannot be dropped and nothing is written.
+__global__ __launch_bounds__(256) void stream_read(const u32x4 *__restrict__ src, size_t n16, uint32_t *out) {
+    uint32_t acc = 0;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x) {
+        const u32x4 v = __builtin_nontemporal_load(src + i);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9E3779B9u) out[0] = acc;
 }
 
 namespace {
@@ -108,6 +121,27 @@ int main(int argc, char **argv) {
         CK(hipGetLastError());
         CK(hipDeviceSynchronize());
         std::printf("copy_known: %zu bytes read, %zu bytes written\n", bytes, bytes);
+    }
+
+    {  // streaming-read ceiling: 1 GiB per launch, 2048 workgroups (8 per CU), 10 launches
+        const size_t bytes = (size_t)1 << 30;
+        uint32_t *sink = dev<uint32_t>(1, 0);
+        hipEvent_t s0, s1;
+        CK(hipEventCreate(&s0));
+        CK(hipEventCreate(&s1));
+        hipLaunchKernelGGL(stream_read, dim3(2048), dim3(256), 0, 0, reinterpret_cast<const u32x4 *>(W), bytes / 16, sink);
+        CK(hipGetLastError());
+        CK(hipEventRecord(s0, 0));
+        for (int i = 0; i < 10; ++i)
+            hipLaunchKernelGGL(stream_read, dim3(2048), dim3(256), 0, 0,
+                               reinterpret_cast<const u32x4 *>(W + (size_t)(i & 1) * bytes), bytes / 16, sink);
+        CK(hipGetLastError());
+        CK(hipEventRecord(s1, 0));
+        CK(hipEventSynchronize(s1));
+        float ms = 0.0f;
+        CK(hipEventElapsedTime(&ms, s0, s1));
+        std::printf("stream_read: %zu bytes per launch, %.2f us/launch, %.1f GB/s\n", bytes, ms * 1e3 / 10,
+                    bytes / (ms * 1e-3 / 10) / 1e9);
     }
 
     const Shape shapes[] = {

@@ -118,6 +118,38 @@ def calibration_copy():
     del src, dst
 
 
+def oracle_decodes():
+    """The oracle's own greedy AR and Jacobi decoding rates (tokens/s, wall clock on the host
+    threads): full decodes of the tiny and small workloads, and a shortened 7B decode (16-token
+    prompt, 2 blocks of n = 16). Jacobi guesses are the oracle's AR continuation corrupted at
+    p = 0.3 and re-drawn each iteration, as in the GPU benchmark; the outputs must equal."""
+    import oracle
+    from paper_2403_00835_amd import workload
+    from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT, LLAMA7B, SMALL, TINY
+    out = {}
+    for name, cfg, plen, n, max_new in (("tiny", TINY, 16, 8, 32), ("small", SMALL, 128, 16, 256),
+                                        ("7b_2blocks", LLAMA7B, 16, 16, 32)):
+        log(f"[bench] oracle decodes: {name}")
+        ws = workload.make_weights(cfg)
+        om = oracle.Model(cfg, [workload.as_f32(cfg, t) for t in ws])
+        del ws
+        prompt = workload.make_prompt(cfg, plen, seed=13)
+        t0 = time.perf_counter()
+        ar = om.ar_decode(prompt, max_new)
+        t_ar = time.perf_counter() - t0
+        spec = oracle.GuessSpec(GUESS_STREAM_REINJECT, BLOCK_SHRINK, ar, p=0.3, seed=3)
+        t0 = time.perf_counter()
+        jo, st = om.jacobi_decode(prompt, n, max_new, spec)
+        t_j = time.perf_counter() - t0
+        if not np.array_equal(jo, ar):
+            raise RuntimeError(f"oracle Jacobi output differs from oracle AR ({name})")
+        out[name] = {"prompt": plen, "n": n, "tokens": max_new, "ar_tokens_per_s": round(max_new / t_ar, 3),
+                     "jacobi_tokens_per_s": round(max_new / t_j, 3), "jacobi_iterations": st["steps"],
+                     "cores": oracle.num_threads()}
+        del om
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +158,9 @@ def main():
     ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long", "7b_batched", "7b_loss"])
     ap.add_argument("--p", type=float, default=0.3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--oracle-decode", action="store_true",
+                    help="also time the oracle's AR and Jacobi decoding (tiny, small, shortened 7B; about "
+                         "a minute of host time) and add it to the line as oracle_decode")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, copy 1 GiB device-to-device (a kernel of known traffic "
                          "for scaling hardware byte counters)")
@@ -267,6 +302,8 @@ def main():
                      "frac_of_stream_read": round(achieved / ceiling, 4) if ceiling else None},
         "cpu_baseline": cpu,
     }
+    if args.oracle_decode:
+        line["oracle_decode"] = oracle_decodes()
     print(json.dumps(line), flush=True)
 
 

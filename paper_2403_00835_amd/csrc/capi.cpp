@@ -44,6 +44,7 @@ struct cllm_ctx {
     void *kc = nullptr, *vt = nullptr;
     float *rcos = nullptr, *rsin = nullptr;
     // workspace
+    float *part = nullptr;  // K-split partial products of the down projection: kDownSplits x rows x d
     float *X = nullptr, *ssq = nullptr, *pmax = nullptr, *opart = nullptr, *mpart = nullptr, *lpart = nullptr,
           *dbg = nullptr;
     int *pidx = nullptr;
@@ -262,6 +263,7 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
     base.ssq_out = c->ssq;
     base.ldx = c->d;
     base.An = c->An;
+    base.part = c->part;
     base.Fp = c->Fp;
     base.V = c->V;
 
@@ -1028,6 +1030,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->rcos, (size_t)c->ctx_alloc * h2))) return bail(s);
     if ((s = dalloc_t(c, &c->rsin, (size_t)c->ctx_alloc * h2))) return bail(s);
     if ((s = dalloc_t(c, &c->X, rows * c->d))) return bail(s);
+    if ((s = dalloc_t(c, &c->part, (size_t)kDownSplits * rows * c->d))) return bail(s);
     if ((s = dalloc_t(c, &c->ssq, (size_t)(c->d / 16) * rows))) return bail(s);
     // activation operands: one fp32 plane, or hi and lo bf16 planes (4 bytes per element either way)
     if ((s = dalloc(c, &c->Q, act_plane(c->cap, c->d) * 4))) return bail(s);

@@ -11,7 +11,8 @@ struct RowInfo;
 constexpr int kLmTiles = 4;   // 16-column tiles per workgroup: LM head
 constexpr int kNtQkv = 3;     // QKV (each tile holds rotate-half partners; 256 workgroups at 7B)
 constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups at 7B, one per CU)
-constexpr int kNtResid = 1;   // O and down projections
+constexpr int kNtResid = 1;   // O projection
+constexpr int kDownSplits = 4;  // down projection: K split over 4 workgroups per 64-column group
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4, GEMM_LOGITS = 5 };
@@ -45,11 +46,14 @@ struct GemmParams {
     int ctx_alloc;
     const float *rcos, *rsin;
     int d, hd;
-    // E_RESID: X += Y (rows of ldx floats); next RMSNorm operand An = X (.) gain; new partials
+    // E_RESID (O) and the down product: X += Y (rows of ldx floats); next RMSNorm operand
+    // An = X (.) gain; its per-16-column sums of squares. The down product's Y is summed from
+    // kDownSplits K-split partial products in `part` (kDownSplits x row capacity x ldx floats).
     float *Xout, *ssq_out;
     int ldx;
     const float *gain;
     void *An;
+    float *part;
     // E_SWIGLU
     void *H;
     int Fp;

@@ -375,6 +375,96 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
     return hipGetLastError();
 }
 
+// The down product's epilogue: the K-split partial products of kDownSplits workgroups per
+// column group summed in a fixed tree, (p0 + p1) + (p2 + p3) (splits past the last are absent
+// terms), then X += Y, the next RMSNorm operand X (.) gain (one operand vector per thread) and
+// the per-16-column sums of squares: each thread sums its VEC columns in order, the threads of
+// a 16-column tile then add their sums in order. Rows past the iteration's rows (device row
+// table) exit.
+template <Prec P>
+__global__ __launch_bounds__(256) void down_reduce_kernel(GemmParams p, int nsplit, size_t zstride, int rows_launch) {
+    using PT = PrecT<P>;
+    using T = typename PT::T;
+    constexpr int VEC = PT::VEC, G = 16 / VEC;  // columns per thread, threads per 16-column tile
+    const int groups = p.cols / VEC;
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int row = (int)(i / groups), g = (int)(i % groups);  // G consecutive threads share a tile
+    const bool live = row < rows_launch && row < p.rr.tab->R;
+    float ss = 0.0f;
+    if (live) {
+        const int c0 = g * VEC;
+        const size_t o = (size_t)row * p.ldx + c0;
+        float y[VEC], x[VEC];
+#pragma unroll
+        for (int h = 0; h < VEC / 4; ++h) {
+            f32x4 q[kDownSplits];
+#pragma unroll
+            for (int z = 0; z < kDownSplits; ++z)
+                q[z] = z < nsplit ? *reinterpret_cast<const f32x4 *>(p.part + z * zstride + o + 4 * h)
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+            const f32x4 xv = *reinterpret_cast<const f32x4 *>(p.Xout + o + 4 * h);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                y[4 * h + e] = (q[0][e] + q[1][e]) + (q[2][e] + q[3][e]);
+                x[4 * h + e] = xv[e] + y[4 * h + e];
+            }
+        }
+        alignas(16) T hi[VEC], lo[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            ss += x[e] * x[e];
+            const float a = x[e] * p.gain[c0 + e];
+            if constexpr (P == Prec::BF16) {
+                hi[e] = f2bf(a);
+                lo[e] = f2bf(a - bf2f(hi[e]));
+            } else {
+                hi[e] = a;
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < VEC / 4; ++h)
+            *reinterpret_cast<f32x4 *>(p.Xout + o + 4 * h) = f32x4{x[4 * h], x[4 * h + 1], x[4 * h + 2], x[4 * h + 3]};
+        T *an = reinterpret_cast<T *>(p.An);
+        const size_t ai = act_idx<P>(row, c0, p.ldx);  // VEC consecutive columns: one operand vector
+        *reinterpret_cast<u32x4 *>(an + ai) = *reinterpret_cast<const u32x4 *>(hi);
+        if constexpr (P == Prec::BF16)
+            *reinterpret_cast<u32x4 *>(an + act_plane(p.rr.cap, p.ldx) + ai) = *reinterpret_cast<const u32x4 *>(lo);
+    }
+    // the tile's G partial sums in order (G consecutive lanes; every lane takes part)
+    float tot = 0.0f;
+    const int base = (threadIdx.x & 63) & ~(G - 1);
+#pragma unroll
+    for (int k = 0; k < G; ++k) tot += __shfl(ss, base + k);
+    if (live && g % G == 0) p.ssq_out[(size_t)row * p.T + g / G] = tot;
+}
+
+// The down product: K split over kDownSplits ranges (fp32 partials in p.part, 64-column
+// workgroups, D k-steps in flight), then down_reduce_kernel. e0 marks the product's start, e1
+// the reduction's end.
+template <Prec P, int RG, int D>
+static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    static_assert(kDownSplits == 4, "down_reduce_kernel sums four partials");
+    if (!p.part || p.rt0 != 0 || p.cols % 16 != 0 || p.ldx < p.cols) return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.kc = (p.Ks + kDownSplits - 1) / kDownSplits;
+    q.Zout = p.part;
+    q.ldz = p.ldx;
+    q.V = p.cols;
+    q.zstride = (size_t)p.rr.cap * p.ldx;
+    hipError_t err = launch_gemm_t<P, kLmTiles, RG, E_LOGITS, D>(q, row_tiles, s, e0, nullptr);
+    if (err != hipSuccess) return err;
+    const int nsplit = (p.Ks + q.kc - 1) / q.kc;
+    const int rows_launch = row_tiles * 16 * RG;
+    const size_t n = (size_t)rows_launch * (p.cols / PrecT<P>::VEC);
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (e1)
+        hipExtLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(256), 0, s, nullptr, e1, 0, p, nsplit, q.zstride,
+                              rows_launch);
+    else
+        hipLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(256), 0, s, p, nsplit, q.zstride, rows_launch);
+    return hipGetLastError();
+}
+
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
@@ -387,8 +477,9 @@ static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_til
         case GEMM_QKV:
             return launch_gemm_t<P, 6, RG, E_QKV, 2>(p, row_tiles, s, e0, e1);
         case GEMM_O:
-        case GEMM_DOWN:
             return launch_gemm_t<P, 4, RG, E_RESID, 3>(p, row_tiles, s, e0, e1);
+        case GEMM_DOWN:
+            return launch_down<P, RG, 3>(p, row_tiles, s, e0, e1);
         case GEMM_GATE_UP:
             return launch_gemm_t<P, 6, RG, E_SWIGLU, 2>(p, row_tiles, s, e0, e1);
         case GEMM_LM:
@@ -402,8 +493,9 @@ static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_til
     case GEMM_QKV:
         return launch_gemm_t<P, kNtQkv, RG, E_QKV>(p, row_tiles, s, e0, e1);
     case GEMM_O:
-    case GEMM_DOWN:
         return launch_gemm_t<P, kNtResid, RG, E_RESID>(p, row_tiles, s, e0, e1);
+    case GEMM_DOWN:
+        return launch_down<P, RG, kGemmDepth>(p, row_tiles, s, e0, e1);
     case GEMM_GATE_UP:
         return launch_gemm_t<P, kNtGateUp, RG, E_SWIGLU>(p, row_tiles, s, e0, e1);
     case GEMM_LM:

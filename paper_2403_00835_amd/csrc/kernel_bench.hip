@@ -148,9 +148,10 @@ int main(int argc, char **argv) {
         {"qkv", GEMM_QKV, kNtQkv, 3 * kD, kD},
         {"o", GEMM_O, kNtResid, kD, kD},
         {"gate_up", GEMM_GATE_UP, kNtGateUp, 2 * kFp, kD},
-        {"down", GEMM_DOWN, kNtResid, kD, kFp},
+        {"down", GEMM_DOWN, kLmTiles, kD, kFp},
         {"lm_head", GEMM_LM, kLmTiles, n_wg_lm * 16 * kLmTiles, kD},
     };
+    float *part = dev<float>((size_t)kDownSplits * cap * kD, 0);  // K-split partials of the down product
     hipEvent_t e0, e1;
     CK(hipEventCreate(&e0));
     CK(hipEventCreate(&e1));
@@ -185,6 +186,7 @@ int main(int argc, char **argv) {
         p.pidx = pidx;
         p.dbg = nullptr;
         p.V = kV;
+        p.part = part;
         const size_t per = (size_t)(s.cols / 16) * p.Ks * kTileBytes;  // packed weight bytes per launch
         const int copies = (int)(kWBytes / per);
         if (copies < 2 || s.cols % 32 != 0) {

@@ -61,12 +61,18 @@ typedef struct cllm_config {
  * max_block (1..64) bounds the Jacobi block length n; max_new bounds tokens per decode;
  * max_batch (1..64; 0 means 1) is the number of sequence slots. Each slot is an independent
  * sequence with its own KV cache and state; every call taking `seq` addresses slot seq in
- * [0, max_batch). A batched iteration runs up to max_batch blocks of up to max_block rows. */
+ * [0, max_batch). A batched iteration runs up to max_batch blocks of up to max_block rows.
+ * prefill_chunk: prompt rows per forward pass of cllm_prefill (0 means 512; rounded up to a
+ * multiple of 64, at most 4096, and to no more than max_ctx rounded up to 64). A prompt is
+ * processed in chunks of that many rows; a row's values do not depend on the chunk size (every
+ * reduction has an order fixed by the model shape), so the size changes speed and activation
+ * memory only (about 200 KiB per row at the LLaMA-2-7B shape). */
 typedef struct cllm_runtime_opts {
     int32_t max_ctx, max_block, max_new;
     int32_t device;  /* HIP device ordinal */
     void *stream;    /* hipStream_t or NULL */
     int32_t max_batch;
+    int32_t prefill_chunk;
 } cllm_runtime_opts;
 
 /* Guess provider of the decode (reading of the paper's random initial n-token sequence).
@@ -206,10 +212,12 @@ cllm_status cllm_jacobi_decode_batch(cllm_ctx *ctx, int32_t B, const int32_t *se
 /* Forget the state of a slot (it must be prefilled again). Errors: ERR_ARG. */
 cllm_status cllm_reset(cllm_ctx *ctx, int32_t seq);
 
-/* Debug: when enabled, every later cllm_jacobi_step / cllm_jacobi_step_batch (and the last
- * chunk of cllm_prefill) also copies the fp32 logits of its rows into host_buf (row-major
- * rows x vocab, batch entries' rows in order; capacity host_floats floats, at least
- * max(64, max_batch * max_block) * vocab). Errors: ERR_ARG. */
+/* Debug: when enabled, every later cllm_jacobi_step / cllm_jacobi_step_batch also copies the
+ * fp32 logits of its rows into host_buf (row-major rows x vocab, batch entries' rows in order),
+ * and cllm_prefill copies those of the prompt's last 64-row tile (prompt rows
+ * 64 floor((len - 1) / 64) .. len - 1) to host rows 0.., so the last prompt row's logits are
+ * host row (len - 1) mod 64. host_floats: capacity of host_buf in floats, at least
+ * max(64, max_batch * max_block) * vocab. Errors: ERR_ARG. */
 cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, size_t host_floats);
 
 /* Trajectory recording (the paper's profiling of Jacobi trajectories, Section 5: fast-forwarded

@@ -29,7 +29,7 @@ class cllm_config(ctypes.Structure):
 
 class cllm_runtime_opts(ctypes.Structure):
     _fields_ = [("max_ctx", _i32), ("max_block", _i32), ("max_new", _i32), ("device", _i32), ("stream", _vp),
-                ("max_batch", _i32)]
+                ("max_batch", _i32), ("prefill_chunk", _i32)]
 
 
 class cllm_guess_spec(ctypes.Structure):
@@ -138,14 +138,14 @@ class Model:
     """One context of libcllm.so: model weights, KV cache and workspace on one GPU."""
 
     def __init__(self, cfg: ModelConfig, max_ctx, max_block=16, max_new=256, device=0, stream=None,
-                 weights=None, path=None, max_batch=1, random_seed=None):
+                 weights=None, path=None, max_batch=1, random_seed=None, prefill_chunk=0):
         """weights: host tensors (cllm_model_set_weights); path: a weight file (cllm_model_load);
         random_seed: seeded synthetic weights drawn on the GPU (cllm_model_init_random)."""
         self.cfg = cfg
         self.L = lib()
         self.max_block = max_block
         self.max_batch = max_batch
-        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream, max_batch)
+        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream, max_batch, prefill_chunk)
         h = _vp()
         if path is not None:
             st = self.L.cllm_model_load(os.fsencode(path), ctypes.byref(opts), ctypes.byref(h))

@@ -31,6 +31,8 @@ struct cllm_ctx {
     int n_wg_lm = 0;  // LM-head workgroups (argmax partials per row)
     int max_batch = 1;
     int cap = 0;        // row capacity of one iteration (multiple of 64): activation buffer rows
+    int pchunk = 0;     // prompt rows per prefill pass (multiple of 64, <= cap)
+    int dbg_rows = 0;   // rows of a step's debug logits: max(64, max_batch * max_block) rounded up
     size_t kv_seq = 0;  // KV cache elements per sequence slot
     int64_t streamed_bytes = 0;
 
@@ -439,7 +441,7 @@ cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
         bool &f;
         ~Flag() { f = false; }
     } flag{c->in_prefill};
-    const int chunk = c->cap;
+    const int chunk = c->pchunk;
     const int nchunks = ceil_div(len, chunk);
     for (int k = 0; k < nchunks; ++k) {
         const int start = k * chunk;
@@ -498,7 +500,7 @@ cllm_status step_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, cons
     for (int b = 0; b < B; ++b)
         if (h[seq_ids[b]].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
     if (c->dbg_on && c->dbg_host)
-        HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)std::min(R, c->cap) * c->V * 4, hipMemcpyDeviceToHost));
+        HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)std::min(R, c->dbg_rows) * c->V * 4, hipMemcpyDeviceToHost));
     for (int b = 0; b < B; ++b) {
         const Ctl &ct = h[seq_ids[b]];
         for (int i = 0; i < m[b]; ++i) blocks_out[(size_t)b * ostride + i] = ct.pred[i];
@@ -971,7 +973,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
         return CLLM_ERR_ARG;
     if (opts->max_block < 1 || opts->max_block > kMaxBlock || opts->max_ctx < 2 ||
         opts->max_ctx > kMaxChunks * kAttnChunk - 2 * kMaxRows || opts->max_new < 1 || opts->max_batch < 0 ||
-        opts->max_batch > kMaxSeqs)
+        opts->max_batch > kMaxSeqs || opts->prefill_chunk < 0 || opts->prefill_chunk > kMaxPrefillRows)
         return CLLM_ERR_ARG;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || opts->device < 0 || opts->device >= ndev) {
@@ -999,7 +1001,10 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->stream = static_cast<hipStream_t>(opts->stream);
     c->max_batch = opts->max_batch > 0 ? opts->max_batch : 1;
     c->opts.max_batch = c->max_batch;
-    c->cap = round_up(std::max(kMaxRows, c->max_batch * opts->max_block), kMaxRows);
+    c->dbg_rows = round_up(std::max(kMaxRows, c->max_batch * opts->max_block), kMaxRows);
+    c->pchunk = std::min(round_up(opts->prefill_chunk > 0 ? opts->prefill_chunk : kDefaultPrefillRows, kMaxRows),
+                         round_up(opts->max_ctx, kMaxRows));
+    c->cap = std::max(c->dbg_rows, c->pchunk);
     c->kv_seq = (size_t)c->NL * c->ctx_alloc * c->d;
     c->slot.assign(c->max_batch, cllm_ctx::Slot{});
 
@@ -1042,7 +1047,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->opart, (size_t)c->H * c->nch * rows * c->hd))) return bail(s);
     if ((s = dalloc_t(c, &c->mpart, (size_t)c->H * c->nch * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->lpart, (size_t)c->H * c->nch * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->dbg, rows * c->V))) return bail(s);
+    if ((s = dalloc_t(c, &c->dbg, rows * c->V))) return bail(s);  // a prefill chunk's rows too
     if ((s = dalloc_t(c, &c->ctl, (size_t)c->max_batch))) return bail(s);
     if ((s = dalloc_t(c, &c->tab, 1))) return bail(s);
     if ((s = dalloc_t(c, &c->rows, rows))) return bail(s);
@@ -1192,11 +1197,11 @@ cllm_status cllm_prefill(cllm_ctx *c, int32_t seq, const int32_t *prompt, int32_
     std::vector<Ctl> h(c->max_batch);
     if ((s = read_ctl(c, h.data()))) return s;
     if (h[seq].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill");
-    if (c->dbg_on && c->dbg_host) {  // rows of the last chunk's last 64-row tile, at their chunk rows
-        const int last = (len - 1) % c->cap;
+    if (c->dbg_on && c->dbg_host) {  // rows of the last chunk's last 64-row tile, to host rows 0..
+        const int last = (len - 1) % c->pchunk;
         const int r0 = last / kMaxRows * kMaxRows;
-        HIPCHK(c, hipMemcpy(c->dbg_host + (size_t)r0 * c->V, c->dbg + (size_t)r0 * c->V,
-                            (size_t)(last + 1 - r0) * c->V * 4, hipMemcpyDeviceToHost));
+        HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg + (size_t)r0 * c->V, (size_t)(last + 1 - r0) * c->V * 4,
+                            hipMemcpyDeviceToHost));
     }
     c->slot[seq].prefilled = true;
     c->slot[seq].L = h[seq].L;
@@ -1261,8 +1266,8 @@ cllm_status cllm_reset(cllm_ctx *c, int32_t seq) {
 cllm_status cllm_debug_logits(cllm_ctx *c, int32_t enable, float *host_buf, size_t host_floats) {
     if (!c) return CLLM_ERR_ARG;
     if (enable) {
-        if (!host_buf || host_floats < (size_t)c->cap * c->V)
-            return fail(c, CLLM_ERR_ARG, "debug buffer needs %zu floats", (size_t)c->cap * c->V);
+        if (!host_buf || host_floats < (size_t)c->dbg_rows * c->V)
+            return fail(c, CLLM_ERR_ARG, "debug buffer needs %zu floats", (size_t)c->dbg_rows * c->V);
         c->dbg_on = true;
         c->dbg_host = host_buf;
         c->dbg_cap = host_floats;

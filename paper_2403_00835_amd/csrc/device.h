@@ -14,6 +14,8 @@ constexpr int kWave = 64;
 constexpr int kMaxBlock = 64;      // largest Jacobi block (rows per iteration)
 constexpr int kMaxRows = 64;       // rows of one GEMM row tile; activation buffers hold a multiple
 constexpr int kMaxSeqs = 64;       // sequences of one batched iteration
+constexpr int kDefaultPrefillRows = 512;  // prompt rows per prefill pass unless the caller sets it
+constexpr int kMaxPrefillRows = kMaxSeqs * kMaxBlock;  // = the largest batched iteration
 constexpr int kGemmWaves = 8;      // waves per GEMM workgroup; they split K
 constexpr int kAttnChunk = 64;     // keys per attention workgroup, at absolute positions
 constexpr int kMaxChunks = 1024;   // attention chunks per sequence: context <= 65536

@@ -77,6 +77,9 @@ def test_bad_config_rejected_before_device(lib):
     cfg = binding.cllm_config(2, 64, 4, 16, 172, 256, 1e-6, 10000.0, 0)
     too_big_block = binding.cllm_runtime_opts(64, 65, 8, 0, None)
     assert lib.cllm_model_create(ctypes.byref(cfg), ctypes.byref(too_big_block), ctypes.byref(h)) == 1
+    for chunk in (-1, 4097):  # prefill chunk outside [0, 4096]
+        bad_chunk = binding.cllm_runtime_opts(64, 8, 8, 0, None, 1, chunk)
+        assert lib.cllm_model_create(ctypes.byref(cfg), ctypes.byref(bad_chunk), ctypes.byref(h)) == 1
 
 
 def test_weight_file_header_layout(tmp_path):

@@ -16,11 +16,12 @@ pytestmark = pytest.mark.gpu
 
 
 class Pair:
-    def __init__(self, cfg, max_ctx, max_block, max_new):
+    def __init__(self, cfg, max_ctx, max_block, max_new, prefill_chunk=0):
         from paper_2403_00835_amd import binding
         self.cfg = cfg
         ws = workload.make_weights(cfg)
-        self.gpu = binding.Model(cfg, max_ctx=max_ctx, max_block=max_block, max_new=max_new, weights=ws)
+        self.gpu = binding.Model(cfg, max_ctx=max_ctx, max_block=max_block, max_new=max_new, weights=ws,
+                                 prefill_chunk=prefill_chunk)
         self.orc = oracle.Model(cfg, [workload.as_f32(cfg, t) for t in ws])
         self.tol = TOL[cfg.dtype]
         self.max_ctx = max_ctx
@@ -30,6 +31,12 @@ class Pair:
 def tiny():
     log("[gpu] building tiny fp32 pair")
     return Pair(TINY, max_ctx=256, max_block=64, max_new=128)
+
+
+@pytest.fixture(scope="module")
+def tiny_chunked():
+    log("[gpu] building tiny fp32 pair with 64-row prefill chunks")
+    return Pair(TINY, max_ctx=256, max_block=64, max_new=128, prefill_chunk=64)
 
 
 @pytest.fixture(scope="module")
@@ -93,11 +100,45 @@ def test_tiny_teacher_forced_iterations(tiny):
     _teacher_forced(tiny, prompt, n=8, steps=20)
 
 
-def test_tiny_long_prompt_spans_chunks(tiny):
-    # 150-token prompt: three prefill chunks, several attention chunks, ragged tails.
-    log("[gpu] tiny teacher-forced, prompt 150, n=13")
+def test_tiny_long_prompt_spans_chunks(tiny_chunked):
+    # 150-token prompt in 64-row prefill chunks: three chunks, several attention chunks, ragged tails.
+    log("[gpu] tiny teacher-forced, prompt 150 in 64-row prefill chunks, n=13")
     prompt = workload.make_prompt(TINY, 150, seed=7)
-    _teacher_forced(tiny, prompt, n=13, steps=8)
+    _teacher_forced(tiny_chunked, prompt, n=13, steps=8)
+
+
+@pytest.mark.parametrize("cfg", [TINY, SMALL], ids=["tiny", "small"])
+def test_prefill_chunk_size_leaves_values_unchanged(cfg):
+    # The prefill's rows are computed with reduction orders fixed by the model shape, so the
+    # chunk size (64-row passes, 128-row passes, one pass of the whole prompt) changes no value:
+    # the prompt's last logits, the KV cache (seen through the next iteration's logits) and a
+    # whole decode are bit-identical.
+    from paper_2403_00835_amd import binding
+    log(f"[gpu] {cfg.dtype} d={cfg.d_model}: prefill chunk sizes 64 / 128 / default give identical values")
+    ws = workload.make_weights(cfg)
+    prompt = workload.make_prompt(cfg, 300, seed=17)
+    res = []
+    for chunk in (64, 128, 0):
+        m = binding.Model(cfg, max_ctx=512, max_block=16, max_new=64, weights=ws, prefill_chunk=chunk)
+        try:
+            m.debug_logits(True)
+            y0 = m.prefill(prompt)
+            pre = m.last_logits(64)[(len(prompt) - 1) % 64].copy()
+            blk = np.array([y0] + list(workload.make_prompt(cfg, 15, seed=18)), dtype=np.int32)
+            out, a = m.jacobi_step(blk)
+            step = m.last_logits(blk.size).copy()
+            m.debug_logits(False)
+            m.reset()
+            dec, _ = m.jacobi_decode(prompt, 16, 64, policy=GUESS_UNIFORM, seed=6)
+            res.append((y0, pre, out.copy(), a, step, dec.copy()))
+        finally:
+            m.close()
+    for r in res[1:]:
+        assert r[0] == res[0][0] and r[3] == res[0][3]
+        np.testing.assert_array_equal(r[1], res[0][1])
+        np.testing.assert_array_equal(r[2], res[0][2])
+        np.testing.assert_array_equal(r[4], res[0][4])
+        np.testing.assert_array_equal(r[5], res[0][5])
 
 
 def test_tiny_full_block_of_64(tiny):

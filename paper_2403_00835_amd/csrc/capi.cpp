@@ -235,12 +235,15 @@ struct IterShape {
     bool with_lm;
     int lm_rt0;         // >= 0: the LM head runs only on this 64-row tile (a prefill chunk's last row)
     bool tail = true;   // false: the decoder layers only (no LM head, scan or commit)
+    bool prompt = false;  // prompt rows (a prefill chunk): bf16 products take the prompt GEMM
 };
 
 cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev, const int32_t *stream_dev) {
     const bool tiled = sh.R > kMaxRows;
     const int rg = tiled ? 4 : rows_to_rg(sh.R);
     const int row_tiles = tiled ? ceil_div(sh.R, kMaxRows) : 1;
+    // prompt rows of a bf16 model: the LDS-tiled prompt GEMM (every prompt row, any chunk size)
+    const bool prompt_gemm = sh.prompt && c->bf16;
     hipStream_t s = c->stream;
     hipEvent_t e0, e1;
     const RowsRef rr{c->tab, c->rows, c->cap};
@@ -302,7 +305,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         q.Kc = kc;
         q.Vt = vt;
         timing_events(c, CLLM_KT_GEMM_QKV, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_QKV, c->bf16, rg, row_tiles, q, s, e0, e1));
+        HIPCHK(c, prompt_gemm ? launch_gemm_prompt(GEMM_QKV, sh.R, q, s, e0, e1)
+                              : launch_gemm(GEMM_QKV, c->bf16, rg, row_tiles, q, s, e0, e1));
 
         ap.Kc = kc;
         ap.Vt = vt;
@@ -325,7 +329,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         o.lda = c->d;
         o.gain = c->g_ffn[l];
         timing_events(c, CLLM_KT_GEMM_O, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_O, c->bf16, rg, row_tiles, o, s, e0, e1));
+        HIPCHK(c, prompt_gemm ? launch_gemm_prompt(GEMM_O, sh.R, o, s, e0, e1)
+                              : launch_gemm(GEMM_O, c->bf16, rg, row_tiles, o, s, e0, e1));
 
         GemmParams gu = base;
         gu.W = c->w_gu[l];
@@ -335,7 +340,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         gu.lda = c->d;
         gu.H = c->Hb;
         timing_events(c, CLLM_KT_GEMM_GATE_UP, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_GATE_UP, c->bf16, rg, row_tiles, gu, s, e0, e1));
+        HIPCHK(c, prompt_gemm ? launch_gemm_prompt(GEMM_GATE_UP, sh.R, gu, s, e0, e1)
+                              : launch_gemm(GEMM_GATE_UP, c->bf16, rg, row_tiles, gu, s, e0, e1));
 
         GemmParams dn = base;  // X += H W_d^T; writes the next layer's (or the final) RMSNorm operand
         dn.W = c->w_d[l];
@@ -345,7 +351,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         dn.lda = c->Fp;
         dn.gain = l + 1 < c->NL ? c->g_attn[l + 1] : c->g_final;
         timing_events(c, CLLM_KT_GEMM_DOWN, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_DOWN, c->bf16, rg, row_tiles, dn, s, e0, e1));
+        HIPCHK(c, prompt_gemm ? launch_gemm_prompt(GEMM_DOWN, sh.R, dn, s, e0, e1)
+                              : launch_gemm(GEMM_DOWN, c->bf16, rg, row_tiles, dn, s, e0, e1));
     }
     if (!sh.tail) return CLLM_OK;
 
@@ -449,8 +456,9 @@ cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
         cllm_status st = setup(c, MODE_PREFILL, 1, &seq, &rows, prompt + start, chunk, k == 0);
         if (st) return st;
         const bool last = k == nchunks - 1;
-        const IterShape sh{rows, 1, rows, std::min(c->nch, ceil_div(start + rows, kAttnChunk)), last,
-                           last ? (rows - 1) / kMaxRows : -1};
+        IterShape sh{rows, 1, rows, std::min(c->nch, ceil_div(start + rows, kAttnChunk)), last,
+                     last ? (rows - 1) / kMaxRows : -1};
+        sh.prompt = true;
         st = enqueue_iteration(c, sh, nullptr, nullptr);
         if (st) return st;
     }
@@ -1004,7 +1012,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     c->dbg_rows = round_up(std::max(kMaxRows, c->max_batch * opts->max_block), kMaxRows);
     c->pchunk = std::min(round_up(opts->prefill_chunk > 0 ? opts->prefill_chunk : kDefaultPrefillRows, kMaxRows),
                          round_up(opts->max_ctx, kMaxRows));
-    c->cap = std::max(c->dbg_rows, c->pchunk);
+    c->cap = round_up(std::max(c->dbg_rows, c->pchunk), kPromptRows);  // whole prompt-GEMM row tiles
     c->kv_seq = (size_t)c->NL * c->ctx_alloc * c->d;
     c->slot.assign(c->max_batch, cllm_ctx::Slot{});
 

@@ -353,6 +353,198 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
+// ------------------------------------------------------------------------------------------
+// Prompt GEMM (prefill passes, bf16): Y[rows x N] = A[rows x K] * W^T over the same packed
+// operands, for workgroup tiles of 16 RG rows x 16 NT columns. The 8 waves form a WM x (8 / WM)
+// grid over the tile and each accumulates its sub-tile over every k-step in order (one MFMA per
+// plane, hi then lo); the operands of a k-step (2 RG activation blocks and NT weight tiles of
+// 1 KiB each) are loaded once per workgroup, DP k-steps ahead into registers, and staged through
+// a double buffer in LDS, so every weight and activation byte is fetched once per workgroup
+// instead of once per wave. A row's reduction order depends only on K, never on the rows of a
+// pass, so every prompt row gets the same values whatever the chunk size; the order differs from
+// gemm_kernel's (which keeps eight k-step classes so decode rows are exact across row counts),
+// so prompt rows always take this kernel. Epilogues and the RMSNorm row factor are gemm_kernel's.
+// ------------------------------------------------------------------------------------------
+// LDS of the prompt GEMM (floats): three staging buffers during the main loop; afterwards the
+// output tile (and, for E_RESID, the epilogue scratch before it) reuse them; the row factors sit
+// in the last ROWS floats, apart from both.
+template <int NT, int RG, int EP>
+__host__ __device__ constexpr int prompt_lds_floats() {
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;
+    constexpr int stage = 3 * BLK * kWave * 4;
+    constexpr int after = (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1);
+    return (stage > after ? stage : after) + ROWS;
+}
+
+template <int NT, int RG, int WM, int EP, int DP>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
+    constexpr int BLK = 2 * RG + NT, NLW = BLK / W;  // 1 KiB blocks per k-step, loads per wave
+    static_assert(RG % WM == 0 && NT % WN == 0 && BLK % W == 0, "tile split");
+    static_assert(DP % 6 == 0, "the unrolled block covers the register ring, 3 LDS buffers and 2 operand sets");
+    constexpr bool ROWSCALE = EP != E_RESID;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    // Workgroup L runs on XCD L % 8 (round-robin dispatch). Column group cg belongs to XCD cg % 8,
+    // and each XCD takes its column groups in turn with their row tiles consecutively, so the row
+    // tiles of a column group run together and read its weights once from HBM into that XCD's L2.
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int wg = (slot / p.row_tiles) * 8 + xcd, row0 = (slot % p.row_tiles) * ROWS;
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg);
+    const int m = p.rr.tab->R - row0;
+    if (m <= 0 || wg >= p.n_wg) return;
+    const int rg0 = row0 >> 4, t0 = wg * NT;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = w / WN, wn = w % WN;
+    const int Ks = p.Ks;
+
+    extern __shared__ float smem[];
+    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [3][BLK][64] during the main loop
+    float *s_red = smem;                               // then epilogue scratch (E_RESID) ...
+    float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);  // ... and the output tile
+    float *s_inv = smem + prompt_lds_floats<NT, RG, EP>() - ROWS;  // row factors (apart from both)
+
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // This wave's blocks b = w + i W of every k-step: block b < 2 RG is activation plane b / RG,
+    // row group b % RG; block 2 RG + j is weight tile t0 + j (clamped). A k-step advances an
+    // activation block by 64 vectors and a weight block by one k-step of tiles.
+    const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
+    const u32x4 *src[NLW];
+    int adv[NLW];
+#pragma unroll
+    for (int i = 0; i < NLW; ++i) {
+        const int b = w + i * W;
+        if (b < 2 * RG) {
+            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RG) * act_plane(p.rr.cap, p.lda);
+            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RG) * ks_a * kWave * 8) + lane;
+            adv[i] = kWave;
+        } else {
+            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
+            adv[i] = tiles * kWave;
+        }
+    }
+    u32x4 ring[DP][NLW];
+    auto load = [&](int slot, int s) {
+        const size_t ss = (size_t)min(s, Ks - 1);  // past the end: a harmless reload of the last k-step
+#pragma unroll
+        for (int i = 0; i < NLW; ++i) ring[slot][i] = src[i][ss * adv[i]];
+    };
+    auto stage = [&](int slot, int buf) {
+#pragma unroll
+        for (int i = 0; i < NLW; ++i) s_stage[((size_t)buf * BLK + w + i * W) * kWave + lane] = ring[slot][i];
+    };
+    struct Ops {
+        u32x4 a[2][RGW], b[NTW];
+    };
+    auto fetch = [&](Ops &o, int buf) {
+        const u32x4 *bp = s_stage + (size_t)buf * BLK * kWave + lane;
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+            for (int r = 0; r < RGW; ++r) o.a[pl][r] = bp[(pl * RG + wm * RGW + r) * kWave];
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) o.b[j] = bp[(2 * RG + wn * NTW + j) * kWave];
+    };
+    f32x4 acc[RGW][NTW];
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto mfmas = [&](const Ops &o) {
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+            for (int r = 0; r < RGW; ++r)
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) acc[r][j] = mfma_kstep<P>(o.a[pl][r], o.b[j], acc[r][j]);
+    };
+
+    // Pipeline: k-step t is loaded into ring slot t % DP (DP k-steps ahead), staged into LDS
+    // buffer t % 3 two k-steps ahead, and read into operand set t % 2 one k-step ahead, so the
+    // MFMAs of k-step t overlap the LDS reads of t + 1 and the loads of t + 2 + DP. A buffer is
+    // rewritten three k-steps after it was staged: its readers (the iteration before) have passed
+    // the barrier in between. Memory operations past the last k-step are harmless repeats (the
+    // addresses are clamped; their MFMAs are skipped), so every iteration issues the same loads.
+#pragma unroll
+    for (int q = 0; q < DP; ++q) load(q, q);
+    stage(0, 0);
+    load(0, DP);
+    stage(1, 1);
+    load(1, DP + 1);
+    __syncthreads();
+    Ops ops[2];
+    fetch(ops[0], 0);
+    const int nblk = (Ks + DP - 1) / DP;
+    for (int bi = 0; bi < nblk; ++bi) {
+#pragma unroll
+        for (int q = 0; q < DP; ++q) {
+            const int s = bi * DP + q;
+            fetch(ops[(q + 1) & 1], (q + 1) % 3);
+            if (s < Ks) mfmas(ops[q & 1]);  // uniform over the workgroup
+            stage((q + 2) % DP, (q + 2) % 3);
+            load((q + 2) % DP, s + 2 + DP);
+            __syncthreads();
+        }
+    }
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+    __syncthreads();
+    // C layout of a 16 x 16 tile: lane l, register v -> row 4 (l / 16) + v, column l % 16
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = 16 * (wm * RGW + r) + 4 * (lane >> 4) + v;
+                float x = acc[r][j][v];
+                if constexpr (ROWSCALE) x *= s_inv[row];
+                s_tile[row * (COLS + 1) + 16 * (wn * NTW + j) + (lane & 15)] = x;
+            }
+    __syncthreads();
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+template <int NT, int RG, int WM, int EP, int DP>
+static hipError_t launch_prompt_t(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const size_t lds = (size_t)prompt_lds_floats<NT, RG, EP>() * sizeof(float);
+    // every row tile that starts below `rows` must lie inside the activation buffers
+    if (rows < 1 || rows > p.rr.cap || p.rr.cap % ROWS != 0 || p.lda % 32 != 0 || p.cols % 16 != 0)
+        return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.n_wg = (p.cols + COLS - 1) / COLS;
+    q.row_tiles = (rows + ROWS - 1) / ROWS;
+    const dim3 grid((unsigned)((q.n_wg + 7) / 8 * 8 * q.row_tiles));  // column groups padded to 8 XCDs
+    auto kern = gemm_prompt_kernel<NT, RG, WM, EP, DP>;
+    if (e0 || e1)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_prompt(GemmKind kind, int rows, const GemmParams &p, hipStream_t s, hipEvent_t e0,
+                              hipEvent_t e1) {
+    switch (kind) {
+    // tiles measured at the LLaMA-2-7B shape, 512 rows (each kernel is bound by the rate at which
+    // one CU pulls operand bytes, ~55 GB/s): 64 x 256 for QKV (151 us) and gate/up (190 us; 128 x
+    // 128: 169 / 222 us), 64 x 128 for O (48 us) and down (102 us; 128 x 128: 77 / 165 us)
+    case GEMM_QKV:
+        return launch_prompt_t<16, 4, 2, E_QKV, kPromptDepth>(p, rows, s, e0, e1);
+    case GEMM_GATE_UP:
+        return launch_prompt_t<16, 4, 2, E_SWIGLU, kPromptDepth>(p, rows, s, e0, e1);
+    case GEMM_O:
+    case GEMM_DOWN:  // X += H W_d^T with the residual epilogue (no K split)
+        return launch_prompt_t<8, 4, 2, E_RESID, kPromptDepth>(p, rows, s, e0, e1);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
 // Grid: column workgroups (ceil(p.cols / (16 * NT))) x row tiles of 16 * RG rows (from row tile
 // p.rt0) x K splits (E_LOGITS with p.kc > 0).
 template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves>

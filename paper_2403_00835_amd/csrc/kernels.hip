@@ -150,15 +150,26 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void attn_kernel(AttnParams p) 
     // while a chunk is computed (the index is clamped, so the last prefetch stays in bounds).
     const int nmine = w < nvis ? (nvis - 1 - w) / W + 1 : 0;
     auto chunk_of = [&](int i) { return min(w + i * W, nvis - 1); };
+    // The rows' queries (PLANES x NKK vectors per lane) are loaded once per workgroup, one block
+    // per wave, and shared through LDS; the first chunk's loads are issued meanwhile.
+    constexpr int NQ = PT::PLANES * NKK;
+    static_assert(NQ <= W, "one query block per wave");
+    __shared__ u32x4 s_q[NQ][kWave];
+    u32x4 qblk = u32x4{0u, 0u, 0u, 0u};
+    if (w < NQ) {
+        const int pl = w / NKK, kk = w % NKK;
+        qblk = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) +
+                                                act_idx<P>(qld, h * HD + kk * PT::KSTEP + g * PT::VEC, d));
+    }
+    AttnChunk<P, HD> buf[2];
+    attn_load_chunk<P, HD>(buf[0], Kh, Vh, chunk_of(0), dt, lane);
+    if (w < NQ) s_q[w][lane] = qblk;
+    __syncthreads();
     u32x4 qv[PT::PLANES][NKK];
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
-        for (int pl = 0; pl < PT::PLANES; ++pl)
-            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(
-                Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, h * HD + kk * PT::KSTEP + g * PT::VEC, d));
-    AttnChunk<P, HD> buf[2];
-    attn_load_chunk<P, HD>(buf[0], Kh, Vh, chunk_of(0), dt, lane);
+        for (int pl = 0; pl < PT::PLANES; ++pl) qv[pl][kk] = s_q[pl * NKK + kk][lane];
 
     auto process = [&](const AttnChunk<P, HD> &ch, int c) {
         const int key0 = c * kAttnChunk;
@@ -550,24 +561,32 @@ __global__ void decode_init_kernel(ScanParams p) {
     c->m = c->nb;
 }
 
-// Acceptance, commit, emit and the next block of one sequence, from its predictions c->pred
-// (one thread).
-__device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stream, int32_t *mlog, int32_t *rec) {
-    for (int i = 0; i < (c->mode == MODE_PREFILL ? 1 : m); ++i)
-        if (c->pred[i] < 0) {
-            c->err |= 1;
-            c->done = 1;
-            c->m = 0;
-            return;
-        }
-    if (c->mode == MODE_PREFILL) {  // every row is committed; pred[0] is the last row's argmax
+// State update of one sequence after an iteration whose accepted length a is known (one thread):
+// commit (L += a), statistics, pending = pred[a-1] and, in a decode, the next block's size and
+// where its tokens come from. The emitted tokens and the next block's tokens are written by the
+// caller's threads. A prefill chunk commits all its rows (pred[0] is its last row's argmax).
+struct NextBlock {
+    int newm;     // rows of the next iteration (0: none)
+    int e;        // output position of the next block's first token
+    int a, m;     // accepted length, rows of the finished iteration
+    int usepred;  // z[j] = pred[a-1+j] where a-1+j < m, else a fresh guess draw
+    int draw;     // draw index of fresh guesses
+};
+
+__device__ void commit_scalar(Ctl *c, int m, int a, int err, int32_t *mlog, int32_t *rec, NextBlock *nb) {
+    nb->newm = 0;
+    if (err) {
+        c->err |= 1;
+        c->done = 1;
+        c->m = 0;
+        return;
+    }
+    if (c->mode == MODE_PREFILL) {
         c->L += m;
         c->pending = c->pred[0];
         c->m = 0;
         return;
     }
-    int a = 1;
-    while (a < m && c->z[a] == c->pred[a - 1]) ++a;
     if (rec) {  // trajectory record header (its z and pred were written by the scan's threads)
         rec[0] = c->L;
         rec[1] = c->e;
@@ -586,43 +605,42 @@ __device__ void commit_and_next(Ctl *c, int m, int32_t *out, const int32_t *stre
         c->m = 0;
         return;
     }
-    for (int k = 0; k < a; ++k) out[c->e + k] = c->z[k];
-    c->e += a;
+    c->e += a;  // z[0..a) were emitted by the caller's threads
     if (c->e >= c->max_new) {
         c->done = 1;
         c->m = 0;
         return;
     }
     const int e = c->e, n = c->n;
-    const int draw = c->policy == 2 ? c->steps : 0;
-    int newm;
+    nb->e = e;
+    nb->a = a;
+    nb->m = m;
+    nb->draw = c->policy == 2 ? c->steps : 0;
     if (c->block_policy == 0) {
         if (e == c->b0 + c->nb) {  // block converged; its last prediction seeds the next block
             c->b0 = e;
             c->nb = (c->max_new - e) < n ? (c->max_new - e) : n;
             c->blocks += 1;
-            newm = c->nb;
-            for (int j = 1; j < newm; ++j) c->z[j] = draw_guess(c, stream, e + j, draw);
-        } else {
-            newm = c->b0 + c->nb - e;
-            for (int j = 1; j < newm; ++j)
-                c->z[j] = c->policy == 2 ? draw_guess(c, stream, e + j, draw) : c->pred[a - 1 + j];
+            nb->newm = c->nb;
+            nb->usepred = 0;
+        } else {  // shrink: the unfixed rest of the block
+            nb->newm = c->b0 + c->nb - e;
+            nb->usepred = c->policy != 2;
         }
-    } else {
-        newm = (c->max_new - e) < n ? (c->max_new - e) : n;
-        for (int j = 1; j < newm; ++j) {
-            const int src = a - 1 + j;
-            c->z[j] = (c->policy != 2 && src < m) ? c->pred[src] : draw_guess(c, stream, e + j, draw);
-        }
+    } else {  // slide: the next min(n, remaining) positions
+        nb->newm = (c->max_new - e) < n ? (c->max_new - e) : n;
+        nb->usepred = c->policy != 2;
     }
     c->z[0] = c->pending;
-    c->m = newm;
+    c->m = nb->newm;
 }
 
 // One workgroup per batch entry: the final argmax of each of its rows over the LM-head
 // workgroups (16 threads per row take strided workgroups, then a 16-way tree; (max, lowest id)
-// is exact, so the order is free), then commit_and_next. A prefill chunk needs only its last
-// row. With one batch entry the workgroup also lays out the next row table.
+// is exact, so the order is free); the accepted length (a = 1 + the leading k >= 1 with
+// z[k] = pred[k-1], from one wave's ballot); the emitted tokens; the state update (one thread);
+// the next block's tokens (one thread per position). A prefill chunk needs only its last row.
+// With one batch entry the workgroup also lays out the next row table.
 __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     const int bi = blockIdx.x;
     const RowTab *tab = p.tab;
@@ -631,6 +649,9 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     const int m = tab->m[bi], r0 = tab->r0[bi];
     Ctl *c = p.ctl + seq;
     const int tid = threadIdx.x;
+    __shared__ int s_pred[kMaxBlock];
+    __shared__ NextBlock s_nb;
+    __shared__ int s_a, s_err;
     if (m > 0) {
         if (p.advance_only) {
             if (tid == 0) {
@@ -684,16 +705,40 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
                 }
                 const int pr = (nn || i == 0x7fffffff) ? -1 : i;
                 c->pred[tid] = pr;
+                s_pred[tid] = pr;
                 if (rec) {
                     rec[5 + tid] = c->z[tid];
                     rec[5 + kMaxBlock + tid] = pr;
                 }
             }
             __syncthreads();
+            if (tid < kWave) {  // wave 0: error check, accepted length, emitted tokens
+                const bool in = tid < nrows;
+                const int zk = in ? c->z[tid] : 0;
+                const unsigned long long bad = __ballot(in && s_pred[tid] < 0);
+                const unsigned long long miss = __ballot(in && tid >= 1 && zk != s_pred[tid - 1]);
+                const int a = miss ? __builtin_ctzll(miss) : nrows;
+                if (!bad && !prefill && c->mode == MODE_DECODE && tid < a && p.out) {
+                    int32_t *out = p.out + (size_t)seq * p.out_stride;
+                    out[c->e + tid] = zk;
+                }
+                if (tid == 0) {
+                    s_a = a;
+                    s_err = bad != 0;
+                }
+            }
+            __syncthreads();
             if (tid == 0)
-                commit_and_next(c, m, p.out ? p.out + (size_t)seq * p.out_stride : nullptr,
-                                p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr,
-                                p.mlog ? p.mlog + (size_t)seq * p.out_stride : nullptr, rec);
+                commit_scalar(c, m, s_a, s_err, p.mlog ? p.mlog + (size_t)seq * p.out_stride : nullptr, rec, &s_nb);
+            __syncthreads();
+            const int newm = s_nb.newm;
+            if (tid >= 1 && tid < newm) {  // the next block's guesses (z[0] = pending, set above)
+                const int src = s_nb.a - 1 + tid;
+                c->z[tid] = (s_nb.usepred && src < s_nb.m)
+                                ? s_pred[src]
+                                : draw_guess(c, p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr,
+                                             s_nb.e + tid, s_nb.draw);
+            }
         }
     }
     if (p.plan_inline) {

@@ -311,9 +311,11 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         ap.Kc = kc;
         ap.Vt = vt;
         timing_events(c, CLLM_KT_ATTN, rg, &e0, &e1);
-        // one kernel for a single sequence with a short context (its slices re-read the head's
-        // K from L2); the chunk-parallel pair otherwise. Both give bit-identical values.
-        if (sh.nseq == 1 && sh.nch <= kFusedChunks && c->hd <= 128) {
+        // one kernel for one sequence's block (<= 64 rows) over a short context (its slices
+        // re-read the head's K from L2); the chunk-parallel pair otherwise, including prompt
+        // passes of more than 64 rows, whose row groups would re-read every chunk. Both give
+        // bit-identical values.
+        if (sh.nseq == 1 && sh.nch <= kFusedChunks && c->hd <= 128 && sh.maxm <= kMaxRows) {
             HIPCHK(c, launch_attn_fused(c->bf16, ceil_div(std::max(sh.maxm, 1), 16), sh.nseq, ap, s, e0, e1));
         } else {
             HIPCHK(c, launch_attn(c->bf16, attn_rg, sh.nch, sh.nseq, ap, s, e0, e1));

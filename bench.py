@@ -274,7 +274,7 @@ def main():
         "config": {"workload": f"{wl.name}: prompt {P}, n={n}, {max_new} new tokens, guesses = GPU greedy "
                                f"continuation corrupted at p={args.p} and re-drawn each iteration, shrink blocks",
                    "prompt_len": P, "n": n, "max_new": max_new, "p": args.p, "batch": 1,
-                   "layers": cfg.n_layers, "d_model": cfg.d_model},
+                   "layers": cfg.n_layers, "d_model": cfg.d_model, "prefill_chunk": 512},
         "jacobi_step_ms": round(iter_ms, 4),
         "iteration_ms": {"mean": round(iter_ms, 4),
                          "p10": round(float(np.median([x["iter_ms_p10"] for x in stats])), 4),

@@ -1,6 +1,7 @@
 // kernel_bench: standalone driver of libcllm's weight-streaming GEMM kernels at the LLaMA-2-7B
 // shape (d 4096, FFN 11008, vocab 32000, head_dim 128, bf16) for one iteration of `rows` rows
-// (more than 64 rows: row tiles of 64, as in batched iterations and prefill chunks).
+// (more than 64 rows: row tiles of 64, as in batched iterations). With more than 64 rows the
+// prompt GEMM (prefill passes: QKV, O, gate/up, down) is timed as well at the same row count.
 //
 // Each product of an iteration (QKV, O, gate/up, down, LM head) is launched `iters` times through
 // the library's own launchers, in the library's launch configuration, over rotating copies of its
@@ -155,7 +156,7 @@ int main(int argc, char **argv) {
     hipEvent_t e0, e1;
     CK(hipEventCreate(&e0));
     CK(hipEventCreate(&e1));
-    for (const Shape &s : shapes) {
+    auto params = [&](const Shape &s) {
         GemmParams p{};
         p.Ks = s.K / 32;
         p.cols = s.cols;
@@ -187,6 +188,10 @@ int main(int argc, char **argv) {
         p.dbg = nullptr;
         p.V = kV;
         p.part = part;
+        return p;
+    };
+    for (const Shape &s : shapes) {
+        GemmParams p = params(s);
         const size_t per = (size_t)(s.cols / 16) * p.Ks * kTileBytes;  // packed weight bytes per launch
         const int copies = (int)(kWBytes / per);
         if (copies < 2 || s.cols % 32 != 0) {
@@ -211,6 +216,32 @@ int main(int argc, char **argv) {
         const double flops = 2.0 * rows * s.cols * s.K;  // algorithmic (the MFMA work is twice: hi, lo)
         std::printf("%-8s rows=%d row_tiles=%d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s  %7.1f TFLOP/s\n", s.name,
                     rows, row_tiles, per, us, per / us / 1e3, flops / us / 1e6);
+    }
+    if (rows > kMaxRows) {
+        for (int k = 0; k < 4; ++k) {  // QKV, O, gate/up, down
+            const Shape &s = shapes[k];
+            GemmParams p = params(s);
+            const size_t per = (size_t)(s.cols / 16) * p.Ks * kTileBytes;
+            const int copies = (int)(kWBytes / per);
+            for (int i = 0; i < 2; ++i) {
+                p.W = W + (size_t)(i % copies) * per;
+                CK(launch_gemm_prompt(s.kind, rows, p, 0, nullptr, nullptr));
+            }
+            CK(hipDeviceSynchronize());
+            CK(hipEventRecord(e0, 0));
+            for (int i = 0; i < iters; ++i) {
+                p.W = W + (size_t)((i + 2) % copies) * per;
+                CK(launch_gemm_prompt(s.kind, rows, p, 0, nullptr, nullptr));
+            }
+            CK(hipEventRecord(e1, 0));
+            CK(hipEventSynchronize(e1));
+            float ms = 0.0f;
+            CK(hipEventElapsedTime(&ms, e0, e1));
+            const double us = ms * 1e3 / iters;
+            const double flops = 2.0 * rows * s.cols * s.K;
+            std::printf("prompt %-8s rows=%d weights=%zu bytes  %8.2f us/launch  %7.1f TFLOP/s (MFMA work: twice)\n",
+                        s.name, rows, per, us, flops / us / 1e6);
+        }
     }
     CK(hipDeviceSynchronize());
     std::printf("done\n");

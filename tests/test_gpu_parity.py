@@ -201,6 +201,14 @@ def test_small_teacher_forced_iterations(small):
     _teacher_forced(small, prompt, n=16, steps=10, stream=ar, p=0.3)
 
 
+def test_small_ragged_prompt_vs_oracle(small):
+    # 300 prompt rows in one pass of the prompt GEMM: five 64-row tiles, the last one ragged
+    # (44 live rows), and the chunk-parallel attention; then teacher-forced iterations.
+    log("[gpu] small bf16 teacher-forced, prompt 300 (ragged prompt tiles), n=16")
+    prompt = workload.make_prompt(SMALL, 300, seed=23)
+    _teacher_forced(small, prompt, n=16, steps=4)
+
+
 def test_small_decode_is_valid_greedy(small):
     log("[gpu] small bf16 decode, stream re-drawn p=0.3, n=16, 96 new")
     prompt = workload.make_prompt(SMALL, 128)

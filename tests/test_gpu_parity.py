@@ -209,6 +209,22 @@ def test_small_ragged_prompt_vs_oracle(small):
     _teacher_forced(small, prompt, n=16, steps=4)
 
 
+def test_bf16_ragged_widths_vs_oracle():
+    # Output widths that are not multiples of the GEMM column groups: QKV 960 and gate/up 1728
+    # columns (the prompt GEMM's 256-column groups and the decode GEMM's tile groups end ragged),
+    # O and down 320 columns (2.5 prompt groups), a 1000-token LM head; a 150-token prompt in one
+    # prompt pass of three 64-row tiles, the last ragged; then teacher-forced iterations.
+    from paper_2403_00835_amd.configs import ModelConfig
+    cfg = ModelConfig(n_layers=2, d_model=320, n_heads=5, head_dim=64, ffn_dim=864, vocab=1000)
+    log("[gpu] bf16 ragged widths (d 320, FFN 864, vocab 1000), prompt 150, n=12")
+    pair = Pair(cfg, max_ctx=256, max_block=16, max_new=64)
+    try:
+        prompt = workload.make_prompt(cfg, 150, seed=29)
+        _teacher_forced(pair, prompt, n=12, steps=5)
+    finally:
+        pair.gpu.close()
+
+
 def test_small_decode_is_valid_greedy(small):
     log("[gpu] small bf16 decode, stream re-drawn p=0.3, n=16, 96 new")
     prompt = workload.make_prompt(SMALL, 128)

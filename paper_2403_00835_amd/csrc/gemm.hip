@@ -359,8 +359,8 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
 // grid over the tile and each accumulates its sub-tile over every k-step in order (one MFMA per
 // plane, hi then lo); the operands of a k-step (2 RG activation blocks and NT weight tiles of
 // 1 KiB each) are loaded once per workgroup, DP k-steps ahead into registers, and staged through
-// a double buffer in LDS, so every weight and activation byte is fetched once per workgroup
-// instead of once per wave. A row's reduction order depends only on K, never on the rows of a
+// three LDS buffers, so every weight and activation byte is fetched once per workgroup instead
+// of once per wave. A row's reduction order depends only on K, never on the rows of a
 // pass, so every prompt row gets the same values whatever the chunk size; the order differs from
 // gemm_kernel's (which keeps eight k-step classes so decode rows are exact across row counts),
 // so prompt rows always take this kernel. Epilogues and the RMSNorm row factor are gemm_kernel's.

@@ -8,7 +8,8 @@
 - Properties at full size, in the benchmark's launch configuration (prompt 512, n = 16, 256 new
   tokens, guesses re-drawn at p = 0.3, shrink): GPU Jacobi equals GPU AR bit-exactly under every
   guess and block policy, iterations accept >= 1 token and at most the block, the run is
-  deterministic; and the long workload (prompt 2048, n = 64, 512 new).
+  deterministic, the 512-row prompt pass gives the same values as 64-row passes; and the long
+  workload (prompt 2048, n = 64, 512 new).
 """
 import numpy as np
 import pytest
@@ -95,6 +96,38 @@ def test_7b_full_size_jacobi_equals_ar(gpu):
     out3, st3 = gpu.jacobi_decode(prompt, 16, 256, policy=GUESS_STREAM_REINJECT, stream=ar, p=0.3, seed=3)
     np.testing.assert_array_equal(out2, out3)
     assert st2["steps"] == st3["steps"]
+
+
+def test_7b_prompt_chunking_leaves_values_unchanged(gpu):
+    # The benchmark's prefill (one 512-row pass of the prompt GEMM and the chunk-parallel
+    # attention) against eight 64-row passes of a second context with bit-identical weights
+    # (drawn on the device): the prompt's last logits, a 16-row iteration's logits over the
+    # cache it left and a 64-token decode are bit-identical.
+    from paper_2403_00835_amd import binding
+    prompt = workload.make_prompt(CFG, 512, seed=4)
+    blk = workload.make_prompt(CFG, 15, seed=5)
+    res = []
+    for chunk, ctx in [(0, gpu), (64, None)]:
+        if ctx is None:
+            log("[gpu7b] second context: weights drawn on the device, 64-row prefill passes")
+            ctx = binding.Model(CFG, max_ctx=704, max_block=16, max_new=64, random_seed=workload.SEED_WEIGHTS,
+                                prefill_chunk=chunk)
+        try:
+            ctx.debug_logits(True)
+            y0 = ctx.prefill(prompt)
+            pre = ctx.last_logits(64)[(512 - 1) % 64].copy()
+            out, a = ctx.jacobi_step(np.concatenate([[y0], blk]).astype(np.int32))
+            step = ctx.last_logits(16).copy()
+            ctx.debug_logits(False)
+            dec, _ = ctx.jacobi_decode(prompt, 16, 64, policy=GUESS_UNIFORM, seed=6)
+            res.append((y0, pre, out.copy(), a, step, dec.copy()))
+        finally:
+            if ctx is not gpu:
+                ctx.close()
+    log(f"  y0 {res[0][0]} / {res[1][0]}, accepted {res[0][3]} / {res[1][3]}")
+    assert res[0][0] == res[1][0] and res[0][3] == res[1][3]
+    for i in (1, 2, 4, 5):
+        np.testing.assert_array_equal(res[0][i], res[1][i])
 
 
 def test_7b_exact_guesses_and_step_api(gpu):

@@ -639,27 +639,36 @@ __device__ void commit_scalar(Ctl *c, int m, int a, int err, int32_t *mlog, int3
 // workgroups (16 threads per row take strided workgroups, then a 16-way tree; (max, lowest id)
 // is exact, so the order is free); the accepted length (a = 1 + the leading k >= 1 with
 // z[k] = pred[k-1], from one wave's ballot); the emitted tokens; the state update (one thread);
-// the next block's tokens (one thread per position). A prefill chunk needs only its last row.
-// With one batch entry the workgroup also lays out the next row table.
+// the next block's tokens (one thread per position). The sequence's control block is worked on
+// in LDS (one parallel copy in, one out), so the state update is not a chain of global-memory
+// round trips. A prefill chunk needs only its last row. With one batch entry the workgroup also
+// lays out the next row table.
 __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     const int bi = blockIdx.x;
     const RowTab *tab = p.tab;
     if (bi >= tab->nseq) return;
     const int seq = tab->seq[bi];
     const int m = tab->m[bi], r0 = tab->r0[bi];
-    Ctl *c = p.ctl + seq;
+    Ctl *gc = p.ctl + seq;
     const int tid = threadIdx.x;
     __shared__ int s_pred[kMaxBlock];
     __shared__ NextBlock s_nb;
     __shared__ int s_a, s_err;
+    __shared__ Ctl s_ctl;
+    static_assert(sizeof(Ctl) % 4 == 0, "the control block is copied as 32-bit words");
+    constexpr int kCtlWords = (int)(sizeof(Ctl) / 4);
     if (m > 0) {
         if (p.advance_only) {
             if (tid == 0) {
-                c->L += m;
-                c->m = 0;
+                gc->L += m;
+                gc->m = 0;
             }
         } else {
-            const bool prefill = c->mode == MODE_PREFILL;
+            // the copy into LDS overlaps the argmax loads; the barrier after them publishes it
+            for (int i = tid; i < kCtlWords; i += blockDim.x)
+                reinterpret_cast<int32_t *>(&s_ctl)[i] = reinterpret_cast<const int32_t *>(gc)[i];
+            Ctl *c = &s_ctl;
+            const bool prefill = gc->mode == MODE_PREFILL;
             const int nrows = prefill ? 1 : m;            // <= 64
             const int rbase = r0 + (prefill ? m - 1 : 0);
             const int row = tid & 63, j = tid >> 6;
@@ -739,6 +748,9 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
                                 : draw_guess(c, p.stream ? p.stream + (size_t)seq * p.stream_stride : nullptr,
                                              s_nb.e + tid, s_nb.draw);
             }
+            __syncthreads();
+            for (int i = tid; i < kCtlWords; i += blockDim.x)
+                reinterpret_cast<int32_t *>(gc)[i] = reinterpret_cast<const int32_t *>(&s_ctl)[i];
         }
     }
     if (p.plan_inline) {

@@ -217,7 +217,9 @@ cllm_status cllm_reset(cllm_ctx *ctx, int32_t seq);
  * and cllm_prefill copies those of the prompt's last 64-row tile (prompt rows
  * 64 floor((len - 1) / 64) .. len - 1) to host rows 0.., so the last prompt row's logits are
  * host row (len - 1) mod 64. host_floats: capacity of host_buf in floats, at least
- * max(64, max_batch * max_block) * vocab. Errors: ERR_ARG. */
+ * max(64, max_batch * max_block) * vocab. The first enable allocates the context's device
+ * logits buffer (row capacity x vocab floats; freed with the context).
+ * Errors: ERR_ARG, ERR_OOM, ERR_DEVICE. */
 cllm_status cllm_debug_logits(cllm_ctx *ctx, int32_t enable, float *host_buf, size_t host_floats);
 
 /* Trajectory recording (the paper's profiling of Jacobi trajectories, Section 5: fast-forwarded

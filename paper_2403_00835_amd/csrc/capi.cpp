@@ -1057,7 +1057,6 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if ((s = dalloc_t(c, &c->opart, (size_t)c->H * c->nch * rows * c->hd))) return bail(s);
     if ((s = dalloc_t(c, &c->mpart, (size_t)c->H * c->nch * rows))) return bail(s);
     if ((s = dalloc_t(c, &c->lpart, (size_t)c->H * c->nch * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->dbg, rows * c->V))) return bail(s);  // a prefill chunk's rows too
     if ((s = dalloc_t(c, &c->ctl, (size_t)c->max_batch))) return bail(s);
     if ((s = dalloc_t(c, &c->tab, 1))) return bail(s);
     if ((s = dalloc_t(c, &c->rows, rows))) return bail(s);
@@ -1278,6 +1277,10 @@ cllm_status cllm_debug_logits(cllm_ctx *c, int32_t enable, float *host_buf, size
     if (enable) {
         if (!host_buf || host_floats < (size_t)c->dbg_rows * c->V)
             return fail(c, CLLM_ERR_ARG, "debug buffer needs %zu floats", (size_t)c->dbg_rows * c->V);
+        if (!c->dbg) {  // device logits of up to the row capacity (a prefill chunk's rows too), on first use
+            cllm_status s = check_ctx(c);
+            if (s || (s = dalloc_t(c, &c->dbg, (size_t)c->cap * c->V))) return s;
+        }
         c->dbg_on = true;
         c->dbg_host = host_buf;
         c->dbg_cap = host_floats;

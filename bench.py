@@ -14,7 +14,7 @@ batched loop; value = tokens of all sequences / second) measure the other config
 a step is one forward + backward of the loss head over 16 teacher/student pairs (one n = 16
 block) and 48 AR rows, on device arrays; value = loss rows / second.
 
-Prints one JSON line. --gpus above 1 is refused: this build runs on one GPU.
+Prints one JSON line. --gpus above 1 is refused: the path runs on one GPU.
 """
 import argparse
 import hashlib
@@ -167,7 +167,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (--gpus must be 1)",
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (--gpus must be 1)",
               file=sys.stderr, flush=True)
         sys.exit(2)
 

@@ -508,6 +508,158 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmPar
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
+// The same prompt product with the operand blocks loaded from global memory straight into LDS
+// (LDS DMA: no register round trip, no LDS write instructions), into a ring of NB buffers
+// NB - 1 k-steps ahead, with a small LDS footprint so that two or three workgroups share a CU
+// and hide each other's latency. A k-step's blocks are complete once this wave's DMA count has
+// dropped to the later k-steps' loads (explicit vmcnt wait) and every wave has passed a barrier;
+// the barrier is issued without the compiler's LDS fence (which would wait for every
+// outstanding DMA), with compiler-only fences so no LDS access moves across it. The buffer a
+// k-step refills was last read in the previous k-step, before that barrier. Each wave
+// accumulates its sub-tile over every k-step in order (hi then lo plane), as
+// gemm_prompt_kernel does, so both give bit-identical values.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+    // s_waitcnt with vmcnt = N (bits 3:0 and 15:14) and the other counters at their maxima
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void barrier_no_fence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int NT, int RG, int EP, int NB>
+__host__ __device__ constexpr int prompt_dma_lds_floats() {
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;
+    constexpr int stage = NB * BLK * kWave * 4;
+    constexpr int after = (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1);
+    return (stage > after ? stage : after) + ROWS;
+}
+
+template <int NT, int RG, int WM, int EP, int NB>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_dma_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
+    constexpr int BLK = 2 * RG + NT, NLW = BLK / W;  // 1 KiB blocks per k-step, DMA loads per wave
+    static_assert(RG % WM == 0 && NT % WN == 0 && BLK % W == 0 && NB >= 3, "tile split, ring depth");
+    constexpr bool ROWSCALE = EP != E_RESID;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    // XCD-grouped column groups with their row tiles consecutive (as gemm_prompt_kernel)
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int wg = (slot / p.row_tiles) * 8 + xcd, row0 = (slot % p.row_tiles) * ROWS;
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg);
+    const int m = p.rr.tab->R - row0;
+    if (m <= 0 || wg >= p.n_wg) return;
+    const int rg0 = row0 >> 4, t0 = wg * NT;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = w / WN, wn = w % WN;
+    const int Ks = p.Ks;
+
+    extern __shared__ float smem[];
+    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64] during the main loop
+    float *s_red = smem;                               // then epilogue scratch (E_RESID) ...
+    float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);  // ... and the output tile
+    float *s_inv = smem + prompt_dma_lds_floats<NT, RG, EP, NB>() - ROWS;  // row factors (apart)
+
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // This wave's blocks b = w + i W of every k-step (as gemm_prompt_kernel)
+    const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
+    const u32x4 *src[NLW];
+    int adv[NLW];
+#pragma unroll
+    for (int i = 0; i < NLW; ++i) {
+        const int b = w + i * W;
+        if (b < 2 * RG) {
+            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RG) * act_plane(p.rr.cap, p.lda);
+            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RG) * ks_a * kWave * 8) + lane;
+            adv[i] = kWave;
+        } else {
+            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
+            adv[i] = tiles * kWave;
+        }
+    }
+    // k-step s into ring buffer s % NB; past the last k-step a harmless reload of it
+    auto issue = [&](int s) {
+        const size_t ss = (size_t)min(s, Ks - 1);
+        u32x4 *buf = s_stage + (size_t)(s % NB) * BLK * kWave;
+#pragma unroll
+        for (int i = 0; i < NLW; ++i)
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[i] + ss * adv[i]),
+                                             (__attribute__((address_space(3))) void *)(buf + (size_t)(w + i * W) * kWave),
+                                             16, 0, 0);
+    };
+    f32x4 acc[RGW][NTW];
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int q = 0; q < NB - 1; ++q) issue(q);
+    for (int s = 0; s < Ks; ++s) {
+        wait_vm<(NB - 2) * NLW>();  // this wave's blocks of k-step s have landed
+        barrier_no_fence();         // every wave's; buffer (s - 1) % NB has no reader left
+        issue(s + NB - 1);
+        const u32x4 *bp = s_stage + (size_t)(s % NB) * BLK * kWave + lane;
+        u32x4 a[2][RGW], b[NTW];
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+            for (int r = 0; r < RGW; ++r) a[pl][r] = bp[(pl * RG + wm * RGW + r) * kWave];
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) b[j] = bp[(2 * RG + wn * NTW + j) * kWave];
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+            for (int r = 0; r < RGW; ++r)
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) acc[r][j] = mfma_kstep<P>(a[pl][r], b[j], acc[r][j]);
+    }
+    wait_vm<0>();  // the trailing reloads have landed before the buffers are reused
+    __syncthreads();
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+    __syncthreads();
+    // C layout of a 16 x 16 tile: lane l, register v -> row 4 (l / 16) + v, column l % 16
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = 16 * (wm * RGW + r) + 4 * (lane >> 4) + v;
+                float x = acc[r][j][v];
+                if constexpr (ROWSCALE) x *= s_inv[row];
+                s_tile[row * (COLS + 1) + 16 * (wn * NTW + j) + (lane & 15)] = x;
+            }
+    __syncthreads();
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+template <int NT, int RG, int WM, int EP, int NB>
+static hipError_t launch_prompt_dma(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    const size_t lds = (size_t)prompt_dma_lds_floats<NT, RG, EP, NB>() * sizeof(float);
+    if (rows < 1 || rows > p.rr.cap || p.rr.cap % ROWS != 0 || p.lda % 32 != 0 || p.cols % 16 != 0)
+        return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.n_wg = (p.cols + COLS - 1) / COLS;
+    q.row_tiles = (rows + ROWS - 1) / ROWS;
+    const dim3 grid((unsigned)((q.n_wg + 7) / 8 * 8 * q.row_tiles));  // column groups padded to 8 XCDs
+    auto kern = gemm_prompt_dma_kernel<NT, RG, WM, EP, NB>;
+    if (e0 || e1)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    return hipGetLastError();
+}
+
 template <int NT, int RG, int WM, int EP, int DP>
 static hipError_t launch_prompt_t(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -530,13 +682,14 @@ static hipError_t launch_prompt_t(const GemmParams &p, int rows, hipStream_t s, 
 hipError_t launch_gemm_prompt(GemmKind kind, int rows, const GemmParams &p, hipStream_t s, hipEvent_t e0,
                               hipEvent_t e1) {
     switch (kind) {
-    // tiles measured at the LLaMA-2-7B shape, 512 rows (each kernel is bound by the rate at which
-    // one CU pulls operand bytes, ~55 GB/s): 64 x 256 for QKV (151 us) and gate/up (190 us; 128 x
-    // 128: 169 / 222 us), 64 x 128 for O (48 us) and down (102 us; 128 x 128: 77 / 165 us)
+    // measured at the LLaMA-2-7B shape, 512 rows, random operands: QKV and gate/up take the LDS-DMA
+    // kernel with three buffers (64 x 128 tiles for QKV: 114 us, LDS-staged 64 x 256: 167 us;
+    // 64 x 256 for gate/up: 177-199 us, LDS-staged: 245 us); O and down the LDS-staged kernel
+    // with 64 x 128 tiles (55 and 111 us; the DMA kernel measured no faster for O, slower for down)
     case GEMM_QKV:
-        return launch_prompt_t<16, 4, 2, E_QKV, kPromptDepth>(p, rows, s, e0, e1);
+        return launch_prompt_dma<8, 4, 2, E_QKV, 3>(p, rows, s, e0, e1);
     case GEMM_GATE_UP:
-        return launch_prompt_t<16, 4, 2, E_SWIGLU, kPromptDepth>(p, rows, s, e0, e1);
+        return launch_prompt_dma<16, 4, 2, E_SWIGLU, 3>(p, rows, s, e0, e1);
     case GEMM_O:
     case GEMM_DOWN:  // X += H W_d^T with the residual epilogue (no K split)
         return launch_prompt_t<8, 4, 2, E_RESID, kPromptDepth>(p, rows, s, e0, e1);

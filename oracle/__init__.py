@@ -43,7 +43,7 @@ class _Stats(ctypes.Structure):
 
 def build(verbose=False):
     """Compile oracle.c into liboracle.so (always recompiles)."""
-    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    cmd = ["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

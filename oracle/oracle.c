@@ -19,11 +19,10 @@
  *
  * Precision: every intermediate is a double. With round_bf16 set (the bf16 precision contract),
  * the weights hold bf16 values and the keys and values written to the cache (after RoPE) are
- * rounded to bfloat16 (round to nearest, ties to even); no other value is rounded. The input of
- * a product that follows an RMSNorm is x (.) g and the RMSNorm row factor
- * 1/sqrt(mean(x^2) + eps) scales the product's output (mathematically the same as normalising
- * first). Argmax decisions are taken on the logits rounded to fp32, the precision the GPU path
- * decides in; ties go to the lowest id.
+ * rounded to bfloat16 (round to nearest, ties to even); no other value is rounded. Each
+ * RMSNorm is applied as written, x / sqrt(mean(x^2) + eps) (.) g, and its output is the input
+ * of the product that follows. Argmax decisions are taken on the logits rounded to fp32, the
+ * precision the GPU path decides in; ties go to the lowest id.
  *
  * Reading of the acceptance rule (the algorithm's fast-forward count): the block z holds the
  * known-correct pending token at index 0, the model's output at row k is the prediction for
@@ -131,18 +130,6 @@ void orc_rmsnorm(const double *x, int32_t n, const float *g, double eps, int32_t
         double y = x[k] * inv * (double)g[k];
         out[k] = round_bf16 ? orc_bf16(y) : y;
     }
-}
-
-/* Input of a matrix product that follows an RMSNorm: the operand is x (.) g and the row factor
- * inv is applied to the product, y = inv * (operand . W^T), which equals rmsnorm(x) . W^T. */
-static void norm_operand(const double *x, int32_t n, const float *g, double eps, double *a, double *inv) {
-    *inv = orc_rms_inv(x, n, eps);
-    for (int32_t k = 0; k < n; ++k) a[k] = x[k] * (double)g[k];
-}
-
-static void scale_rows(double *y, int32_t rows, int32_t cols, const double *inv) {
-    for (int32_t r = 0; r < rows; ++r)
-        for (int32_t c = 0; c < cols; ++c) y[(size_t)r * cols + c] *= inv[r];
 }
 
 /* Rotate-half RoPE at absolute position t: the pair (x_j, x_{j+hd/2}) is rotated by the angle
@@ -262,32 +249,53 @@ void orc_model_free(orc_model *m) {
     free(m);
 }
 
-/* y[r][o] = sum_i a[r][i] * W[o][i] for rows r < rows. */
+/* y[r][o] = sum_i a[r][i] * W[o][i] for rows r < rows; every sum is taken over i in increasing
+ * order, one multiply and one add per term (no fused multiply-add: the build has none). For
+ * speed each thread owns a contiguous range of outputs o and takes the rows eight at a time
+ * (copied side by side, so that one pass over a weight row feeds eight independent sums); the
+ * value of every sum is that of the plain loop. */
+#define ORC_ROWS 8
 static void linear(const double *a, int32_t rows, const float *W, int32_t in, int32_t out, double *y) {
-#pragma omp parallel for schedule(static)
-    for (int32_t o = 0; o < out; ++o) {
-        const float *w = W + (size_t)o * in;
-        for (int32_t r = 0; r < rows; ++r) {
-            const double *x = a + (size_t)r * in;
-            double acc = 0.0;
-            for (int32_t i = 0; i < in; ++i) acc += x[i] * (double)w[i];
-            y[(size_t)r * out + o] = acc;
+#pragma omp parallel
+    {
+#ifdef _OPENMP
+        const int nt = omp_get_num_threads(), t = omp_get_thread_num();
+#else
+        const int nt = 1, t = 0;
+#endif
+        const int32_t o0 = (int32_t)((int64_t)out * t / nt), o1 = (int32_t)((int64_t)out * (t + 1) / nt);
+        double *xt = (double *)malloc(sizeof(double) * (size_t)(in > 0 ? in : 1) * ORC_ROWS);
+        for (int32_t r0 = 0; xt && r0 < rows; r0 += ORC_ROWS) {
+            const int32_t nr = rows - r0 < ORC_ROWS ? rows - r0 : ORC_ROWS;
+            for (int32_t i = 0; i < in; ++i)
+                for (int32_t r = 0; r < ORC_ROWS; ++r)
+                    xt[(size_t)i * ORC_ROWS + r] = r < nr ? a[(size_t)(r0 + r) * in + i] : 0.0;
+            for (int32_t o = o0; o < o1; ++o) {
+                const float *w = W + (size_t)o * in;
+                double acc[ORC_ROWS] = {0.0};
+                for (int32_t i = 0; i < in; ++i) {
+                    const double wi = (double)w[i];
+                    for (int32_t r = 0; r < ORC_ROWS; ++r) acc[r] += xt[(size_t)i * ORC_ROWS + r] * wi;
+                }
+                for (int32_t r = 0; r < nr; ++r) y[(size_t)(r0 + r) * out + o] = acc[r];
+            }
         }
+        free(xt);
     }
 }
 
-/* Forward of m rows at positions pos0 .. pos0+m-1 against cache rows 0 .. pos0-1.
- * Row i attends to cache positions 0 .. pos0+i; its own key and value are written to the
- * cache at position pos0+i first (this is the causal mask over the block, Section 3.1).
- * logits: m x vocab (may be NULL when only the cache is wanted). */
-/* Forward of m tokens at positions pos0..pos0+m-1 over the cache; writes the rows' logits
- * (m x vocab) and, if hidden is not NULL, the LM head's input rows RMSNorm(x) (.) g_final
- * (m x d_model). */
-static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t pos0, double *logits, double *hidden) {
+/* Forward of m tokens at positions pos0 .. pos0+m-1 against cache rows 0 .. pos0-1. Row i
+ * attends to cache positions 0 .. pos0+i; its own key and value are written to the cache at
+ * position pos0+i first (the causal mask over the block, Section 3.1). If logits is not NULL it
+ * receives the logits of rows lm0 .. m-1 ((m - lm0) x vocab; the LM head runs on those rows
+ * only); if hidden is not NULL it receives the LM head's input rows RMSNorm(x) (.) g_final of
+ * every row (m x d_model). */
+static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t pos0, double *logits, int32_t lm0,
+                        double *hidden) {
     const orc_model *M = st->m;
     const orc_config *c = &M->c;
     int32_t d = c->d_model, F = c->ffn_dim, H = c->n_heads, hd = c->head_dim, V = c->vocab;
-    if (pos0 + m > st->max_ctx) return -1;
+    if (pos0 + m > st->max_ctx || lm0 < 0 || lm0 >= m) return -1;
     double *h = (double *)calloc((size_t)m * d, sizeof(double));
     double *a = (double *)calloc((size_t)m * d, sizeof(double));
     double *q = (double *)calloc((size_t)m * d, sizeof(double));
@@ -297,9 +305,8 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
     double *y = (double *)calloc((size_t)m * d, sizeof(double));
     double *g = (double *)calloc((size_t)m * F, sizeof(double));
     double *u = (double *)calloc((size_t)m * F, sizeof(double));
-    double *inv = (double *)calloc((size_t)m, sizeof(double));
-    if (!h || !a || !q || !kk || !vv || !o || !y || !g || !u || !inv) {
-        free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u); free(inv);
+    if (!h || !a || !q || !kk || !vv || !o || !y || !g || !u) {
+        free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u);
         return -2;
     }
 
@@ -311,13 +318,10 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         double *Vc = st->v + (size_t)l * st->max_ctx * d;
         /* attention sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, a + (size_t)i * d, inv + i);
+            orc_rmsnorm(h + (size_t)i * d, d, M->attn_norm[l], c->rms_eps, 0, a + (size_t)i * d);
         linear(a, m, M->wq[l], d, d, q);
         linear(a, m, M->wk[l], d, d, kk);
         linear(a, m, M->wv[l], d, d, vv);
-        scale_rows(q, m, d, inv);
-        scale_rows(kk, m, d, inv);
-        scale_rows(vv, m, d, inv);
         for (int32_t i = 0; i < m; ++i) {
             for (int32_t hh = 0; hh < H; ++hh) {
                 orc_rope(q + (size_t)i * d + hh * hd, hd, pos0 + i, c->rope_base);
@@ -338,27 +342,20 @@ static int forward_rows(orc_state *st, const int32_t *tok, int32_t m, int32_t po
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
         /* SwiGLU feed-forward sub-layer */
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, a + (size_t)i * d, inv + i);
+            orc_rmsnorm(h + (size_t)i * d, d, M->ffn_norm[l], c->rms_eps, 0, a + (size_t)i * d);
         linear(a, m, M->wg[l], d, F, g);
         linear(a, m, M->wu[l], d, F, u);
-        scale_rows(g, m, F, inv);
-        scale_rows(u, m, F, inv);
         for (size_t ix = 0; ix < (size_t)m * F; ++ix) g[ix] = orc_silu(g[ix]) * u[ix];
         linear(g, m, M->wd[l], F, d, y);
         for (size_t ix = 0; ix < (size_t)m * d; ++ix) h[ix] += y[ix];
     }
     if (logits || hidden) {
         for (int32_t i = 0; i < m; ++i)
-            norm_operand(h + (size_t)i * d, d, M->final_norm, c->rms_eps, a + (size_t)i * d, inv + i);
-        if (hidden)
-            for (int32_t i = 0; i < m; ++i)
-                for (int32_t k = 0; k < d; ++k) hidden[(size_t)i * d + k] = a[(size_t)i * d + k] * inv[i];
-        if (logits) {
-            linear(a, m, M->lm_head, d, V, logits);
-            scale_rows(logits, m, V, inv);
-        }
+            orc_rmsnorm(h + (size_t)i * d, d, M->final_norm, c->rms_eps, 0, a + (size_t)i * d);
+        if (hidden) memcpy(hidden, a, sizeof(double) * (size_t)m * d);
+        if (logits) linear(a + (size_t)lm0 * d, m - lm0, M->lm_head, d, V, logits);
     }
-    free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u); free(inv);
+    free(h); free(a); free(q); free(kk); free(vv); free(o); free(y); free(g); free(u);
     return 0;
 }
 
@@ -398,13 +395,12 @@ int32_t orc_state_pending(const orc_state *st) { return st->pending; }
 int32_t orc_prefill(orc_state *st, const int32_t *prompt, int32_t len, double *logits_last) {
     const orc_config *c = &st->m->c;
     if (len < 1 || len > st->max_ctx) return -1;
-    double *lg = (double *)malloc(sizeof(double) * (size_t)len * c->vocab);
+    double *lg = (double *)malloc(sizeof(double) * (size_t)c->vocab);
     if (!lg) return -2;
-    int rc = forward_rows(st, prompt, len, 0, lg, NULL);
+    int rc = forward_rows(st, prompt, len, 0, lg, len - 1, NULL);
     if (rc) { free(lg); return -3; }
-    const double *last = lg + (size_t)(len - 1) * c->vocab;
-    int32_t y0 = orc_argmax(last, c->vocab);
-    if (logits_last) memcpy(logits_last, last, sizeof(double) * c->vocab);
+    int32_t y0 = orc_argmax(lg, c->vocab);
+    if (logits_last) memcpy(logits_last, lg, sizeof(double) * c->vocab);
     free(lg);
     if (y0 < 0) return -4;
     st->L = len;
@@ -417,14 +413,14 @@ int32_t orc_prefill(orc_state *st, const int32_t *prompt, int32_t len, double *l
  * block are written to the cache provisionally; nothing is committed). */
 int32_t orc_eval_block(orc_state *st, const int32_t *block, int32_t m, double *logits) {
     if (!st->prefilled || m < 1 || st->L + m > st->max_ctx) return -1;
-    return forward_rows(st, block, m, st->L, logits, NULL) ? -3 : 0;
+    return forward_rows(st, block, m, st->L, logits, 0, NULL) ? -3 : 0;
 }
 
 /* The LM head's input rows (m x d_model) of an iteration over block[0..m) at positions
  * L .. L+m-1 (as orc_eval_block: nothing is committed). */
 int32_t orc_eval_block_hidden(orc_state *st, const int32_t *block, int32_t m, double *hidden) {
     if (!st->prefilled || m < 1 || st->L + m > st->max_ctx) return -1;
-    return forward_rows(st, block, m, st->L, NULL, hidden) ? -3 : 0;
+    return forward_rows(st, block, m, st->L, NULL, 0, hidden) ? -3 : 0;
 }
 
 /* Commit a accepted tokens (their cache rows become permanent) and set the pending token. */
@@ -461,7 +457,7 @@ int32_t orc_jacobi_step(orc_state *st, const int32_t *block_in, int32_t m, int32
 int32_t orc_forward_full(const orc_model *m, const int32_t *tokens, int32_t T, double *logits) {
     orc_state *st = orc_state_new(m, T);
     if (!st) return -2;
-    int rc = forward_rows(st, tokens, T, 0, logits, NULL);
+    int rc = forward_rows(st, tokens, T, 0, logits, 0, NULL);
     orc_state_free(st);
     return rc ? -3 : 0;
 }
@@ -482,7 +478,7 @@ int32_t orc_ar_decode(const orc_model *m, const int32_t *prompt, int32_t len, in
     for (int32_t t = 0; rc == 0 && t < max_new; ++t) {
         out[t] = y;
         if (t + 1 == max_new) break;
-        if (forward_rows(st, &y, 1, st->L, lg, NULL)) { rc = -3; break; }
+        if (forward_rows(st, &y, 1, st->L, lg, 0, NULL)) { rc = -3; break; }
         st->L += 1;
         y = orc_argmax(lg, m->c.vocab);
         if (y < 0) rc = -4;

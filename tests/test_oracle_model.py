@@ -181,42 +181,64 @@ def test_provisional_rows_are_overwritten():
 
 
 @pytest.mark.parametrize("bf16_cache", [False, True])
-@pytest.mark.parametrize("key_coord", [0, HD // 2])
-def test_two_token_rope_attention_closed_form(key_coord, bf16_cache):
-    # Head 0 only: the second token's query is c*e_0, the first token's key is kap*c*e_j
-    # (j = 0 or the rotate-half partner hd/2), the second token's key is zero. After RoPE at
-    # positions 1 and 0 the score of key 0 is c^2 kap cos(1) / sqrt(hd) for j = 0 and
-    # c^2 kap sin(1) / sqrt(hd) for j = hd/2; the score of key 1 is 0. So the attention weight
-    # of token 0 is the logistic function of that score. Values route to distinct outputs.
-    # Under the bf16 contract the cached key kap*c and values c enter as their bf16 roundings.
+@pytest.mark.parametrize("partner", [False, True])
+@pytest.mark.parametrize("head,pair,offset", [(0, 0, 0), (H - 1, 0, 0), (2, 1, 3), (H - 1, HD // 2 - 1, 5)])
+def test_two_token_rope_attention_closed_form(head, pair, offset, partner, bf16_cache):
+    # One head h, one rotate-half pair j of it: the second token's query is c*e_j (dims within
+    # head h), the first token's key is kap*c*e_j, or kap*c*e_{j+hd/2} for the partner, the
+    # second token's key is zero. RoPE rotates the pair by t*theta_j with theta_j = base^(-2j/hd);
+    # the key sits at position 0 (no rotation) and the query at position 1, so the score of key 0
+    # is c^2 kap cos(theta_j) / sqrt(hd), or c^2 kap sin(theta_j) / sqrt(hd) for the partner; the
+    # score of key 1 is 0. The attention weight of token 0 is the logistic function of that
+    # score. Values route through head h's dims to distinct outputs. A head offset on the query,
+    # key or value side, a frequency indexed by the dim across heads, or a wrong partner all
+    # change the weight. Under the bf16 contract the cached key (after its rotation) and the
+    # values c enter as their bf16 roundings. With offset > 0 the two tokens sit at positions offset and
+    # offset + 1 behind `offset` filler tokens whose queries, keys and values are zero: both the
+    # key and the query are rotated, the score depends on their distance only, and the last
+    # row's softmax also gives each filler key (score 0, value 0) the weight of key 1.
     cfg = _cfg(1)
     ts = _base_tensors(cfg)
     x0, x1, kap, beta, s = 10, 20, 1.75, 0.875, 1.0
+    base = head * HD
+    key_dim = pair + (HD // 2 if partner else 0)
     Wq = np.zeros((D, D), np.float32)
     Wk = np.zeros((D, D), np.float32)
     Wv = np.zeros((D, D), np.float32)
     Wo = np.zeros((D, D), np.float32)
-    Wq[0, x1] = 1.0
-    Wk[key_coord, x0] = kap
-    Wv[2, x0] = 1.0
-    Wv[5, x1] = 1.0
-    Wo[33, 2] = beta
-    Wo[44, 5] = beta
+    Wq[base + pair, x1] = 1.0
+    Wk[base + key_dim, x0] = kap
+    Wv[base + 2, x0] = 1.0
+    Wv[base + 5, x1] = 1.0
+    Wo[33, base + 2] = beta
+    Wo[44, base + 5] = beta
     ts[1 + 1], ts[1 + 2], ts[1 + 3], ts[1 + 4] = Wq, Wk, Wv, Wo
     m = oracle.Model(cfg, ts, round_bf16=bf16_cache)
-    lg = m.forward_full(np.array([x0, x1], dtype=np.int32))
+    pad = 7
+    lg = m.forward_full(np.array([pad] * offset + [x0, x1], dtype=np.int32))
     c = s / math.sqrt(s * s / D + cfg.rms_eps)
     cached = oracle.bf16 if bf16_cache else (lambda v: v)
-    trig = math.cos(1.0) if key_coord == 0 else math.sin(1.0)
-    w = expit(c * trig * cached(kap * c) / math.sqrt(HD))
+    theta = cfg.rope_base ** (-2.0 * pair / HD)
+    # key rotated by offset*theta (then cached), query by (offset+1)*theta; without rounding the
+    # score is c^2 kap cos(theta) (sin(theta) for the partner)
+    phi, psi = offset * theta, (offset + 1) * theta
+    kj, kp = (-kap * c * math.sin(phi), kap * c * math.cos(phi)) if partner else \
+        (kap * c * math.cos(phi), kap * c * math.sin(phi))
+    sc = c * (math.cos(psi) * cached(kj) + math.sin(psi) * cached(kp)) / math.sqrt(HD)
+    if not bf16_cache:
+        trig = math.sin(theta) if partner else math.cos(theta)
+        assert abs(sc - c * c * kap * trig / math.sqrt(HD)) < 1e-12
+    w0, w1 = math.exp(sc) / (math.exp(sc) + offset + 1), 1.0 / (math.exp(sc) + offset + 1)
     vc = cached(c)
-    expect_h = [np.zeros(D), np.zeros(D)]
-    expect_h[0][x0] += s
-    expect_h[0][33] += beta * vc
-    expect_h[1][x1] += s
-    expect_h[1][33] += beta * vc * w
-    expect_h[1][44] += beta * vc * (1 - w)
-    for t in range(2):
+    expect_h = [np.zeros(D) for _ in range(offset + 2)]
+    for t in range(offset):
+        expect_h[t][pad] += s
+    expect_h[offset][x0] += s
+    expect_h[offset][33] += beta * vc / (offset + 1)  # its query is zero: uniform over its prefix
+    expect_h[offset + 1][x1] += s
+    expect_h[offset + 1][33] += beta * vc * w0
+    expect_h[offset + 1][44] += beta * vc * w1
+    for t in range(offset + 2):
         h = expect_h[t]
         nh = h / math.sqrt(np.mean(h * h) + cfg.rms_eps)
         np.testing.assert_allclose(lg[t], s * nh[:V], rtol=0, atol=1e-12)

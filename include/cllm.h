@@ -172,7 +172,10 @@ cllm_status cllm_jacobi_step(cllm_ctx *ctx, int32_t seq, const int32_t *block_in
 
 /* Jacobi decoding of max_new tokens after a prefill of the prompt, in blocks of n
  * (1 <= n <= max_block), with the iteration loop resident on the device (no host round trip
- * per iteration). out_tokens receives max_new ids (y0 first). guess may be NULL (uniform
+ * per iteration): the appendix algorithm "Jacobi Decoding with KV Cache" (prefill, then per
+ * block the iterations of eq. jacobi_decoding until the block reproduces itself, keeping the KV
+ * of accepted tokens), applied to one n-token truncation after another as Section 3.2.1 decodes
+ * long responses; Section 3.1 fixes the result, the greedy output of eq. ar_decoding. out_tokens receives max_new ids (y0 first). guess may be NULL (uniform
  * guesses, shrink). stats may be NULL. The output equals greedy AR decoding.
  * Errors: those of cllm_prefill, ERR_ARG (n, max_new, guess stream too short),
  * ERR_CAPACITY (len + max_new + n > max_ctx or max_new above the context's max_new). */
@@ -185,8 +188,10 @@ cllm_status cllm_jacobi_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt
 cllm_status cllm_ar_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t len, int32_t max_new,
                            int32_t *out_tokens, cllm_decode_stats *stats);
 
-/* Batched Jacobi iteration (the batched ragged variant of the iteration): one forward pass over
- * the blocks of B sequence slots at once, each against its own cache. Entry b is slot
+/* Batched Jacobi iteration (the batched ragged variant of the iteration; the paper generates
+ * its Jacobi trajectories at batch size 16, appendix "Computation cost for CLLMs training"): one
+ * forward pass over the blocks of B sequence slots at once, each against its own cache, each
+ * entry one iteration of eq. jacobi_decoding with the cache (Section 3.1). Entry b is slot
  * seq_ids[b] (distinct, prefilled) with block blocks_in[b * max_block + i], i < m[b]
  * (1 <= m[b] <= max_block, blocks_in[b * max_block] == the slot's pending token). Outputs as
  * cllm_jacobi_step, per entry: blocks_out[b * max_block + i] and accepted[b]. Every row is
@@ -196,8 +201,11 @@ cllm_status cllm_ar_decode(cllm_ctx *ctx, int32_t seq, const int32_t *prompt, in
 cllm_status cllm_jacobi_step_batch(cllm_ctx *ctx, int32_t B, const int32_t *seq_ids, const int32_t *blocks_in,
                                    const int32_t *m, int32_t *blocks_out, int32_t *accepted);
 
-/* Batched Jacobi decoding: prefill B prompts (prompt b is prompts[off_b .. off_b + lens[b]),
- * off_b = lens[0] + ... + lens[b-1]) into slots seq_ids[b], then decode max_new tokens for
+/* Batched Jacobi decoding (the appendix algorithm "Jacobi Decoding with KV Cache" for B sequences
+ * at once, as the appendix "Computation cost for CLLMs training" generates trajectories at
+ * batch size 16; each sequence's output is Section 3.1's greedy fixed point): prefill B prompts
+ * (prompt b is prompts[off_b .. off_b + lens[b]), off_b = lens[0] + ... + lens[b-1]) into
+ * slots seq_ids[b], then decode max_new tokens for
  * each in blocks of n, all sequences in one device-resident loop whose iterations run the
  * blocks of every unfinished sequence together (sequences finish at different iterations).
  * guesses: B specs (NULL = uniform guesses, shrink); a spec's draws use its slot id as `seq`.

@@ -11,8 +11,9 @@
  * Conventions for every call:
  *   - Token arrays are HOST int32 arrays owned by the caller; they are read or written only
  *     during the call. Ids must lie in [0, vocab).
- *   - The library owns all device memory (weights, KV cache, workspace); everything is
- *     released by cllm_model_free.
+ *   - The library owns its device memory (weights, KV cache, workspace) and releases it in
+ *     cllm_model_free, except an iteration workspace the caller hands over in
+ *     cllm_runtime_opts.workspace (e.g. a PyTorch tensor), which stays the caller's.
  *   - Work is queued on the stream given at creation (a hipStream_t; NULL = the default
  *     stream). cllm_prefill, cllm_jacobi_step, cllm_jacobi_decode and cllm_ar_decode return
  *     after the device work has completed.
@@ -66,14 +67,31 @@ typedef struct cllm_config {
  * multiple of 64, at most 4096, and to no more than max_ctx rounded up to 64). A prompt is
  * processed in chunks of that many rows; a row's values do not depend on the chunk size (every
  * reduction has an order fixed by the model shape), so the size changes speed and activation
- * memory only (about 200 KiB per row at the LLaMA-2-7B shape). */
+ * memory only (about 200 KiB per row at the LLaMA-2-7B shape).
+ * workspace, workspace_bytes: optional caller-owned device memory of the context's GPU (for
+ * example a PyTorch tensor on that device), 256-byte aligned, of at least cllm_workspace_bytes()
+ * bytes, or NULL (0 bytes) for library-allocated memory. When given, the context's iteration
+ * workspace (activation operands, split and attention partials, argmax partials, control blocks,
+ * the row table, token staging and decode outputs: every buffer made at creation except the
+ * weights, the RoPE tables and the KV cache) is carved from it and zeroed at creation; the
+ * library never frees it, and the caller keeps it alive and leaves it untouched until
+ * cllm_model_free returns. Buffers made on demand later (debug logits, trajectory records, the
+ * loss head's workspace) are still the library's. Errors of cllm_model_create: ERR_ARG (not
+ * device memory of that GPU, misaligned, or bytes without a pointer), ERR_CAPACITY (too small). */
 typedef struct cllm_runtime_opts {
     int32_t max_ctx, max_block, max_new;
     int32_t device;  /* HIP device ordinal */
     void *stream;    /* hipStream_t or NULL */
     int32_t max_batch;
     int32_t prefill_chunk;
+    void *workspace;        /* caller-owned device buffer, or NULL */
+    size_t workspace_bytes;
 } cllm_runtime_opts;
+
+/* Bytes of the iteration workspace of a context created with cfg and opts (their workspace
+ * fields are ignored): the least workspace_bytes that cllm_model_create accepts with a caller
+ * workspace. No device call. Errors: ERR_ARG (as cllm_model_create's checks), ERR_OOM. */
+cllm_status cllm_workspace_bytes(const cllm_config *cfg, const cllm_runtime_opts *opts, size_t *bytes);
 
 /* Guess provider of the decode (reading of the paper's random initial n-token sequence).
  * policy CLLM_GUESS_UNIFORM: uniform ids. CLLM_GUESS_STREAM: stream[t], corrupted with rate p,

@@ -29,7 +29,7 @@ class cllm_config(ctypes.Structure):
 
 class cllm_runtime_opts(ctypes.Structure):
     _fields_ = [("max_ctx", _i32), ("max_block", _i32), ("max_new", _i32), ("device", _i32), ("stream", _vp),
-                ("max_batch", _i32), ("prefill_chunk", _i32)]
+                ("max_batch", _i32), ("prefill_chunk", _i32), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class cllm_guess_spec(ctypes.Structure):
@@ -55,7 +55,7 @@ EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_init_rando
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
            "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_loss_head_device", "cllm_hidden_rows", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
-           "cllm_streamed_weight_bytes", "cllm_status_string", "cllm_last_error"]
+           "cllm_streamed_weight_bytes", "cllm_workspace_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
 
@@ -101,6 +101,7 @@ def lib():
                                           P(_i64)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
         L.cllm_timing_read.argtypes = [_vp, P(_i64), P(_dbl)]
+        L.cllm_workspace_bytes.argtypes = [P(cllm_config), P(cllm_runtime_opts), P(ctypes.c_size_t)]
         L.cllm_streamed_weight_bytes.argtypes = [_vp]
         L.cllm_streamed_weight_bytes.restype = _i64
         L.cllm_status_string.argtypes = [_i32]
@@ -134,18 +135,32 @@ def thr53(p):
     return int(round(min(max(float(p), 0.0), 1.0) * float(1 << 53)))
 
 
+def workspace_bytes(cfg: ModelConfig, max_ctx, max_block=16, max_new=256, max_batch=1, prefill_chunk=0):
+    """Bytes of caller-owned workspace a context of these options takes (cllm_workspace_bytes)."""
+    opts = cllm_runtime_opts(max_ctx, max_block, max_new, 0, None, max_batch, prefill_chunk, None, 0)
+    n = ctypes.c_size_t(0)
+    st = lib().cllm_workspace_bytes(ctypes.byref(make_config(cfg)), ctypes.byref(opts), ctypes.byref(n))
+    if st != CLLM_OK:
+        raise CllmError(st, "cllm_workspace_bytes failed")
+    return int(n.value)
+
+
 class Model:
     """One context of libcllm.so: model weights, KV cache and workspace on one GPU."""
 
     def __init__(self, cfg: ModelConfig, max_ctx, max_block=16, max_new=256, device=0, stream=None,
-                 weights=None, path=None, max_batch=1, random_seed=None, prefill_chunk=0):
+                 weights=None, path=None, max_batch=1, random_seed=None, prefill_chunk=0, workspace=None):
         """weights: host tensors (cllm_model_set_weights); path: a weight file (cllm_model_load);
-        random_seed: seeded synthetic weights drawn on the GPU (cllm_model_init_random)."""
+        random_seed: seeded synthetic weights drawn on the GPU (cllm_model_init_random);
+        workspace: (device pointer, bytes) of caller-owned device memory for the iteration
+        workspace (see workspace_bytes), kept alive by the caller until close()."""
         self.cfg = cfg
         self.L = lib()
         self.max_block = max_block
         self.max_batch = max_batch
-        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream, max_batch, prefill_chunk)
+        ws_ptr, ws_bytes = workspace if workspace is not None else (None, 0)
+        opts = cllm_runtime_opts(max_ctx, max_block, max_new, device, stream, max_batch, prefill_chunk, ws_ptr,
+                                 ws_bytes)
         h = _vp()
         if path is not None:
             st = self.L.cllm_model_load(os.fsencode(path), ctypes.byref(opts), ctypes.byref(h))

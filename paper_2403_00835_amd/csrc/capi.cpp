@@ -62,6 +62,10 @@ struct cllm_ctx {
     std::vector<hipEvent_t> it_ev;  // one per queued decode iteration
     int stream_cap = 0;
     std::vector<void *> allocs;
+    // caller-owned workspace (cllm_runtime_opts.workspace): the iteration buffers are carved from
+    // it instead of being allocated; it is never freed by the library
+    uint8_t *ws_base = nullptr;
+    size_t ws_size = 0, ws_off = 0;
 
     // host state per slot
     struct Slot {
@@ -154,6 +158,77 @@ cllm_status dalloc_t(cllm_ctx *c, T **p, size_t count) {
     cllm_status s = dalloc(c, &v, count * sizeof(T));
     *p = reinterpret_cast<T *>(v);
     return s;
+}
+
+// The iteration workspace of a context: activation operands, split and attention partials,
+// argmax partials, control blocks, the row table, token staging and decode outputs (every buffer
+// made at creation except the weights, the RoPE tables and the KV cache). Each buffer starts at a
+// 256-byte boundary.
+struct WsBuf {
+    void **p;
+    size_t bytes;
+};
+constexpr size_t kWsAlign = 256;
+
+std::vector<WsBuf> workspace_bufs(cllm_ctx *c) {
+    const size_t rows = c->cap, d = c->d;
+    const size_t mb = c->max_batch, max_new = c->opts.max_new;
+    c->zin_cap = std::max(c->cap, c->max_batch * c->opts.max_block);
+    c->stream_cap = c->opts.max_new + kMaxBlock;
+    auto P = [](auto **q) { return reinterpret_cast<void **>(q); };
+    // activation operands: one fp32 plane, or hi and lo bf16 planes (4 bytes per element either way)
+    return {
+        {P(&c->X), rows * d * 4},
+        {P(&c->part), (size_t)kDownSplits * rows * d * 4},
+        {P(&c->ssq), (d / 16) * rows * 4},
+        {P(&c->Q), act_plane(c->cap, c->d) * 4},
+        {P(&c->O), act_plane(c->cap, c->d) * 4},
+        {P(&c->An), act_plane(c->cap, c->d) * 4},
+        {P(&c->Hb), act_plane(c->cap, c->Fp) * 4},
+        {P(&c->pmax), (size_t)c->n_wg_lm * rows * 4},
+        {P(&c->pidx), (size_t)c->n_wg_lm * rows * 4},
+        {P(&c->opart), (size_t)c->H * c->nch * rows * c->hd * 4},
+        {P(&c->mpart), (size_t)c->H * c->nch * rows * 4},
+        {P(&c->lpart), (size_t)c->H * c->nch * rows * 4},
+        {P(&c->ctl), mb * sizeof(Ctl)},
+        {P(&c->tab), sizeof(RowTab)},
+        {P(&c->rows), rows * sizeof(RowInfo)},
+        {P(&c->zin), (size_t)c->zin_cap * 4},
+        {P(&c->out_dev), max_new * mb * 4},
+        {P(&c->mlog_dev), max_new * mb * 4},
+        {P(&c->stream_dev), (size_t)c->stream_cap * mb * 4},
+    };
+}
+
+size_t workspace_total(const std::vector<WsBuf> &bufs) {
+    size_t t = 0;
+    for (const WsBuf &b : bufs) t += (std::max<size_t>(b.bytes, 16) + kWsAlign - 1) / kWsAlign * kWsAlign;
+    return t;
+}
+
+// Place the workspace buffers: carved in order from the caller's buffer when one was given
+// (zeroed on the stream), else one hipMalloc each.
+cllm_status place_workspace(cllm_ctx *c) {
+    const std::vector<WsBuf> bufs = workspace_bufs(c);
+    if (!c->ws_base) {
+        for (const WsBuf &b : bufs) {
+            cllm_status s = dalloc(c, b.p, b.bytes);
+            if (s) return s;
+        }
+        return CLLM_OK;
+    }
+    const size_t need = workspace_total(bufs);
+    if (need > c->ws_size)
+        return fail(c, CLLM_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu bytes this context needs",
+                    c->ws_size, need);
+    c->ws_off = 0;
+    for (const WsBuf &b : bufs) {
+        *b.p = c->ws_base + c->ws_off;
+        c->ws_off += (std::max<size_t>(b.bytes, 16) + kWsAlign - 1) / kWsAlign * kWsAlign;
+    }
+    hipError_t e = hipMemsetAsync(c->ws_base, 0, need, c->stream);
+    if (e != hipSuccess) return fail(c, CLLM_ERR_DEVICE, "hipMemsetAsync failed: %s", hipGetErrorString(e));
+    return CLLM_OK;
 }
 
 // Timing events for the selected kernel class and row-group count (null when not timed).
@@ -969,29 +1044,30 @@ void cllm_model_free(cllm_ctx *c) {
     delete c;
 }
 
-cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *opts, cllm_ctx **out) {
-    if (!cfg || !opts || !out) return CLLM_ERR_ARG;
-    *out = nullptr;
+}  // extern "C"
+
+namespace {
+
+bool config_ok(const cllm_config *cfg, const cllm_runtime_opts *opts) {
     const bool bf16 = cfg->dtype == CLLM_DTYPE_BF16;
-    const int kstep = bf16 ? 32 : 16;
     if ((cfg->dtype != CLLM_DTYPE_BF16 && cfg->dtype != CLLM_DTYPE_F32) || cfg->n_layers < 1 || cfg->d_model < 1 ||
         cfg->n_heads < 1 || cfg->n_heads * cfg->head_dim != cfg->d_model ||
         !(cfg->head_dim == 32 || cfg->head_dim == 64 || cfg->head_dim == 128 ||
           (bf16 ? cfg->head_dim == 256 : cfg->head_dim == 16)) ||
         cfg->d_model % 64 != 0 || cfg->d_model > 8192 ||
         cfg->ffn_dim < 1 || cfg->vocab < 2 || !(cfg->rms_eps >= 0.0f) || !(cfg->rope_base > 0.0f))
-        return CLLM_ERR_ARG;
+        return false;
     if (opts->max_block < 1 || opts->max_block > kMaxBlock || opts->max_ctx < 2 ||
         opts->max_ctx > kMaxChunks * kAttnChunk - 2 * kMaxRows || opts->max_new < 1 || opts->max_batch < 0 ||
         opts->max_batch > kMaxSeqs || opts->prefill_chunk < 0 || opts->prefill_chunk > kMaxPrefillRows)
-        return CLLM_ERR_ARG;
-    int ndev = 0;
-    if (hipGetDeviceCount(&ndev) != hipSuccess || opts->device < 0 || opts->device >= ndev) {
-        (void)hipGetLastError();
-        return CLLM_ERR_DEVICE;
-    }
-    cllm_ctx *c = new (std::nothrow) cllm_ctx;
-    if (!c) return CLLM_ERR_OOM;
+        return false;
+    return !(opts->workspace_bytes > 0 && !opts->workspace);
+}
+
+// Shape-derived fields of a context (no device calls).
+void derive_shape(cllm_ctx *c, const cllm_config *cfg, const cllm_runtime_opts *opts) {
+    const bool bf16 = cfg->dtype == CLLM_DTYPE_BF16;
+    const int kstep = bf16 ? 32 : 16;
     c->cfg = *cfg;
     c->opts = *opts;
     c->bf16 = bf16;
@@ -1016,6 +1092,40 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
                          round_up(opts->max_ctx, kMaxRows));
     c->cap = round_up(std::max(c->dbg_rows, c->pchunk), kPromptRows);  // whole prompt-GEMM row tiles
     c->kv_seq = (size_t)c->NL * c->ctx_alloc * c->d;
+}
+
+}  // namespace
+
+extern "C" {
+
+cllm_status cllm_workspace_bytes(const cllm_config *cfg, const cllm_runtime_opts *opts, size_t *bytes) {
+    if (!cfg || !opts || !bytes) return CLLM_ERR_ARG;
+    *bytes = 0;
+    cllm_runtime_opts o = *opts;
+    o.workspace = nullptr;
+    o.workspace_bytes = 0;
+    if (!config_ok(cfg, &o)) return CLLM_ERR_ARG;
+    cllm_ctx *c = new (std::nothrow) cllm_ctx;
+    if (!c) return CLLM_ERR_OOM;
+    derive_shape(c, cfg, &o);
+    *bytes = workspace_total(workspace_bufs(c));
+    delete c;
+    return CLLM_OK;
+}
+
+cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *opts, cllm_ctx **out) {
+    if (!cfg || !opts || !out) return CLLM_ERR_ARG;
+    *out = nullptr;
+    if (!config_ok(cfg, opts)) return CLLM_ERR_ARG;
+    const int kstep = cfg->dtype == CLLM_DTYPE_BF16 ? 32 : 16;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || opts->device < 0 || opts->device >= ndev) {
+        (void)hipGetLastError();
+        return CLLM_ERR_DEVICE;
+    }
+    cllm_ctx *c = new (std::nothrow) cllm_ctx;
+    if (!c) return CLLM_ERR_OOM;
+    derive_shape(c, cfg, opts);
     c->slot.assign(c->max_batch, cllm_ctx::Slot{});
 
     auto bail = [&](cllm_status s) {
@@ -1025,7 +1135,6 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     if (hipSetDevice(opts->device) != hipSuccess) return bail(CLLM_ERR_DEVICE);
     cllm_status s;
     const size_t E = c->elem;
-    const size_t rows = c->cap;
     if ((s = dalloc(c, &c->embed, (size_t)c->V * c->d * E))) return bail(s);
     c->g_attn.assign(c->NL, nullptr);
     c->g_ffn.assign(c->NL, nullptr);
@@ -1044,28 +1153,19 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     const int h2 = c->hd / 2;
     if ((s = dalloc_t(c, &c->rcos, (size_t)c->ctx_alloc * h2))) return bail(s);
     if ((s = dalloc_t(c, &c->rsin, (size_t)c->ctx_alloc * h2))) return bail(s);
-    if ((s = dalloc_t(c, &c->X, rows * c->d))) return bail(s);
-    if ((s = dalloc_t(c, &c->part, (size_t)kDownSplits * rows * c->d))) return bail(s);
-    if ((s = dalloc_t(c, &c->ssq, (size_t)(c->d / 16) * rows))) return bail(s);
-    // activation operands: one fp32 plane, or hi and lo bf16 planes (4 bytes per element either way)
-    if ((s = dalloc(c, &c->Q, act_plane(c->cap, c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->O, act_plane(c->cap, c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->An, act_plane(c->cap, c->d) * 4))) return bail(s);
-    if ((s = dalloc(c, &c->Hb, act_plane(c->cap, c->Fp) * 4))) return bail(s);
-    if ((s = dalloc_t(c, &c->pmax, (size_t)c->n_wg_lm * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->pidx, (size_t)c->n_wg_lm * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->opart, (size_t)c->H * c->nch * rows * c->hd))) return bail(s);
-    if ((s = dalloc_t(c, &c->mpart, (size_t)c->H * c->nch * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->lpart, (size_t)c->H * c->nch * rows))) return bail(s);
-    if ((s = dalloc_t(c, &c->ctl, (size_t)c->max_batch))) return bail(s);
-    if ((s = dalloc_t(c, &c->tab, 1))) return bail(s);
-    if ((s = dalloc_t(c, &c->rows, rows))) return bail(s);
-    c->zin_cap = std::max(c->cap, c->max_batch * opts->max_block);
-    if ((s = dalloc_t(c, &c->zin, (size_t)c->zin_cap))) return bail(s);
-    if ((s = dalloc_t(c, &c->out_dev, (size_t)opts->max_new * c->max_batch))) return bail(s);
-    if ((s = dalloc_t(c, &c->mlog_dev, (size_t)opts->max_new * c->max_batch))) return bail(s);
-    c->stream_cap = opts->max_new + kMaxBlock;
-    if ((s = dalloc_t(c, &c->stream_dev, (size_t)c->stream_cap * c->max_batch))) return bail(s);
+    if (opts->workspace) {
+        // the caller's device buffer: device memory of this context's GPU
+        hipPointerAttribute_t a{};
+        if (hipPointerGetAttributes(&a, opts->workspace) != hipSuccess || a.type != hipMemoryTypeDevice ||
+            a.device != opts->device) {
+            (void)hipGetLastError();
+            return bail(CLLM_ERR_ARG);
+        }
+        c->ws_base = static_cast<uint8_t *>(opts->workspace);
+        c->ws_size = opts->workspace_bytes;
+        if (reinterpret_cast<uintptr_t>(c->ws_base) % kWsAlign != 0) return bail(CLLM_ERR_ARG);
+    }
+    if ((s = place_workspace(c))) return bail(s);
 
     // RoPE table: angle t * base^(-2j/hd) in double, rounded once to fp32.
     std::vector<float> hc((size_t)c->ctx_alloc * h2), hs((size_t)c->ctx_alloc * h2);

@@ -103,3 +103,16 @@ def test_truncated_weight_file_rejected(lib, tmp_path):
     p = tmp_path / "bad.bin"
     p.write_bytes(b"NOTCLLM!" + b"\0" * 56)
     assert lib.cllm_model_load(str(p).encode(), ctypes.byref(opts), ctypes.byref(h)) == 6
+
+
+def test_workspace_bytes_without_device(lib):
+    # the size query needs no GPU; it grows with the row capacity and rejects what creation rejects
+    from paper_2403_00835_amd import binding
+    from paper_2403_00835_amd.configs import LLAMA7B, TINY
+    a = binding.workspace_bytes(TINY, max_ctx=256, max_block=8, max_new=32)
+    b = binding.workspace_bytes(TINY, max_ctx=256, max_block=8, max_new=32, max_batch=16)
+    assert 0 < a < b and a % 256 == 0
+    c = binding.workspace_bytes(LLAMA7B, max_ctx=704, max_block=16, max_new=256)
+    assert c > 64 * 4096 * 4 * 5  # at least the 512-row activation planes
+    with pytest.raises(binding.CllmError):
+        binding.workspace_bytes(TINY, max_ctx=256, max_block=65, max_new=32)

@@ -12,7 +12,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# CLLM_HOST_SANITIZE=1: the build with address and undefined-behaviour checks (build_host_sanitized)
+_SANITIZE = os.environ.get("CLLM_HOST_SANITIZE") == "1"
+_LIB = os.path.join(_HERE, "liboracle.hostsan.so" if _SANITIZE else "liboracle.so")
 _lib = None
 
 _vp = ctypes.c_void_p
@@ -52,10 +54,24 @@ def build(verbose=False):
     _lib = None
 
 
+def build_host_sanitized(clang, verbose=False):
+    """Compile oracle.c with address and undefined-behaviour checks (clang, the sanitizer runtime
+    shared with the other host-sanitized libraries) into liboracle.hostsan.so."""
+    out = os.path.join(_HERE, "liboracle.hostsan.so")
+    cmd = [clang, "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined", "-shared-libasan",
+           "-fopenmp", "-fPIC", "-shared", "-o", out + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+
+
 def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB):
+            if _SANITIZE:
+                raise RuntimeError(f"{_LIB} is not built (build.py --host-sanitize)")
             build()
         L = ctypes.CDLL(_LIB)
         L.orc_num_threads.restype = _i32

@@ -10,7 +10,10 @@ import numpy as np
 from .configs import ModelConfig
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libcllm.so")
+# CLLM_HOST_SANITIZE=1 selects the build with address and undefined-behaviour checks on the host
+# code (build.py --host-sanitize), for runs of the CPU tests under the sanitizer runtime.
+HOST_SANITIZE = os.environ.get("CLLM_HOST_SANITIZE") == "1"
+LIB_PATH = os.path.join(_HERE, "libcllm.hostsan.so" if HOST_SANITIZE else "libcllm.so")
 
 CLLM_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_ARG", 2: "ERR_STATE", 3: "ERR_CAPACITY", 4: "ERR_OOM", 5: "ERR_IO",

@@ -1017,7 +1017,12 @@ cllm_status load_weights(cllm_ctx *c, const WeightSource &src) {
 extern "C" {
 
 const char *cllm_status_string(cllm_status s) {
-    switch (s) {
+    // A C caller may pass any int; in C++ loading an enum object whose value lies outside the
+    // enumerators' range is undefined, so the value is read from the object's bytes.
+    int32_t v = 0;
+    static_assert(sizeof(cllm_status) == sizeof(int32_t), "cllm_status is an int");
+    std::memcpy(&v, &s, sizeof v);
+    switch (v) {
     case CLLM_OK: return "ok";
     case CLLM_ERR_ARG: return "invalid argument";
     case CLLM_ERR_STATE: return "invalid state";

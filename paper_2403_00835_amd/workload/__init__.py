@@ -14,7 +14,9 @@ from ..configs import SEED_BATCH, ModelConfig, SEED_PROMPT, SEED_WEIGHTS
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")
-_LIB = os.path.join(_HERE, "libcllm_workload.so")
+# CLLM_HOST_SANITIZE=1: the build with address and undefined-behaviour checks (build_host_sanitized)
+_SANITIZE = os.environ.get("CLLM_HOST_SANITIZE") == "1"
+_LIB = os.path.join(_HERE, "libcllm_workload.hostsan.so" if _SANITIZE else "libcllm_workload.so")
 _lib = None
 
 WEIGHT_STD = 0.02
@@ -31,10 +33,23 @@ def build(verbose=False):
     _lib = None
 
 
+def build_host_sanitized(clang, verbose=False):
+    """Compile gen.c with address and undefined-behaviour checks into libcllm_workload.hostsan.so."""
+    out = os.path.join(_HERE, "libcllm_workload.hostsan.so")
+    cmd = [clang, "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined", "-shared-libasan",
+           "-fopenmp", "-fPIC", "-shared", "-o", out + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+
+
 def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB):
+            if _SANITIZE:
+                raise RuntimeError(f"{_LIB} is not built (build.py --host-sanitize)")
             build()
         L = ctypes.CDLL(_LIB)
         u64, i64, i32, dbl = ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_double

@@ -73,17 +73,22 @@ def measured_traffic(summary=TRAFFIC_SUMMARY, files=GEMM_SOURCES):
     return float(m_bytes.group(1))
 
 
-def oracle_iteration_s(cfg, ws, n, reps=3):
+ORACLE_CONTEXT = 16  # prompt tokens of the oracle's iteration sample
+
+
+def oracle_iteration_s(cfg, ws, n, reps=5):
     """Seconds of the oracle, as it stands, for one Jacobi iteration of n rows at this shape
-    after a 16-token prefill (attention over 16 instead of several hundred keys is about 2% of
-    the iteration's work at the 7B shape): the median of `reps` evaluations of the block."""
+    after a prefill of ORACLE_CONTEXT tokens (the timed workloads iterate at contexts of 512 and
+    more; attention over 16 instead of several hundred keys is about 2% of the iteration's work at
+    the 7B shape, and a 512-token prefill would cost the oracle about a minute): the median of
+    `reps` evaluations of the block."""
     import oracle
     from paper_2403_00835_amd import workload
     log("[bench] cpu baseline: oracle on the host")
     tensors = [workload.as_f32(cfg, t) for t in ws]
     om = oracle.Model(cfg, tensors)
-    st = oracle.State(om, 16 + n + 1)
-    prompt = workload.make_prompt(cfg, 16, seed=11)
+    st = oracle.State(om, ORACLE_CONTEXT + n + 1)
+    prompt = workload.make_prompt(cfg, ORACLE_CONTEXT, seed=11)
     y0 = st.prefill(prompt)
     block = np.array([y0] + list(workload.make_prompt(cfg, n - 1, seed=12)), dtype=np.int32)
     times = []
@@ -99,10 +104,10 @@ def cpu_baseline(cfg, ws, mean_accept, n):
     """The oracle's tokens/s: one n-row iteration, scaled by the GPU run's mean accepted length."""
     dt, cores = oracle_iteration_s(cfg, ws, n)
     return {"value": mean_accept / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"one Jacobi iteration of {n} rows at the 7B shape after a 16-token prefill "
-                      f"(median of 3: {dt:.2f} s), scaled by the GPU run's mean accepted length "
-                      f"{mean_accept:.2f}",
-            "iteration_s": dt}
+            "sample": f"one Jacobi iteration of {n} rows at the 7B shape at a context of {ORACLE_CONTEXT} keys "
+                      f"(the workload's is 512-768) after a {ORACLE_CONTEXT}-token prefill (median of 5: "
+                      f"{dt:.2f} s), scaled by the GPU run's mean accepted length {mean_accept:.2f}",
+            "context": ORACLE_CONTEXT, "iteration_s": dt}
 
 
 def calibration_copy():
@@ -173,7 +178,7 @@ def main():
 
     import torch
     from paper_2403_00835_amd import binding, workload
-    from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM_REINJECT, WORKLOADS
+    from paper_2403_00835_amd.configs import BLOCK_SHRINK, GUESS_STREAM, GUESS_STREAM_REINJECT, WORKLOADS
 
     if args.workload == "7b_loss":
         return main_loss(args)
@@ -254,6 +259,24 @@ def main():
     if not np.array_equal(tr_out, ar):
         raise RuntimeError("traced Jacobi output differs from greedy AR output")
 
+    # the printed algorithm's policy on the same request, outside the timed steps: the corrupted
+    # stream initialises each block, then the model's own predictions iterate (shrink blocks)
+    torch.cuda.synchronize()
+    p0 = time.perf_counter()
+    pp_out, pp_st = model.jacobi_decode(prompt, n, max_new, policy=GUESS_STREAM, block_policy=BLOCK_SHRINK,
+                                        stream=ar, p=args.p, seed=3)
+    torch.cuda.synchronize()
+    pp_s = time.perf_counter() - p0
+    if not np.array_equal(pp_out, ar):
+        raise RuntimeError("Jacobi output (printed policy) differs from greedy AR output")
+    printed = {"policy": f"guesses = GPU greedy continuation corrupted at p={args.p} for each block's initial "
+                         f"state, then the model's own predictions (the printed algorithm), shrink blocks",
+               "iterations": pp_st["steps"], "mean_accepted": round(max_new / pp_st["steps"], 3),
+               "tokens_per_s": round(max_new / pp_s, 3),
+               "decode_tokens_per_s": round(max_new / (pp_st["decode_ms"] / 1e3), 3),
+               "iteration_ms": round(pp_st["decode_ms"] / pp_st["steps"], 4),
+               "speedup_vs_ar": round(max_new / pp_s / ar_tps, 3)}
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, ws, mean_accept, n)
@@ -291,6 +314,7 @@ def main():
         "speedup_vs_ar": round(value / ar_tps, 3),
         "step_hbm_gbps": round(step_gbps, 1),
         "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "printed_policy": printed,
         "trajectory": {"decode_ms_recorded": round(tr_st["decode_ms"], 3),
                        "decode_ms_unrecorded_mean": round(decode_ms / len(stats), 3),
                        "fast_forward_mean": round(tc["fast_forward_mean"], 4), "stationary": tc["stationary"],
@@ -382,9 +406,10 @@ def main_batched(args, wl):
         dt, cores = oracle_iteration_s(cfg, ws, n)
         tok_per_row = tokens / rows
         cpu = {"value": n / dt * tok_per_row, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-               "sample": f"one Jacobi iteration of {n} rows of one sequence at the 7B shape (median of 3) after a 16-token "
-                         f"prefill ({dt:.2f} s), scaled to tokens by the GPU run's {tok_per_row:.3f} tokens per "
-                         f"row", "iteration_s": dt}
+               "sample": f"one Jacobi iteration of {n} rows of one sequence at the 7B shape at a context of "
+                         f"{ORACLE_CONTEXT} keys (median of 5) after a {ORACLE_CONTEXT}-token prefill ({dt:.2f} s), "
+                         f"scaled to tokens by the GPU run's {tok_per_row:.3f} tokens per row",
+               "context": ORACLE_CONTEXT, "iteration_s": dt}
     line = {
         "metric": METRIC,
         "value": round(value, 3),

@@ -352,6 +352,17 @@ cllm_status cllm_loss_head_device(cllm_ctx *ctx, const float *teacher, const flo
  * ERR_CAPACITY (L + m > max_ctx), ERR_OOM, ERR_DEVICE. */
 cllm_status cllm_hidden_rows(cllm_ctx *ctx, int32_t seq, const int32_t *block, int32_t m, float *rows_out);
 
+/* cllm_hidden_rows without any allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments, kernels and results (bit for bit), but the staging rows live in a fixed device array
+ * of the library (64 x 8192 floats = 2 MiB per GPU, held until the process ends) instead
+ * of a context buffer grown by hipMalloc; the call makes no hipMalloc, hipFree or other
+ * allocating call. Every call on one GPU, from any context, uses that GPU's one array: calls that
+ * overlap on one GPU (two host threads, or contexts on different streams) race and must be
+ * serialised by the caller. Errors: those of cllm_hidden_rows, ERR_CAPACITY (m x d_model above
+ * the array), ERR_STATE (no array address for the context's device). */
+cllm_status cllm_hidden_rows_noalloc(cllm_ctx *ctx, int32_t seq, const int32_t *block, int32_t m, float *rows_out);
+
 /* Committed length L and pending token of a sequence slot. Errors: ERR_ARG, ERR_STATE. */
 cllm_status cllm_seq_state(const cllm_ctx *ctx, int32_t seq, int32_t *committed_len, int32_t *pending);
 

@@ -57,7 +57,7 @@ TRACE_STRIDE = 5 + 2 * 64  # CLLM_TRACE_STRIDE
 EXPORTS = ["cllm_model_create", "cllm_model_set_weights", "cllm_model_init_random", "cllm_model_load", "cllm_model_free", "cllm_prefill",
            "cllm_jacobi_step", "cllm_jacobi_decode", "cllm_ar_decode", "cllm_jacobi_step_batch",
            "cllm_jacobi_decode_batch", "cllm_reset", "cllm_debug_logits", "cllm_trace_enable", "cllm_trace_read",
-           "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_loss_head_device", "cllm_hidden_rows", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
+           "cllm_trace_count", "cllm_collect_states", "cllm_loss_head", "cllm_loss_head_device", "cllm_hidden_rows", "cllm_hidden_rows_noalloc", "cllm_seq_state", "cllm_timing_enable", "cllm_timing_read",
            "cllm_streamed_weight_bytes", "cllm_workspace_bytes", "cllm_status_string", "cllm_last_error"]
 
 _lib = None
@@ -100,6 +100,7 @@ def lib():
         L.cllm_loss_head.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _vp, _vp, _vp, P(_dbl)]
         L.cllm_loss_head_device.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp]
         L.cllm_hidden_rows.argtypes = [_vp, _i32, _vp, _i32, _vp]
+        L.cllm_hidden_rows_noalloc.argtypes = [_vp, _i32, _vp, _i32, _vp]
         L.cllm_collect_states.argtypes = [_vp, _i64, _vp, _i64, _i32, _dbl, ctypes.c_uint64, _vp, _vp, _vp, _i64,
                                           P(_i64)]
         L.cllm_timing_enable.argtypes = [_vp, _i32, _i32, _i32]
@@ -339,6 +340,14 @@ class Model:
         b = np.ascontiguousarray(block, dtype=np.int32)
         out = np.empty((b.size, self.cfg.d_model), dtype=np.float32)
         self._check(self.L.cllm_hidden_rows(self.h, seq, _p(b), b.size, _p(out)))
+        return out
+
+    def hidden_rows_noalloc(self, block, seq=0):
+        """cllm_hidden_rows_noalloc: hidden_rows with the staging rows in the library's fixed
+        per-GPU scratch (no allocation)."""
+        b = np.ascontiguousarray(block, dtype=np.int32)
+        out = np.empty((b.size, self.cfg.d_model), dtype=np.float32)
+        self._check(self.L.cllm_hidden_rows_noalloc(self.h, seq, _p(b), b.size, _p(out)))
         return out
 
     def trace_enable(self, enable=True):

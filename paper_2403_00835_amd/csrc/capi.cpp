@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -776,6 +777,40 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
 }  // namespace
 
 // ------------------------------------------------------------------------------------------
+// Fixed scratch of cllm_hidden_rows_noalloc: the staging buffer of the LM-head input rows of one
+// call (m x d_model floats, at most kMaxBlock x 8192), a file-scope device array instead of an
+// allocation. Every GPU the library runs on holds its own copy until the process ends; its
+// address on a device is taken once, at the first context creation on that device (the array's
+// name is not a device address in host code). Calls on one GPU share it.
+// ------------------------------------------------------------------------------------------
+constexpr size_t kNoAllocFloats = (size_t)kMaxBlock * 8192;
+static __device__ __align__(256) float scratch[kNoAllocFloats];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_dev[kMaxDevices] = {};  // scratch's device address per device ordinal
+
+// With device `dev` current: look up scratch's address on it (once per device).
+cllm_status scratch_setup(cllm_ctx *c, int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return fail(c, CLLM_ERR_ARG, "device ordinal %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[dev]) return CLLM_OK;
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+        return fail(c, CLLM_ERR_DEVICE, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    g_scratch_dev[dev] = static_cast<float *>(p);
+    return CLLM_OK;
+}
+
+float *scratch_of(int dev) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return dev >= 0 && dev < kMaxDevices ? g_scratch_dev[dev] : nullptr;
+}
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
 // C ABI
 // ------------------------------------------------------------------------------------------
 namespace {
@@ -1139,6 +1174,7 @@ cllm_status cllm_model_create(const cllm_config *cfg, const cllm_runtime_opts *o
     };
     if (hipSetDevice(opts->device) != hipSuccess) return bail(CLLM_ERR_DEVICE);
     cllm_status s;
+    if ((s = scratch_setup(c, opts->device))) return bail(s);
     const size_t E = c->elem;
     if ((s = dalloc(c, &c->embed, (size_t)c->V * c->d * E))) return bail(s);
     c->g_attn.assign(c->NL, nullptr);
@@ -1584,6 +1620,31 @@ cllm_status cllm_hidden_rows(cllm_ctx *c, int32_t seq, const int32_t *block, int
     if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
     HIPCHK(c, launch_hidden_rows(c->X, c->d, m, c->d, c->g_final, c->cfg.rms_eps, w.hid, c->stream));
     HIPCHK(c, hipMemcpyAsync(rows_out, w.hid, (size_t)m * c->d * sizeof(float), hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    return CLLM_OK;
+}
+
+cllm_status cllm_hidden_rows_noalloc(cllm_ctx *c, int32_t seq, const int32_t *block, int32_t m, float *rows_out) {
+    if (!c) return CLLM_ERR_ARG;
+    cllm_status s;
+    if ((s = check_ctx(c)) || (s = check_seq(c, seq))) return s;
+    if (!block || !rows_out) return fail(c, CLLM_ERR_ARG, "NULL pointer");
+    if (m < 1 || m > c->opts.max_block) return fail(c, CLLM_ERR_ARG, "m=%d outside [1, max_block]", m);
+    if ((size_t)m * c->d > kNoAllocFloats)
+        return fail(c, CLLM_ERR_CAPACITY, "hidden rows (no allocation): %d rows x %d floats exceed the %zu-float scratch",
+                    m, c->d, kNoAllocFloats);
+    if (!c->slot[seq].prefilled) return fail(c, CLLM_ERR_STATE, "hidden rows before prefill (slot %d)", seq);
+    if ((s = check_ids(c, block, m))) return s;
+    if (c->slot[seq].L + m > c->opts.max_ctx) return fail(c, CLLM_ERR_CAPACITY, "L + m exceeds max_ctx");
+    float *hid = scratch_of(c->opts.device);
+    if (!hid) return fail(c, CLLM_ERR_STATE, "no scratch address for device %d", c->opts.device);
+    // as cllm_hidden_rows, with the staging rows in the device's scratch
+    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, false))) return s;
+    IterShape sh{m, 1, m, ceil_div(c->slot[seq].L + m, kAttnChunk), false, -1};
+    sh.tail = false;
+    if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
+    HIPCHK(c, launch_hidden_rows(c->X, c->d, m, c->d, c->g_final, c->cfg.rms_eps, hid, c->stream));
+    HIPCHK(c, hipMemcpyAsync(rows_out, hid, (size_t)m * c->d * sizeof(float), hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
     return CLLM_OK;
 }

@@ -71,6 +71,9 @@ struct GemmParams {
     int ldz;
     int kc;
     size_t zstride;
+    // launches of several row tiles (bf16): 0 = the row-tiled kernel; 1 = gemm_kernel over the
+    // row tiles (the same values; kept as the reference of the kernel driver's check)
+    int tile_kernel;
 };
 
 // Launch a product of `kind` over row_tiles tiles of 16 * rg rows (rg = 4 when row_tiles > 1);

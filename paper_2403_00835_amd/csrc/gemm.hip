@@ -3,6 +3,7 @@
 // the training loss head.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "device.h"
@@ -243,26 +244,33 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams &p, float *s_tile
     }
 }
 
+// LDS floats of gemm_kernel's body
+template <int NT, int RG, int W>
+__host__ __device__ constexpr int tile_lds_floats() {
+    return W * NT * 256 + 16 * RG * (16 * NT + 1) + kMaxRows;
+}
+
+// The body of gemm_kernel for column group wg, row tile p.rt0 + rt and K range z (E_LOGITS with
+// p.kc > 0); smem holds tile_lds_floats<NT, RG, W>() floats.
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
-__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
+__device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int z, float *smem) {
     static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    const int wg = blockIdx.x;  // column group
     if constexpr (EP == E_LOGITS) {
         if (p.kc > 0) {  // split K: k-steps [z kc, min((z + 1) kc, Ks)), partial products to plane z
-            const int ks0 = blockIdx.z * p.kc;
+            const int ks0 = z * p.kc;
             p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
             p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;  // 16-byte lane vectors
             p.Ks = min(p.kc, p.Ks - ks0);
-            p.Zout += (size_t)blockIdx.z * p.zstride;
+            p.Zout += (size_t)z * p.zstride;
         }
     }
     // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
     // capacity); m of them are live. A launch of one row tile (MT false) always has live rows, so
     // nothing waits for the row count before the first loads; with several row tiles (MT) a tile
     // with no live row exits first.
-    const int row0 = (p.rt0 + (int)blockIdx.y) * ROWS;
+    const int row0 = (p.rt0 + rt) * ROWS;
     request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T);
     const int m = p.rr.tab->R - row0;
     if constexpr (MT) {
@@ -275,7 +283,6 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int t0 = wg * NT;
 
-    extern __shared__ float smem[];
     float *s_red = smem;                   // W waves x NT x 256 (also ROWS x COLS for E_RESID)
     float *s_tile = s_red + W * NT * 256;  // ROWS x (COLS + 1)
     float *s_inv = s_tile + ROWS * (COLS + 1);      // ROWS
@@ -351,6 +358,12 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     }
 
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
+__global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
+    extern __shared__ float smem[];
+    gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -642,6 +655,195 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_dma_kernel(Gem
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
+// ------------------------------------------------------------------------------------------
+// Row-tiled decode GEMM (iterations of more than 64 rows, bf16): workgroup tiles of 64 rows x
+// 16 NT columns with the operand blocks brought into LDS by DMA (as gemm_prompt_dma_kernel, NB
+// buffers, NB - 1 k-steps in flight) and gemm_kernel's reduction order, so that every row gets
+// the bits a one-tile iteration gives it (batched, AR and Jacobi decoding stay bit-identical):
+// k-step k is accumulated into the set of its class k % 8 (from zero, the hi then the lo MFMA, in
+// increasing k, as wave k % 8 of gemm_kernel accumulates it), and the eight class sums are folded
+// at the end in gemm_kernel's tree ((x0 + x4) + (x2 + x6)) + ((x1 + x5) + (x3 + x7)). The RMSNorm
+// row factor and the epilogues are gemm_kernel's. With p.kc > 0 (E_LOGITS) grid z splits K into
+// ranges of kc k-steps, the classes of a range counted from its first k-step, as gemm_kernel
+// splits it.
+// ------------------------------------------------------------------------------------------
+// tiles (16 columns) per workgroup and ring depth of the row-tiled products (measured at the
+// LLaMA-2-7B shape, 96 to 512 rows; QKV and O stay faster on gemm_kernel)
+constexpr int kRowsNtGateUp = 12, kRowsNbGateUp = 4;
+constexpr int kRowsNtDown = 8, kRowsNbDown = 4;
+
+template <int NT, int EP, int NB>
+__host__ __device__ constexpr int rows_lds_floats() {
+    constexpr int RG = 4, ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;
+    constexpr int stage = NB * BLK * kWave * 4;
+    constexpr int after = (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1);
+    return (stage > after ? stage : after) + ROWS;
+}
+
+// An iteration of at most 64 rows (one row tile; the row count is known only on the device) takes
+// gemm_kernel's body with NT_T tiles per workgroup and D_T k-steps in flight instead: its column
+// groups are narrower, so more workgroups share the work (one row tile of the row-tiled kernel
+// would occupy fewer than half the CUs).
+template <int NT, int EP, int NB, int NT_T, int D_T>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int RG = 4, WM = 2, W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
+    constexpr int BLK = 2 * RG + NT;
+    static_assert(NT % WN == 0 && NB >= 3, "tile split, ring depth");
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    extern __shared__ float smem[];
+    request_together(p.rr.tab, p.cols, p.rt0);
+    if (p.rr.tab->R - p.rt0 * ROWS <= ROWS) {
+        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
+        if ((int)blockIdx.x < nwt) gemm_tile_body<P, NT_T, RG, EP, D_T, W, true>(p, blockIdx.x, 0, blockIdx.z, smem);
+        return;
+    }
+    if constexpr (EP == E_LOGITS) {
+        if (p.kc > 0) {  // split K as gemm_kernel does
+            const int ks0 = blockIdx.z * p.kc;
+            p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
+            p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;
+            p.Ks = min(p.kc, p.Ks - ks0);
+            p.Zout += (size_t)blockIdx.z * p.zstride;
+        }
+    }
+    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD
+    // (its L2 serves the weight tiles to all of them). The launch covers its largest row count; the
+    // live row tiles (from the device row table) take the first workgroups of each XCD, so the
+    // workgroups past them, which exit at once, are dispatched last.
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg, p.row_tiles);
+    const int live = min(p.row_tiles, (p.rr.tab->R - p.rt0 * ROWS + ROWS - 1) / ROWS);
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int wg = (slot / live) * 8 + xcd, row0 = (p.rt0 + slot % live) * ROWS;
+    if (wg >= p.n_wg) return;
+    const int m = p.rr.tab->R - row0;
+    const int rg0 = row0 >> 4, t0 = wg * NT;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = w / WN, wn = w % WN;
+    const int Ks = p.Ks;
+
+    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64] during the main loop
+    float *s_red = smem;
+    float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);
+    float *s_inv = smem + rows_lds_floats<NT, EP, NB>() - ROWS;
+
+    f32x4 sq_pre[2];
+    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // DMA blocks of a k-step: block b < 2 RG is activation plane b / RG, row group b % RG; block
+    // 2 RG + j is weight tile t0 + j (clamped; its columns are never written). Wave w issues
+    // blocks w, w + W, ... (NLW of them; where the last round has no block for a wave, it loads the
+    // last block again into its place), so every wave has the same number of loads in flight.
+    constexpr int NLW = (BLK + W - 1) / W;
+    const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
+    const u32x4 *src[NLW];
+    int adv[NLW], dst[NLW];
+#pragma unroll
+    for (int i = 0; i < NLW; ++i) {
+        const int b = min(w + i * W, BLK - 1);
+        dst[i] = b;
+        if (b < 2 * RG) {
+            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RG) * act_plane(p.rr.cap, p.lda);
+            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RG) * ks_a * kWave * 8) + lane;
+            adv[i] = kWave;
+        } else {
+            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
+            adv[i] = tiles * kWave;
+        }
+    }
+    auto issue = [&](int s, int buf) {  // k-step s (< Ks) into ring buffer buf
+        u32x4 *bb = s_stage + (size_t)buf * BLK * kWave;
+#pragma unroll
+        for (int i = 0; i < NLW; ++i)
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[i] + (size_t)s * adv[i]),
+                                             (__attribute__((address_space(3))) void *)(bb + (size_t)dst[i] * kWave),
+                                             16, 0, 0);
+    };
+    // one accumulator set per class: k-step k goes to set k % 8, the k-steps in increasing order
+    f32x4 acc[8][RGW][NTW];
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+        for (int r = 0; r < RGW; ++r)
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) acc[c][r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // past the last k-step the ring reloads k-step Ks - 1 (harmless, never computed)
+#pragma unroll
+    for (int q = 0; q < NB - 1; ++q) issue(min(q, Ks - 1), q);
+    int buf = 0;  // ring buffer of the k-step being computed
+    for (int k0 = 0; k0 < Ks; k0 += 8) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int k = k0 + c;
+            if (k < Ks) {  // uniform over the workgroup
+                wait_vm<(NB - 2) * NLW>();  // this wave's blocks of k-step k have landed
+                barrier_no_fence();         // every wave's; the buffer refilled next has no reader left
+                issue(min(k + NB - 1, Ks - 1), buf == 0 ? NB - 1 : buf - 1);
+                const u32x4 *bp = s_stage + (size_t)buf * BLK * kWave + lane;
+                u32x4 a[2][RGW], b[NTW];
+#pragma unroll
+                for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+                    for (int r = 0; r < RGW; ++r) a[pl][r] = bp[(pl * RG + wm * RGW + r) * kWave];
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) b[j] = bp[(2 * RG + wn * NTW + j) * kWave];
+#pragma unroll
+                for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+                    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+                        for (int j = 0; j < NTW; ++j) acc[c][r][j] = mfma_kstep<P>(a[pl][r], b[j], acc[c][r][j]);
+                buf = buf == NB - 1 ? 0 : buf + 1;
+            }
+        }
+    }
+    wait_vm<0>();  // the trailing reloads have landed before the buffers are reused
+    __syncthreads();
+
+    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+    __syncthreads();
+    // gemm_kernel's tree over the class sums, then its row factor
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = 16 * (wm * RGW + r) + 4 * (lane >> 4) + v;
+                float x = ((acc[0][r][j][v] + acc[4][r][j][v]) + (acc[2][r][j][v] + acc[6][r][j][v])) +
+                          ((acc[1][r][j][v] + acc[5][r][j][v]) + (acc[3][r][j][v] + acc[7][r][j][v]));
+                if constexpr (ROWSCALE) x *= s_inv[row];
+                s_tile[row * (COLS + 1) + 16 * (wn * NTW + j) + (lane & 15)] = x;
+            }
+    __syncthreads();
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+template <int NT, int EP, int NB, int NT_T, int D_T>
+static hipError_t launch_rows_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int COLS = 16 * NT;
+    constexpr int lds_rows = rows_lds_floats<NT, EP, NB>(), lds_tile = tile_lds_floats<NT_T, 4, kGemmWaves>();
+    const size_t lds = (size_t)(lds_rows > lds_tile ? lds_rows : lds_tile) * sizeof(float);
+    if (row_tiles < 1 || (p.rt0 + row_tiles) * 64 > p.rr.cap || p.lda % 32 != 0 || p.cols % 16 != 0)
+        return hipErrorInvalidValue;
+    if (EP != E_LOGITS && p.kc != 0) return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.n_wg = (p.cols + COLS - 1) / COLS;
+    q.row_tiles = row_tiles;
+    const int splits = EP == E_LOGITS && p.kc > 0 ? (p.Ks + p.kc - 1) / p.kc : 1;
+    const int n_tile = (p.cols + 16 * NT_T - 1) / (16 * NT_T);  // column groups of the one-tile body
+    const dim3 grid((unsigned)std::max((q.n_wg + 7) / 8 * 8 * row_tiles, n_tile), 1, (unsigned)splits);
+    auto kern = gemm_rows_kernel<NT, EP, NB, NT_T, D_T>;
+    if (e0 || e1)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    return hipGetLastError();
+}
+
 template <int NT, int RG, int WM, int EP, int NB>
 static hipError_t launch_prompt_dma(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -704,7 +906,7 @@ template <Prec P, int NT, int RG, int EP, int D = kGemmDepth, int W = kGemmWaves
 static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     static_assert(W * NT * 256 >= ROWS * COLS, "E_RESID reuses the reduction buffer");
-    const size_t lds = (size_t)(W * NT * 256 + ROWS * (COLS + 1) + kMaxRows) * sizeof(float);
+    const size_t lds = (size_t)tile_lds_floats<NT, RG, W>() * sizeof(float);
     auto kern = row_tiles > 1 ? gemm_kernel<P, NT, RG, EP, D, W, true> : gemm_kernel<P, NT, RG, EP, D, W, false>;
     GemmParams q = p;
     q.row_tiles = row_tiles;
@@ -786,7 +988,9 @@ __global__ __launch_bounds__(256) void down_reduce_kernel(GemmParams p, int nspl
 // The down product: K split over kDownSplits ranges (fp32 partials in p.part, 64-column
 // workgroups, D k-steps in flight), then down_reduce_kernel. e0 marks the product's start, e1
 // the reduction's end.
-template <Prec P, int RG, int D>
+// ROWK: the split products through the row-tiled kernel (bf16, several row tiles; the same values
+// as gemm_kernel's).
+template <Prec P, int RG, int D, bool ROWK = false>
 static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     static_assert(kDownSplits == 4, "down_reduce_kernel sums four partials");
     if (!p.part || p.rt0 != 0 || p.cols % 16 != 0 || p.ldx < p.cols) return hipErrorInvalidValue;
@@ -796,7 +1000,11 @@ static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s,
     q.ldz = p.ldx;
     q.V = p.cols;
     q.zstride = (size_t)p.rr.cap * p.ldx;
-    hipError_t err = launch_gemm_t<P, kLmTiles, RG, E_LOGITS, D>(q, row_tiles, s, e0, nullptr);
+    hipError_t err;
+    if constexpr (ROWK)
+        err = launch_rows_t<kRowsNtDown, E_LOGITS, kRowsNbDown, kLmTiles, D>(q, row_tiles, s, e0, nullptr);
+    else
+        err = launch_gemm_t<P, kLmTiles, RG, E_LOGITS, D>(q, row_tiles, s, e0, nullptr);
     if (err != hipSuccess) return err;
     const int nsplit = (p.Ks + q.kc - 1) / q.kc;
     const int rows_launch = row_tiles * 16 * RG;
@@ -813,6 +1021,13 @@ static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s,
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
+    if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel) {
+        // More than 64 rows, bf16: gate/up and the down product take the row-tiled kernel (the
+        // same values); at 7B, 96 / 160 / 256 / 512 rows: gate/up 59 / 112 / 115 / 221 us against
+        // 77 / 110 / 144 / 278, down (with its reduction) 36 / 62 / 62 / 116 against 46 / 62 / 80 / 143
+        if (kind == GEMM_GATE_UP) return launch_rows_t<kRowsNtGateUp, E_SWIGLU, kRowsNbGateUp, 6, 2>(p, row_tiles, s, e0, e1);
+        if (kind == GEMM_DOWN) return launch_down<P, RG, 3, true>(p, row_tiles, s, e0, e1);
+    }
     if (row_tiles > 1) {
         // More than 64 rows (measured at 160 and 512 rows, 7B): QKV and gate/up take 96-column
         // workgroups (two k-steps in flight), O and down 64-column workgroups (three k-steps in

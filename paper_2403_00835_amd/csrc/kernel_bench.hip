@@ -12,10 +12,22 @@
 // finite values: the timing and the traffic of these kernels do not depend on them.
 //
 // Usage: kernel_bench [rows (1..512, default 16)] [iters (default 20)]
+//        kernel_bench check [rows (1..512, default 160)]
+// The check mode fills weights, operands and the RMSNorm inputs with seeded random values and
+// runs each decode product (QKV, O, gate/up, down) twice over the same inputs, launched for at
+// least two row tiles as batched iterations are: as the library launches it (the row-tiled kernel
+// for gate/up and down, which takes gemm_kernel's body when the live rows fit one tile) and
+// through gemm_kernel over the same row tiles; every output (Q operand, cached keys and values,
+// residual rows, next RMSNorm operand and its sums of squares, SwiGLU rows) must be
+// bit-identical.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
 
 #include "device.h"
 #include "launch.h"
@@ -49,6 +61,22 @@ __global__ __launch_bounds__(256) void stream_read(const u32x4 *__restrict__ src
     if (acc == 0x9E3779B9u) out[0] = acc;
 }
 
+// Seeded fill: bf16 values of magnitude below `scale` (no NaN or infinity), or positive fp32
+// values in [lo, lo + span).
+__global__ void fill_bf16(uint16_t *x, size_t n, uint64_t seed, float scale) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+        const uint64_t h = mix64(seed ^ (i * 0x9E3779B97F4A7C15ull));
+        const float u = (float)(h >> 40) * 0x1.0p-24f * 2.0f - 1.0f;
+        x[i] = f2bf(u * scale);
+    }
+}
+__global__ void fill_f32(float *x, size_t n, uint64_t seed, float lo, float span) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+        const uint64_t h = mix64(seed ^ (i * 0x9E3779B97F4A7C15ull));
+        x[i] = lo + (float)(h >> 40) * 0x1.0p-24f * span;
+    }
+}
+
 namespace {
 
 constexpr int kD = 4096, kF = 11008, kV = 32000, kHd = 128, kCtx = 1024, kL = 512;
@@ -73,7 +101,10 @@ struct Shape {
 
 }  // namespace
 
+int check_main(int rows);
+
 int main(int argc, char **argv) {
+    if (argc > 1 && std::string(argv[1]) == "check") return check_main(argc > 2 ? std::atoi(argv[2]) : 160);
     const int rows = argc > 1 ? std::atoi(argv[1]) : 16;
     const int iters = argc > 2 ? std::atoi(argv[2]) : 20;
     if (rows < 1 || rows > 512 || iters < 1) {
@@ -190,8 +221,13 @@ int main(int argc, char **argv) {
         p.part = part;
         return p;
     };
+    // more than 64 rows: the row-tiled kernel (as iterations launch it), then gemm_kernel over the
+    // same row tiles for comparison
+    for (int pass = 0; pass < (rows > kMaxRows ? 2 : 1); ++pass)
     for (const Shape &s : shapes) {
         GemmParams p = params(s);
+        p.tile_kernel = pass;
+        if (pass == 1 && s.kind == GEMM_LM) continue;
         const size_t per = (size_t)(s.cols / 16) * p.Ks * kTileBytes;  // packed weight bytes per launch
         const int copies = (int)(kWBytes / per);
         if (copies < 2 || s.cols % 32 != 0) {
@@ -214,8 +250,8 @@ int main(int argc, char **argv) {
         CK(hipEventElapsedTime(&ms, e0, e1));
         const double us = ms * 1e3 / iters;
         const double flops = 2.0 * rows * s.cols * s.K;  // algorithmic (the MFMA work is twice: hi, lo)
-        std::printf("%-8s rows=%d row_tiles=%d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s  %7.1f TFLOP/s\n", s.name,
-                    rows, row_tiles, per, us, per / us / 1e3, flops / us / 1e6);
+        std::printf("%s%-8s rows=%d row_tiles=%d weights=%zu bytes  %8.2f us/launch  %7.1f GB/s  %7.1f TFLOP/s\n",
+                    pass ? "tile " : "", s.name, rows, row_tiles, per, us, per / us / 1e3, flops / us / 1e6);
     }
     if (rows > kMaxRows) {
         for (int k = 0; k < 4; ++k) {  // QKV, O, gate/up, down
@@ -246,4 +282,144 @@ int main(int argc, char **argv) {
     CK(hipDeviceSynchronize());
     std::printf("done\n");
     return 0;
+}
+
+// ------------------------------------------------------------------------------------------
+// check mode
+// ------------------------------------------------------------------------------------------
+namespace {
+
+template <typename T>
+std::vector<T> to_host(const T *d, size_t n) {
+    std::vector<T> h(n);
+    CK(hipMemcpy(h.data(), d, n * sizeof(T), hipMemcpyDeviceToHost));
+    return h;
+}
+
+template <typename T>
+size_t count_diff(const std::vector<T> &a, const std::vector<T> &b) {
+    size_t n = 0;
+    for (size_t i = 0; i < a.size(); ++i) n += std::memcmp(&a[i], &b[i], sizeof(T)) != 0;
+    return n;
+}
+
+}  // namespace
+
+int check_main(int rows) {
+    if (rows < 1 || rows > 512) {
+        std::fprintf(stderr, "kernel_bench check: rows must lie in 1..512\n");
+        return 2;
+    }
+    // at least two row tiles, as batched iterations launch them (their live rows may fit in one)
+    const int row_tiles = std::max(2, (rows + kMaxRows - 1) / kMaxRows), cap = row_tiles * kMaxRows;
+    const size_t nW = (size_t)(2 * kFp) * kD;  // the largest packed product (gate/up), elements
+    uint16_t *W = dev<uint16_t>(nW, 0);
+    RowTab th{};
+    th.R = rows;
+    th.nseq = 1;
+    th.m[0] = rows;
+    th.L[0] = kL;
+    RowTab *tab = dev<RowTab>(1, 0);
+    CK(hipMemcpy(tab, &th, sizeof(RowTab), hipMemcpyHostToDevice));
+    static RowInfo rh[512];
+    for (int i = 0; i < cap; ++i) rh[i] = RowInfo{0, kL + i, 0, i};
+    RowInfo *rinfo = dev<RowInfo>(cap, 0);
+    CK(hipMemcpy(rinfo, rh, sizeof(RowInfo) * cap, hipMemcpyHostToDevice));
+    const size_t nAd = 2 * act_plane(cap, kD), nAf = 2 * act_plane(cap, kFp);
+    uint16_t *A_d = dev<uint16_t>(nAd, 0), *A_f = dev<uint16_t>(nAf, 0);
+    float *ssq = dev<float>((size_t)(kD / 16) * cap, 0), *gain = dev<float>(kD, 0);
+    float *rcos = dev<float>((size_t)kCtx * (kHd / 2), 0), *rsin = dev<float>((size_t)kCtx * (kHd / 2), 0);
+    float *X0 = dev<float>((size_t)cap * kD, 0);
+    const dim3 fg(1024), fb(256);
+    hipLaunchKernelGGL(fill_bf16, fg, fb, 0, 0, W, nW, 1ull, 0.05f);
+    hipLaunchKernelGGL(fill_bf16, fg, fb, 0, 0, A_d, nAd, 2ull, 1.0f);
+    hipLaunchKernelGGL(fill_bf16, fg, fb, 0, 0, A_f, nAf, 3ull, 1.0f);
+    hipLaunchKernelGGL(fill_f32, fg, fb, 0, 0, ssq, (size_t)(kD / 16) * cap, 4ull, 1.0f, 15.0f);
+    hipLaunchKernelGGL(fill_f32, fg, fb, 0, 0, gain, (size_t)kD, 5ull, 0.5f, 1.0f);
+    hipLaunchKernelGGL(fill_f32, fg, fb, 0, 0, rcos, (size_t)kCtx * (kHd / 2), 6ull, -1.0f, 2.0f);
+    hipLaunchKernelGGL(fill_f32, fg, fb, 0, 0, rsin, (size_t)kCtx * (kHd / 2), 7ull, -1.0f, 2.0f);
+    hipLaunchKernelGGL(fill_f32, fg, fb, 0, 0, X0, (size_t)cap * kD, 8ull, -2.0f, 4.0f);
+    CK(hipGetLastError());
+    // outputs
+    const size_t nQ = 2 * act_plane(cap, kD), nKV = (size_t)kCtx * kD, nH = 2 * act_plane(cap, kFp);
+    uint16_t *Q = dev<uint16_t>(nQ, 0), *Kc = dev<uint16_t>(nKV, 0), *Vt = dev<uint16_t>(nKV, 0);
+    uint16_t *H = dev<uint16_t>(nH, 0), *An = dev<uint16_t>(nAd, 0);
+    float *X = dev<float>((size_t)cap * kD, 0), *ssq_out = dev<float>((size_t)(kD / 16) * cap, 0);
+    float *part = dev<float>((size_t)kDownSplits * cap * kD, 0);
+    const int n_wg_lm = (kV + 16 * kLmTiles - 1) / (16 * kLmTiles);
+    float *pmax = dev<float>((size_t)n_wg_lm * cap, 0);
+    int *pidx = dev<int>((size_t)n_wg_lm * cap, 0);
+
+    struct Prod {
+        const char *name;
+        GemmKind kind;
+        int cols, K;
+    };
+    const Prod prods[] = {{"qkv", GEMM_QKV, 3 * kD, kD}, {"o", GEMM_O, kD, kD}, {"gate_up", GEMM_GATE_UP, 2 * kFp, kD},
+                          {"down", GEMM_DOWN, kD, kFp}};
+    int bad = 0;
+    for (const Prod &pr : prods) {
+        GemmParams p{};
+        p.W = reinterpret_cast<const uint8_t *>(W);
+        p.Ks = pr.K / 32;
+        p.cols = pr.cols;
+        p.A = pr.kind == GEMM_DOWN ? (const void *)A_f : (const void *)A_d;
+        p.lda = pr.K;
+        p.rr = RowsRef{tab, rinfo, cap};
+        p.ssq = ssq;
+        p.T = kD / 16;
+        p.K = kD;
+        p.eps = 1e-6f;
+        p.Q = Q;
+        p.Kc = Kc;
+        p.Vt = Vt;
+        p.kv_seq = 0;
+        p.ctx_alloc = kCtx;
+        p.rcos = rcos;
+        p.rsin = rsin;
+        p.d = kD;
+        p.hd = kHd;
+        p.Xout = X;
+        p.ssq_out = ssq_out;
+        p.ldx = kD;
+        p.gain = gain;
+        p.An = An;
+        p.part = part;
+        p.H = H;
+        p.Fp = kFp;
+        p.pmax = pmax;
+        p.pidx = pidx;
+        p.V = kV;
+        std::vector<std::vector<uint16_t>> out16[2];
+        std::vector<std::vector<float>> out32[2];
+        for (int way = 0; way < 2; ++way) {
+            CK(hipMemset(Q, 0, nQ * 2));
+            CK(hipMemset(Kc, 0, nKV * 2));
+            CK(hipMemset(Vt, 0, nKV * 2));
+            CK(hipMemset(H, 0, nH * 2));
+            CK(hipMemset(An, 0, nAd * 2));
+            CK(hipMemset(ssq_out, 0, (size_t)(kD / 16) * cap * 4));
+            CK(hipMemcpy(X, X0, (size_t)cap * kD * 4, hipMemcpyDeviceToDevice));
+            GemmParams q = p;
+            q.tile_kernel = way;  // 0: the row-tiled kernel, 1: gemm_kernel over the row tiles
+            CK(launch_gemm(pr.kind, true, 4, row_tiles, q, 0, nullptr, nullptr));
+            CK(hipDeviceSynchronize());
+            out16[way] = {to_host(Q, nQ), to_host(Kc, nKV), to_host(Vt, nKV), to_host(H, nH), to_host(An, nAd)};
+            out32[way] = {to_host(X, (size_t)cap * kD), to_host(ssq_out, (size_t)(kD / 16) * cap)};
+        }
+        size_t d16 = 0, d32 = 0, n = 0;
+        for (int i = 0; i < 5; ++i) {
+            d16 += count_diff(out16[0][i], out16[1][i]);
+            n += out16[0][i].size();
+        }
+        for (int i = 0; i < 2; ++i) {
+            d32 += count_diff(out32[0][i], out32[1][i]);
+            n += out32[0][i].size();
+        }
+        std::printf("check %-8s rows=%d row_tiles=%d: %zu of %zu output values differ\n", pr.name, rows, row_tiles,
+                    d16 + d32, n);
+        bad += (d16 + d32) != 0;
+    }
+    std::printf(bad ? "check FAILED\n" : "check ok\n");
+    return bad ? 1 : 0;
 }

@@ -928,8 +928,10 @@ static hipError_t launch_gemm_t(const GemmParams &p, int row_tiles, hipStream_t 
 // the per-16-column sums of squares: each thread sums its VEC columns in order, the threads of
 // a 16-column tile then add their sums in order. Rows past the iteration's rows (device row
 // table) exit.
+constexpr int kReduceThreads = 64;  // one wave per workgroup: the reduction is latency-bound
+
 template <Prec P>
-__global__ __launch_bounds__(256) void down_reduce_kernel(GemmParams p, int nsplit, size_t zstride, int rows_launch) {
+__global__ __launch_bounds__(kReduceThreads) void down_reduce_kernel(GemmParams p, int nsplit, size_t zstride, int rows_launch) {
     using PT = PrecT<P>;
     using T = typename PT::T;
     constexpr int VEC = PT::VEC, G = 16 / VEC;  // columns per thread, threads per 16-column tile
@@ -1009,12 +1011,12 @@ static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s,
     const int nsplit = (p.Ks + q.kc - 1) / q.kc;
     const int rows_launch = row_tiles * 16 * RG;
     const size_t n = (size_t)rows_launch * (p.cols / PrecT<P>::VEC);
-    const dim3 grid((unsigned)((n + 255) / 256));
+    const dim3 grid((unsigned)((n + kReduceThreads - 1) / kReduceThreads));
     if (e1)
-        hipExtLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(256), 0, s, nullptr, e1, 0, p, nsplit, q.zstride,
+        hipExtLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(kReduceThreads), 0, s, nullptr, e1, 0, p, nsplit, q.zstride,
                               rows_launch);
     else
-        hipLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(256), 0, s, p, nsplit, q.zstride, rows_launch);
+        hipLaunchKernelGGL(down_reduce_kernel<P>, grid, dim3(kReduceThreads), 0, s, p, nsplit, q.zstride, rows_launch);
     return hipGetLastError();
 }
 

@@ -239,6 +239,11 @@ def main():
     gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * f_pad * 4 + n * (d // 16) * 4
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
+    # the same launches against the bf16 MFMA peak: algorithmic flops 2 * rows * (2 F) * d per
+    # launch at the mean block rows of the timed iterations (the sample rotates over layers and
+    # iterations); the executed MFMA work is twice that (hi and lo planes of the operand)
+    mean_rows = sum(s["rows"] for s in stats) / iters
+    gu_tflops = 2.0 * mean_rows * 2 * f_pad * d / gu_avg_s / 1e12 if gu_ms > 0 else 0.0
     traffic = measured_traffic() if (args.workload == "7b" and n == 16) else None
     ceiling = stream_ceiling()
     mean_ctx = P + max_new / 2
@@ -324,6 +329,10 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
                      "launches": launches, "stream_read_gbps": ceiling,
                      "frac_of_stream_read": round(achieved / ceiling, 4) if ceiling else None},
+        "roofline_mfma": {"bound": "mfma", "kernel": "gemm gate/up + SwiGLU (per layer)",
+                          "achieved": round(gu_tflops, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                          "frac": round(gu_tflops / BF16_PEAK_TFLOPS, 4),
+                          "executed_mfma_tflops": round(2 * gu_tflops, 2), "mean_rows": round(mean_rows, 2)},
         "cpu_baseline": cpu,
     }
     if args.oracle_decode:

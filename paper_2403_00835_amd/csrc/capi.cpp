@@ -48,6 +48,8 @@ struct cllm_ctx {
     float *rcos = nullptr, *rsin = nullptr;
     // workspace
     float *part = nullptr;  // K-split partial products of the down projection: kDownSplits x rows x d
+    float *spart = nullptr;  // class-pair split partials of multi-row products (bf16): 4 x rows x max columns
+    float *sinv = nullptr;   // their RMSNorm row factors: rows
     float *X = nullptr, *ssq = nullptr, *pmax = nullptr, *opart = nullptr, *mpart = nullptr, *lpart = nullptr,
           *dbg = nullptr;
     int *pidx = nullptr;
@@ -181,6 +183,9 @@ std::vector<WsBuf> workspace_bufs(cllm_ctx *c) {
     return {
         {P(&c->X), rows * d * 4},
         {P(&c->part), (size_t)kDownSplits * rows * d * 4},
+        {P(&c->spart), c->bf16 ? 4 * rows * std::max({3 * d, 2 * (size_t)c->Fp, (size_t)c->n_wg_lm * 16 * kLmTiles}) * 4
+                               : 16},
+        {P(&c->sinv), rows * 4},
         {P(&c->ssq), (d / 16) * rows * 4},
         {P(&c->Q), act_plane(c->cap, c->d) * 4},
         {P(&c->O), act_plane(c->cap, c->d) * 4},
@@ -345,6 +350,8 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
     base.ldx = c->d;
     base.An = c->An;
     base.part = c->part;
+    base.spart = c->bf16 ? c->spart : nullptr;
+    base.sinv = c->sinv;
     base.Fp = c->Fp;
     base.V = c->V;
 

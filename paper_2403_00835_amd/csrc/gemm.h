@@ -56,6 +56,11 @@ struct GemmParams {
     const float *gain;
     void *An;
     float *part;
+    // class-pair K split of multi-row products (bf16): four planes of t_c = x_c + x_(c+4), each
+    // row capacity x cols floats, in the MFMA's C layout per 16 x 16 block
+    float *spart;
+    // the RMSNorm row factors of those products' rows [row capacity], written by the split launch
+    float *sinv;
     // E_SWIGLU
     void *H;
     int Fp;

@@ -844,6 +844,268 @@ static hipError_t launch_rows_t(const GemmParams &p, int row_tiles, hipStream_t 
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------------
+// Class-pair K split of the decode GEMM (bf16, iterations of more than 64 rows). gemm_kernel's
+// tree ((x0 + x4) + (x2 + x6)) + ((x1 + x5) + (x3 + x7)) over the eight k-step class sums equals
+// (t0 + t2) + (t1 + t3) with t_c = x_c + x_(c+4). Grid z = c in {0, 1, 2, 3}: a workgroup walks
+// the k-steps k = c (mod 4) in increasing order and accumulates those with k = c (mod 8) into one
+// set and those with k = c + 4 (mod 8) into another (from zero, the hi then the lo MFMA, as wave
+// k % 8 of gemm_kernel accumulates them), then writes t_c of its 16 RGT x 16 NT tile, fp32, to
+// plane c of p.spart; gemm_split_reduce_kernel forms (t0 + t2) + (t1 + t3), applies the RMSNorm
+// row factor and runs gemm_kernel's epilogue. Every row therefore gets the bits of a one-tile
+// iteration. Two accumulator sets instead of eight allow workgroup tiles four times larger (each
+// k-step's operand rows and weight tiles, brought into LDS by DMA through a ring of NB buffers,
+// serve more outputs), and the four K quarters are four times finer units of work. An iteration
+// whose live rows fit one 64-row tile (known only on the device) takes gemm_kernel's body with
+// NT_T tiles per workgroup and D_T k-steps in flight inside the split launch, and the reduction
+// launch then has nothing to do.
+//
+// p.spart, plane c: [row group of 16 rows][16-column tile][lane][4] fp32 in the MFMA's C layout
+// (lane l, register v: row 4 (l / 16) + v, column l % 16 of the tile), row capacity x p.cols
+// floats per plane.
+// ------------------------------------------------------------------------------------------
+// 16-column tiles per workgroup and ring depth of the split products (64-row tiles; measured at
+// the LLaMA-2-7B shape, 160 and 512 rows: gate/up 74.6 / 195 us, QKV 45.0 / 100 us before the
+// reduction; O is no faster than gemm_kernel once its reduction is added)
+constexpr int kSplitNtQkv = 24, kSplitNbQkv = 3, kSplitNtGateUp = 24, kSplitNbGateUp = 3;
+constexpr int kSplitNtLm = 24, kSplitNbLm = 3;
+
+template <int RGT, int NT, int NB>
+__host__ __device__ constexpr int split_lds_floats() {
+    return NB * (2 * RGT + NT) * kWave * 4;
+}
+
+template <int RGT, int NT, int NB, int WM, int EP, int NT_T, int D_T, int MAP = 1>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int W = kGemmWaves, WN = W / WM, RGW = RGT / WM, NTW = NT / WN;
+    constexpr int BLK = 2 * RGT + NT, NLW = (BLK + W - 1) / W;
+    constexpr int ROWS = 16 * RGT;
+    static_assert(RGT % WM == 0 && NT % WN == 0 && NB >= 3, "tile split, ring depth");
+    extern __shared__ float smem[];
+    request_together(p.rr.tab, p.cols, p.rt0);
+    if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
+        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
+        if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
+            gemm_tile_body<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, 0, smem);
+        return;
+    }
+    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;
+    // the launch covers its largest row count, the live row tiles take the first workgroups of
+    // each XCD and the others exit at once.
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
+    request_together(p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq, p.T);
+    const int live = min(p.row_tiles, (p.rr.tab->R - p.rt0 * ROWS + ROWS - 1) / ROWS);
+    if (live <= 0) return;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    int c, wg;
+    if constexpr (MAP == 0) {  // grid z = class pair; column groups on XCDs in turn
+        c = blockIdx.z;
+        wg = (slot / live) * 8 + xcd;
+    } else {  // XCD x takes class pair x % 4 and every other column group from x / 4
+        c = xcd & 3;
+        wg = (slot / live) * 2 + (xcd >> 2);
+    }
+    const int row0 = (p.rt0 + slot % live) * ROWS;
+    if (wg >= p.n_wg) return;
+    const int rg0 = row0 >> 4, t0 = wg * NT;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = w / WN, wn = w % WN;
+    const int nq = (p.Ks - c + 3) >> 2;  // k-steps c, c + 4, ... below Ks (the launcher has Ks >= 4)
+    const int last = c + 4 * (nq - 1);
+    // one workgroup per row tile also computes the tile's RMSNorm row factors for the reduction
+    const bool factors = ROWSCALE && wg == 0 && c == 0;
+    f32x4 sq_pre[2];
+    if (factors) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64]
+    // DMA blocks of a k-step: block b < 2 RGT is activation plane b / RGT, row group b % RGT; block
+    // 2 RGT + j is weight tile t0 + j (clamped; its columns are never written). Wave w issues blocks
+    // w, w + W, ... (NLW of them; where the last round has no block for a wave, it loads the last
+    // block again into its place), so every wave has the same number of loads in flight.
+    const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
+    const u32x4 *src[NLW];
+    int adv[NLW], dst[NLW];
+#pragma unroll
+    for (int i = 0; i < NLW; ++i) {
+        const int b = min(w + i * W, BLK - 1);
+        dst[i] = b;
+        if (b < 2 * RGT) {
+            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RGT) * act_plane(p.rr.cap, p.lda);
+            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RGT) * ks_a * kWave * 8) + lane;
+            adv[i] = kWave;
+        } else {
+            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RGT, tiles - 1) * kTileBytes) + lane;
+            adv[i] = tiles * kWave;
+        }
+    }
+    auto issue = [&](int k, int buf) {  // k-step k (< Ks) into ring buffer buf
+        u32x4 *bb = s_stage + (size_t)buf * BLK * kWave;
+#pragma unroll
+        for (int i = 0; i < NLW; ++i)
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[i] + (size_t)k * adv[i]),
+                                             (__attribute__((address_space(3))) void *)(bb + (size_t)dst[i] * kWave),
+                                             16, 0, 0);
+    };
+    f32x4 acc[2][RGW][NTW];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < RGW; ++r)
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) acc[h][r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // past the last k-step the ring reloads the last one (harmless, never computed)
+#pragma unroll
+    for (int q = 0; q < NB - 1; ++q) issue(min(c + 4 * q, last), q);
+    int buf = 0;  // ring buffer of the k-step being computed
+    for (int q0 = 0; q0 < nq; q0 += 2) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {  // k-step c + 4 (q0 + h): class c for h = 0, c + 4 for h = 1
+            const int q = q0 + h;
+            if (q < nq) {  // uniform over the workgroup
+                wait_vm<(NB - 2) * NLW>();  // this wave's blocks of the k-step have landed
+                barrier_no_fence();         // every wave's; the buffer refilled next has no reader left
+                issue(min(c + 4 * (q + NB - 1), last), buf == 0 ? NB - 1 : buf - 1);
+                const u32x4 *bp = s_stage + (size_t)buf * BLK * kWave + lane;
+                u32x4 a[2][RGW], b[NTW];
+#pragma unroll
+                for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+                    for (int r = 0; r < RGW; ++r) a[pl][r] = bp[(pl * RGT + wm * RGW + r) * kWave];
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) b[j] = bp[(2 * RGT + wn * NTW + j) * kWave];
+#pragma unroll
+                for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+                    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+                        for (int j = 0; j < NTW; ++j) acc[h][r][j] = mfma_kstep<P>(a[pl][r], b[j], acc[h][r][j]);
+                buf = buf == NB - 1 ? 0 : buf + 1;
+            }
+        }
+    }
+    wait_vm<0>();  // the trailing reloads have landed before the workgroup ends
+
+    float *Z = p.spart + (size_t)c * p.rr.cap * p.cols;
+#pragma unroll
+    for (int r = 0; r < RGW; ++r)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+            const int t = t0 + wn * NTW + j;
+            if (t < tiles) {
+                f32x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = acc[0][r][j][e] + acc[1][r][j][e];
+                *reinterpret_cast<f32x4 *>(Z + (((size_t)(rg0 + wm * RGW + r) * tiles + t) * kWave + lane) * 4) = v;
+            }
+        }
+    if (factors) {  // uniform over the workgroup
+        __syncthreads();  // every wave is past its last read of the ring
+        float *s_inv = smem;
+        row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
+        __syncthreads();
+        if (tid < ROWS) p.sinv[row0 + tid] = s_inv[tid];
+    }
+}
+
+// (t0 + t2) + (t1 + t3) of the class-pair partials for a 64-row tile x 16 NT columns, the RMSNorm
+// row factor (computed once per row tile by the split launch) and gemm_kernel's epilogue. Grid: column groups x row tiles (from p.rt0); row tiles
+// past the iteration's rows exit.
+template <int NT, int EP>
+__host__ __device__ constexpr int split_reduce_lds_floats() {
+    constexpr int ROWS = kMaxRows, COLS = 16 * NT;
+    return (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1) + ROWS;
+}
+
+template <int NT, int EP>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int W = kGemmWaves, RG = kMaxRows / 16, ROWS = kMaxRows, COLS = 16 * NT;
+    constexpr int NV = RG * NT * kWave / (W * kWave);  // 16-byte vectors per thread and plane
+    static_assert((RG * NT) % W == 0, "every thread takes the same number of vectors");
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
+    extern __shared__ float smem[];
+    const int wg = blockIdx.x, row0 = (p.rt0 + blockIdx.y) * ROWS;
+    request_together(p.rr.tab, p.spart, p.cols, p.rr.cap, p.sinv, p.rt0);
+    const int m = p.rr.tab->R - row0;
+    if (m <= 0 || p.rr.tab->R - p.rt0 * ROWS <= ROWS) return;  // no rows, or the split launch did all
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    float *s_red = smem;                                       // epilogue scratch (E_RESID)
+    float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);  // ROWS x (COLS + 1)
+    float *s_inv = s_tile + ROWS * (COLS + 1);                 // ROWS
+    const int tiles = p.cols >> 4, t0 = wg * NT, rg0 = row0 >> 4;
+    const size_t plane = (size_t)p.rr.cap * p.cols;
+    // vector u = tid + i W 64: row group (u / 64) / NT, tile (u / 64) % NT, lane u % 64
+    f32x4 z[NV][4];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int u = tid + i * W * kWave, blk = u >> 6;
+        const int r = blk / NT, t = min(t0 + blk % NT, tiles - 1);
+        const float *src = p.spart + (((size_t)(rg0 + r) * tiles + t) * kWave + (u & 63)) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) z[i][c] = *reinterpret_cast<const f32x4 *>(src + c * plane);
+    }
+    if constexpr (ROWSCALE) {  // the row factors the split launch computed (row_factor_reduce's values)
+        if (tid < ROWS) s_inv[tid] = p.sinv[row0 + tid];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int u = tid + i * W * kWave, blk = u >> 6, l = u & 63;
+        const int r = blk / NT, j = blk % NT;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = 16 * r + 4 * (l >> 4) + v;
+            float x = (z[i][0][v] + z[i][2][v]) + (z[i][1][v] + z[i][3][v]);
+            if constexpr (ROWSCALE) x *= s_inv[row];
+            s_tile[row * (COLS + 1) + 16 * j + (l & 15)] = x;
+        }
+    }
+    __syncthreads();
+    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+// The product through the class-pair split: gemm_split_kernel over row_tiles tiles of 64 rows (from
+// row tile p.rt0), then gemm_split_reduce_kernel with NT_E tiles per workgroup. e0 marks the
+// product's start, e1 the reduction's end.
+template <int NT, int NB, int EP, int NT_E, int NT_T, int D_T, int MAP = 1>
+static hipError_t launch_split_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int RGT = 4, WM = 2, ROWS = 16 * RGT, COLS = 16 * NT;
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
+    if (!p.spart || (ROWSCALE && !p.sinv) || row_tiles < 1 || (p.rt0 + row_tiles) * ROWS > p.rr.cap ||
+        p.lda % 32 != 0 || p.cols % 16 != 0 || p.Ks < 4 || p.kc != 0)
+        return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.n_wg = (p.cols + COLS - 1) / COLS;
+    q.row_tiles = row_tiles;
+    constexpr int lds_split = split_lds_floats<RGT, NT, NB>(), lds_tile = tile_lds_floats<NT_T, 4, kGemmWaves>();
+    const size_t lds = (size_t)(lds_split > lds_tile ? lds_split : lds_tile) * sizeof(float);
+    const int n_tile = (p.cols + 16 * NT_T - 1) / (16 * NT_T);  // column groups of the one-tile body
+    const dim3 grid = MAP == 0 ? dim3((unsigned)std::max((q.n_wg + 7) / 8 * 8 * row_tiles, n_tile), 1, 4)
+                               : dim3((unsigned)std::max((q.n_wg + 1) / 2 * 8 * row_tiles, n_tile), 1, 1);
+    auto kern = gemm_split_kernel<RGT, NT, NB, WM, EP, NT_T, D_T, MAP>;
+    if (e0)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, nullptr, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    GemmParams r = p;
+    r.n_wg = (p.cols + 16 * NT_E - 1) / (16 * NT_E);
+    r.row_tiles = row_tiles;
+    const size_t lds_r = (size_t)split_reduce_lds_floats<NT_E, EP>() * sizeof(float);
+    const dim3 grid_r((unsigned)r.n_wg, (unsigned)r.row_tiles);
+    auto red = gemm_split_reduce_kernel<NT_E, EP>;
+    if (e1)
+        hipExtLaunchKernelGGL(red, grid_r, dim3(kGemmWaves * kWave), lds_r, s, nullptr, e1, 0, r);
+    else
+        hipLaunchKernelGGL(red, grid_r, dim3(kGemmWaves * kWave), lds_r, s, r);
+    return hipGetLastError();
+}
+
 template <int NT, int RG, int WM, int EP, int NB>
 static hipError_t launch_prompt_dma(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -1023,6 +1285,16 @@ static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s,
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
+    if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel && p.spart) {
+        // More than 64 rows, bf16: QKV and gate/up through the class-pair K split (the same values)
+        if (kind == GEMM_QKV)
+            return launch_split_t<kSplitNtQkv, kSplitNbQkv, E_QKV, 4, 6, 2>(p, row_tiles, s, e0, e1);
+        if (kind == GEMM_GATE_UP)
+            return launch_split_t<kSplitNtGateUp, kSplitNbGateUp, E_SWIGLU, 4, 6, 2>(p, row_tiles, s, e0, e1);
+        // the reduction's column groups are the LM head's argmax workgroups (kLmTiles tiles each)
+        if (kind == GEMM_LM)
+            return launch_split_t<kSplitNtLm, kSplitNbLm, E_ARGMAX, kLmTiles, kLmTiles, 3>(p, row_tiles, s, e0, e1);
+    }
     if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel) {
         // More than 64 rows, bf16: gate/up and the down product take the row-tiled kernel (the
         // same values); at 7B, 96 / 160 / 256 / 512 rows: gate/up 59 / 112 / 115 / 221 us against

@@ -14,12 +14,14 @@
 // Usage: kernel_bench [rows (1..512, default 16)] [iters (default 20)]
 //        kernel_bench check [rows (1..512, default 160)]
 // The check mode fills weights, operands and the RMSNorm inputs with seeded random values and
-// runs each decode product (QKV, O, gate/up, down) twice over the same inputs, launched for at
-// least two row tiles as batched iterations are: as the library launches it (the row-tiled kernel
-// for gate/up and down, which takes gemm_kernel's body when the live rows fit one tile) and
-// through gemm_kernel over the same row tiles; every output (Q operand, cached keys and values,
-// residual rows, next RMSNorm operand and its sums of squares, SwiGLU rows) must be
-// bit-identical.
+// runs each decode product (QKV, O, gate/up, down, LM head) twice over the same inputs, launched
+// for the row tiles the rows fill and for at least two row tiles as batched iterations are: as the
+// library launches it (with several row tiles: QKV, gate/up and the LM head through the
+// class-pair K split, the down ranges through the row-tiled kernel, each taking gemm_kernel's
+// body when the live rows fit one tile) and through gemm_kernel over the same row tiles; every
+// output (Q operand, cached keys and values, residual rows, next RMSNorm operand and its sums of
+// squares, SwiGLU rows, the LM head's
+// per-workgroup argmax values and indices) must be bit-identical.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -184,6 +186,8 @@ int main(int argc, char **argv) {
         {"lm_head", GEMM_LM, kLmTiles, n_wg_lm * 16 * kLmTiles, kD},
     };
     float *part = dev<float>((size_t)kDownSplits * cap * kD, 0);  // K-split partials of the down product
+    float *spart = dev<float>((size_t)4 * cap * std::max(2 * kFp, kV), 0);       // class-pair split partials
+    float *sinv = dev<float>((size_t)cap, 0);                      // and their row factors
     hipEvent_t e0, e1;
     CK(hipEventCreate(&e0));
     CK(hipEventCreate(&e1));
@@ -219,11 +223,13 @@ int main(int argc, char **argv) {
         p.dbg = nullptr;
         p.V = kV;
         p.part = part;
+        p.spart = spart;
+        p.sinv = sinv;
         return p;
     };
-    // more than 64 rows: the row-tiled kernel (as iterations launch it), then gemm_kernel over the
-    // same row tiles for comparison
-    for (int pass = 0; pass < (rows > kMaxRows ? 2 : 1); ++pass)
+    // more than 32 rows: the products as iterations launch them (class-pair split, row-tiled
+    // kernel), then gemm_kernel over the same row tiles for comparison
+    for (int pass = 0; pass < (rg == 4 ? 2 : 1); ++pass)
     for (const Shape &s : shapes) {
         GemmParams p = params(s);
         p.tile_kernel = pass;
@@ -310,9 +316,11 @@ int check_main(int rows) {
         std::fprintf(stderr, "kernel_bench check: rows must lie in 1..512\n");
         return 2;
     }
-    // at least two row tiles, as batched iterations launch them (their live rows may fit in one)
+    // launched for the row tiles the rows fill and, as batched iterations launch them, for at
+    // least two (their live rows may fit in one)
     const int row_tiles = std::max(2, (rows + kMaxRows - 1) / kMaxRows), cap = row_tiles * kMaxRows;
-    const size_t nW = (size_t)(2 * kFp) * kD;  // the largest packed product (gate/up), elements
+    const int launch_tiles[2] = {(rows + kMaxRows - 1) / kMaxRows, row_tiles};
+    const size_t nW = (size_t)std::max(2 * kFp, kV) * kD;  // the largest packed product (LM head), elements
     uint16_t *W = dev<uint16_t>(nW, 0);
     RowTab th{};
     th.R = rows;
@@ -346,6 +354,8 @@ int check_main(int rows) {
     uint16_t *H = dev<uint16_t>(nH, 0), *An = dev<uint16_t>(nAd, 0);
     float *X = dev<float>((size_t)cap * kD, 0), *ssq_out = dev<float>((size_t)(kD / 16) * cap, 0);
     float *part = dev<float>((size_t)kDownSplits * cap * kD, 0);
+    float *spart = dev<float>((size_t)4 * cap * std::max(2 * kFp, kV), 0);
+    float *sinv = dev<float>((size_t)cap, 0);
     const int n_wg_lm = (kV + 16 * kLmTiles - 1) / (16 * kLmTiles);
     float *pmax = dev<float>((size_t)n_wg_lm * cap, 0);
     int *pidx = dev<int>((size_t)n_wg_lm * cap, 0);
@@ -356,9 +366,12 @@ int check_main(int rows) {
         int cols, K;
     };
     const Prod prods[] = {{"qkv", GEMM_QKV, 3 * kD, kD}, {"o", GEMM_O, kD, kD}, {"gate_up", GEMM_GATE_UP, 2 * kFp, kD},
-                          {"down", GEMM_DOWN, kD, kFp}};
+                          {"down", GEMM_DOWN, kD, kFp}, {"lm_head", GEMM_LM, n_wg_lm * 16 * kLmTiles, kD}};
     int bad = 0;
+    for (int lt = 0; lt < 2; ++lt)
     for (const Prod &pr : prods) {
+        if (lt == 1 && launch_tiles[1] == launch_tiles[0]) break;
+        const int tiles_l = launch_tiles[lt];
         GemmParams p{};
         p.W = reinterpret_cast<const uint8_t *>(W);
         p.Ks = pr.K / 32;
@@ -385,6 +398,8 @@ int check_main(int rows) {
         p.gain = gain;
         p.An = An;
         p.part = part;
+        p.spart = spart;
+        p.sinv = sinv;
         p.H = H;
         p.Fp = kFp;
         p.pmax = pmax;
@@ -392,6 +407,7 @@ int check_main(int rows) {
         p.V = kV;
         std::vector<std::vector<uint16_t>> out16[2];
         std::vector<std::vector<float>> out32[2];
+        std::vector<int> outi[2];
         for (int way = 0; way < 2; ++way) {
             CK(hipMemset(Q, 0, nQ * 2));
             CK(hipMemset(Kc, 0, nKV * 2));
@@ -400,23 +416,29 @@ int check_main(int rows) {
             CK(hipMemset(An, 0, nAd * 2));
             CK(hipMemset(ssq_out, 0, (size_t)(kD / 16) * cap * 4));
             CK(hipMemcpy(X, X0, (size_t)cap * kD * 4, hipMemcpyDeviceToDevice));
+            CK(hipMemset(pmax, 0, (size_t)n_wg_lm * cap * 4));
+            CK(hipMemset(pidx, 0, (size_t)n_wg_lm * cap * 4));
             GemmParams q = p;
-            q.tile_kernel = way;  // 0: the row-tiled kernel, 1: gemm_kernel over the row tiles
-            CK(launch_gemm(pr.kind, true, 4, row_tiles, q, 0, nullptr, nullptr));
+            q.tile_kernel = way;  // 0: as iterations launch it, 1: gemm_kernel over the row tiles
+            CK(launch_gemm(pr.kind, true, 4, tiles_l, q, 0, nullptr, nullptr));
             CK(hipDeviceSynchronize());
             out16[way] = {to_host(Q, nQ), to_host(Kc, nKV), to_host(Vt, nKV), to_host(H, nH), to_host(An, nAd)};
-            out32[way] = {to_host(X, (size_t)cap * kD), to_host(ssq_out, (size_t)(kD / 16) * cap)};
+            out32[way] = {to_host(X, (size_t)cap * kD), to_host(ssq_out, (size_t)(kD / 16) * cap),
+                          to_host(pmax, (size_t)n_wg_lm * cap)};
+            outi[way] = to_host(pidx, (size_t)n_wg_lm * cap);
         }
         size_t d16 = 0, d32 = 0, n = 0;
         for (int i = 0; i < 5; ++i) {
             d16 += count_diff(out16[0][i], out16[1][i]);
             n += out16[0][i].size();
         }
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < 3; ++i) {
             d32 += count_diff(out32[0][i], out32[1][i]);
             n += out32[0][i].size();
         }
-        std::printf("check %-8s rows=%d row_tiles=%d: %zu of %zu output values differ\n", pr.name, rows, row_tiles,
+        d32 += count_diff(outi[0], outi[1]);
+        n += outi[0].size();
+        std::printf("check %-8s rows=%d row_tiles=%d: %zu of %zu output values differ\n", pr.name, rows, tiles_l,
                     d16 + d32, n);
         bad += (d16 + d32) != 0;
     }

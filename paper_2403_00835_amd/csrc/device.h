@@ -117,6 +117,23 @@ __device__ __forceinline__ void request_together(const Ts &...v) {
     (..., [](const auto &x) { asm volatile("" ::"s"(x)); }(v));
 }
 
+// Wait until at most N of this wave's vector memory loads are outstanding (loads retire in
+// order, so every older one has landed: for LDS DMA, its bytes are in LDS).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+    // s_waitcnt with vmcnt = N (bits 3:0 and 15:14) and the other counters at their maxima
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the compiler's memory fence (which would wait for every outstanding
+// load, DMA included); compiler-only fences keep LDS accesses from moving across it.
+__device__ __forceinline__ void barrier_no_fence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // One k-step of C += A * B on 16x16 tiles. a holds this lane's 16 bytes of the activation row
 // (row = lane % 16), b this lane's 16 bytes of the weight row (column = lane % 16); both hold
 // the same K indices, so the K-slot assignment inside the instruction does not matter.

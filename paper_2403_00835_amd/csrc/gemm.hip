@@ -531,19 +531,6 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmPar
 // k-step refills was last read in the previous k-step, before that barrier. Each wave
 // accumulates its sub-tile over every k-step in order (hi then lo plane), as
 // gemm_prompt_kernel does, so both give bit-identical values.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-    static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
-    // s_waitcnt with vmcnt = N (bits 3:0 and 15:14) and the other counters at their maxima
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ void barrier_no_fence() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 template <int NT, int RG, int EP, int NB>
 __host__ __device__ constexpr int prompt_dma_lds_floats() {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;

@@ -281,7 +281,10 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void attn_kernel(AttnParams p) 
 //   softmax over keys j <= L + i (fp32, base-2 exponent with the 1/sqrt(hd) scale folded in)
 //   O^T = Vt_chunk * P^T  (the lane's own S^T registers are the B operand; the V^T loads use
 //                          the same K-slot assignment)
-// Each (h, c, row) writes a partial (max, sum, unnormalised output).
+// Each (h, c, row) writes a partial (max, sum, unnormalised output). With several waves (bf16),
+// the chunk's K and V blocks are brought into LDS once per workgroup (LDS DMA, the blocks dealt
+// to the waves in turn) and every wave reads its operands there, instead of each wave loading
+// the whole chunk from L2; the operands, and so every value, are the same.
 // ------------------------------------------------------------------------------------------
 template <Prec P, int HD, int RG>
 __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) {
@@ -301,8 +304,9 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     const int c = blockIdx.x, h = blockIdx.y;
     const int key0 = c * kAttnChunk;
     if (key0 > L + min(m - 1, rbase + 16 * RG - 1)) return;  // no key of this chunk is visible to any row
-    const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
-    if (rbase + 16 * rg >= m) return;  // this wave's rows are all past the block
+    const int lane = threadIdx.x & 63, rg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    constexpr bool SHARED = P == Prec::BF16 && RG > 1;  // K and V staged in LDS for all waves
+    if (!SHARED && rbase + 16 * rg >= m) return;  // this wave's rows are all past the block
     const int g = lane >> 4, r16 = lane & 15;
     const int d = p.d;
     const int qi = rbase + 16 * rg + r16;   // row within the block
@@ -315,7 +319,28 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     const T *Vh = reinterpret_cast<const T *>(p.Vt) + kvo;
     const T *Q = reinterpret_cast<const T *>(p.Q);
 
-    // Every load of the workgroup is issued up front: Q rows, the chunk's 64 keys and values.
+    // K block (kt, kk): keys key0 + 16kt + lane%16, dims kk*KSTEP + (lane/16)*VEC ..; V^T block
+    // (dt, kp) (bf16): row = dim 16*dt + lane%16, K slots = keys 32kp+4g+(0..3), 32kp+16+4g+(0..3);
+    // the caches hold exactly these 16 bytes per lane contiguously (one KiB per block).
+    auto k_block = [&](int kt, int kk) {
+        return reinterpret_cast<const u32x4 *>(Kh + ((size_t)((key0 >> 4) + kt) * NKK + kk) * (kWave * PT::VEC)) + lane;
+    };
+    auto v_block = [&](int dt, int kp) {
+        return reinterpret_cast<const u32x4 *>(Vh + ((size_t)((key0 >> 5) + kp) * NDT + dt) * (kWave * 8)) + lane;
+    };
+    constexpr int NKB = 4 * NKK, NVB = 2 * NDT;  // K and V blocks of the chunk (bf16)
+    __shared__ u32x4 s_kv[SHARED ? NKB + NVB : 1][kWave];
+    if constexpr (SHARED) {
+        static_assert((NKB + NVB) % RG == 0, "every wave issues the same number of blocks");
+#pragma unroll
+        for (int j = 0; j < (NKB + NVB) / RG; ++j) {
+            const int i = rg + j * RG;
+            const u32x4 *src = i < NKB ? k_block(i / NKK, i % NKK) : v_block((i - NKB) >> 1, (i - NKB) & 1);
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(src),
+                                             (__attribute__((address_space(3))) void *)(&s_kv[i][0]), 16, 0, 0);
+        }
+    }
+    // Every global load of the workgroup is issued up front: Q rows, the chunk's keys and values.
     u32x4 qv[PT::PLANES][NKK], kv[4][NKK];
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
@@ -323,22 +348,30 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
 #pragma unroll
         for (int pl = 0; pl < PT::PLANES; ++pl)
             qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, dcol, d));
+        if constexpr (!SHARED) {
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)  // keys key0 + 16kt + lane%16, dims kk*KSTEP + (lane/16)*VEC ..
-            kv[kt][kk] = *reinterpret_cast<const u32x4 *>(
-                Kh + ((size_t)((key0 >> 4) + kt) * NKK + kk) * (kWave * PT::VEC) + lane * PT::VEC);
-    }
-    // V^T operand: row = dim 16*dt + lane%16; K slots = keys 32kp+4g+(0..3), 32kp+16+4g+(0..3) (bf16),
-    // or keys 16kt+4g+(0..3) (fp32); the cache holds exactly these 16 bytes per lane contiguously.
-    u32x4 vv[NDT][2];
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-        if constexpr (P == Prec::BF16) {
-#pragma unroll
-            for (int kp = 0; kp < 2; ++kp)
-                vv[dt][kp] = *reinterpret_cast<const u32x4 *>(
-                    Vh + ((size_t)((key0 >> 5) + kp) * NDT + dt) * (kWave * 8) + lane * 8);
+            for (int kt = 0; kt < 4; ++kt) kv[kt][kk] = *k_block(kt, kk);
         }
+    }
+    u32x4 vv[NDT][2];
+    if constexpr (P == Prec::BF16 && !SHARED) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int kp = 0; kp < 2; ++kp) vv[dt][kp] = *v_block(dt, kp);
+    }
+    if constexpr (SHARED) {
+        wait_vm<0>();        // this wave's blocks (and queries) have landed
+        barrier_no_fence();  // every wave's
+        if (rbase + 16 * rg >= m) return;  // this wave's rows are all past the block
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) kv[kt][kk] = s_kv[kt * NKK + kk][lane];
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int kp = 0; kp < 2; ++kp) vv[dt][kp] = s_kv[NKB + 2 * dt + kp][lane];
     }
 
     f32x4 st[4];

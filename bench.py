@@ -162,6 +162,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="7b", choices=["7b", "small", "7b_long", "7b_batched", "7b_loss"])
     ap.add_argument("--p", type=float, default=0.3)
+    ap.add_argument("--prefill-chunk", type=int, default=512,
+                    help="prompt rows per prefill pass (prefill values do not depend on it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--oracle-decode", action="store_true",
                     help="also time the oracle's AR and Jacobi decoding (tiny, small, shortened 7B; about "
@@ -194,6 +196,7 @@ def main():
     ws = workload.make_weights(cfg)
     log(f"[bench] weights drawn in {time.time() - t0:.1f} s; uploading")
     model = binding.Model(cfg, max_ctx=P + max_new + n + 64, max_block=max(n, 16), max_new=max_new,
+                          prefill_chunk=args.prefill_chunk,
                           stream=stream.cuda_stream, weights=ws)
     prompt = workload.make_prompt(cfg, P)
     log("[bench] GPU AR decode (guess stream and AR baseline)")
@@ -302,7 +305,7 @@ def main():
         "config": {"workload": f"{wl.name}: prompt {P}, n={n}, {max_new} new tokens, guesses = GPU greedy "
                                f"continuation corrupted at p={args.p} and re-drawn each iteration, shrink blocks",
                    "prompt_len": P, "n": n, "max_new": max_new, "p": args.p, "batch": 1,
-                   "layers": cfg.n_layers, "d_model": cfg.d_model, "prefill_chunk": 512},
+                   "layers": cfg.n_layers, "d_model": cfg.d_model, "prefill_chunk": args.prefill_chunk},
         "jacobi_step_ms": round(iter_ms, 4),
         "iteration_ms": {"mean": round(iter_ms, 4),
                          "p10": round(float(np.median([x["iter_ms_p10"] for x in stats])), 4),
@@ -356,7 +359,7 @@ def main_batched(args, wl):
     log(f"[bench] generating {cfg.streamed_params() / 1e9:.2f} B streamed parameters")
     ws = workload.make_weights(cfg)
     model = binding.Model(cfg, max_ctx=wl.prompt_len_range[1] + max_new + n + 64, max_block=n, max_new=max_new,
-                          max_batch=B, stream=stream.cuda_stream, weights=ws)
+                          max_batch=B, stream=stream.cuda_stream, weights=ws, prefill_chunk=args.prefill_chunk)
     log(f"[bench] batched GPU AR decode of {B} sequences (guess streams and AR baseline)")
     ar, ar_stats = model.jacobi_decode_batch(ids, prompts, 1, max_new)
     ar_tps = B * max_new / ((ar_stats[0]["prefill_ms"] + ar_stats[0]["decode_ms"]) / 1e3)
@@ -436,7 +439,8 @@ def main_batched(args, wl):
                                f"{max_new} new tokens each, guesses = GPU greedy continuation corrupted at per-sequence "
                                f"p uniform in {list(wl.p_range)} and re-drawn each iteration, shrink blocks, one "
                                f"batched loop",
-                   "batch": B, "n": n, "max_new": max_new, "layers": cfg.n_layers, "d_model": d},
+                   "batch": B, "n": n, "max_new": max_new, "layers": cfg.n_layers, "d_model": d,
+                   "prefill_chunk": args.prefill_chunk},
         "batched_iterations_per_step": sum(iters) / len(iters),
         "mean_rows_per_iteration": round(mean_rows, 2),
         "batched_iteration_ms": round(decode_ms / sum(iters), 4),

@@ -237,15 +237,16 @@ def main():
     wbytes = model.streamed_weight_bytes()
     d, F = cfg.d_model, cfg.ffn_dim
     # gate/up launch: packed weights (2 * F_pad * d bf16) + operand rows read (hi and lo bf16
-    # planes, 4 bytes per value) + SwiGLU rows written (4 bytes per value) + row-factor partials
+    # planes, 4 bytes per value) + SwiGLU rows written (4 bytes per value) + row-factor partials,
+    # at the mean block rows of the timed iterations (the sampled launches rotate over layers and
+    # iterations, whose blocks shrink)
     f_pad = (F + 31) // 32 * 32
-    gu_bytes = 2 * f_pad * d * 2 + n * d * 4 + n * f_pad * 4 + n * (d // 16) * 4
+    mean_rows = sum(s["rows"] for s in stats) / iters
+    gu_bytes = round(2 * f_pad * d * 2 + mean_rows * (d * 4 + f_pad * 4 + (d // 16) * 4))
     gu_avg_s = gu_ms / 1e3 / max(launches, 1)
     achieved = gu_bytes / gu_avg_s / 1e9
     # the same launches against the bf16 MFMA peak: algorithmic flops 2 * rows * (2 F) * d per
-    # launch at the mean block rows of the timed iterations (the sample rotates over layers and
-    # iterations); the executed MFMA work is twice that (hi and lo planes of the operand)
-    mean_rows = sum(s["rows"] for s in stats) / iters
+    # launch at the mean block rows; the executed MFMA work is twice that (hi and lo planes)
     gu_tflops = 2.0 * mean_rows * 2 * f_pad * d / gu_avg_s / 1e12 if gu_ms > 0 else 0.0
     traffic = measured_traffic() if (args.workload == "7b" and n == 16) else None
     ceiling = stream_ceiling()

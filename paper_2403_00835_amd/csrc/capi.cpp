@@ -689,7 +689,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     sp.stream_stride = c->stream_cap;
     HIPCHK(c, launch_decode_init(B, sp, c->stream));
     HIPCHK(c, launch_plan(PlanParams{c->ctl, c->tab, c->rows, c->cap}, c->stream));
-    const IterShape sh{B * n, B, n, std::min(c->nch, ceil_div(maxlen + max_new + n, kAttnChunk)), true, -1};
+    IterShape sh{B * n, B, n, std::min(c->nch, ceil_div(maxlen + max_new + n, kAttnChunk)), true, -1};
     // Device-resident loop: every launch reads its rows from the row table. The host only
     // queues iterations: as many as are certainly needed by the sequence with the most tokens
     // left (each iteration fixes at most n tokens of a sequence), then reads the control blocks.
@@ -703,6 +703,12 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             need = std::max(need, ceil_div(left, n));
         }
         if (need == 0) break;
+        // Launch shape of this round: the blocks of the sequences still running (a finished
+        // sequence's block is empty in the row table, and a row's values do not depend on the
+        // launch shape), so the products of the last rounds launch for fewer row tiles.
+        int active = 0;
+        for (int b = 0; b < B; ++b) active += h[seq_ids[b]].done ? 0 : 1;
+        sh.R = std::max(active, 1) * n;
         for (int i = 0; i < need; ++i) {
             if ((s = enqueue_iteration(c, sh, c->out_dev, any_stream ? c->stream_dev : nullptr))) return s;
             if (nev == c->it_ev.size()) {

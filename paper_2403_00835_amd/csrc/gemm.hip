@@ -1272,8 +1272,9 @@ static hipError_t launch_down(const GemmParams &p, int row_tiles, hipStream_t s,
 template <Prec P, int RG>
 static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0,
                                  hipEvent_t e1) {
-    if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel && p.spart) {
-        // More than 64 rows, bf16: QKV and gate/up through the class-pair K split (the same values)
+    if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel && p.spart && p.Ks >= 4) {
+        // More than 64 rows, bf16 (K of at least four k-steps): QKV, gate/up and the LM head
+        // through the class-pair K split (the same values)
         if (kind == GEMM_QKV)
             return launch_split_t<kSplitNtQkv, kSplitNbQkv, E_QKV, 4, 6, 2>(p, row_tiles, s, e0, e1);
         if (kind == GEMM_GATE_UP)

@@ -20,7 +20,7 @@ import pytest
 
 import oracle
 from paper_2403_00835_amd import workload
-from paper_2403_00835_amd.configs import (BLOCK_SHRINK, BLOCK_SLIDE, GUESS_STREAM, GUESS_STREAM_REINJECT,
+from paper_2403_00835_amd.configs import (ModelConfig, BLOCK_SHRINK, BLOCK_SLIDE, GUESS_STREAM, GUESS_STREAM_REINJECT,
                                           GUESS_UNIFORM, LLAMA7B, SMALL, TINY, WORKLOADS)
 from tests.parity import log
 
@@ -164,6 +164,21 @@ def test_small_batched_steps_equal_single(small):
     prompts = [workload.make_prompt(SMALL, L, seed=34, seq=b) for b, L in enumerate([50, 130, 200, 77])]
     log("[gpu-batch] small: 4 sequences, 4 batched steps vs single steps")
     _batched_steps_equal_single(SMALL, batched, single, prompts, 32, 4, seed=2)
+
+
+def test_narrow_bf16_batched_steps_equal_single():
+    # d_model 64 in bf16: two k-steps per product, fewer than the class-pair split's four, so
+    # iterations of more than 64 rows take gemm_kernel over the row tiles for QKV, O, gate/up and
+    # the LM head (and the row-tiled kernel for the down ranges); rows keep the single-step bits
+    cfg = ModelConfig(n_layers=2, d_model=64, n_heads=2, head_dim=32, ffn_dim=172, vocab=256, dtype="bf16")
+    ws, batched, single = _models(cfg, max_ctx=256, max_block=32, max_new=64, max_batch=4)
+    try:
+        prompts = [workload.make_prompt(cfg, L, seed=38, seq=b) for b, L in enumerate([20, 45, 90, 7])]
+        log("[gpu-batch] narrow bf16 (d 64): 4 sequences of 32-row blocks, 6 batched steps vs single steps")
+        _batched_steps_equal_single(cfg, batched, single, prompts, 32, 6, seed=3)
+    finally:
+        batched.close()
+        single.close()
 
 
 def test_small_batched_decode(small):

@@ -360,10 +360,35 @@ __device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
+// gemm_kernel's body for the first row tile of a launch whose rows fit one tile (p.rt0 == 0),
+// with only as many 16-row groups as the iteration has rows (at most RG; the count is known only
+// on the device: blocks shrink as tokens are accepted). A row's sums do not depend on the row
+// groups computed beside it, so every row keeps its values, and an iteration of few rows streams
+// the weights with fewer operand rows and MFMAs. smem holds tile_lds_floats<NT, RG, W>() floats.
+template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
+__device__ __forceinline__ void gemm_tile_body_live(const GemmParams &p, int wg, int z, float *smem) {
+    if constexpr (RG > 1) {
+        if (p.rt0 == 0) {
+            const int m = p.rr.tab->R;
+            if (m <= 16) return gemm_tile_body<P, NT, 1, EP, D, W, MT>(p, wg, 0, z, smem);
+            if constexpr (RG > 2) {
+                if (m <= 32) return gemm_tile_body<P, NT, 2, EP, D, W, MT>(p, wg, 0, z, smem);
+            }
+            if constexpr (RG > 3) {
+                if (m <= 48) return gemm_tile_body<P, NT, 3, EP, D, W, MT>(p, wg, 0, z, smem);
+            }
+        }
+    }
+    gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, wg, 0, z, smem);
+}
+
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     extern __shared__ float smem[];
-    gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+    if constexpr (MT)
+        gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+    else
+        gemm_tile_body_live<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.z, smem);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -683,7 +708,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParam
     request_together(p.rr.tab, p.cols, p.rt0);
     if (p.rr.tab->R - p.rt0 * ROWS <= ROWS) {
         const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
-        if ((int)blockIdx.x < nwt) gemm_tile_body<P, NT_T, RG, EP, D_T, W, true>(p, blockIdx.x, 0, blockIdx.z, smem);
+        if ((int)blockIdx.x < nwt) gemm_tile_body_live<P, NT_T, RG, EP, D_T, W, true>(p, blockIdx.x, blockIdx.z, smem);
         return;
     }
     if constexpr (EP == E_LOGITS) {
@@ -874,7 +899,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmPara
     if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
         const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
         if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
-            gemm_tile_body<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, 0, smem);
+            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, smem);
         return;
     }
     // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;

@@ -887,49 +887,21 @@ __host__ __device__ constexpr int split_lds_floats() {
     return NB * (2 * RGT + NT) * kWave * 4;
 }
 
-template <int RGT, int NT, int NB, int WM, int EP, int NT_T, int D_T, int MAP = 1>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmParams p) {
+// The class-pair product of one tile of 16 RGT live rows (row0 on): the k-steps c, c + 4, ... into
+// two accumulator sets over a WM x (8 / WM) wave grid, t_c written to plane c of p.spart.
+// smem holds split_lds_floats<4, NT, NB>() floats (the launch's 64-row tile).
+template <int RGT, int WM, int NT, int NB>
+__device__ __forceinline__ void split_tile_body(const GemmParams &p, int c, int wg, int row0, float *smem) {
     constexpr Prec P = Prec::BF16;
     constexpr int W = kGemmWaves, WN = W / WM, RGW = RGT / WM, NTW = NT / WN;
     constexpr int BLK = 2 * RGT + NT, NLW = (BLK + W - 1) / W;
-    constexpr int ROWS = 16 * RGT;
     static_assert(RGT % WM == 0 && NT % WN == 0 && NB >= 3, "tile split, ring depth");
-    extern __shared__ float smem[];
-    request_together(p.rr.tab, p.cols, p.rt0);
-    if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
-        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
-        if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
-            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, smem);
-        return;
-    }
-    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;
-    // the launch covers its largest row count, the live row tiles take the first workgroups of
-    // each XCD and the others exit at once.
-    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
-    request_together(p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq, p.T);
-    const int live = min(p.row_tiles, (p.rr.tab->R - p.rt0 * ROWS + ROWS - 1) / ROWS);
-    if (live <= 0) return;
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    int c, wg;
-    if constexpr (MAP == 0) {  // grid z = class pair; column groups on XCDs in turn
-        c = blockIdx.z;
-        wg = (slot / live) * 8 + xcd;
-    } else {  // XCD x takes class pair x % 4 and every other column group from x / 4
-        c = xcd & 3;
-        wg = (slot / live) * 2 + (xcd >> 2);
-    }
-    const int row0 = (p.rt0 + slot % live) * ROWS;
-    if (wg >= p.n_wg) return;
     const int rg0 = row0 >> 4, t0 = wg * NT;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w / WN, wn = w % WN;
     const int nq = (p.Ks - c + 3) >> 2;  // k-steps c, c + 4, ... below Ks (the launcher has Ks >= 4)
     const int last = c + 4 * (nq - 1);
-    // one workgroup per row tile also computes the tile's RMSNorm row factors for the reduction
-    const bool factors = ROWSCALE && wg == 0 && c == 0;
-    f32x4 sq_pre[2];
-    if (factors) row_factor_preload<W>(p, row0, tid, sq_pre);
 
     u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64]
     // DMA blocks of a k-step: block b < 2 RGT is activation plane b / RGT, row group b % RGT; block
@@ -1013,6 +985,60 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmPara
                 *reinterpret_cast<f32x4 *>(Z + (((size_t)(rg0 + wm * RGW + r) * tiles + t) * kWave + lane) * 4) = v;
             }
         }
+}
+
+template <int RGT, int NT, int NB, int WM, int EP, int NT_T, int D_T, int MAP = 1>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int W = kGemmWaves;
+    constexpr int ROWS = 16 * RGT;
+    static_assert(RGT == 4 && WM == 2, "64-row tiles; the last tile's live row groups pick their own wave grid");
+    extern __shared__ float smem[];
+    request_together(p.rr.tab, p.cols, p.rt0);
+    if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
+        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
+        if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
+            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, smem);
+        return;
+    }
+    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;
+    // the launch covers its largest row count, the live row tiles take the first workgroups of
+    // each XCD and the others exit at once.
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
+    request_together(p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq, p.T);
+    const int R = p.rr.tab->R;
+    const int live = min(p.row_tiles, (R - p.rt0 * ROWS + ROWS - 1) / ROWS);
+    if (live <= 0) return;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    int c, wg;
+    if constexpr (MAP == 0) {  // grid z = class pair; column groups on XCDs in turn
+        c = blockIdx.z;
+        wg = (slot / live) * 8 + xcd;
+    } else {  // XCD x takes class pair x % 4 and every other column group from x / 4
+        c = xcd & 3;
+        wg = (slot / live) * 2 + (xcd >> 2);
+    }
+    const int row0 = (p.rt0 + slot % live) * ROWS;
+    if (wg >= p.n_wg) return;
+    const int tid = threadIdx.x;
+    // one workgroup per row tile also computes the tile's RMSNorm row factors for the reduction
+    const bool factors = ROWSCALE && wg == 0 && c == 0;
+    f32x4 sq_pre[2];
+    if (factors) row_factor_preload<W>(p, row0, tid, sq_pre);
+
+    // The last live tile runs only its live 16-row groups (rows past the iteration's rows have
+    // no partials; the reduction writes nothing for them). Every row's t_c is the same whatever
+    // the tile's row groups and wave grid.
+    const int mt = R - row0;
+    if (mt <= 16)
+        split_tile_body<1, 1, NT, NB>(p, c, wg, row0, smem);
+    else if (mt <= 32)
+        split_tile_body<2, 2, NT, NB>(p, c, wg, row0, smem);
+    else if (mt <= 48)
+        split_tile_body<3, 1, NT, NB>(p, c, wg, row0, smem);
+    else
+        split_tile_body<4, 2, NT, NB>(p, c, wg, row0, smem);
+
     if (factors) {  // uniform over the workgroup
         __syncthreads();  // every wave is past its last read of the ring
         float *s_inv = smem;

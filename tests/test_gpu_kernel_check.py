@@ -5,9 +5,10 @@ tiles: the class-pair K split for QKV, gate/up and the LM head, the row-tiled ke
 product's K ranges, each taking gemm_kernel's body when the live rows fit one tile) and through
 gemm_kernel over the same row tiles. Every output (Q operand, cached keys and values, residual
 rows, next RMSNorm operand and its sums of squares, SwiGLU rows, argmax partials) must be
-bit-identical, from one 16-row group to eight 64-row tiles, ragged tails included: the split and
-the row-tiled kernels keep gemm_kernel's reduction order, which is what makes batched, Jacobi
-and AR decoding give the same bits for a row."""
+bit-identical, from one 16-row group to eight 64-row tiles, ragged tails included (a one-tile
+launch and the last tile of a split launch run only their live 16-row groups, 1 to 4 of them): the
+split and the row-tiled kernels keep gemm_kernel's reduction order, which is what makes batched,
+Jacobi and AR decoding give the same bits for a row."""
 import os
 import subprocess
 
@@ -19,7 +20,7 @@ from tests.parity import log
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("rows", [16, 33, 64, 65, 96, 160, 289, 512])
+@pytest.mark.parametrize("rows", [16, 17, 33, 48, 64, 65, 96, 120, 160, 200, 289, 512])
 def test_multi_row_gemms_bit_identical(rows):
     exe = build.KERNEL_BENCH
     if not os.path.exists(exe):

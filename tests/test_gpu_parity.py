@@ -225,6 +225,27 @@ def test_bf16_ragged_widths_vs_oracle():
         pair.gpu.close()
 
 
+@pytest.mark.parametrize("dtype,hd", [("bf16", 32), ("bf16", 256), ("f32", 32), ("f32", 64), ("f32", 128)])
+def test_head_widths_vs_oracle(dtype, hd):
+    # The head widths the library accepts beside those of the tiny, small and 7B configurations
+    # (bf16 32 and 256, fp32 32, 64 and 128: other attention and RoPE instances; 256 takes the
+    # chunk-parallel attention in every iteration). Prompt 150 (three 64-key chunks, a ragged
+    # prompt tile), then blocks of 40 rows whose guesses come from the greedy continuation
+    # corrupted at p = 0.1, so they shrink by several tokens per iteration: one-tile GEMM
+    # launches sized for 64 rows that run 3, 2 or 1 live 16-row groups.
+    from paper_2403_00835_amd.configs import ModelConfig
+    H = 4 if hd <= 64 else 2
+    cfg = ModelConfig(n_layers=2, d_model=H * hd, n_heads=H, head_dim=hd, ffn_dim=344, vocab=1000, dtype=dtype)
+    log(f"[gpu] {dtype} head_dim {hd} ({H} heads), prompt 150, n=40")
+    pair = Pair(cfg, max_ctx=512, max_block=40, max_new=256)
+    try:
+        prompt = workload.make_prompt(cfg, 150, seed=31)
+        stream, _ = pair.gpu.ar_decode(prompt, 256)
+        _teacher_forced(pair, prompt, n=40, steps=8, stream=stream, p=0.1)
+    finally:
+        pair.gpu.close()
+
+
 def test_small_decode_is_valid_greedy(small):
     log("[gpu] small bf16 decode, stream re-drawn p=0.3, n=16, 96 new")
     prompt = workload.make_prompt(SMALL, 128)

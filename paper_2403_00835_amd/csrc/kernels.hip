@@ -341,13 +341,16 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
         }
     }
     // Every global load of the workgroup is issued up front: Q rows, the chunk's keys and values.
+    // A wave whose rows are all past the block (it only helps stage K and V) loads no queries.
+    const bool wave_live = rbase + 16 * rg < m;  // uniform over the wave
     u32x4 qv[PT::PLANES][NKK], kv[4][NKK];
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
         const int dcol = h * HD + kk * PT::KSTEP + g * PT::VEC;
 #pragma unroll
         for (int pl = 0; pl < PT::PLANES; ++pl)
-            qv[pl][kk] = *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, dcol, d));
+            qv[pl][kk] = wave_live ? *reinterpret_cast<const u32x4 *>(Q + pl * act_plane(p.rr.cap, d) + act_idx<P>(qld, dcol, d))
+                                   : u32x4{0u, 0u, 0u, 0u};
         if constexpr (!SHARED) {
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) kv[kt][kk] = *k_block(kt, kk);
@@ -363,7 +366,7 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
     if constexpr (SHARED) {
         wait_vm<0>();        // this wave's blocks (and queries) have landed
         barrier_no_fence();  // every wave's
-        if (rbase + 16 * rg >= m) return;  // this wave's rows are all past the block
+        if (!wave_live) return;  // this wave's rows are all past the block
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll

@@ -253,7 +253,7 @@ __host__ __device__ constexpr int tile_lds_floats() {
 // The body of gemm_kernel for column group wg, row tile p.rt0 + rt and K range z (E_LOGITS with
 // p.kc > 0); smem holds tile_lds_floats<NT, RG, W>() floats.
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
-__device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int z, float *smem) {
+__device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int z, float *smem, int row0_at = -1) {
     static_assert(W == 8, "the K split and its reduction tree are defined for 8 waves");
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
@@ -267,10 +267,10 @@ __device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int
         }
     }
     // This workgroup's row tile: rows [row0, row0 + ROWS) of the iteration (within the row
-    // capacity); m of them are live. A launch of one row tile (MT false) always has live rows, so
-    // nothing waits for the row count before the first loads; with several row tiles (MT) a tile
-    // with no live row exits first.
-    const int row0 = (p.rt0 + rt) * ROWS;
+    // capacity; row0_at, when given, places it); m of them are live. A launch of one row tile
+    // (MT false) always has live rows, so nothing waits for the row count before the first loads;
+    // with several row tiles (MT) a tile with no live row exits first.
+    const int row0 = row0_at >= 0 ? row0_at : (p.rt0 + rt) * ROWS;
     request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T);
     const int m = p.rr.tab->R - row0;
     if constexpr (MT) {
@@ -360,35 +360,34 @@ __device__ __forceinline__ void gemm_tile_body(GemmParams p, int wg, int rt, int
     gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
 }
 
-// gemm_kernel's body for the first row tile of a launch whose rows fit one tile (p.rt0 == 0),
-// with only as many 16-row groups as the iteration has rows (at most RG; the count is known only
-// on the device: blocks shrink as tokens are accepted). A row's sums do not depend on the row
-// groups computed beside it, so every row keeps its values, and an iteration of few rows streams
-// the weights with fewer operand rows and MFMAs. smem holds tile_lds_floats<NT, RG, W>() floats.
+// gemm_kernel's body for row tile rt of a launch (rows from (p.rt0 + rt) 16 RG on) with only as
+// many 16-row groups as the tile has live rows (at most RG). A row's sums do not depend on the
+// row groups computed beside it, so every row keeps its values, and a tile of few rows (a
+// shrinking block, the last tile of a batched iteration) streams the weights with fewer operand
+// rows and MFMAs. A one-tile launch (MT false) reads the row count before its first loads (the
+// host knows only the block size, not the rows each queued iteration will have); a launch of
+// several tiles reads it anyway, to let dead tiles exit. smem holds tile_lds_floats<NT, RG, W>()
+// floats.
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
-__device__ __forceinline__ void gemm_tile_body_live(const GemmParams &p, int wg, int z, float *smem) {
+__device__ __forceinline__ void gemm_tile_body_live(const GemmParams &p, int wg, int rt, int z, float *smem) {
     if constexpr (RG > 1) {
-        if (p.rt0 == 0) {
-            const int m = p.rr.tab->R;
-            if (m <= 16) return gemm_tile_body<P, NT, 1, EP, D, W, MT>(p, wg, 0, z, smem);
-            if constexpr (RG > 2) {
-                if (m <= 32) return gemm_tile_body<P, NT, 2, EP, D, W, MT>(p, wg, 0, z, smem);
-            }
-            if constexpr (RG > 3) {
-                if (m <= 48) return gemm_tile_body<P, NT, 3, EP, D, W, MT>(p, wg, 0, z, smem);
-            }
+        const int row0 = (p.rt0 + rt) * 16 * RG;
+        const int m = p.rr.tab->R - row0;
+        if (m <= 16) return gemm_tile_body<P, NT, 1, EP, D, W, MT>(p, wg, 0, z, smem, row0);
+        if constexpr (RG > 2) {
+            if (m <= 32) return gemm_tile_body<P, NT, 2, EP, D, W, MT>(p, wg, 0, z, smem, row0);
+        }
+        if constexpr (RG > 3) {
+            if (m <= 48) return gemm_tile_body<P, NT, 3, EP, D, W, MT>(p, wg, 0, z, smem, row0);
         }
     }
-    gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, wg, 0, z, smem);
+    gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, wg, rt, z, smem);
 }
 
 template <Prec P, int NT, int RG, int EP, int D, int W, bool MT>
 __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
     extern __shared__ float smem[];
-    if constexpr (MT)
-        gemm_tile_body<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
-    else
-        gemm_tile_body_live<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.z, smem);
+    gemm_tile_body_live<P, NT, RG, EP, D, W, MT>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -692,44 +691,17 @@ __host__ __device__ constexpr int rows_lds_floats() {
     return (stage > after ? stage : after) + ROWS;
 }
 
-// An iteration of at most 64 rows (one row tile; the row count is known only on the device) takes
-// gemm_kernel's body with NT_T tiles per workgroup and D_T k-steps in flight instead: its column
-// groups are narrower, so more workgroups share the work (one row tile of the row-tiled kernel
-// would occupy fewer than half the CUs).
-template <int NT, int EP, int NB, int NT_T, int D_T>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParams p) {
+// The row-tiled product of one tile of 16 RGT live rows (row0 on, m of them live) over a WM x
+// (8 / WM) wave grid: eight class sums per output folded in gemm_kernel's tree, its row factor
+// and epilogue. smem holds rows_lds_floats<NT, EP, NB>() floats (the launch's 64-row tile).
+template <int RGT, int WM, int NT, int EP, int NB>
+__device__ __forceinline__ void rows_tile_body(const GemmParams &p, int wg, int row0, int m, float *smem) {
     constexpr Prec P = Prec::BF16;
-    constexpr int RG = 4, WM = 2, W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
-    constexpr int BLK = 2 * RG + NT;
-    static_assert(NT % WN == 0 && NB >= 3, "tile split, ring depth");
+    constexpr int W = kGemmWaves, WN = W / WM, RGW = RGT / WM, NTW = NT / WN;
+    constexpr int BLK = 2 * RGT + NT;
+    static_assert(RGT % WM == 0 && NT % WN == 0 && NB >= 3, "tile split, ring depth");
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    extern __shared__ float smem[];
-    request_together(p.rr.tab, p.cols, p.rt0);
-    if (p.rr.tab->R - p.rt0 * ROWS <= ROWS) {
-        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
-        if ((int)blockIdx.x < nwt) gemm_tile_body_live<P, NT_T, RG, EP, D_T, W, true>(p, blockIdx.x, blockIdx.z, smem);
-        return;
-    }
-    if constexpr (EP == E_LOGITS) {
-        if (p.kc > 0) {  // split K as gemm_kernel does
-            const int ks0 = blockIdx.z * p.kc;
-            p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
-            p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;
-            p.Ks = min(p.kc, p.Ks - ks0);
-            p.Zout += (size_t)blockIdx.z * p.zstride;
-        }
-    }
-    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD
-    // (its L2 serves the weight tiles to all of them). The launch covers its largest row count; the
-    // live row tiles (from the device row table) take the first workgroups of each XCD, so the
-    // workgroups past them, which exit at once, are dispatched last.
-    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg, p.row_tiles);
-    const int live = min(p.row_tiles, (p.rr.tab->R - p.rt0 * ROWS + ROWS - 1) / ROWS);
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    const int wg = (slot / live) * 8 + xcd, row0 = (p.rt0 + slot % live) * ROWS;
-    if (wg >= p.n_wg) return;
-    const int m = p.rr.tab->R - row0;
+    constexpr int ROWS = 16 * RGT, COLS = 16 * NT;
     const int rg0 = row0 >> 4, t0 = wg * NT;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -739,15 +711,16 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParam
     u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64] during the main loop
     float *s_red = smem;
     float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);
-    float *s_inv = smem + rows_lds_floats<NT, EP, NB>() - ROWS;
+    float *s_inv = smem + rows_lds_floats<NT, EP, NB>() - kMaxRows;
 
     f32x4 sq_pre[2];
     if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
 
-    // DMA blocks of a k-step: block b < 2 RG is activation plane b / RG, row group b % RG; block
-    // 2 RG + j is weight tile t0 + j (clamped; its columns are never written). Wave w issues
-    // blocks w, w + W, ... (NLW of them; where the last round has no block for a wave, it loads the
-    // last block again into its place), so every wave has the same number of loads in flight.
+    // DMA blocks of a k-step: block b < 2 RGT is activation plane b / RGT, row group b % RGT;
+    // block 2 RGT + j is weight tile t0 + j (clamped; its columns are never written). Wave w
+    // issues blocks w, w + W, ... (NLW of them; where the last round has no block for a wave, it
+    // loads the last block again into its place), so every wave has the same number of loads in
+    // flight.
     constexpr int NLW = (BLK + W - 1) / W;
     const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
     const u32x4 *src[NLW];
@@ -756,12 +729,12 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParam
     for (int i = 0; i < NLW; ++i) {
         const int b = min(w + i * W, BLK - 1);
         dst[i] = b;
-        if (b < 2 * RG) {
-            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RG) * act_plane(p.rr.cap, p.lda);
-            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RG) * ks_a * kWave * 8) + lane;
+        if (b < 2 * RGT) {
+            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RGT) * act_plane(p.rr.cap, p.lda);
+            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RGT) * ks_a * kWave * 8) + lane;
             adv[i] = kWave;
         } else {
-            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
+            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RGT, tiles - 1) * kTileBytes) + lane;
             adv[i] = tiles * kWave;
         }
     }
@@ -799,9 +772,9 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParam
 #pragma unroll
                 for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
-                    for (int r = 0; r < RGW; ++r) a[pl][r] = bp[(pl * RG + wm * RGW + r) * kWave];
+                    for (int r = 0; r < RGW; ++r) a[pl][r] = bp[(pl * RGT + wm * RGW + r) * kWave];
 #pragma unroll
-                for (int j = 0; j < NTW; ++j) b[j] = bp[(2 * RG + wn * NTW + j) * kWave];
+                for (int j = 0; j < NTW; ++j) b[j] = bp[(2 * RGT + wn * NTW + j) * kWave];
 #pragma unroll
                 for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
@@ -831,7 +804,56 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParam
                 s_tile[row * (COLS + 1) + 16 * (wn * NTW + j) + (lane & 15)] = x;
             }
     __syncthreads();
-    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+    gemm_epilogue<P, NT, RGT, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
+}
+
+// An iteration of at most 64 rows (one row tile; the row count is known only on the device) takes
+// gemm_kernel's body with NT_T tiles per workgroup and D_T k-steps in flight instead: its column
+// groups are narrower, so more workgroups share the work (one row tile of the row-tiled kernel
+// would occupy fewer than half the CUs). The last live tile of a longer iteration runs only its
+// live 16-row groups.
+template <int NT, int EP, int NB, int NT_T, int D_T>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_rows_kernel(GemmParams p) {
+    constexpr Prec P = Prec::BF16;
+    constexpr int RG = 4, W = kGemmWaves;
+    constexpr int ROWS = 16 * RG;
+    extern __shared__ float smem[];
+    request_together(p.rr.tab, p.cols, p.rt0);
+    if (p.rr.tab->R - p.rt0 * ROWS <= ROWS) {
+        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
+        if ((int)blockIdx.x < nwt) gemm_tile_body_live<P, NT_T, RG, EP, D_T, W, true>(p, blockIdx.x, 0, blockIdx.z, smem);
+        return;
+    }
+    if constexpr (EP == E_LOGITS) {
+        if (p.kc > 0) {  // split K as gemm_kernel does
+            const int ks0 = blockIdx.z * p.kc;
+            p.W += (size_t)ks0 * (p.cols >> 4) * kTileBytes;
+            p.A = reinterpret_cast<const uint8_t *>(p.A) + (size_t)ks0 * kWave * 16;
+            p.Ks = min(p.kc, p.Ks - ks0);
+            p.Zout += (size_t)blockIdx.z * p.zstride;
+        }
+    }
+    // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD
+    // (its L2 serves the weight tiles to all of them). The launch covers its largest row count; the
+    // live row tiles (from the device row table) take the first workgroups of each XCD, so the
+    // workgroups past them, which exit at once, are dispatched last.
+    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg, p.row_tiles);
+    const int live = min(p.row_tiles, (p.rr.tab->R - p.rt0 * ROWS + ROWS - 1) / ROWS);
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int wg = (slot / live) * 8 + xcd, row0 = (p.rt0 + slot % live) * ROWS;
+    if (wg >= p.n_wg) return;
+    const int m = p.rr.tab->R - row0;
+    // 16-row groups of this tile with live rows (every row's values are the same whatever the
+    // tile's row groups and wave grid); one or three groups take a one-row wave grid, which needs
+    // NT a multiple of the 8 waves
+    if constexpr (NT % W == 0) {
+        if (m <= 16) return rows_tile_body<1, 1, NT, EP, NB>(p, wg, row0, m, smem);
+        if (m <= 32) return rows_tile_body<2, 2, NT, EP, NB>(p, wg, row0, m, smem);
+        if (m <= 48) return rows_tile_body<3, 1, NT, EP, NB>(p, wg, row0, m, smem);
+    } else {
+        if (m <= 32) return rows_tile_body<2, 2, NT, EP, NB>(p, wg, row0, m, smem);
+    }
+    rows_tile_body<4, 2, NT, EP, NB>(p, wg, row0, m, smem);
 }
 
 template <int NT, int EP, int NB, int NT_T, int D_T>
@@ -998,7 +1020,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmPara
     if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
         const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
         if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
-            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, smem);
+            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, 0, smem);
         return;
     }
     // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;

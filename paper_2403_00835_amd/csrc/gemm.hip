@@ -1098,7 +1098,9 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(G
     float *s_inv = s_tile + ROWS * (COLS + 1);                 // ROWS
     const int tiles = p.cols >> 4, t0 = wg * NT, rg0 = row0 >> 4;
     const size_t plane = (size_t)p.rr.cap * p.cols;
-    // vector u = tid + i W 64: row group (u / 64) / NT, tile (u / 64) % NT, lane u % 64
+    // vector u = tid + i W 64: row group (u / 64) / NT, tile (u / 64) % NT, lane u % 64; row
+    // groups past the iteration's rows (the split launch wrote no partials there; their rows are
+    // not written out) load nothing
     f32x4 z[NV][4];
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
@@ -1106,7 +1108,8 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(G
         const int r = blk / NT, t = min(t0 + blk % NT, tiles - 1);
         const float *src = p.spart + (((size_t)(rg0 + r) * tiles + t) * kWave + (u & 63)) * 4;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) z[i][c] = *reinterpret_cast<const f32x4 *>(src + c * plane);
+        for (int c = 0; c < 4; ++c)
+            z[i][c] = 16 * r < m ? *reinterpret_cast<const f32x4 *>(src + c * plane) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     if constexpr (ROWSCALE) {  // the row factors the split launch computed (row_factor_reduce's values)
         if (tid < ROWS) s_inv[tid] = p.sinv[row0 + tid];

@@ -181,6 +181,29 @@ def test_narrow_bf16_batched_steps_equal_single():
         single.close()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_max_batch_and_block(dtype):
+    # The largest batched iteration the library takes: 64 sequences with blocks of up to 64 rows
+    # (4096 rows, 64 row tiles; bf16 products through the class-pair split, fp32 through
+    # gemm_kernel over the row tiles). Batched steps equal single steps bit for bit (logits
+    # included), and a batched decode of the 64 sequences equals their single-sequence AR decodes.
+    if dtype == "f32":
+        cfg = TINY
+    else:
+        cfg = ModelConfig(n_layers=2, d_model=256, n_heads=4, head_dim=64, ffn_dim=688, vocab=1000, dtype="bf16")
+    ws, batched, single = _models(cfg, max_ctx=320, max_block=64, max_new=64, max_batch=64)
+    try:
+        lens = np.random.default_rng(40).integers(1, 130, 64)
+        prompts = [workload.make_prompt(cfg, int(L), seed=40, seq=b) for b, L in enumerate(lens)]
+        log(f"[gpu-batch] {dtype}: 64 sequences x blocks of up to 64 rows, 3 batched steps vs single steps")
+        _batched_steps_equal_single(cfg, batched, single, prompts, 64, 3, seed=4)
+        log(f"[gpu-batch] {dtype}: batched decode of 64 sequences (n=64, 48 new) vs single AR")
+        _batched_decode_equals_ar(cfg, batched, single, prompts, 64, 48)
+    finally:
+        batched.close()
+        single.close()
+
+
 def test_small_batched_decode(small):
     ws, batched, single = small
     prompts = [workload.make_prompt(SMALL, L, seed=35, seq=b) for b, L in enumerate([60, 140, 200, 90])]

@@ -246,6 +246,29 @@ def test_head_widths_vs_oracle(dtype, hd):
         pair.gpu.close()
 
 
+def test_tiny_largest_context_ar_equals_jacobi():
+    # The longest context the library accepts (65,408 positions: 1,022 64-key chunks): a 65,200-
+    # token prompt in 512-row prefill passes, then GPU AR and GPU Jacobi decoding (n = 64, guesses
+    # from the AR continuation corrupted at p = 0.3) give the same 128 tokens; every iteration
+    # combines over 1,019 or more chunks (the chunk-parallel attention).
+    from paper_2403_00835_amd import binding
+    max_ctx = 65408
+    ws = workload.make_weights(TINY)
+    gpu = binding.Model(TINY, max_ctx=max_ctx, max_block=64, max_new=128, weights=ws, prefill_chunk=512)
+    try:
+        prompt = workload.make_prompt(TINY, 65200, seed=41)
+        log("[gpu] tiny, prompt 65200 (largest context), AR vs Jacobi n=64, 128 new")
+        ar, _ = gpu.ar_decode(prompt, 128)
+        out, st = gpu.jacobi_decode(prompt, 64, 128, policy=GUESS_STREAM_REINJECT, stream=ar, p=0.3, seed=6)
+        np.testing.assert_array_equal(out, ar)
+        log(f"  {st['steps']} Jacobi iterations")
+        assert st["steps"] < 128
+        with pytest.raises(binding.CllmError):  # one position past the capacity
+            gpu.ar_decode(workload.make_prompt(TINY, max_ctx - 127, seed=41), 128)
+    finally:
+        gpu.close()
+
+
 def test_small_decode_is_valid_greedy(small):
     log("[gpu] small bf16 decode, stream re-drawn p=0.3, n=16, 96 new")
     prompt = workload.make_prompt(SMALL, 128)

@@ -334,6 +334,14 @@ def test_abi_errors_on_device(tiny):
     with pytest.raises(binding.CllmError) as e:
         g.jacobi_step(np.array([(y0 + 1) % 256, 2], dtype=np.int32))
     assert e.value.status == 2  # block_in[0] is not the pending token
+    empty = np.zeros(0, dtype=np.int32)
+    for call in (lambda: g.jacobi_step(empty), lambda: g.prefill(empty), lambda: g.jacobi_decode(empty, 8, 16),
+                 lambda: g.jacobi_decode(prompt, 0, 16), lambda: g.jacobi_decode(prompt, 8, 0),
+                 lambda: g.ar_decode(prompt, 0)):
+        with pytest.raises(binding.CllmError) as e:
+            call()
+        assert e.value.status == 1  # empty block or prompt, n = 0, max_new = 0
+    assert g.prefill(prompt) == y0  # (the empty prefill changed nothing)
     with pytest.raises(binding.CllmError) as e:
         g.jacobi_step(np.array([y0] + [0] * 8, dtype=np.int32))
     assert e.value.status == 1  # m > max_block

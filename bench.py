@@ -168,6 +168,10 @@ def main():
     ap.add_argument("--oracle-decode", action="store_true",
                     help="also time the oracle's AR and Jacobi decoding (tiny, small, shortened 7B; about "
                          "a minute of host time) and add it to the line as oracle_decode")
+    ap.add_argument("--sweep-n", action="store_true",
+                    help="single-sequence workloads: after the timed steps, decode the same request once per "
+                         "block size n in 1, 8, 16, 24, 32, 48, 64 with sliding blocks (every iteration carries "
+                         "n rows) and add the iteration cost against n to the line as n_sweep")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, copy 1 GiB device-to-device (a kernel of known traffic "
                          "for scaling hardware byte counters)")
@@ -341,7 +345,44 @@ def main():
     }
     if args.oracle_decode:
         line["oracle_decode"] = oracle_decodes()
+    if args.sweep_n:
+        model.close()
+        line["n_sweep"] = sweep_n(cfg, ws, prompt, ar, max_new, args, stream, wbytes)
     print(json.dumps(line), flush=True)
+
+
+def sweep_n(cfg, ws, prompt, ar, max_new, args, stream, wbytes):
+    """Iteration cost against the block size n on one request (the cost side of the paper's
+    ablation over n): sliding blocks, so every iteration has n rows; guesses re-drawn from the
+    corrupted greedy continuation (the headline's emulation). n = 1 is greedy AR decoding."""
+    import torch
+    from paper_2403_00835_amd import binding
+    from paper_2403_00835_amd.configs import BLOCK_SLIDE, GUESS_STREAM_REINJECT
+    P = len(prompt)
+    model = binding.Model(cfg, max_ctx=P + max_new + 128, max_block=64, max_new=max_new,
+                          prefill_chunk=args.prefill_chunk, stream=stream.cuda_stream, weights=ws)
+    out = []
+    try:
+        for n in (1, 8, 16, 24, 32, 48, 64):
+            if n == 1:
+                tok, st = model.ar_decode(prompt, max_new)
+            else:
+                tok, st = model.jacobi_decode(prompt, n, max_new, policy=GUESS_STREAM_REINJECT,
+                                              block_policy=BLOCK_SLIDE, stream=ar, p=args.p, seed=3)
+            torch.cuda.synchronize()
+            if not np.array_equal(tok, ar):
+                raise RuntimeError(f"n={n}: output differs from greedy AR output")
+            it_ms = st["iter_ms_full_p50"]  # iterations with n rows (the last ones may have fewer)
+            kv = cfg.n_layers * 2 * (P + max_new / 2) * cfg.d_model * 2
+            out.append({"n": n, "iterations": st["steps"], "mean_accepted": round(max_new / st["steps"], 3),
+                        "iteration_ms": round(it_ms, 4),
+                        "decode_tokens_per_s": round(max_new / (st["decode_ms"] / 1e3), 3),
+                        "step_hbm_gbps": round((wbytes + kv) / (it_ms / 1e3) / 1e9, 1),
+                        "gemm_tflops": round(2.0 * cfg.streamed_params() * n / (it_ms / 1e3) / 1e12, 2)})
+            log(f"[bench] n={n}: {out[-1]}")
+    finally:
+        model.close()
+    return out
 
 
 def main_batched(args, wl):

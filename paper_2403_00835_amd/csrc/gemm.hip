@@ -901,8 +901,8 @@ static hipError_t launch_rows_t(const GemmParams &p, int row_tiles, hipStream_t 
 // 16-column tiles per workgroup and ring depth of the split products (64-row tiles; measured at
 // the LLaMA-2-7B shape, 160 and 512 rows: gate/up 74.6 / 195 us, QKV 45.0 / 100 us before the
 // reduction; O is no faster than gemm_kernel once its reduction is added)
-constexpr int kSplitNtQkv = 24, kSplitNbQkv = 3, kSplitNtGateUp = 24, kSplitNbGateUp = 3;
-constexpr int kSplitNtLm = 24, kSplitNbLm = 3;
+constexpr int kSplitNtQkv = 16, kSplitNbQkv = 3, kSplitNtGateUp = 16, kSplitNbGateUp = 3;
+constexpr int kSplitNtLm = 16, kSplitNbLm = 3;
 
 template <int RGT, int NT, int NB>
 __host__ __device__ constexpr int split_lds_floats() {
@@ -1009,37 +1009,26 @@ __device__ __forceinline__ void split_tile_body(const GemmParams &p, int c, int 
         }
 }
 
-template <int RGT, int NT, int NB, int WM, int EP, int NT_T, int D_T, int MAP = 1>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmParams p) {
-    constexpr Prec P = Prec::BF16;
+// The split product of an iteration of more than 64 rows; an iteration whose rows fit one tile
+// (known only on the device) is left to gemm_one_tile_kernel, launched beside it, so this kernel
+// keeps to 128 registers and two workgroups share a CU.
+template <int NT, int NB, int EP>
+__global__ __launch_bounds__(kGemmWaves * kWave, 2) void gemm_split_kernel(GemmParams p) {
     constexpr int W = kGemmWaves;
-    constexpr int ROWS = 16 * RGT;
-    static_assert(RGT == 4 && WM == 2, "64-row tiles; the last tile's live row groups pick their own wave grid");
+    constexpr int ROWS = kMaxRows;
     extern __shared__ float smem[];
-    request_together(p.rr.tab, p.cols, p.rt0);
-    if (p.rr.tab->R - p.rt0 * kMaxRows <= kMaxRows) {  // one 64-row tile: gemm_kernel's body
-        const int nwt = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
-        if (blockIdx.z == 0 && (int)blockIdx.x < nwt)
-            gemm_tile_body_live<P, NT_T, 4, EP, D_T, W, true>(p, blockIdx.x, 0, 0, smem);
-        return;
-    }
     // Column groups on XCDs in turn, the live row tiles of a column group consecutive on one XCD;
     // the launch covers its largest row count, the live row tiles take the first workgroups of
     // each XCD and the others exit at once.
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
-    request_together(p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq, p.T);
+    request_together(p.rr.tab, p.cols, p.rt0, p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq,
+                     p.T);
     const int R = p.rr.tab->R;
+    if (R - p.rt0 * ROWS <= ROWS) return;  // one 64-row tile: gemm_one_tile_kernel's
     const int live = min(p.row_tiles, (R - p.rt0 * ROWS + ROWS - 1) / ROWS);
-    if (live <= 0) return;
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    int c, wg;
-    if constexpr (MAP == 0) {  // grid z = class pair; column groups on XCDs in turn
-        c = blockIdx.z;
-        wg = (slot / live) * 8 + xcd;
-    } else {  // XCD x takes class pair x % 4 and every other column group from x / 4
-        c = xcd & 3;
-        wg = (slot / live) * 2 + (xcd >> 2);
-    }
+    // XCD x takes class pair x % 4 and every other column group from x / 4
+    const int c = xcd & 3, wg = (slot / live) * 2 + (xcd >> 2);
     const int row0 = (p.rt0 + slot % live) * ROWS;
     if (wg >= p.n_wg) return;
     const int tid = threadIdx.x;
@@ -1050,16 +1039,24 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmPara
 
     // The last live tile runs only its live 16-row groups (rows past the iteration's rows have
     // no partials; the reduction writes nothing for them). Every row's t_c is the same whatever
-    // the tile's row groups and wave grid.
+    // the tile's row groups and wave grid; one or three groups take a one-row wave grid, which
+    // needs NT a multiple of the 8 waves.
     const int mt = R - row0;
-    if (mt <= 16)
-        split_tile_body<1, 1, NT, NB>(p, c, wg, row0, smem);
-    else if (mt <= 32)
-        split_tile_body<2, 2, NT, NB>(p, c, wg, row0, smem);
-    else if (mt <= 48)
-        split_tile_body<3, 1, NT, NB>(p, c, wg, row0, smem);
-    else
-        split_tile_body<4, 2, NT, NB>(p, c, wg, row0, smem);
+    if constexpr (NT % W == 0) {
+        if (mt <= 16)
+            split_tile_body<1, 1, NT, NB>(p, c, wg, row0, smem);
+        else if (mt <= 32)
+            split_tile_body<2, 2, NT, NB>(p, c, wg, row0, smem);
+        else if (mt <= 48)
+            split_tile_body<3, 1, NT, NB>(p, c, wg, row0, smem);
+        else
+            split_tile_body<4, 2, NT, NB>(p, c, wg, row0, smem);
+    } else {
+        if (mt <= 32)
+            split_tile_body<2, 2, NT, NB>(p, c, wg, row0, smem);
+        else
+            split_tile_body<4, 2, NT, NB>(p, c, wg, row0, smem);
+    }
 
     if (factors) {  // uniform over the workgroup
         __syncthreads();  // every wave is past its last read of the ring
@@ -1068,6 +1065,17 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_kernel(GemmPara
         __syncthreads();
         if (tid < ROWS) p.sinv[row0 + tid] = s_inv[tid];
     }
+}
+
+// gemm_kernel's body (over the live 16-row groups, NT tiles per workgroup) for an iteration whose
+// rows fit one 64-row tile, launched beside the split product; an iteration of more rows leaves
+// it to the split product and the reduction.
+template <int NT, int EP, int D>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_one_tile_kernel(GemmParams p) {
+    extern __shared__ float smem[];
+    request_together(p.rr.tab, p.rt0);
+    if (p.rr.tab->R - p.rt0 * kMaxRows > kMaxRows) return;
+    gemm_tile_body_live<Prec::BF16, NT, 4, EP, D, kGemmWaves, true>(p, blockIdx.x, 0, 0, smem);
 }
 
 // (t0 + t2) + (t1 + t3) of the class-pair partials for a 64-row tile x 16 NT columns, the RMSNorm
@@ -1134,27 +1142,33 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(G
 // The product through the class-pair split: gemm_split_kernel over row_tiles tiles of 64 rows (from
 // row tile p.rt0), then gemm_split_reduce_kernel with NT_E tiles per workgroup. e0 marks the
 // product's start, e1 the reduction's end.
-template <int NT, int NB, int EP, int NT_E, int NT_T, int D_T, int MAP = 1>
+template <int NT, int NB, int EP, int NT_E, int NT_T, int D_T>
 static hipError_t launch_split_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    constexpr int RGT = 4, WM = 2, ROWS = 16 * RGT, COLS = 16 * NT;
+    constexpr int ROWS = kMaxRows, COLS = 16 * NT;
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
     if (!p.spart || (ROWSCALE && !p.sinv) || row_tiles < 1 || (p.rt0 + row_tiles) * ROWS > p.rr.cap ||
         p.lda % 32 != 0 || p.cols % 16 != 0 || p.Ks < 4 || p.kc != 0)
         return hipErrorInvalidValue;
+    // the one-tile body (exits unless the rows fit one tile), then the split product and the
+    // reduction (both exit when they do)
+    GemmParams t = p;
+    t.n_wg = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
+    t.row_tiles = 1;
+    const size_t lds_t = (size_t)tile_lds_floats<NT_T, 4, kGemmWaves>() * sizeof(float);
+    auto one = gemm_one_tile_kernel<NT_T, EP, D_T>;
+    if (e0)
+        hipExtLaunchKernelGGL(one, dim3((unsigned)t.n_wg), dim3(kGemmWaves * kWave), lds_t, s, e0, nullptr, 0, t);
+    else
+        hipLaunchKernelGGL(one, dim3((unsigned)t.n_wg), dim3(kGemmWaves * kWave), lds_t, s, t);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
     GemmParams q = p;
     q.n_wg = (p.cols + COLS - 1) / COLS;
     q.row_tiles = row_tiles;
-    constexpr int lds_split = split_lds_floats<RGT, NT, NB>(), lds_tile = tile_lds_floats<NT_T, 4, kGemmWaves>();
-    const size_t lds = (size_t)(lds_split > lds_tile ? lds_split : lds_tile) * sizeof(float);
-    const int n_tile = (p.cols + 16 * NT_T - 1) / (16 * NT_T);  // column groups of the one-tile body
-    const dim3 grid = MAP == 0 ? dim3((unsigned)std::max((q.n_wg + 7) / 8 * 8 * row_tiles, n_tile), 1, 4)
-                               : dim3((unsigned)std::max((q.n_wg + 1) / 2 * 8 * row_tiles, n_tile), 1, 1);
-    auto kern = gemm_split_kernel<RGT, NT, NB, WM, EP, NT_T, D_T, MAP>;
-    if (e0)
-        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, nullptr, 0, q);
-    else
-        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
-    hipError_t err = hipGetLastError();
+    const size_t lds = (size_t)split_lds_floats<4, NT, NB>() * sizeof(float);
+    const dim3 grid((unsigned)((q.n_wg + 1) / 2 * 8 * row_tiles));
+    hipLaunchKernelGGL((gemm_split_kernel<NT, NB, EP>), grid, dim3(kGemmWaves * kWave), lds, s, q);
+    err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmParams r = p;
     r.n_wg = (p.cols + 16 * NT_E - 1) / (16 * NT_E);

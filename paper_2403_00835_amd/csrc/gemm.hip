@@ -1011,9 +1011,9 @@ __device__ __forceinline__ void split_tile_body(const GemmParams &p, int c, int 
 
 // The split product of an iteration of more than 64 rows; an iteration whose rows fit one tile
 // (known only on the device) is left to gemm_one_tile_kernel, launched beside it, so this kernel
-// keeps to 128 registers and two workgroups share a CU.
+// keeps to 128 registers (at least four waves per SIMD) and two workgroups share a CU.
 template <int NT, int NB, int EP>
-__global__ __launch_bounds__(kGemmWaves * kWave, 2) void gemm_split_kernel(GemmParams p) {
+__global__ __launch_bounds__(kGemmWaves * kWave, 4) void gemm_split_kernel(GemmParams p) {
     constexpr int W = kGemmWaves;
     constexpr int ROWS = kMaxRows;
     extern __shared__ float smem[];

@@ -317,6 +317,8 @@ struct IterShape {
     int lm_rt0;         // >= 0: the LM head runs only on this 64-row tile (a prefill chunk's last row)
     bool tail = true;   // false: the decoder layers only (no LM head, scan or commit)
     bool prompt = false;  // prompt rows (a prefill chunk): bf16 products take the prompt GEMM
+    uint64_t lm_mask = 0;   // != 0: the LM head runs only on these 64-row tiles (packed prefill)
+    uint64_t adv_mask = 0;  // prefill entries whose chunk does not end their prompt
 };
 
 cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev, const int32_t *stream_dev) {
@@ -468,13 +470,23 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
         lm.pidx = c->pidx;
         lm.dbg = c->dbg_on ? c->dbg : nullptr;
         int lm_tiles = row_tiles;
-        if (sh.lm_rt0 >= 0 && tiled) {
-            lm.rt0 = sh.lm_rt0;
-            lm_tiles = 1;
+        if (sh.lm_mask && tiled) {  // one launch per tile that holds a prompt's last row
+            for (int t = 0; t < row_tiles; ++t) {
+                if (!((sh.lm_mask >> t) & 1)) continue;
+                lm.rt0 = t;
+                timing_events(c, CLLM_KT_LM_HEAD, rg, &e0, &e1);
+                HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, 1, lm, s, e0, e1));
+            }
+        } else {
+            if (sh.lm_rt0 >= 0 && tiled) {
+                lm.rt0 = sh.lm_rt0;
+                lm_tiles = 1;
+            }
+            timing_events(c, CLLM_KT_LM_HEAD, rg, &e0, &e1);
+            HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, lm_tiles, lm, s, e0, e1));
         }
-        timing_events(c, CLLM_KT_LM_HEAD, rg, &e0, &e1);
-        HIPCHK(c, launch_gemm(GEMM_LM, c->bf16, rg, lm_tiles, lm, s, e0, e1));
         sp.advance_only = 0;
+        sp.advance_mask = sh.adv_mask;
     } else {
         sp.advance_only = 1;
     }
@@ -485,24 +497,26 @@ cllm_status enqueue_iteration(cllm_ctx *c, const IterShape &sh, int32_t *out_dev
 }
 
 // Host edits for nseq batch entries: slot seq[b] gets mode and block size m[b]; its tokens are
-// copied from host zs + b * zstride. set_L (one entry: a prefill's first chunk) resets L to 0.
+// copied from host zs + b * zstride (packed: entry after entry). Entries with their bit set in
+// reset_mask (a prompt's first prefill chunk) restart at L = 0.
 cllm_status setup(cllm_ctx *c, int mode, int nseq, const int32_t *seq, const int32_t *m, const int32_t *zs, int zstride,
-                  bool set_L) {
+                  uint64_t reset_mask, bool packed = false) {
     SetupParams sp{};
     sp.ctl = c->ctl;
     sp.tab = c->tab;
     sp.rows = c->rows;
     sp.zin = c->zin;
     sp.zstride = zstride;
+    sp.packed = packed ? 1 : 0;
     sp.nseq = nseq;
     sp.mode = mode;
-    sp.set_L = set_L ? 1 : 0;
-    sp.L = 0;
-    size_t ntok = 0;
+    sp.reset_mask = reset_mask;
+    size_t ntok = 0, npacked = 0;
     for (int b = 0; b < nseq; ++b) {
         sp.seq[b] = seq[b];
         sp.m[b] = m[b];
-        ntok = std::max(ntok, (size_t)b * zstride + m[b]);
+        npacked += m[b];
+        ntok = std::max(ntok, packed ? npacked : (size_t)b * zstride + m[b]);
     }
     if (ntok > (size_t)c->zin_cap) return fail(c, CLLM_ERR_CAPACITY, "token staging too small");
     if (ntok) HIPCHK(c, hipMemcpyAsync(c->zin, zs, ntok * 4, hipMemcpyHostToDevice, c->stream));
@@ -538,12 +552,66 @@ cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
     for (int k = 0; k < nchunks; ++k) {
         const int start = k * chunk;
         const int rows = std::min(chunk, len - start);
-        cllm_status st = setup(c, MODE_PREFILL, 1, &seq, &rows, prompt + start, chunk, k == 0);
+        cllm_status st = setup(c, MODE_PREFILL, 1, &seq, &rows, prompt + start, chunk, k == 0 ? 1 : 0);
         if (st) return st;
         const bool last = k == nchunks - 1;
         IterShape sh{rows, 1, rows, std::min(c->nch, ceil_div(start + rows, kAttnChunk)), last,
                      last ? (rows - 1) / kMaxRows : -1};
         sh.prompt = true;
+        st = enqueue_iteration(c, sh, nullptr, nullptr);
+        if (st) return st;
+    }
+    return CLLM_OK;
+}
+
+// Prefill of B prompts packed into passes of up to the prefill chunk: each pass takes the
+// remaining rows of the prompts in order (a prompt may span passes), so short prompts share a
+// pass instead of each streaming the weights on its own. The LM head runs on the 64-row tiles
+// that hold a prompt's last row; entries whose rows do not end their prompt only advance. Every
+// prompt row takes the prompt GEMM and the chunk-parallel attention at absolute positions, so the
+// caches and first tokens are those of one prefill per prompt.
+cllm_status prefill_packed_impl(cllm_ctx *c, int B, const int32_t *seq_ids, const int32_t *prompts,
+                                const size_t *off, const int32_t *lens) {
+    for (int b = 0; b < B; ++b) c->slot[seq_ids[b]].prefilled = false;
+    c->in_prefill = true;
+    struct Flag {  // cleared on every return
+        bool &f;
+        ~Flag() { f = false; }
+    } flag{c->in_prefill};
+    const int chunk = c->pchunk;
+    std::vector<int> done(B, 0);  // prompt rows already prefilled
+    std::vector<int32_t> seq, m, toks;
+    int b = 0;
+    while (b < B) {
+        seq.clear();
+        m.clear();
+        toks.clear();
+        uint64_t reset = 0, adv = 0, lm = 0;
+        int R = 0, maxm = 0, nch = 1;
+        while (b < B && R < chunk && (int)seq.size() < kMaxSeqs) {
+            const int e = (int)seq.size(), take = std::min(lens[b] - done[b], chunk - R);
+            seq.push_back(seq_ids[b]);
+            m.push_back(take);
+            toks.insert(toks.end(), prompts + off[b] + done[b], prompts + off[b] + done[b] + take);
+            if (done[b] == 0) reset |= 1ull << e;
+            done[b] += take;
+            nch = std::max(nch, ceil_div(done[b], kAttnChunk));
+            maxm = std::max(maxm, take);
+            R += take;
+            if (done[b] == lens[b]) {
+                lm |= 1ull << ((R - 1) / kMaxRows);
+                ++b;
+            } else {
+                adv |= 1ull << e;
+            }
+        }
+        const int ne = (int)seq.size();
+        cllm_status st = setup(c, MODE_PREFILL, ne, seq.data(), m.data(), toks.data(), 0, reset, true);
+        if (st) return st;
+        IterShape sh{R, ne, maxm, std::min(c->nch, nch), lm != 0, -1};
+        sh.prompt = true;
+        sh.lm_mask = R > kMaxRows ? lm : 0;
+        sh.adv_mask = adv;
         st = enqueue_iteration(c, sh, nullptr, nullptr);
         if (st) return st;
     }
@@ -585,7 +653,7 @@ cllm_status step_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, cons
         maxm = std::max(maxm, m[b]);
         nch = std::max(nch, ceil_div(c->slot[q].L + m[b], kAttnChunk));
     }
-    if ((s = setup(c, MODE_STEP, B, seq_ids, m, blocks_in, zstride, false))) return s;
+    if ((s = setup(c, MODE_STEP, B, seq_ids, m, blocks_in, zstride, 0))) return s;
     const IterShape sh{R, B, maxm, nch, true, -1};
     if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
     std::vector<Ctl> h(c->max_batch);
@@ -659,8 +727,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
                                      (size_t)max_new * 4, hipMemcpyHostToDevice, c->stream));
         }
     HIPCHK(c, hipEventRecord(ev[0], c->stream));
-    for (int b = 0; b < B; ++b)
-        if ((s = prefill_impl(c, seq_ids[b], prompts + off[b], lens[b]))) return s;
+    if ((s = prefill_packed_impl(c, B, seq_ids, prompts, off.data(), lens))) return s;
     HIPCHK(c, hipEventRecord(ev[1], c->stream));
     // Decode parameters into the control blocks (the prefill left L and pending there).
     std::vector<Ctl> h(c->max_batch);
@@ -681,7 +748,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     HIPCHK(c, hipMemcpyAsync(c->ctl, h.data(), sizeof(Ctl) * c->max_batch, hipMemcpyHostToDevice, c->stream));
     // the batch entries into the row table, then the first blocks and their rows
     std::vector<int32_t> zero_m(B, 0);
-    if ((s = setup(c, MODE_DECODE, B, seq_ids, zero_m.data(), nullptr, 0, false))) return s;
+    if ((s = setup(c, MODE_DECODE, B, seq_ids, zero_m.data(), nullptr, 0, 0))) return s;
     ScanParams sp{};
     sp.ctl = c->ctl;
     sp.tab = c->tab;
@@ -1627,7 +1694,7 @@ cllm_status cllm_hidden_rows(cllm_ctx *c, int32_t seq, const int32_t *block, int
     auto &w = c->loss;
     if ((s = loss_buf(c, &w.hid, &w.hd_n, (size_t)m * c->d))) return s;
     // the decoder layers over the block at the committed length (provisional KV rows, no commit)
-    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, false))) return s;
+    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, 0))) return s;
     IterShape sh{m, 1, m, ceil_div(c->slot[seq].L + m, kAttnChunk), false, -1};
     sh.tail = false;
     if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;
@@ -1652,7 +1719,7 @@ cllm_status cllm_hidden_rows_noalloc(cllm_ctx *c, int32_t seq, const int32_t *bl
     float *hid = scratch_of(c->opts.device);
     if (!hid) return fail(c, CLLM_ERR_STATE, "no scratch address for device %d", c->opts.device);
     // as cllm_hidden_rows, with the staging rows in the device's scratch
-    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, false))) return s;
+    if ((s = setup(c, MODE_STEP, 1, &seq, &m, block, m, 0))) return s;
     IterShape sh{m, 1, m, ceil_div(c->slot[seq].L + m, kAttnChunk), false, -1};
     sh.tail = false;
     if ((s = enqueue_iteration(c, sh, nullptr, nullptr))) return s;

@@ -677,7 +677,8 @@ __device__ void commit_scalar(Ctl *c, int m, int a, int err, int32_t *mlog, int3
 // z[k] = pred[k-1], from one wave's ballot); the emitted tokens; the state update (one thread);
 // the next block's tokens (one thread per position). The sequence's control block is worked on
 // in LDS (one parallel copy in, one out), so the state update is not a chain of global-memory
-// round trips. A prefill chunk needs only its last row. With one batch entry the workgroup also
+// round trips. A prefill chunk that ends its prompt needs only its last row; one that does not
+// (and every chunk of a pass without the LM head) only advances L. With one batch entry the workgroup also
 // lays out the next row table.
 __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     const int bi = blockIdx.x;
@@ -694,7 +695,7 @@ __global__ __launch_bounds__(1024) void scan_commit_kernel(ScanParams p) {
     static_assert(sizeof(Ctl) % 4 == 0, "the control block is copied as 32-bit words");
     constexpr int kCtlWords = (int)(sizeof(Ctl) / 4);
     if (m > 0) {
-        if (p.advance_only) {
+        if (p.advance_only || ((p.advance_mask >> bi) & 1)) {
             if (tid == 0) {
                 gc->L += m;
                 gc->m = 0;
@@ -929,15 +930,16 @@ __global__ __launch_bounds__(256) void setup_kernel(SetupParams p) {
         int R = 0;
         for (int b = 0; b < p.nseq; ++b) {
             Ctl *c = p.ctl + p.seq[b];
-            if (p.set_L) {
-                c->L = p.L;
+            if ((p.reset_mask >> b) & 1) {
+                c->L = 0;
                 c->err = 0;
                 c->done = 0;
             }
             c->mode = p.mode;
             c->m = p.m[b];
+            const size_t zo = p.packed ? (size_t)R : (size_t)b * p.zstride;
             if (p.mode != MODE_PREFILL)
-                for (int i = 0; i < p.m[b]; ++i) c->z[i] = p.zin[(size_t)b * p.zstride + i];
+                for (int i = 0; i < p.m[b]; ++i) c->z[i] = p.zin[zo + i];
             p.tab->seq[b] = p.seq[b];
             p.tab->r0[b] = R;
             p.tab->m[b] = p.m[b];
@@ -950,9 +952,11 @@ __global__ __launch_bounds__(256) void setup_kernel(SetupParams p) {
         p.tab->R = R;
     }
     __syncthreads();
-    for (int b = 0; b < p.nseq; ++b)
+    for (int b = 0; b < p.nseq; ++b) {
+        const size_t zo = p.packed ? (size_t)s_r0[b] : (size_t)b * p.zstride;
         for (int i = threadIdx.x; i < p.m[b]; i += blockDim.x)
-            p.rows[s_r0[b] + i] = RowInfo{b, s_L[b] + i, p.zin[(size_t)b * p.zstride + i], i};
+            p.rows[s_r0[b] + i] = RowInfo{b, s_L[b] + i, p.zin[zo + i], i};
+    }
 }
 
 hipError_t launch_setup(const SetupParams &p, hipStream_t s) {

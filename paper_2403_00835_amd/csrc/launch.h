@@ -43,6 +43,7 @@ struct ScanParams {
     const int32_t *stream;  // guess streams (may be null), stream_stride per slot
     int out_stride, stream_stride;
     int advance_only;       // prefill chunk without LM head: commit all rows, no predictions
+    uint64_t advance_mask;  // prefill: bit b set = entry b's chunk does not end its prompt (commit only)
     int plan_inline;        // one batch entry: the scan also lays out the next row table
     int32_t *mlog;          // block size of each decode iteration (out_stride entries per slot), or null
     int32_t *trace;         // decode trajectory records (trace_cap per slot, kTraceStride int32 each), or null
@@ -50,14 +51,15 @@ struct ScanParams {
 };
 
 // Host-side edits of the control blocks and the row table, applied on the stream in order with
-// the kernels. Entry b's tokens are zin[b * zstride + i]; a prefill chunk (one entry) may hold
-// up to the row capacity.
+// the kernels. Entry b's tokens are zin[b * zstride + i], or with packed set zin[r0_b + i] (r0_b:
+// the rows of the entries before it); a prefill pass may hold up to the row capacity.
 struct SetupParams {
     Ctl *ctl;
     RowTab *tab;
     RowInfo *rows;
     const int32_t *zin;
-    int zstride, nseq, mode, set_L, L;
+    int zstride, nseq, mode, packed;
+    uint64_t reset_mask;  // bit b: entry b starts a prompt (L = 0, error and done flags cleared)
     int32_t seq[64], m[64];
 };
 

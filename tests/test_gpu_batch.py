@@ -9,7 +9,8 @@ it (fixed reduction orders that do not depend on the rows sharing the pass), so:
   one-kernel attention, the batched ones the chunk-parallel pair, so this also pins the two
   attention paths to each other bit for bit); a batched decode of sequences with
   different prompt lengths and guess policies equals, per sequence, the single-sequence GPU AR
-  decode; prompts longer than 64 rows run as one row-tiled prefill chunk; on tiny the result is
+  decode; prompts longer than 64 rows run as one row-tiled prefill chunk, and a batched decode
+  packs its prompts into shared prefill passes (a prompt may span passes); on tiny the result is
   also the oracle's greedy AR continuation.
 - LLaMA-2-7B shape at the batched workload's full size (16 sequences, prompts uniform in
   [256, 1024], n = 32, 256 new tokens, corruption rates uniform in [0.1, 0.6]): batched Jacobi
@@ -209,6 +210,26 @@ def test_small_batched_decode(small):
     prompts = [workload.make_prompt(SMALL, L, seed=35, seq=b) for b, L in enumerate([60, 140, 200, 90])]
     log("[gpu-batch] small: batched decode of 4 sequences (n=16, 64 new) vs single AR")
     _batched_decode_equals_ar(SMALL, batched, single, prompts, 16, 64)
+
+
+def test_small_packed_prefill_passes():
+    # A batched decode prefills its prompts packed into passes of the prefill chunk: with a chunk
+    # of 128 rows, prompts of 60..260 tokens share passes, span passes, and several end in one
+    # pass (the LM head then runs on each 64-row tile that holds a prompt's last row). Every
+    # sequence equals its single-sequence AR decode, whose prefill runs one prompt at a time in
+    # passes of 512 rows.
+    from paper_2403_00835_amd import binding
+    ws = workload.make_weights(SMALL)
+    packed = binding.Model(SMALL, max_ctx=512, max_block=16, max_new=48, max_batch=6, weights=ws, prefill_chunk=128)
+    single = binding.Model(SMALL, max_ctx=512, max_block=16, max_new=48, weights=ws)
+    try:
+        lens = [60, 140, 30, 260, 20, 90]
+        prompts = [workload.make_prompt(SMALL, L, seed=36, seq=b) for b, L in enumerate(lens)]
+        log("[gpu-batch] small: 6 prompts packed into 128-row prefill passes, batched decode (n=16, 48 new) vs single AR")
+        _batched_decode_equals_ar(SMALL, packed, single, prompts, 16, 48)
+    finally:
+        packed.close()
+        single.close()
 
 
 def test_7b_batched_ragged_full_size():

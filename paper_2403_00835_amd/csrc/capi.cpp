@@ -63,6 +63,10 @@ struct cllm_ctx {
     int32_t *out_dev = nullptr, *stream_dev = nullptr;  // per slot: max_new outputs, stream_cap guesses
     int32_t *mlog_dev = nullptr;  // per slot: block size of each decode iteration (max_new entries)
     std::vector<hipEvent_t> it_ev;  // one per queued decode iteration
+    // decode loop: the control blocks as they stand before a round's last iteration (pinned
+    // host memory, read while that iteration runs) and the event after their copy
+    Ctl *ctl_snap = nullptr;
+    hipEvent_t snap_ev = nullptr;
     int stream_cap = 0;
     std::vector<void *> allocs;
     // caller-owned workspace (cllm_runtime_opts.workspace): the iteration buffers are carved from
@@ -757,11 +761,27 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     HIPCHK(c, launch_decode_init(B, sp, c->stream));
     HIPCHK(c, launch_plan(PlanParams{c->ctl, c->tab, c->rows, c->cap}, c->stream));
     IterShape sh{B * n, B, n, std::min(c->nch, ceil_div(maxlen + max_new + n, kAttnChunk)), true, -1};
+    if (!c->ctl_snap) {
+        void *hp = nullptr;
+        HIPCHK(c, hipHostMalloc(&hp, sizeof(Ctl) * c->max_batch, hipHostMallocDefault));
+        c->ctl_snap = static_cast<Ctl *>(hp);
+        HIPCHK(c, hipEventCreateWithFlags(&c->snap_ev, hipEventDisableTiming));
+    }
     // Device-resident loop: every launch reads its rows from the row table. The host only
     // queues iterations: as many as are certainly needed by the sequence with the most tokens
-    // left (each iteration fixes at most n tokens of a sequence), then reads the control blocks.
+    // left (each iteration fixes at most n tokens of a sequence). The control blocks are copied
+    // out before a round's last iteration and read while it runs, so the next round is queued
+    // before the GPU runs dry; that iteration may still fix up to n tokens of each sequence
+    // (lag), so the next round is shorter by one. When nothing is certainly needed beyond the
+    // iterations in flight, the host waits for them and looks again.
     int64_t queued = 0;
     size_t nev = 0;  // iteration events recorded
+    int lag = 0;     // iterations queued after the state in h was taken
+    auto check_err = [&]() -> cllm_status {
+        for (int b = 0; b < B; ++b)
+            if (h[seq_ids[b]].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
+        return CLLM_OK;
+    };
     while (true) {
         int need = 0;
         for (int b = 0; b < B; ++b) {
@@ -769,7 +789,14 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
             const int left = ct.done ? 0 : max_new - (queued ? ct.e : 0);
             need = std::max(need, ceil_div(left, n));
         }
-        if (need == 0) break;
+        need -= lag;
+        if (need <= 0) {
+            if (lag == 0) break;
+            if ((s = read_ctl(c, h.data()))) return s;  // the iterations in flight have finished
+            lag = 0;
+            if ((s = check_err())) return s;
+            continue;
+        }
         // Launch shape of this round: the blocks of the sequences still running (a finished
         // sequence's block is empty in the row table, and a row's values do not depend on the
         // launch shape), so the products of the last rounds launch for fewer row tiles.
@@ -777,6 +804,11 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
         for (int b = 0; b < B; ++b) active += h[seq_ids[b]].done ? 0 : 1;
         sh.R = std::max(active, 1) * n;
         for (int i = 0; i < need; ++i) {
+            if (i == need - 1) {  // the state before the round's last iteration
+                HIPCHK(c, hipMemcpyAsync(c->ctl_snap, c->ctl, sizeof(Ctl) * c->max_batch, hipMemcpyDeviceToHost,
+                                         c->stream));
+                HIPCHK(c, hipEventRecord(c->snap_ev, c->stream));
+            }
             if ((s = enqueue_iteration(c, sh, c->out_dev, any_stream ? c->stream_dev : nullptr))) return s;
             if (nev == c->it_ev.size()) {
                 hipEvent_t e;
@@ -787,14 +819,10 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
         }
         queued += need;
         HIPCHK(c, hipEventRecord(ev[2], c->stream));
-        if ((s = read_ctl(c, h.data()))) return s;
-        bool all_done = true;
-        for (int b = 0; b < B; ++b) {
-            const Ctl &ct = h[seq_ids[b]];
-            if (ct.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
-            all_done = all_done && ct.done;
-        }
-        if (all_done) break;
+        HIPCHK(c, hipEventSynchronize(c->snap_ev));
+        std::copy(c->ctl_snap, c->ctl_snap + c->max_batch, h.begin());
+        lag = 1;
+        if ((s = check_err())) return s;
         if (queued > (int64_t)max_new + 1) return fail(c, CLLM_ERR_STATE, "decode did not finish");
     }
     float pre_ms = 0.f, dec_ms = 0.f;
@@ -1161,6 +1189,8 @@ void cllm_model_free(cllm_ctx *c) {
     for (void *p : c->allocs) (void)hipFree(p);
     for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
     for (hipEvent_t e : c->it_ev) (void)hipEventDestroy(e);
+    if (c->snap_ev) (void)hipEventDestroy(c->snap_ev);
+    if (c->ctl_snap) (void)hipHostFree(c->ctl_snap);
     delete c;
 }
 

@@ -1009,9 +1009,10 @@ __device__ __forceinline__ void split_tile_body(const GemmParams &p, int c, int 
         }
 }
 
-// The split product of an iteration of more than 64 rows; an iteration whose rows fit one tile
-// (known only on the device) is left to gemm_one_tile_kernel, launched beside it, so this kernel
-// keeps to 128 registers (at least four waves per SIMD) and two workgroups share a CU.
+// The split product of a launch of several 64-row tiles, whatever the rows the iteration turns
+// out to have (known only on the device): one that fits one tile takes the same path (the same
+// values as gemm_kernel's). The kernel keeps to 128 registers (at least four waves per SIMD), so
+// two workgroups share a CU.
 template <int NT, int NB, int EP>
 __global__ __launch_bounds__(kGemmWaves * kWave, 4) void gemm_split_kernel(GemmParams p) {
     constexpr int W = kGemmWaves;
@@ -1024,7 +1025,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave, 4) void gemm_split_kernel(GemmP
     request_together(p.rr.tab, p.cols, p.rt0, p.W, p.A, p.Ks, p.lda, p.rr.cap, p.n_wg, p.row_tiles, p.spart, p.ssq,
                      p.T);
     const int R = p.rr.tab->R;
-    if (R - p.rt0 * ROWS <= ROWS) return;  // one 64-row tile: gemm_one_tile_kernel's
+    if (R - p.rt0 * ROWS <= 0) return;
     const int live = min(p.row_tiles, (R - p.rt0 * ROWS + ROWS - 1) / ROWS);
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
     // XCD x takes class pair x % 4 and every other column group from x / 4
@@ -1067,17 +1068,6 @@ __global__ __launch_bounds__(kGemmWaves * kWave, 4) void gemm_split_kernel(GemmP
     }
 }
 
-// gemm_kernel's body (over the live 16-row groups, NT tiles per workgroup) for an iteration whose
-// rows fit one 64-row tile, launched beside the split product; an iteration of more rows leaves
-// it to the split product and the reduction.
-template <int NT, int EP, int D>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_one_tile_kernel(GemmParams p) {
-    extern __shared__ float smem[];
-    request_together(p.rr.tab, p.rt0);
-    if (p.rr.tab->R - p.rt0 * kMaxRows > kMaxRows) return;
-    gemm_tile_body_live<Prec::BF16, NT, 4, EP, D, kGemmWaves, true>(p, blockIdx.x, 0, 0, smem);
-}
-
 // (t0 + t2) + (t1 + t3) of the class-pair partials for a 64-row tile x 16 NT columns, the RMSNorm
 // row factor (computed once per row tile by the split launch) and gemm_kernel's epilogue. Grid: column groups x row tiles (from p.rt0); row tiles
 // past the iteration's rows exit.
@@ -1098,7 +1088,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(G
     const int wg = blockIdx.x, row0 = (p.rt0 + blockIdx.y) * ROWS;
     request_together(p.rr.tab, p.spart, p.cols, p.rr.cap, p.sinv, p.rt0);
     const int m = p.rr.tab->R - row0;
-    if (m <= 0 || p.rr.tab->R - p.rt0 * ROWS <= ROWS) return;  // no rows, or the split launch did all
+    if (m <= 0) return;  // a row tile past the iteration's rows
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     float *s_red = smem;                                       // epilogue scratch (E_RESID)
@@ -1142,33 +1132,24 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_split_reduce_kernel(G
 // The product through the class-pair split: gemm_split_kernel over row_tiles tiles of 64 rows (from
 // row tile p.rt0), then gemm_split_reduce_kernel with NT_E tiles per workgroup. e0 marks the
 // product's start, e1 the reduction's end.
-template <int NT, int NB, int EP, int NT_E, int NT_T, int D_T>
+template <int NT, int NB, int EP, int NT_E>
 static hipError_t launch_split_t(const GemmParams &p, int row_tiles, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int ROWS = kMaxRows, COLS = 16 * NT;
     constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;
     if (!p.spart || (ROWSCALE && !p.sinv) || row_tiles < 1 || (p.rt0 + row_tiles) * ROWS > p.rr.cap ||
         p.lda % 32 != 0 || p.cols % 16 != 0 || p.Ks < 4 || p.kc != 0)
         return hipErrorInvalidValue;
-    // the one-tile body (exits unless the rows fit one tile), then the split product and the
-    // reduction (both exit when they do)
-    GemmParams t = p;
-    t.n_wg = (p.cols + 16 * NT_T - 1) / (16 * NT_T);
-    t.row_tiles = 1;
-    const size_t lds_t = (size_t)tile_lds_floats<NT_T, 4, kGemmWaves>() * sizeof(float);
-    auto one = gemm_one_tile_kernel<NT_T, EP, D_T>;
-    if (e0)
-        hipExtLaunchKernelGGL(one, dim3((unsigned)t.n_wg), dim3(kGemmWaves * kWave), lds_t, s, e0, nullptr, 0, t);
-    else
-        hipLaunchKernelGGL(one, dim3((unsigned)t.n_wg), dim3(kGemmWaves * kWave), lds_t, s, t);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
     GemmParams q = p;
     q.n_wg = (p.cols + COLS - 1) / COLS;
     q.row_tiles = row_tiles;
     const size_t lds = (size_t)split_lds_floats<4, NT, NB>() * sizeof(float);
     const dim3 grid((unsigned)((q.n_wg + 1) / 2 * 8 * row_tiles));
-    hipLaunchKernelGGL((gemm_split_kernel<NT, NB, EP>), grid, dim3(kGemmWaves * kWave), lds, s, q);
-    err = hipGetLastError();
+    auto split = gemm_split_kernel<NT, NB, EP>;
+    if (e0)
+        hipExtLaunchKernelGGL(split, grid, dim3(kGemmWaves * kWave), lds, s, e0, nullptr, 0, q);
+    else
+        hipLaunchKernelGGL(split, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     GemmParams r = p;
     r.n_wg = (p.cols + 16 * NT_E - 1) / (16 * NT_E);
@@ -1366,12 +1347,12 @@ static hipError_t launch_gemm_rg(GemmKind kind, const GemmParams &p, int row_til
         // More than 64 rows, bf16 (K of at least four k-steps): QKV, gate/up and the LM head
         // through the class-pair K split (the same values)
         if (kind == GEMM_QKV)
-            return launch_split_t<kSplitNtQkv, kSplitNbQkv, E_QKV, 4, 6, 2>(p, row_tiles, s, e0, e1);
+            return launch_split_t<kSplitNtQkv, kSplitNbQkv, E_QKV, 4>(p, row_tiles, s, e0, e1);
         if (kind == GEMM_GATE_UP)
-            return launch_split_t<kSplitNtGateUp, kSplitNbGateUp, E_SWIGLU, 4, 6, 2>(p, row_tiles, s, e0, e1);
+            return launch_split_t<kSplitNtGateUp, kSplitNbGateUp, E_SWIGLU, 4>(p, row_tiles, s, e0, e1);
         // the reduction's column groups are the LM head's argmax workgroups (kLmTiles tiles each)
         if (kind == GEMM_LM)
-            return launch_split_t<kSplitNtLm, kSplitNbLm, E_ARGMAX, kLmTiles, kLmTiles, 3>(p, row_tiles, s, e0, e1);
+            return launch_split_t<kSplitNtLm, kSplitNbLm, E_ARGMAX, kLmTiles>(p, row_tiles, s, e0, e1);
     }
     if (row_tiles > 1 && P == Prec::BF16 && !p.tile_kernel) {
         // More than 64 rows, bf16: gate/up and the down product take the row-tiled kernel (the

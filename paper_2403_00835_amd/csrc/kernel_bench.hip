@@ -17,8 +17,8 @@
 // runs each decode product (QKV, O, gate/up, down, LM head) twice over the same inputs, launched
 // for the row tiles the rows fill and for at least two row tiles as batched iterations are: as the
 // library launches it (with several row tiles: QKV, gate/up and the LM head through the
-// class-pair K split, the down ranges through the row-tiled kernel, each taking gemm_kernel's
-// body when the live rows fit one tile) and through gemm_kernel over the same row tiles; every
+// class-pair K split, also when the live rows fit one tile, the down ranges through the row-tiled
+// kernel, which then takes gemm_kernel's body) and through gemm_kernel over the same row tiles; every
 // output (Q operand, cached keys and values, residual rows, next RMSNorm operand and its sums of
 // squares, SwiGLU rows, the LM head's
 // per-workgroup argmax values and indices) must be bit-identical.

@@ -41,7 +41,8 @@ typedef enum cllm_status {
     CLLM_ERR_IO = 5,       /* weight file could not be read */
     CLLM_ERR_FORMAT = 6,   /* weight file header or size is wrong */
     CLLM_ERR_DEVICE = 7,   /* a HIP call failed; the context is unusable */
-    CLLM_ERR_NUMERIC = 8   /* a logit was NaN */
+    CLLM_ERR_NUMERIC = 8   /* a logit was NaN; the sequence stops, and the slot's next prefill
+                              clears its key and value caches before it runs */
 } cllm_status;
 
 #define CLLM_DTYPE_F32 0

@@ -77,6 +77,10 @@ struct cllm_ctx {
     // host state per slot
     struct Slot {
         bool prefilled = false;
+        // a NaN logit was reported: the cache may hold NaN rows past the committed length, which a
+        // later request's attention would multiply by zero probabilities (giving NaN), so the
+        // slot's next prefill clears its cache first
+        bool dirty = false;
         int L = 0, pending = 0;
         int64_t trace_n = 0;  // trajectory records of the slot's last recorded decode
     };
@@ -528,6 +532,22 @@ cllm_status setup(cllm_ctx *c, int mode, int nseq, const int32_t *seq, const int
     return CLLM_OK;
 }
 
+// A NaN logit in slot seq (see Slot::dirty).
+cllm_status numeric_fail(cllm_ctx *c, int seq, const char *where) {
+    c->slot[seq].dirty = true;
+    return fail(c, CLLM_ERR_NUMERIC, "NaN logit%s (slot %d)", where, seq);
+}
+
+// Zero the key and value caches of a slot that reported a NaN logit, before its next prefill.
+cllm_status clear_if_dirty(cllm_ctx *c, int seq) {
+    if (!c->slot[seq].dirty) return CLLM_OK;
+    const size_t bytes = c->kv_seq * c->elem;
+    HIPCHK(c, hipMemsetAsync(static_cast<uint8_t *>(c->kc) + (size_t)seq * bytes, 0, bytes, c->stream));
+    HIPCHK(c, hipMemsetAsync(static_cast<uint8_t *>(c->vt) + (size_t)seq * bytes, 0, bytes, c->stream));
+    c->slot[seq].dirty = false;
+    return CLLM_OK;
+}
+
 // Read the control blocks of every slot (h: max_batch entries).
 cllm_status read_ctl(cllm_ctx *c, Ctl *h) {
     HIPCHK(c, hipMemcpyAsync(h, c->ctl, sizeof(Ctl) * c->max_batch, hipMemcpyDeviceToHost, c->stream));
@@ -546,6 +566,7 @@ cllm_status check_ids(cllm_ctx *c, const int32_t *ids, int n) {
 // row tile only.
 cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
     c->slot[seq].prefilled = false;
+    if (cllm_status st = clear_if_dirty(c, seq)) return st;
     c->in_prefill = true;
     struct Flag {  // cleared on every return
         bool &f;
@@ -576,7 +597,10 @@ cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
 // caches and first tokens are those of one prefill per prompt.
 cllm_status prefill_packed_impl(cllm_ctx *c, int B, const int32_t *seq_ids, const int32_t *prompts,
                                 const size_t *off, const int32_t *lens) {
-    for (int b = 0; b < B; ++b) c->slot[seq_ids[b]].prefilled = false;
+    for (int b = 0; b < B; ++b) {
+        c->slot[seq_ids[b]].prefilled = false;
+        if (cllm_status st = clear_if_dirty(c, seq_ids[b])) return st;
+    }
     c->in_prefill = true;
     struct Flag {  // cleared on every return
         bool &f;
@@ -663,7 +687,7 @@ cllm_status step_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, cons
     std::vector<Ctl> h(c->max_batch);
     if ((s = read_ctl(c, h.data()))) return s;
     for (int b = 0; b < B; ++b)
-        if (h[seq_ids[b]].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
+        if (h[seq_ids[b]].err) return numeric_fail(c, seq_ids[b], "");
     if (c->dbg_on && c->dbg_host)
         HIPCHK(c, hipMemcpy(c->dbg_host, c->dbg, (size_t)std::min(R, c->dbg_rows) * c->V * 4, hipMemcpyDeviceToHost));
     for (int b = 0; b < B; ++b) {
@@ -738,7 +762,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     if ((s = read_ctl(c, h.data()))) return s;
     for (int b = 0; b < B; ++b) {
         Ctl &ct = h[seq_ids[b]];
-        if (ct.err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill (slot %d)", seq_ids[b]);
+        if (ct.err) return numeric_fail(c, seq_ids[b], " in the prefill");
         ct.n = n;
         ct.max_new = max_new;
         ct.policy = gs[b].policy;
@@ -779,7 +803,7 @@ cllm_status decode_batch_impl(cllm_ctx *c, int32_t B, const int32_t *seq_ids, co
     int lag = 0;     // iterations queued after the state in h was taken
     auto check_err = [&]() -> cllm_status {
         for (int b = 0; b < B; ++b)
-            if (h[seq_ids[b]].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit (slot %d)", seq_ids[b]);
+            if (h[seq_ids[b]].err) return numeric_fail(c, seq_ids[b], "");
         return CLLM_OK;
     };
     while (true) {
@@ -1456,7 +1480,7 @@ cllm_status cllm_prefill(cllm_ctx *c, int32_t seq, const int32_t *prompt, int32_
     if ((s = prefill_impl(c, seq, prompt, len))) return s;
     std::vector<Ctl> h(c->max_batch);
     if ((s = read_ctl(c, h.data()))) return s;
-    if (h[seq].err) return fail(c, CLLM_ERR_NUMERIC, "NaN logit in the prefill");
+    if (h[seq].err) return numeric_fail(c, seq, " in the prefill");
     if (c->dbg_on && c->dbg_host) {  // rows of the last chunk's last 64-row tile, to host rows 0..
         const int last = (len - 1) % c->pchunk;
         const int r0 = last / kMaxRows * kMaxRows;

@@ -362,6 +362,36 @@ def test_abi_errors_on_device(tiny):
     assert 1 <= a <= 3
 
 
+def test_nan_logits_are_reported():
+    # A NaN logit is an error, not a token: the embeddings of ids 128..255 are NaN, so a prompt
+    # holding one fails in the prefill, and a clean prompt whose uniform-random guesses (or the
+    # model's own predictions) bring one into a block fails in the decode, alone or batched; the
+    # status is ERR_NUMERIC and a clean prefill works afterwards.
+    from paper_2403_00835_amd import binding
+    log("[gpu] NaN logits: prefill, decode and batched decode report ERR_NUMERIC")
+    ws = workload.make_weights(TINY)
+    ws[0] = ws[0].copy()
+    ws[0][128:] = np.nan
+    g = binding.Model(TINY, max_ctx=128, max_block=8, max_new=32, max_batch=2, weights=ws)
+    try:
+        clean = workload.make_prompt(TINY, 12) % 128
+        bad = clean.copy()
+        bad[5] = 200
+        with pytest.raises(binding.CllmError) as e:
+            g.prefill(bad)
+        assert e.value.status == 8
+        with pytest.raises(binding.CllmError) as e:
+            g.jacobi_decode(clean, 8, 32, policy=GUESS_UNIFORM, seed=5)
+        assert e.value.status == 8
+        with pytest.raises(binding.CllmError) as e:
+            g.jacobi_decode_batch([0, 1], [clean, clean[:7]], 8, 32)
+        assert e.value.status == 8
+        y0 = g.prefill(clean)
+        assert 0 <= y0 < 256
+    finally:
+        g.close()
+
+
 def test_weight_file_roundtrip(tiny, tmp_path):
     from paper_2403_00835_amd import binding
     log("[gpu] weight file load")

@@ -608,19 +608,20 @@ cllm_status prefill_packed_impl(cllm_ctx *c, int B, const int32_t *seq_ids, cons
     } flag{c->in_prefill};
     const int chunk = c->pchunk;
     std::vector<int> done(B, 0);  // prompt rows already prefilled
-    std::vector<int32_t> seq, m, toks;
+    std::vector<int32_t> seq, m;
     int b = 0;
     while (b < B) {
         seq.clear();
         m.clear();
-        toks.clear();
+        // the pass's tokens are one contiguous run of the concatenated prompts (the caller's
+        // buffer, valid for the whole call)
+        const int32_t *zs = prompts + off[b] + done[b];
         uint64_t reset = 0, adv = 0, lm = 0;
         int R = 0, maxm = 0, nch = 1;
         while (b < B && R < chunk && (int)seq.size() < kMaxSeqs) {
             const int e = (int)seq.size(), take = std::min(lens[b] - done[b], chunk - R);
             seq.push_back(seq_ids[b]);
             m.push_back(take);
-            toks.insert(toks.end(), prompts + off[b] + done[b], prompts + off[b] + done[b] + take);
             if (done[b] == 0) reset |= 1ull << e;
             done[b] += take;
             nch = std::max(nch, ceil_div(done[b], kAttnChunk));
@@ -634,7 +635,7 @@ cllm_status prefill_packed_impl(cllm_ctx *c, int B, const int32_t *seq_ids, cons
             }
         }
         const int ne = (int)seq.size();
-        cllm_status st = setup(c, MODE_PREFILL, ne, seq.data(), m.data(), toks.data(), 0, reset, true);
+        cllm_status st = setup(c, MODE_PREFILL, ne, seq.data(), m.data(), zs, 0, reset, true);
         if (st) return st;
         IterShape sh{R, ne, maxm, std::min(c->nch, nch), lm != 0, -1};
         sh.prompt = true;

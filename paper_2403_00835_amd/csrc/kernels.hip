@@ -458,8 +458,10 @@ __global__ __launch_bounds__(kWave * RG) void attn_partial_kernel(AttnParams p) 
 
 // Combine the chunk partials of one (head, row) in chunk order and write the O operand.
 // Wave 0 derives the chunk weights w_c = 2^(m_c - M) into LDS; every thread (one output dim)
-// then sums w_c * O_c in chunk order. The loads are issued in two rounds: the row count and the
-// row's position, then the chunk maxima, sums and the first kCombinePre chunks' values together.
+// then sums w_c * O_c in chunk order, and the denominator sum w_c * l_c in chunk order beside
+// it (each thread forms the same value; no thread waits for another's). The loads are issued
+// in two rounds: the row count and the row's position, then the chunk maxima, sums and the
+// first kCombinePre chunks' values together.
 constexpr int kCombinePre = 16;  // chunks whose values are requested with the maxima
 
 template <Prec P>
@@ -477,7 +479,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
     const int cap = p.rr.cap;
     const size_t b0 = (size_t)h * p.nch * cap + row;
     __shared__ float s_w[kMaxChunks], s_l[kMaxChunks];
-    __shared__ float s_den;
     const int dim = tid;
     const bool has_dim = dim < p.hd;
     float pre[kCombinePre];
@@ -500,27 +501,30 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
         }
     }
     __syncthreads();
-    if (tid == 0) {
-        float den = 0.0f;
-        for (int c = 0; c < nlive; ++c) den += s_w[c] * s_l[c];
-        s_den = den;
-    }
-    __syncthreads();
     if (!has_dim) return;
-    float num = 0.0f;
+    float num = 0.0f, den = 0.0f;
 #pragma unroll
     for (int c = 0; c < kCombinePre; ++c)
-        if (c < nlive) num += s_w[c] * pre[c];
+        if (c < nlive) {
+            den += s_w[c] * s_l[c];
+            num += s_w[c] * pre[c];
+        }
     int c = kCombinePre;
     for (; c + 4 <= nlive; c += 4) {
         float o[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) o[u] = p.Opart[(b0 + (size_t)(c + u) * cap) * p.hd + dim];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) num += s_w[c + u] * o[u];
+        for (int u = 0; u < 4; ++u) {
+            den += s_w[c + u] * s_l[c + u];
+            num += s_w[c + u] * o[u];
+        }
     }
-    for (; c < nlive; ++c) num += s_w[c] * p.Opart[(b0 + (size_t)c * cap) * p.hd + dim];
-    put_act<P>(reinterpret_cast<T *>(p.O), act_plane(cap, p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / s_den);
+    for (; c < nlive; ++c) {
+        den += s_w[c] * s_l[c];
+        num += s_w[c] * p.Opart[(b0 + (size_t)c * cap) * p.hd + dim];
+    }
+    put_act<P>(reinterpret_cast<T *>(p.O), act_plane(cap, p.d), act_idx<P>(row, h * p.hd + dim, p.d), num / den);
 }
 
 // ------------------------------------------------------------------------------------------

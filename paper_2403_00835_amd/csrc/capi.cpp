@@ -595,6 +595,7 @@ cllm_status prefill_impl(cllm_ctx *c, int seq, const int32_t *prompt, int len) {
 // that hold a prompt's last row; entries whose rows do not end their prompt only advance. Every
 // prompt row takes the prompt GEMM and the chunk-parallel attention at absolute positions, so the
 // caches and first tokens are those of one prefill per prompt.
+static_assert(kMaxPrefillRows <= 64 * kMaxRows && kMaxSeqs <= 64, "one mask bit per row tile and per entry");
 cllm_status prefill_packed_impl(cllm_ctx *c, int B, const int32_t *seq_ids, const int32_t *prompts,
                                 const size_t *off, const int32_t *lens) {
     for (int b = 0; b < B; ++b) {

@@ -164,6 +164,19 @@ def test_tiny_decode_equals_oracle(tiny):
     assert st["decode_ms"] > 0 and st["prefill_ms"] > 0
 
 
+def test_tiny_short_decodes_equal_ar(tiny):
+    # The decode loop queues rounds of iterations it knows are needed and reads the sequence
+    # state while a round's last iteration runs: decodes of 1-3 tokens, a block longer than the
+    # output and an output one longer than a block end with exactly max_new tokens, the greedy ones.
+    log("[gpu] tiny short decodes (max_new 1-3, n up to 64) vs GPU AR")
+    prompt = workload.make_prompt(TINY, 9, seed=12)
+    ar, _ = tiny.gpu.ar_decode(prompt, 17)
+    for n, max_new in [(1, 1), (8, 1), (8, 2), (64, 3), (16, 17), (2, 17)]:
+        out, st = tiny.gpu.jacobi_decode(prompt, n, max_new, policy=GUESS_UNIFORM, seed=n)
+        np.testing.assert_array_equal(out, ar[:max_new])
+        assert st["tokens"] == max_new and 1 <= st["steps"] <= max_new
+
+
 @pytest.mark.parametrize("policy,block_policy", [(GUESS_UNIFORM, BLOCK_SHRINK), (GUESS_STREAM, BLOCK_SHRINK),
                                                  (GUESS_STREAM_REINJECT, BLOCK_SHRINK),
                                                  (GUESS_STREAM_REINJECT, BLOCK_SLIDE), (GUESS_STREAM, BLOCK_SLIDE)])

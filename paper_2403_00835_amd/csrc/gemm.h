@@ -14,8 +14,7 @@ constexpr int kNtGateUp = 6;  // gate/up ((gate, up) tile pairs; 229 workgroups 
 constexpr int kNtResid = 1;   // O projection
 constexpr int kDownSplits = 4;  // down projection: K split over 4 workgroups per 64-column group
 constexpr int kGemmDepth = 2; // k-steps in flight per wave
-constexpr int kPromptDepth = 6;  // prompt GEMM: k-steps in flight per workgroup
-constexpr int kPromptRows = 64;  // prompt GEMM: rows of its row tiles (the row capacity is a multiple)
+constexpr int kPromptRows = 128;  // prompt GEMM: its largest row tile (the row capacity is a multiple)
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATE_UP = 2, GEMM_DOWN = 3, GEMM_LM = 4, GEMM_LOGITS = 5 };
 
@@ -88,8 +87,9 @@ hipError_t launch_gemm(GemmKind kind, bool bf16, int rg, int row_tiles, const Ge
 
 // Prompt (prefill) product of `kind` (QKV, O, gate/up, down) over `rows` rows (bf16 models):
 // workgroup tiles of up to kPromptRows rows with operands shared through LDS; every prompt row
-// takes this path, so its values do not depend on the chunking. The down product uses the
-// residual epilogue directly (no K split). The row capacity must be a multiple of kPromptRows.
+// takes this path, so its values do not depend on the chunking. O and down run as fixed K ranges
+// (2 and 4) into fp32 partials, then a reduction with the residual epilogue. The row capacity
+// must be a multiple of kPromptRows.
 hipError_t launch_gemm_prompt(GemmKind kind, int rows, const GemmParams &p, hipStream_t s, hipEvent_t e0,
                               hipEvent_t e1);
 

@@ -394,33 +394,35 @@ __global__ __launch_bounds__(W * kWave) void gemm_kernel(GemmParams p) {
 // Prompt GEMM (prefill passes, bf16): Y[rows x N] = A[rows x K] * W^T over the same packed
 // operands, for workgroup tiles of 16 RG rows x 16 NT columns. The 8 waves form a WM x (8 / WM)
 // grid over the tile and each accumulates its sub-tile over every k-step in order (one MFMA per
-// plane, hi then lo); the operands of a k-step (2 RG activation blocks and NT weight tiles of
-// 1 KiB each) are loaded once per workgroup, DP k-steps ahead into registers, and staged through
-// three LDS buffers, so every weight and activation byte is fetched once per workgroup instead
-// of once per wave. A row's reduction order depends only on K, never on the rows of a
-// pass, so every prompt row gets the same values whatever the chunk size; the order differs from
-// gemm_kernel's (which keeps eight k-step classes so decode rows are exact across row counts),
-// so prompt rows always take this kernel. Epilogues and the RMSNorm row factor are gemm_kernel's.
+// plane, hi then lo). The operands of a k-step (2 RG activation blocks and NT weight tiles of
+// 1 KiB each) are loaded once per workgroup from global memory straight into LDS (LDS DMA: no
+// register round trip, no LDS write instructions), into a ring of NB buffers NB - 1 k-steps
+// ahead, with a small LDS footprint so that two or three workgroups share a CU and hide each
+// other's latency. A k-step's blocks are complete once this wave's DMA count has dropped to the
+// later k-steps' loads (explicit vmcnt wait) and every wave has passed a barrier; the barrier is
+// issued without the compiler's LDS fence (which would wait for every outstanding DMA), with
+// compiler-only fences so no LDS access moves across it. The buffer a k-step refills was last
+// read in the previous k-step, before that barrier. A row's reduction order depends only on K
+// (and on the fixed K ranges of a split launch), never on the rows of a pass, so every prompt
+// row gets the same values whatever the chunk size; the order differs from gemm_kernel's (which
+// keeps eight k-step classes so decode rows are exact across row counts), so prompt rows always
+// take this kernel. Epilogues and the RMSNorm row factor are gemm_kernel's.
 // ------------------------------------------------------------------------------------------
-// LDS of the prompt GEMM (floats): three staging buffers during the main loop; afterwards the
-// output tile (and, for E_RESID, the epilogue scratch before it) reuse them; the row factors sit
-// in the last ROWS floats, apart from both.
-template <int NT, int RG, int EP>
-__host__ __device__ constexpr int prompt_lds_floats() {
+template <int NT, int RG, int EP, int NB>
+__host__ __device__ constexpr int prompt_dma_lds_floats() {
     constexpr int ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;
-    constexpr int stage = 3 * BLK * kWave * 4;
+    constexpr int stage = NB * BLK * kWave * 4;
     constexpr int after = (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1);
     return (stage > after ? stage : after) + ROWS;
 }
 
-template <int NT, int RG, int WM, int EP, int DP>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmParams p) {
+template <int NT, int RG, int WM, int EP, int NB>
+__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_dma_kernel(GemmParams p) {
     constexpr Prec P = Prec::BF16;
     constexpr int W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
-    constexpr int BLK = 2 * RG + NT, NLW = BLK / W;  // 1 KiB blocks per k-step, loads per wave
-    static_assert(RG % WM == 0 && NT % WN == 0 && BLK % W == 0, "tile split");
-    static_assert(DP % 6 == 0, "the unrolled block covers the register ring, 3 LDS buffers and 2 operand sets");
-    constexpr bool ROWSCALE = EP != E_RESID;
+    constexpr int BLK = 2 * RG + NT, NLW = BLK / W;  // 1 KiB blocks per k-step, DMA loads per wave
+    static_assert(RG % WM == 0 && NT % WN == 0 && BLK % W == 0 && NB >= 3, "tile split, ring depth");
+    constexpr bool ROWSCALE = EP != E_RESID && EP != E_LOGITS;  // the product follows an RMSNorm
     constexpr int ROWS = 16 * RG, COLS = 16 * NT;
     // Workgroup L runs on XCD L % 8 (round-robin dispatch). Column group cg belongs to XCD cg % 8,
     // and each XCD takes its column groups in turn with their row tiles consecutively, so the row
@@ -434,13 +436,22 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmPar
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w / WN, wn = w % WN;
-    const int Ks = p.Ks;
+    // E_LOGITS with p.kc > 0: grid y takes k-steps [y kc, min((y + 1) kc, Ks)) and writes its
+    // partial products to plane y
+    int Ks = p.Ks, ks0 = 0;
+    if constexpr (EP == E_LOGITS) {
+        if (p.kc > 0) {
+            ks0 = blockIdx.y * p.kc;
+            Ks = min(p.kc, p.Ks - ks0);
+            p.Zout += (size_t)blockIdx.y * p.zstride;
+        }
+    }
 
     extern __shared__ float smem[];
-    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [3][BLK][64] during the main loop
+    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64] during the main loop
     float *s_red = smem;                               // then epilogue scratch (E_RESID) ...
     float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);  // ... and the output tile
-    float *s_inv = smem + prompt_lds_floats<NT, RG, EP>() - ROWS;  // row factors (apart from both)
+    float *s_inv = smem + prompt_dma_lds_floats<NT, RG, EP, NB>() - ROWS;  // row factors (apart)
 
     f32x4 sq_pre[2];
     if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
@@ -462,151 +473,7 @@ __global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_kernel(GemmPar
             src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
             adv[i] = tiles * kWave;
         }
-    }
-    u32x4 ring[DP][NLW];
-    auto load = [&](int slot, int s) {
-        const size_t ss = (size_t)min(s, Ks - 1);  // past the end: a harmless reload of the last k-step
-#pragma unroll
-        for (int i = 0; i < NLW; ++i) ring[slot][i] = src[i][ss * adv[i]];
-    };
-    auto stage = [&](int slot, int buf) {
-#pragma unroll
-        for (int i = 0; i < NLW; ++i) s_stage[((size_t)buf * BLK + w + i * W) * kWave + lane] = ring[slot][i];
-    };
-    struct Ops {
-        u32x4 a[2][RGW], b[NTW];
-    };
-    auto fetch = [&](Ops &o, int buf) {
-        const u32x4 *bp = s_stage + (size_t)buf * BLK * kWave + lane;
-#pragma unroll
-        for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-            for (int r = 0; r < RGW; ++r) o.a[pl][r] = bp[(pl * RG + wm * RGW + r) * kWave];
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) o.b[j] = bp[(2 * RG + wn * NTW + j) * kWave];
-    };
-    f32x4 acc[RGW][NTW];
-#pragma unroll
-    for (int r = 0; r < RGW; ++r)
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) acc[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto mfmas = [&](const Ops &o) {
-#pragma unroll
-        for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-            for (int r = 0; r < RGW; ++r)
-#pragma unroll
-                for (int j = 0; j < NTW; ++j) acc[r][j] = mfma_kstep<P>(o.a[pl][r], o.b[j], acc[r][j]);
-    };
-
-    // Pipeline: k-step t is loaded into ring slot t % DP (DP k-steps ahead), staged into LDS
-    // buffer t % 3 two k-steps ahead, and read into operand set t % 2 one k-step ahead, so the
-    // MFMAs of k-step t overlap the LDS reads of t + 1 and the loads of t + 2 + DP. A buffer is
-    // rewritten three k-steps after it was staged: its readers (the iteration before) have passed
-    // the barrier in between. Memory operations past the last k-step are harmless repeats (the
-    // addresses are clamped; their MFMAs are skipped), so every iteration issues the same loads.
-#pragma unroll
-    for (int q = 0; q < DP; ++q) load(q, q);
-    stage(0, 0);
-    load(0, DP);
-    stage(1, 1);
-    load(1, DP + 1);
-    __syncthreads();
-    Ops ops[2];
-    fetch(ops[0], 0);
-    const int nblk = (Ks + DP - 1) / DP;
-    for (int bi = 0; bi < nblk; ++bi) {
-#pragma unroll
-        for (int q = 0; q < DP; ++q) {
-            const int s = bi * DP + q;
-            fetch(ops[(q + 1) & 1], (q + 1) % 3);
-            if (s < Ks) mfmas(ops[q & 1]);  // uniform over the workgroup
-            stage((q + 2) % DP, (q + 2) % 3);
-            load((q + 2) % DP, s + 2 + DP);
-            __syncthreads();
-        }
-    }
-
-    if constexpr (ROWSCALE) row_factor_reduce<W, ROWS>(p, row0, tid, sq_pre, s_inv);
-    __syncthreads();
-    // C layout of a 16 x 16 tile: lane l, register v -> row 4 (l / 16) + v, column l % 16
-#pragma unroll
-    for (int r = 0; r < RGW; ++r)
-#pragma unroll
-        for (int j = 0; j < NTW; ++j)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int row = 16 * (wm * RGW + r) + 4 * (lane >> 4) + v;
-                float x = acc[r][j][v];
-                if constexpr (ROWSCALE) x *= s_inv[row];
-                s_tile[row * (COLS + 1) + 16 * (wn * NTW + j) + (lane & 15)] = x;
-            }
-    __syncthreads();
-    gemm_epilogue<P, NT, RG, EP, W>(p, s_tile, s_red, row0, m, wg, tid, lane, w);
-}
-
-// The same prompt product with the operand blocks loaded from global memory straight into LDS
-// (LDS DMA: no register round trip, no LDS write instructions), into a ring of NB buffers
-// NB - 1 k-steps ahead, with a small LDS footprint so that two or three workgroups share a CU
-// and hide each other's latency. A k-step's blocks are complete once this wave's DMA count has
-// dropped to the later k-steps' loads (explicit vmcnt wait) and every wave has passed a barrier;
-// the barrier is issued without the compiler's LDS fence (which would wait for every
-// outstanding DMA), with compiler-only fences so no LDS access moves across it. The buffer a
-// k-step refills was last read in the previous k-step, before that barrier. Each wave
-// accumulates its sub-tile over every k-step in order (hi then lo plane), as
-// gemm_prompt_kernel does, so both give bit-identical values.
-template <int NT, int RG, int EP, int NB>
-__host__ __device__ constexpr int prompt_dma_lds_floats() {
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT, BLK = 2 * RG + NT;
-    constexpr int stage = NB * BLK * kWave * 4;
-    constexpr int after = (EP == E_RESID ? ROWS * COLS : 0) + ROWS * (COLS + 1);
-    return (stage > after ? stage : after) + ROWS;
-}
-
-template <int NT, int RG, int WM, int EP, int NB>
-__global__ __launch_bounds__(kGemmWaves * kWave) void gemm_prompt_dma_kernel(GemmParams p) {
-    constexpr Prec P = Prec::BF16;
-    constexpr int W = kGemmWaves, WN = W / WM, RGW = RG / WM, NTW = NT / WN;
-    constexpr int BLK = 2 * RG + NT, NLW = BLK / W;  // 1 KiB blocks per k-step, DMA loads per wave
-    static_assert(RG % WM == 0 && NT % WN == 0 && BLK % W == 0 && NB >= 3, "tile split, ring depth");
-    constexpr bool ROWSCALE = EP != E_RESID;
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    // XCD-grouped column groups with their row tiles consecutive (as gemm_prompt_kernel)
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    const int wg = (slot / p.row_tiles) * 8 + xcd, row0 = (slot % p.row_tiles) * ROWS;
-    request_together(p.W, p.A, p.ssq, p.Ks, p.cols, p.lda, p.rr.cap, p.T, p.n_wg);
-    const int m = p.rr.tab->R - row0;
-    if (m <= 0 || wg >= p.n_wg) return;
-    const int rg0 = row0 >> 4, t0 = wg * NT;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = w / WN, wn = w % WN;
-    const int Ks = p.Ks;
-
-    extern __shared__ float smem[];
-    u32x4 *s_stage = reinterpret_cast<u32x4 *>(smem);  // [NB][BLK][64] during the main loop
-    float *s_red = smem;                               // then epilogue scratch (E_RESID) ...
-    float *s_tile = smem + (EP == E_RESID ? ROWS * COLS : 0);  // ... and the output tile
-    float *s_inv = smem + prompt_dma_lds_floats<NT, RG, EP, NB>() - ROWS;  // row factors (apart)
-
-    f32x4 sq_pre[2];
-    if constexpr (ROWSCALE) row_factor_preload<W>(p, row0, tid, sq_pre);
-
-    // This wave's blocks b = w + i W of every k-step (as gemm_prompt_kernel)
-    const int tiles = p.cols >> 4, ks_a = p.lda / PrecT<P>::KSTEP;
-    const u32x4 *src[NLW];
-    int adv[NLW];
-#pragma unroll
-    for (int i = 0; i < NLW; ++i) {
-        const int b = w + i * W;
-        if (b < 2 * RG) {
-            const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A) + (b / RG) * act_plane(p.rr.cap, p.lda);
-            src[i] = reinterpret_cast<const u32x4 *>(A + (size_t)(rg0 + b % RG) * ks_a * kWave * 8) + lane;
-            adv[i] = kWave;
-        } else {
-            src[i] = reinterpret_cast<const u32x4 *>(p.W + (size_t)min(t0 + b - 2 * RG, tiles - 1) * kTileBytes) + lane;
-            adv[i] = tiles * kWave;
-        }
+        src[i] += (size_t)ks0 * adv[i];  // the first k-step of this workgroup's K range
     }
     // k-step s into ring buffer s % NB; past the last k-step a harmless reload of it
     auto issue = [&](int s) {
@@ -1182,39 +1049,28 @@ static hipError_t launch_prompt_dma(const GemmParams &p, int rows, hipStream_t s
     return hipGetLastError();
 }
 
-template <int NT, int RG, int WM, int EP, int DP>
-static hipError_t launch_prompt_t(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
-    const size_t lds = (size_t)prompt_lds_floats<NT, RG, EP>() * sizeof(float);
-    // every row tile that starts below `rows` must lie inside the activation buffers
-    if (rows < 1 || rows > p.rr.cap || p.rr.cap % ROWS != 0 || p.lda % 32 != 0 || p.cols % 16 != 0)
-        return hipErrorInvalidValue;
-    GemmParams q = p;
-    q.n_wg = (p.cols + COLS - 1) / COLS;
-    q.row_tiles = (rows + ROWS - 1) / ROWS;
-    const dim3 grid((unsigned)((q.n_wg + 7) / 8 * 8 * q.row_tiles));  // column groups padded to 8 XCDs
-    auto kern = gemm_prompt_kernel<NT, RG, WM, EP, DP>;
-    if (e0 || e1)
-        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, e1, 0, q);
-    else
-        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
-    return hipGetLastError();
-}
+
+template <int NT, int RG, int WM, int NB, int NS>
+static hipError_t launch_prompt_ksplit(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 hipError_t launch_gemm_prompt(GemmKind kind, int rows, const GemmParams &p, hipStream_t s, hipEvent_t e0,
                               hipEvent_t e1) {
     switch (kind) {
     // measured at the LLaMA-2-7B shape, 512 rows, random operands: QKV and gate/up take the LDS-DMA
     // kernel with three buffers (64 x 128 tiles for QKV: 114 us, LDS-staged 64 x 256: 167 us;
-    // 64 x 256 for gate/up: 177-199 us, LDS-staged: 245 us); O and down the LDS-staged kernel
-    // with 64 x 128 tiles (55 and 111 us; the DMA kernel measured no faster for O, slower for down)
+    // 64 x 256 for gate/up: 177-199 us, LDS-staged: 245 us). O and down, whose 4096 columns give
+    // one 64 x 128 workgroup per CU at 512 rows, take the DMA kernel over fixed K ranges and the
+    // reduction: O 64 x 128 tiles and 2 ranges (54.6 us against 56.4 for the LDS-staged kernel;
+    // 37.1 against 52.3 at 256 rows), down 128 x 128 tiles and 4 ranges (103.5 against 116.0;
+    // 61.9 against 102.4 at 256 rows)
     case GEMM_QKV:
         return launch_prompt_dma<8, 4, 2, E_QKV, 3>(p, rows, s, e0, e1);
     case GEMM_GATE_UP:
         return launch_prompt_dma<16, 4, 2, E_SWIGLU, 3>(p, rows, s, e0, e1);
-    case GEMM_O:
-    case GEMM_DOWN:  // X += H W_d^T with the residual epilogue (no K split)
-        return launch_prompt_t<8, 4, 2, E_RESID, kPromptDepth>(p, rows, s, e0, e1);
+    case GEMM_O:  // X += O W_o^T
+        return launch_prompt_ksplit<8, 4, 2, 3, 2>(p, rows, s, e0, e1);
+    case GEMM_DOWN:  // X += H W_d^T
+        return launch_prompt_ksplit<8, 8, 2, 3, 4>(p, rows, s, e0, e1);
     default:
         return hipErrorInvalidValue;
     }
@@ -1305,6 +1161,46 @@ __global__ __launch_bounds__(kReduceThreads) void down_reduce_kernel(GemmParams 
 #pragma unroll
     for (int k = 0; k < G; ++k) tot += __shfl(ss, base + k);
     if (live && g % G == 0) p.ssq_out[(size_t)row * p.T + g / G] = tot;
+}
+
+// A prompt product with the residual epilogue as NS K ranges through the LDS-DMA kernel (fp32
+// partial planes in p.part), then down_reduce_kernel (partials summed in range order, residual,
+// next RMSNorm operand and its sums of squares).
+template <int NT, int RG, int WM, int NB, int NS>
+static hipError_t launch_prompt_ksplit(const GemmParams &p, int rows, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    static_assert(NS >= 1 && NS <= kDownSplits, "down_reduce_kernel sums up to kDownSplits partials");
+    constexpr int ROWS = 16 * RG, COLS = 16 * NT;
+    if (!p.part || rows < 1 || rows > p.rr.cap || p.rr.cap % ROWS != 0 || p.lda % 32 != 0 || p.cols % 16 != 0 ||
+        p.ldx < p.cols || p.Ks < NS)
+        return hipErrorInvalidValue;
+    GemmParams q = p;
+    q.kc = (p.Ks + NS - 1) / NS;
+    q.Zout = p.part;
+    q.ldz = p.ldx;
+    q.V = p.cols;
+    q.zstride = (size_t)p.rr.cap * p.ldx;
+    q.n_wg = (p.cols + COLS - 1) / COLS;
+    q.row_tiles = (rows + ROWS - 1) / ROWS;
+    const int nsplit = (p.Ks + q.kc - 1) / q.kc;
+    const size_t lds = (size_t)prompt_dma_lds_floats<NT, RG, E_LOGITS, NB>() * sizeof(float);
+    const dim3 grid((unsigned)((q.n_wg + 7) / 8 * 8 * q.row_tiles), (unsigned)nsplit);
+    auto kern = gemm_prompt_dma_kernel<NT, RG, WM, E_LOGITS, NB>;
+    if (e0)
+        hipExtLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, e0, nullptr, 0, q);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(kGemmWaves * kWave), lds, s, q);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const int rows_launch = q.row_tiles * ROWS;
+    const size_t n = (size_t)rows_launch * (p.cols / PrecT<Prec::BF16>::VEC);
+    const dim3 grid_r((unsigned)((n + kReduceThreads - 1) / kReduceThreads));
+    if (e1)
+        hipExtLaunchKernelGGL(down_reduce_kernel<Prec::BF16>, grid_r, dim3(kReduceThreads), 0, s, nullptr, e1, 0, p,
+                              nsplit, q.zstride, rows_launch);
+    else
+        hipLaunchKernelGGL(down_reduce_kernel<Prec::BF16>, grid_r, dim3(kReduceThreads), 0, s, p, nsplit, q.zstride,
+                           rows_launch);
+    return hipGetLastError();
 }
 
 // The down product: K split over kDownSplits ranges (fp32 partials in p.part, 64-column

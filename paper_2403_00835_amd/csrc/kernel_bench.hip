@@ -115,7 +115,8 @@ int main(int argc, char **argv) {
     }
     const int rg = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
     const int row_tiles = rows > kMaxRows ? (rows + kMaxRows - 1) / kMaxRows : 1;
-    const int cap = row_tiles * kMaxRows;  // row capacity of the activation buffers
+    // row capacity of the activation buffers: whole decode row tiles and prompt-GEMM row tiles
+    const int cap = (row_tiles * kMaxRows + kPromptRows - 1) / kPromptRows * kPromptRows;
 
     uint8_t *W = dev<uint8_t>(kWBytes, 0x11);  // bf16 0x1111 in every weight
     // one sequence (slot 0) with a block of `rows` rows at positions kL ..

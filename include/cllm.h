@@ -64,9 +64,10 @@ typedef struct cllm_config {
  * max_batch (1..64; 0 means 1) is the number of sequence slots. Each slot is an independent
  * sequence with its own KV cache and state; every call taking `seq` addresses slot seq in
  * [0, max_batch). A batched iteration runs up to max_batch blocks of up to max_block rows.
- * prefill_chunk: prompt rows per forward pass of cllm_prefill (0 means 512; rounded up to a
- * multiple of 64, at most 4096, and to no more than max_ctx rounded up to 64). A prompt is
- * processed in chunks of that many rows; a row's values do not depend on the chunk size (every
+ * prefill_chunk: prompt rows per forward pass of cllm_prefill, and of the shared passes into
+ * which a batched decode packs its prompts (0 means 512; rounded up to a multiple of 64, at most
+ * 4096, and to no more than max_ctx rounded up to 64). A prompt is processed in chunks of that
+ * many rows; a row's values do not depend on the chunk size (every
  * reduction has an order fixed by the model shape), so the size changes speed and activation
  * memory only (about 200 KiB per row at the LLaMA-2-7B shape).
  * workspace, workspace_bytes: optional caller-owned device memory of the context's GPU (for
